@@ -1,0 +1,234 @@
+/*
+ * pbd.h -- C ABI of the PEFT-BD speculative-step library for AMD MI355X (gfx950).
+ *
+ * One speculative step of PEFT-BD (Sec. 3, enumerated algorithm):
+ *   1-2. pbd_draft_block   -- adapter-enabled block-diffusion draft pass: the block
+ *                             [anchor, mask x D] at positions t..t+D attends to the
+ *                             committed prefix KV and bidirectionally inside the
+ *                             block; proposes D tokens in one denoising step.
+ *   3.   pbd_verify_block  -- adapter-disabled causal verify pass over
+ *                             [anchor, x_1..x_D]; writes its K/V at t..t+D.
+ *   4-5. pbd_accept_commit -- greedy longest-prefix acceptance (App. A.1: exact
+ *                             greedy top-1 matching) and KV commit/rollback.
+ * The adapter is LoRA on every linear projection of every block (App. A.2); both
+ * passes have width W = D + 1 ("token width 17", Tab. profile; App. A.4).
+ *
+ * Conventions for every entry point:
+ *  - Pointers named "device" are HIP device pointers; the library never allocates
+ *    device memory.  The caller allocates the packed-weight, KV-cache and workspace
+ *    buffers with the sizes the *_bytes functions return, keeps them alive while
+ *    the context lives, and owns them.  The library allocates only the host-side
+ *    context, freed by pbd_destroy.
+ *  - Calls are asynchronous and ordered on `stream` (a hipStream_t; NULL = the
+ *    legacy default stream).  Per-sequence state (seq_len, anchor) is device
+ *    resident, so a step needs no host synchronisation and can be captured in a
+ *    HIP graph.  A context serves one stream at a time (not thread-safe).
+ *  - Return value: PBD_OK (0) or a negative PBD_ERR_*.  Errors the host can
+ *    detect are reported before anything is enqueued, leaving device state
+ *    untouched.  Errors only the device can detect (capacity overflow, token id
+ *    out of range, forced count out of range) set bits of a sticky device status
+ *    word and skip that sequence's writes; pbd_sync_status reads and clears it.
+ *    pbd_last_error gives a message for the last failed call.
+ *  - Token ids are int32.  Batch sequences are independent (data parallel).
+ */
+#ifndef PBD_H
+#define PBD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct pbd_ctx pbd_ctx;
+typedef void* pbd_stream_t;            /* hipStream_t */
+
+/* status codes */
+#define PBD_OK               0
+#define PBD_ERR_INVALID_ARG (-1)       /* null pointer, bad flag combination, bad value */
+#define PBD_ERR_SHAPE       (-2)       /* shape not supported by the kernels */
+#define PBD_ERR_CAPACITY    (-3)       /* batch > max_batch, buffer too small, length > max_seq */
+#define PBD_ERR_STATE       (-4)       /* context not usable */
+#define PBD_ERR_HIP         (-5)       /* a HIP runtime call failed */
+#define PBD_ERR_UNSUPPORTED (-6)
+
+/* data types of weights, KV cache and GEMM/attention inputs */
+#define PBD_DTYPE_F32  0
+#define PBD_DTYPE_BF16 1
+
+/* pass flags: each pair may be left unset (the pass's default) but not both set */
+#define PBD_PASS_DEFAULT      0u
+#define PBD_PASS_ADAPTER_ON   1u       /* draft default */
+#define PBD_PASS_ADAPTER_OFF  2u       /* verify default */
+#define PBD_PASS_MASK_BLOCK   4u       /* draft default: bidirectional inside the block */
+#define PBD_PASS_MASK_CAUSAL  8u       /* verify default */
+
+/* precision of the activation operands fed to the bf16 matrix cores */
+#define PBD_OPERANDS_BF16    0         /* rounded to bf16 */
+#define PBD_OPERANDS_BF16X2  1         /* bf16 value plus bf16 residual: two MFMAs per weight
+                                          fragment, ~16-bit operand mantissa (default for bf16) */
+
+/* kernel classes timed by the profiling aid */
+#define PBD_KCLASS_GEMM     0          /* layer projection GEMMs (q/k/v, o, gate/up, down) */
+#define PBD_KCLASS_LMHEAD   1          /* tied LM head with fused argmax */
+#define PBD_KCLASS_ATTN     2          /* split-KV attention */
+#define PBD_KCLASS_COMBINE  3          /* split merge + O-projection operand */
+#define PBD_KCLASS_NORM     4          /* RMSNorm / LoRA shrink */
+#define PBD_KCLASS_OTHER    5          /* block assembly, final argmax */
+#define PBD_KCLASS_COUNT    6
+
+/* bits of the device status word */
+#define PBD_STATUS_CAPACITY  1         /* seq_len + W > max_seq, or prompt length out of range */
+#define PBD_STATUS_TOKEN     2         /* a token id outside [0, vocab) */
+#define PBD_STATUS_FORCED_N  4         /* forced accepted count outside [0, D] */
+
+/*
+ * Model and capacity description.  The backbone is a Qwen3-style decoder
+ * (RMSNorm, per-head QK RMSNorm before rotate-half RoPE, grouped-query attention,
+ * SwiGLU MLP, tied embedding/LM head, no biases); the paper evaluates
+ * Qwen3-0.6B (Sec. 4.1) and does not print the architecture.
+ * Supported: head_dim 64 or 128; n_q_heads a multiple of n_kv_heads;
+ * hidden, ffn, n_q_heads*head_dim multiples of 64; vocab a multiple of 16;
+ * 1 <= block <= 32; lora_rank in [0, 64] and a multiple of 8; mask_id in [0, vocab).
+ */
+typedef struct pbd_config {
+    int32_t n_layers;
+    int32_t hidden;
+    int32_t n_q_heads;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t ffn;
+    int32_t vocab;
+    int32_t lora_rank;      /* r */
+    float   lora_alpha;     /* scale s = alpha / r (App. A.2: r = 16, alpha = 32) */
+    int32_t block;          /* D, masked positions per draft (Sec. 3: D = 16) */
+    int32_t mask_id;        /* token id of the diffusion mask */
+    float   rms_eps;
+    float   rope_theta;
+    int32_t qk_norm;        /* 1: per-head RMSNorm of q and k before RoPE */
+    int32_t dtype;          /* PBD_DTYPE_F32 or PBD_DTYPE_BF16 */
+    int32_t max_batch;      /* sequences per call */
+    int32_t max_seq;        /* KV capacity per sequence (positions) */
+} pbd_config;
+
+/*
+ * Canonical weights, all device pointers of element type `dtype`, row-major
+ * [out_features][in_features] for matrices (y = W x).  LoRA (App. A.2):
+ * lora_a[i] is A [r][in], lora_b[i] is B [out][r], for i in order
+ * q, k, v, o, gate, up, down; y = W x + (alpha/r) B (A x) when the adapter is on.
+ */
+typedef struct pbd_layer_weights {
+    const void *attn_norm, *q, *k, *v, *o, *q_norm, *k_norm, *mlp_norm, *gate, *up, *down;
+    const void *lora_a[7];
+    const void *lora_b[7];
+} pbd_layer_weights;
+
+typedef struct pbd_weights {
+    const void* embed;                  /* [vocab][hidden]; also the LM head (tied) */
+    const void* final_norm;             /* [hidden] */
+    const pbd_layer_weights* layers;    /* HOST array of n_layers entries */
+} pbd_weights;
+
+/* Buffer sizes in bytes for a configuration; 0 if the configuration is invalid. */
+size_t pbd_packed_weight_bytes(const pbd_config* cfg);
+size_t pbd_kv_bytes(const pbd_config* cfg);
+size_t pbd_workspace_bytes(const pbd_config* cfg);
+
+/*
+ * Validate `cfg`, repack the canonical weights into `packed` (layouts chosen by
+ * the library for streaming), build the RoPE table, and create a context that
+ * uses `packed`, `kv` and `ws`.  The canonical weights may be freed once
+ * `stream` has completed.  *out receives the context (NULL on failure).
+ */
+int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon,
+                     void* packed, size_t packed_bytes,
+                     void* kv, size_t kv_bytes,
+                     void* ws, size_t ws_bytes,
+                     pbd_stream_t stream, pbd_ctx** out);
+
+/*
+ * Adapter-off causal pass over each prompt (the committed prefix the speculative
+ * steps start from).  tokens: device int32 [batch][max_len] (row b holds
+ * lengths[b] ids, the rest ignored); lengths: device int32 [batch], each in
+ * [1, max_len] and with lengths[b] + D + 1 <= max_seq.  Writes the prompt K/V to
+ * the cache, seq_len[b] = lengths[b] and anchor[b] = greedy next token (device
+ * int32 [batch] each), which is the first generated token.
+ */
+int pbd_prefill(pbd_ctx* ctx, int32_t batch, const int32_t* tokens, const int32_t* lengths,
+                int32_t max_len, int32_t* seq_len, int32_t* anchor, pbd_stream_t stream);
+
+/*
+ * Draft pass (Sec. 3 steps 1-2; App. A.4): block [anchor, mask x D] at positions
+ * seq_len..seq_len+D; by default adapter on and bidirectional block mask.
+ * seq_len, anchor: device int32 [batch] (read).  draft: device int32 [batch][D]
+ * receives argmax over token ids != mask_id of block rows 1..D (ties: lowest id).
+ * logits: NULL or device float [batch][D+1][vocab] receiving all rows' logits.
+ * The KV cache is not written (the block K/V is scratch in the workspace).
+ */
+int pbd_draft_block(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
+                    uint32_t flags, int32_t* draft, float* logits, pbd_stream_t stream);
+
+/*
+ * Verify pass (Sec. 3 step 3): block [anchor, draft[b][0..D-1]] at positions
+ * seq_len..seq_len+D; by default adapter off and causal mask.  Writes the block
+ * K/V into the cache at positions seq_len..seq_len+D.  verify: device int32
+ * [batch][D+1] receives p_0..p_D, the greedy token after each block row.
+ * logits: NULL or device float [batch][D+1][vocab].
+ */
+int pbd_verify_block(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
+                     const int32_t* draft, uint32_t flags, int32_t* verify, float* logits,
+                     pbd_stream_t stream);
+
+/*
+ * Acceptance and commit (Sec. 3 steps 4-5; App. A.1).  For each sequence:
+ * n = largest k <= D with draft[i-1] == verify[i-1] for all i <= k (or
+ * forced_n[b] if forced_n != NULL, device int32 [batch], each in [0, D]);
+ * out_tokens[b][0..n] = draft[0..n-1], verify[n] (device int32 [batch][D+1];
+ * entries past n are set to -1); n_accepted[b] = n (device int32 [batch]);
+ * seq_len[b] += n + 1 and anchor[b] = verify[b][n] (in/out, device).  Cache rows
+ * seq_len..seq_len+n written by the verify are kept; later rows are rolled back
+ * (they lie past the new seq_len and are overwritten by the next verify).
+ */
+int pbd_accept_commit(pbd_ctx* ctx, int32_t batch, const int32_t* draft, const int32_t* verify,
+                      const int32_t* forced_n, int32_t* seq_len, int32_t* anchor,
+                      int32_t* n_accepted, int32_t* out_tokens, pbd_stream_t stream);
+
+/*
+ * Wait for `stream`, read and clear the device status word.  *status receives
+ * the PBD_STATUS_* bits raised since the last call (0 = none).
+ */
+int pbd_sync_status(pbd_ctx* ctx, pbd_stream_t stream, int32_t* status);
+
+/* Attention split tuning: prefix keys per split-KV work item (multiple of 16). */
+int pbd_set_attn_keys_per_split(pbd_ctx* ctx, int32_t keys);
+
+/*
+ * Precision of the GEMM activation operands of bf16 models: PBD_OPERANDS_BF16 or
+ * PBD_OPERANDS_BF16X2 (default).  Weights and the KV cache stay bf16 either way;
+ * accumulation is fp32.  Ignored for fp32 models.
+ */
+int pbd_set_operand_precision(pbd_ctx* ctx, int32_t mode);
+
+/*
+ * Profiling aid: while enabled, every kernel launch of a pass is bracketed by a
+ * pair of HIP events on the call's stream (this adds launch gaps, so time passes
+ * with profiling off).  pbd_profile_enable(ctx, on) also discards earlier
+ * records.  pbd_profile_read waits for the last recorded event and returns the
+ * summed device time and the launch count of kernel class `kclass`
+ * (PBD_KCLASS_*) since the last enable.
+ */
+int pbd_profile_enable(pbd_ctx* ctx, int32_t on);
+int pbd_profile_read(pbd_ctx* ctx, int32_t kclass, double* total_ms, int64_t* launches);
+
+/* Message of the last failed call on ctx (or of the last failed init if ctx is NULL). */
+const char* pbd_last_error(const pbd_ctx* ctx);
+
+/* Free the host context.  Device buffers stay the caller's. */
+void pbd_destroy(pbd_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PBD_H */

@@ -1,0 +1,214 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Tolerances: logits max-abs 1e-4 for the fp32 tiny model; token ids, accepted
+counts and committed tokens exact wherever the oracle's top-1/top-2 margin
+exceeds the tolerance (elsewhere both choices are correct).
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import model as om
+
+from gpu_harness import GpuRun, decisive
+
+pytestmark = pytest.mark.gpu
+
+TOL32 = 1e-4
+
+
+def _tiny(D=16, zero_b=False, **kw):
+    cfg = synth.TINY.with_(block=D, **kw)
+    w = synth.make_weights(cfg, synth.WORKLOADS[0].seed(0), zero_lora_b=zero_b)
+    return cfg, w
+
+
+def _check_tokens(got, ref_logits, tol, exclude=None, rows=None):
+    lg = ref_logits if rows is None else ref_logits[rows]
+    dec = decisive(lg, tol, exclude)
+    lg2 = lg.copy()
+    if exclude is not None:
+        lg2[..., exclude] = -np.inf
+    ref = np.argmax(lg2, axis=-1)
+    assert np.all(got[dec] == ref[dec]), (got, ref, dec)
+    return dec
+
+
+def test_tiny_step_matches_oracle():
+    cfg, w = _tiny()
+    lengths, prompts = synth.workload_inputs(synth.WORKLOADS[0])
+    g = GpuRun(cfg, w, max_batch=1, max_seq=256)
+    anchor = g.prefill(prompts)
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompts[0])
+    assert int(anchor[0]) == st.anchor
+    d, dlg = g.draft()
+    d_ref, dl_ref = om.draft(m, st)
+    dlg = dlg.cpu().numpy()[0]
+    assert np.abs(dlg - dl_ref).max() <= TOL32
+    _check_tokens(d.cpu().numpy()[0], dl_ref[1:], TOL32, exclude=cfg.mask_id)
+    v, vlg = g.verify(d)
+    p_ref, vl_ref, _, _ = om.verify(m, st, d.cpu().numpy()[0])
+    assert np.abs(vlg.cpu().numpy()[0] - vl_ref).max() <= TOL32
+    _check_tokens(v.cpu().numpy()[0], vl_ref, TOL32)
+    n, out = g.accept(d, v)
+    nn, oo = om.accept(d.cpu().numpy()[0], v.cpu().numpy()[0])
+    assert int(n[0]) == nn
+    assert list(out.cpu().numpy()[0][:nn + 1]) == oo
+    assert int(g.seq_len[0]) == len(prompts[0]) + nn + 1
+    assert g.status() == 0
+    g.close()
+
+
+@pytest.mark.parametrize("D,t", [(1, 1), (4, 7), (16, 7), (16, 40), (16, 100), (3, 33)])
+def test_tiny_shapes(D, t):
+    cfg, w = _tiny(D)
+    prompt = synth.make_prompts(cfg, [t], 100 + t)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=192)
+    g.prefill([prompt])
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompt)
+    d, dlg = g.draft()
+    _, dl_ref = om.draft(m, st)
+    assert np.abs(dlg.cpu().numpy()[0] - dl_ref).max() <= TOL32
+    v, vlg = g.verify(d)
+    _, vl_ref, _, _ = om.verify(m, st, d.cpu().numpy()[0])
+    assert np.abs(vlg.cpu().numpy()[0] - vl_ref).max() <= TOL32
+    g.close()
+
+
+def test_tiny_ragged_batch():
+    cfg, w = _tiny(16)
+    lens = [5, 40, 129]
+    prompts = synth.make_prompts(cfg, lens, 7)
+    g = GpuRun(cfg, w, max_batch=4, max_seq=192)
+    anchors = g.prefill(prompts)
+    m = om.OracleModel(w)
+    sts = [om.prefill(m, p) for p in prompts]
+    assert list(anchors) == [s.anchor for s in sts]
+    assert list(g.seq_len.cpu().numpy()) == lens
+    d, dlg = g.draft()
+    v, vlg = g.verify(d)
+    for b, st in enumerate(sts):
+        _, dl_ref = om.draft(m, st)
+        assert np.abs(dlg.cpu().numpy()[b] - dl_ref).max() <= TOL32
+        _, vl_ref, _, _ = om.verify(m, st, d.cpu().numpy()[b])
+        assert np.abs(vlg.cpu().numpy()[b] - vl_ref).max() <= TOL32
+    g.close()
+
+
+def test_tiny_forced_loop_matches_oracle():
+    """Several draft/verify/commit rounds with forced acceptance: committed
+    tokens, lengths and the next pass all follow the oracle."""
+    cfg, w = _tiny(4)
+    prompt = synth.make_prompts(cfg, [9], 3)[0]
+    forced = synth.make_forced_accepts(8, 1, cfg.block, 5)[:, 0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=128)
+    g.prefill([prompt])
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompt)
+    for r in range(8):
+        d, dlg = g.draft()
+        d_np = d.cpu().numpy()[0]
+        d_ref, dl_ref = om.draft(m, st)
+        assert np.abs(dlg.cpu().numpy()[0] - dl_ref).max() <= TOL32
+        v, vlg = g.verify(d)
+        p_ref, vl_ref, k, vv = om.verify(m, st, d_np)
+        assert np.abs(vlg.cpu().numpy()[0] - vl_ref).max() <= TOL32
+        n, out = g.accept(d, v, forced=[int(forced[r])])
+        nn, oo = om.accept(d_np, v.cpu().numpy()[0], forced_n=int(forced[r]))
+        om.commit(st, nn, oo, k, vv)
+        assert int(n[0]) == nn and list(out.cpu().numpy()[0][:nn + 1]) == oo
+        assert int(g.seq_len[0]) == st.seq_len and int(g.anchor[0]) == st.anchor
+    assert g.status() == 0
+    g.close()
+
+
+def test_zero_lora_b_adapter_is_bitwise_no_op():
+    from paper_2607_12422_amd import binding as bd
+    cfg, w = _tiny(16, zero_b=True)
+    prompt = synth.make_prompts(cfg, [50], 9)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=128)
+    g.prefill([prompt])
+    _, on = g.draft(flags=bd.PBD_PASS_ADAPTER_ON)
+    _, off = g.draft(flags=bd.PBD_PASS_ADAPTER_OFF)
+    assert np.array_equal(on.cpu().numpy(), off.cpu().numpy())
+    g.close()
+
+
+def test_causal_override_draft_equals_verify_of_mask_block():
+    from paper_2607_12422_amd import binding as bd
+    cfg, w = _tiny(16, zero_b=True)
+    prompt = synth.make_prompts(cfg, [50], 10)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=128)
+    g.prefill([prompt])
+    _, dl = g.draft(flags=bd.PBD_PASS_MASK_CAUSAL)
+    masks = g.i32(np.full((1, cfg.block), cfg.mask_id))
+    _, vl = g.verify(masks)
+    assert np.array_equal(dl.cpu().numpy(), vl.cpu().numpy())
+    g.close()
+
+
+def test_greedy_drafts_are_fully_accepted():
+    """Drafts equal to the verifier's greedy continuation give n = D and the
+    bonus token (exact greedy matching, App. A.1)."""
+    cfg, w = _tiny(4)
+    prompt = synth.make_prompts(cfg, [20], 11)[0]
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompt)
+    seq = list(prompt) + [st.anchor]
+    cont, margins = [], []
+    for _ in range(5):
+        s2 = om.prefill(m, seq)
+        cont.append(s2.anchor)
+        seq.append(s2.anchor)
+    g = GpuRun(cfg, w, max_batch=1, max_seq=64)
+    g.prefill([prompt])
+    d = g.i32([cont[:4]])
+    v, vlg = g.verify(d)
+    dec = decisive(vlg.cpu().numpy()[0], TOL32)
+    assert dec.all()
+    n, out = g.accept(d, v)
+    assert int(n[0]) == 4
+    assert list(out.cpu().numpy()[0]) == cont
+    g.close()
+
+
+def test_capacity_overflow_sets_status_and_skips():
+    cfg, w = _tiny(16)
+    prompt = synth.make_prompts(cfg, [10], 12)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=64)
+    g.prefill([prompt])
+    g.seq_len.fill_(64 - 10)            # seq_len + W > max_seq
+    d, _ = g.draft(logits=False)
+    v, _ = g.verify(d, logits=False)
+    from paper_2607_12422_amd import binding as bd
+    assert g.status() & bd.PBD_STATUS_CAPACITY
+    g.seq_len.fill_(10)
+    n, out = g.accept(g.i32([[1] * 16]), g.i32([[1] * 17]), forced=[17])
+    assert g.status() & bd.PBD_STATUS_FORCED_N
+    assert int(g.seq_len[0]) == 10
+    g.close()
+
+
+def test_qwen_shape_step_matches_oracle():
+    """Qwen3-0.6B shape, bf16, prefix 512: one draft + verify step."""
+    w_ = synth.WORKLOADS[1]
+    cfg = w_.cfg
+    w = synth.make_weights(cfg, w_.seed(0))
+    lengths, prompts = synth.workload_inputs(w_)
+    g = GpuRun(cfg, w, max_batch=1, max_seq=1024)
+    anchor = g.prefill(prompts)
+    d, dlg = g.draft()
+    v, vlg = g.verify(d)
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompts[0])
+    _, dl_ref = om.draft(m, st)
+    _, vl_ref, _, _ = om.verify(m, st, d.cpu().numpy()[0])
+    ed = np.abs(dlg.cpu().numpy()[0] - dl_ref).max()
+    ev = np.abs(vlg.cpu().numpy()[0] - vl_ref).max()
+    print(f"qwen bf16: draft max-abs {ed:.4f}, verify max-abs {ev:.4f}")
+    assert ed <= 2e-2 and ev <= 2e-2
+    _check_tokens(d.cpu().numpy()[0], dl_ref[1:], 2e-2, exclude=cfg.mask_id)
+    _check_tokens(v.cpu().numpy()[0], vl_ref, 2e-2)
+    g.close()
