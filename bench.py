@@ -86,6 +86,7 @@ def main():
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--kps", type=int, default=0, help="attention keys per split (0: library default)")
     ap.add_argument("--operands", choices=["bf16", "bf16x2"], default="bf16x2")
+    ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of replaying HIP graphs")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -125,33 +126,59 @@ def main():
     setup_s = time.time() - t_setup
 
     n_iter = args.warmup + args.steps
-    # per-step state copies, made before timing (each step starts at the prefill state)
-    seqs = [seq0.clone() for _ in range(n_iter)]
-    ancs = [anc0.clone() for _ in range(n_iter)]
     draft = torch.zeros(B, cfg.block, **i32)
     verify = torch.zeros(B, cfg.width, **i32)
     n_acc = torch.zeros(B, **i32)
     out = torch.zeros(B, cfg.width, **i32)
+    seq = seq0.clone()
+    anc = anc0.clone()
+    # counts committed tokens across steps (each step restarts from the prefill state)
+    committed_acc = torch.zeros(B, dtype=torch.int64, device=dev)
+
+    def do_draft():
+        eng.pbd_draft_block(seq, anc, draft)
+
+    def do_verify():
+        eng.pbd_verify_block(seq, anc, draft, verify)
+
+    def do_accept():
+        eng.pbd_accept_commit(draft, verify, seq, anc, n_acc, out)
+        committed_acc.add_(n_acc + 1)
+        seq.copy_(seq0)
+        anc.copy_(anc0)
+
+    parts = [do_draft, do_verify, do_accept]
+    if not args.eager:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for f in parts:          # warm the allocator and the library outside capture
+                f()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graphs = []
+        for f in parts:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                f()
+            graphs.append(g)
+        parts = [g.replay for g in graphs]
     stream = torch.cuda.current_stream()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n_iter)]
 
     def step(k, record=True):
         e = ev[k]
-        if record:
-            e[0].record(stream)
-        eng.pbd_draft_block(seqs[k], ancs[k], draft, stream=stream)
-        if record:
-            e[1].record(stream)
-        eng.pbd_verify_block(seqs[k], ancs[k], draft, verify, stream=stream)
-        if record:
-            e[2].record(stream)
-        eng.pbd_accept_commit(draft, verify, seqs[k], ancs[k], n_acc, out, stream=stream)
+        for i, f in enumerate(parts):
+            if record:
+                e[i].record(stream)
+            f()
         if record:
             e[3].record(stream)
 
     for k in range(args.warmup):
         step(k, record=False)
     torch.cuda.synchronize()
+    committed_acc.zero_()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     wall0 = time.perf_counter()
@@ -166,7 +193,7 @@ def main():
     d_ms = [ev[k][0].elapsed_time(ev[k][1]) for k in range(args.warmup, n_iter)]
     v_ms = [ev[k][1].elapsed_time(ev[k][2]) for k in range(args.warmup, n_iter)]
     a_ms = [ev[k][2].elapsed_time(ev[k][3]) for k in range(args.warmup, n_iter)]
-    committed = int((torch.stack(seqs[args.warmup:]) - seq0).sum())
+    committed = int(committed_acc.sum())
     status = eng.pbd_sync_status()
     dmed, vmed, amed = statistics.median(d_ms), statistics.median(v_ms), statistics.median(a_ms)
     byt = algorithmic_bytes(cfg, B, lengths)
@@ -181,7 +208,8 @@ def main():
         "data": "synthetic (seeded random-init weights of the model shape, uniform random prompt ids)",
         "config": {"workload": w_.name, "model_shape": cfg.name, "batch": B,
                    "prefix": lengths if B <= 8 else [min(lengths), max(lengths)],
-                   "block": cfg.block, "lora_rank": cfg.lora_rank, "operands": args.operands},
+                   "block": cfg.block, "lora_rank": cfg.lora_rank, "operands": args.operands,
+                   "launch": "eager" if args.eager else "hip-graph"},
         "draft_ms": round(dmed, 4), "verify_ms": round(vmed, 4), "accept_ms": round(amed, 4),
         "draft_ms_p10_p90": [round(x, 4) for x in pct(d_ms)],
         "verify_ms_p10_p90": [round(x, 4) for x in pct(v_ms)],
@@ -201,11 +229,10 @@ def main():
         # Same steps again with the library's per-kernel HIP events (adds gaps, so
         # kernel durations only); roofline of the dominant kernel class.
         eng.pbd_profile_enable(True)
-        for k in range(args.warmup, n_iter):
-            seqs[k].copy_(seq0)
-            ancs[k].copy_(anc0)
-        for k in range(args.warmup, n_iter):
-            step(k, record=False)
+        for k in range(args.steps):
+            do_draft()
+            do_verify()
+            do_accept()
         torch.cuda.synchronize()
         prof = {}
         for ci, name in enumerate(binding.KCLASSES):

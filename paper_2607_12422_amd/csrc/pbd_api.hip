@@ -19,35 +19,33 @@ int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 thread_local std::string g_init_error;
 
+constexpr int MAX_DIM = 16384;   // bound on hidden, ffn and n_q_heads*head_dim
+constexpr int LMHEAD_GRID = 512;  // work-groups of the persistent LM head (two per CU)
+
 // Every size and offset the library uses, derived from a validated config.
 struct Layout {
     int L, H, NQ, NKV, HD, F, V, r, D, W, Bmax, max_seq, dtype;
     size_t esz;
     int FK, EPL;
-    int Mmax, MTmax, TF, nblk, G, QTmax;
+    int Mmax, MTmax, RT, nblk, G, QTmax;
     int kb_qkv, kb_o, kb_gu, kb_d, kb_e;
-    int ft_qkv, ft_o, ft_gu, ft_d, ft_e;
     int tiles_qkv, tiles_o, tiles_gu, tiles_d, tiles_e;
-    int ks_o, ks_d, nqkv, S_max;
+    int nqkv, S_max;
     // packed weights (bytes)
     struct LayerOff {
-        size_t qkv, o, gu, d, attn_norm, mlp_norm, q_norm, k_norm, a[7];
+        size_t qkv, o, gu, d, attn_norm, mlp_norm, q_norm, k_norm;
+        size_t la[7];                  // LoRA shrink tiles, order q k v o gate up down
+        size_t lb_qkv, lb_o, lb_gu, lb_d;  // LoRA expand blocks
     };
     std::vector<LayerOff> lay;
     size_t p_embed, p_final_norm, p_rope, packed_bytes;
     // KV cache
     size_t kv_half, kv_bytes;
     // workspace
-    size_t w_x, w_part, w_qkv, w_xa, w_xa_t[3], w_xo, w_xo_t, w_xm, w_xm_t[2], w_xd, w_xd_t, w_xf;
-    size_t w_xa_lo, w_xo_lo, w_xm_lo, w_xd_lo, w_xf_lo;
+    size_t w_x, w_qkv, w_sq_a, w_sq_m;
+    size_t w_xa[2], w_xo[2], w_xm[2], w_xd[2];      // operand value and residual fragments
     size_t w_attn_o, w_attn_ml, w_arg_val, w_arg_idx, w_tokens, w_pos0, w_nrows, w_status, ws_bytes;
 };
-
-int split_k(int kb) {
-    if (kb % 4 == 0) return 4;
-    if (kb % 2 == 0) return 2;
-    return 1;
-}
 
 int validate(const pbd_config* c, std::string& err) {
     if (!c) { err = "config is NULL"; return PBD_ERR_INVALID_ARG; }
@@ -60,14 +58,14 @@ int validate(const pbd_config* c, std::string& err) {
     }
     PBD_REQ(c->dtype == PBD_DTYPE_F32 || c->dtype == PBD_DTYPE_BF16, PBD_ERR_INVALID_ARG, "dtype %d unknown", c->dtype);
     PBD_REQ(c->n_layers >= 1 && c->n_layers <= 256, PBD_ERR_SHAPE, "n_layers %d out of range", c->n_layers);
-    PBD_REQ(c->hidden >= 64 && c->hidden % 64 == 0 && c->hidden <= MAX_NORM_DIM, PBD_ERR_SHAPE,
-            "hidden %d must be a multiple of 64 and <= %d", c->hidden, MAX_NORM_DIM);
+    PBD_REQ(c->hidden >= 64 && c->hidden % 64 == 0 && c->hidden <= MAX_DIM, PBD_ERR_SHAPE,
+            "hidden %d must be a multiple of 64 and <= %d", c->hidden, MAX_DIM);
     PBD_REQ(c->head_dim == 64 || c->head_dim == 128, PBD_ERR_SHAPE, "head_dim %d must be 64 or 128", c->head_dim);
     PBD_REQ(c->n_kv_heads >= 1 && c->n_q_heads >= c->n_kv_heads && c->n_q_heads % c->n_kv_heads == 0,
             PBD_ERR_SHAPE, "n_q_heads %d must be a multiple of n_kv_heads %d", c->n_q_heads, c->n_kv_heads);
-    PBD_REQ(c->n_q_heads * c->head_dim <= MAX_SHRINK_DIM, PBD_ERR_SHAPE, "n_q_heads*head_dim too large");
-    PBD_REQ(c->ffn >= 64 && c->ffn % 64 == 0 && c->ffn <= MAX_SHRINK_DIM, PBD_ERR_SHAPE,
-            "ffn %d must be a multiple of 64 and <= %d", c->ffn, MAX_SHRINK_DIM);
+    PBD_REQ(c->n_q_heads * c->head_dim <= MAX_DIM, PBD_ERR_SHAPE, "n_q_heads*head_dim too large");
+    PBD_REQ(c->ffn >= 64 && c->ffn % 64 == 0 && c->ffn <= MAX_DIM, PBD_ERR_SHAPE,
+            "ffn %d must be a multiple of 64 and <= %d", c->ffn, MAX_DIM);
     PBD_REQ(c->vocab >= 16 && c->vocab % 16 == 0, PBD_ERR_SHAPE, "vocab %d must be a positive multiple of 16", c->vocab);
     PBD_REQ(c->mask_id >= 0 && c->mask_id < c->vocab, PBD_ERR_INVALID_ARG, "mask_id %d outside [0, vocab)", c->mask_id);
     PBD_REQ(c->block >= 1 && c->block <= 32, PBD_ERR_SHAPE, "block %d must lie in [1, 32]", c->block);
@@ -95,35 +93,37 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.FK = 4 * y.EPL;
     y.Mmax = y.Bmax * y.W;
     y.MTmax = cdiv(y.Mmax, 16);
-    y.TF = cdiv(y.r, y.FK);
+    y.RT = cdiv(y.r, 16);
     y.nblk = cdiv(y.max_seq, 16);
     y.G = y.NQ / y.NKV;
     y.QTmax = cdiv(y.G * y.W, 16);
     y.nqkv = (y.NQ + 2 * y.NKV) * y.HD;
     y.kb_qkv = y.H / y.FK; y.kb_o = y.NQ * y.HD / y.FK; y.kb_gu = y.H / y.FK; y.kb_d = y.F / y.FK; y.kb_e = y.H / y.FK;
-    y.ft_qkv = y.kb_qkv + y.TF; y.ft_o = y.kb_o + y.TF; y.ft_gu = y.kb_gu + y.TF; y.ft_d = y.kb_d + y.TF; y.ft_e = y.kb_e;
     y.tiles_qkv = y.nqkv / 16; y.tiles_o = y.H / 16; y.tiles_gu = 2 * y.F / 16; y.tiles_d = y.H / 16; y.tiles_e = y.V / 16;
-    y.ks_o = split_k(y.kb_o);
-    y.ks_d = split_k(y.kb_d);
     y.S_max = std::min(64, cdiv(y.max_seq, 16));
 
-    const size_t FR = 1024;  // bytes per fragment
+    const size_t FR = 1024;                       // bytes per fragment
+    const size_t EB = (size_t)64 * 4 * y.esz;     // bytes per LoRA expand block
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
-    y.p_embed = take((size_t)y.tiles_e * y.ft_e * FR);
+    y.p_embed = take((size_t)y.tiles_e * y.kb_e * FR);
     y.lay.resize(y.L);
+    const int kb_in[7] = {y.kb_qkv, y.kb_qkv, y.kb_qkv, y.kb_o, y.kb_gu, y.kb_gu, y.kb_d};
     for (int l = 0; l < y.L; ++l) {
         Layout::LayerOff& o = y.lay[l];
-        o.qkv = take((size_t)y.tiles_qkv * y.ft_qkv * FR);
-        o.o = take((size_t)y.tiles_o * y.ft_o * FR);
-        o.gu = take((size_t)y.tiles_gu * y.ft_gu * FR);
-        o.d = take((size_t)y.tiles_d * y.ft_d * FR);
+        o.qkv = take((size_t)y.tiles_qkv * y.kb_qkv * FR);
+        o.o = take((size_t)y.tiles_o * y.kb_o * FR);
+        o.gu = take((size_t)y.tiles_gu * y.kb_gu * FR);
+        o.d = take((size_t)y.tiles_d * y.kb_d * FR);
         o.attn_norm = take(y.H * y.esz);
         o.mlp_norm = take(y.H * y.esz);
         o.q_norm = take(y.HD * y.esz);
         o.k_norm = take(y.HD * y.esz);
-        const int in_f[7] = {y.H, y.H, y.H, y.NQ * y.HD, y.H, y.H, y.F};
-        for (int i = 0; i < 7; ++i) o.a[i] = take((size_t)y.r * in_f[i] * y.esz);
+        for (int i = 0; i < 7; ++i) o.la[i] = take((size_t)y.RT * kb_in[i] * FR);
+        o.lb_qkv = take((size_t)y.tiles_qkv * y.RT * EB);
+        o.lb_o = take((size_t)y.tiles_o * y.RT * EB);
+        o.lb_gu = take((size_t)y.tiles_gu * y.RT * EB);
+        o.lb_d = take((size_t)y.tiles_d * y.RT * EB);
     }
     y.p_final_norm = take(y.H * y.esz);
     y.p_rope = take((size_t)y.max_seq * (y.HD / 2) * 8);
@@ -134,25 +134,15 @@ void make_layout(const pbd_config* c, Layout& y) {
 
     off = 0;
     const size_t xfr = (size_t)y.MTmax * FR;    // one k step of an operand
+    const size_t nlo = y.dtype == PBD_DTYPE_BF16 ? 1 : 0;
     y.w_x = take((size_t)y.Mmax * y.H * 4);
-    y.w_part = take((size_t)std::max(y.ks_o, y.ks_d) * y.Mmax * y.H * 4);
     y.w_qkv = take((size_t)y.Mmax * y.nqkv * 4);
-    y.w_xa = take(y.kb_qkv * xfr);
-    for (int i = 0; i < 3; ++i) y.w_xa_t[i] = take(std::max(y.TF, 1) * xfr);
-    y.w_xo = take(y.kb_o * xfr);
-    y.w_xo_t = take(std::max(y.TF, 1) * xfr);
-    y.w_xm = take(y.kb_gu * xfr);
-    for (int i = 0; i < 2; ++i) y.w_xm_t[i] = take(std::max(y.TF, 1) * xfr);
-    y.w_xd = take(y.kb_d * xfr);
-    y.w_xd_t = take(std::max(y.TF, 1) * xfr);
-    y.w_xf = take(y.kb_e * xfr);
-    // residual halves of split (bf16 hi + bf16 lo) operands
-    const size_t lo = y.dtype == PBD_DTYPE_BF16 ? 1 : 0;
-    y.w_xa_lo = take(lo * y.kb_qkv * xfr);
-    y.w_xo_lo = take(lo * y.kb_o * xfr);
-    y.w_xm_lo = take(lo * y.kb_gu * xfr);
-    y.w_xd_lo = take(lo * y.kb_d * xfr);
-    y.w_xf_lo = take(lo * y.kb_e * xfr);
+    y.w_sq_a = take((size_t)std::max(y.tiles_d, 1) * y.Mmax * 4);
+    y.w_sq_m = take((size_t)std::max(y.tiles_o, 1) * y.Mmax * 4);
+    y.w_xa[0] = take(y.kb_qkv * xfr); y.w_xa[1] = take(nlo * y.kb_qkv * xfr);
+    y.w_xo[0] = take(y.kb_o * xfr);   y.w_xo[1] = take(nlo * y.kb_o * xfr);
+    y.w_xm[0] = take(y.kb_gu * xfr);  y.w_xm[1] = take(nlo * y.kb_gu * xfr);
+    y.w_xd[0] = take(y.kb_d * xfr);   y.w_xd[1] = take(nlo * y.kb_d * xfr);
     const size_t nrow_part = (size_t)y.Bmax * y.NQ * y.W * y.S_max;
     y.w_attn_o = take(nrow_part * y.HD * 4);
     y.w_attn_ml = take(nrow_part * 2 * 4);
@@ -249,40 +239,42 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     const bool lora = q.adapter && y.r > 0;
     const bool split = c->split && dt == PBD_DTYPE_BF16;
     float* x = (float*)(ws + y.w_x);
-    float* part = (float*)(ws + y.w_part);
-    const size_t part_stride = (size_t)y.Mmax * y.H;
+    float* sq_a = (float*)(ws + y.w_sq_a);
+    float* sq_m = (float*)(ws + y.w_sq_m);
     int* pos0 = (int*)(ws + y.w_pos0);
     int* nrows = (int*)(ws + y.w_nrows);
     int* status = (int*)(ws + y.w_status);
+    auto hi = [&](const size_t* o) { return (void*)(ws + o[0]); };
+    auto lo = [&](const size_t* o) { return split ? (void*)(ws + o[1]) : (void*)nullptr; };
 
     AssembleArgs as{};
     as.mode = q.mode; as.W = W; as.H = y.H; as.vocab = y.V; as.mask_id = c->cfg.mask_id; as.max_seq = y.max_seq;
-    as.chunk_pos = q.chunk_pos; as.max_len = q.max_len;
+    as.chunk_pos = q.chunk_pos; as.max_len = q.max_len; as.MT = MT; as.m_stride = y.Mmax;
     as.seq_len = q.seq_len; as.anchor = q.anchor; as.drafts = q.drafts; as.prompt = q.prompt; as.lengths = q.lengths;
     as.tokens = (int*)(ws + y.w_tokens); as.pos0 = pos0; as.nrows = nrows; as.status = status;
-    as.embed = pk + y.p_embed; as.x = x;
+    as.embed = pk + y.p_embed; as.gain = pk + y.lay[0].attn_norm; as.x = x;
+    as.op_hi = hi(y.w_xa); as.op_lo = lo(y.w_xa); as.sq = sq_a;
     PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_assemble(dt, as, B, st), "assemble");
 
     const int s_launch = std::min(y.S_max, cdiv(y.max_seq, c->kps));
+    auto base_gemm = [&](FGemmArgs& g, size_t w_off, int tiles, int kb, const size_t* xop) {
+        g = FGemmArgs{};
+        g.w = (const uint4*)(pk + w_off); g.n_tiles = tiles; g.kb = kb;
+        g.xhi = (const uint4*)hi(xop); g.xlo = (const uint4*)lo(xop);
+        g.M = M; g.MT = MT; g.sq_stride = y.Mmax; g.norm_dim = y.H; g.eps = c->cfg.rms_eps;
+        g.lora = lora ? 1 : 0; g.rt = y.RT; g.scale = scale; g.exclude = -1;
+    };
     for (int l = 0; l < y.L; ++l) {
-        const Layout::LayerOff& lo = y.lay[l];
-        // attention pre-norm (+ LoRA shrink for q, k, v)
-        NormArgs na{};
-        na.M = M; na.MT = MT; na.H = y.H; na.eps = c->cfg.rms_eps; na.x = x;
-        na.partials = part; na.n_partials = l > 0 ? y.ks_d : 0; na.partial_stride = part_stride;
-        na.gain = pk + lo.attn_norm; na.xfrag = ws + y.w_xa; na.xfrag_lo = split ? ws + y.w_xa_lo : nullptr;
-        na.n_src = lora ? 3 : 0; na.r = y.r; na.scale = scale;
-        for (int i = 0; i < 3; ++i) { na.lora_a[i] = pk + lo.a[i]; na.tail[i] = ws + y.w_xa_t[i]; }
-        PBD_TIMED(c, st, PBD_KCLASS_NORM, launch_norm(dt, na, st), "attn norm");
-
-        GemmArgs g{};
-        g.w = (const uint4*)(pk + lo.qkv); g.n_tiles = y.tiles_qkv; g.ft = y.ft_qkv; g.kb = y.kb_qkv; g.ks = 1;
-        g.tail_frags = lora ? y.TF : 0; g.r = y.r; g.tail_mode = TAIL_BY_TILE;
-        g.tile_split0 = y.NQ * y.HD / 16; g.tile_split1 = (y.NQ + y.NKV) * y.HD / 16;
-        g.x = (const uint4*)(ws + y.w_xa); g.xlo = split ? (const uint4*)(ws + y.w_xa_lo) : nullptr;
-        for (int i = 0; i < 3; ++i) g.xt[i] = (const uint4*)(ws + y.w_xa_t[i]);
-        g.M = M; g.MT = MT; g.out = (float*)(ws + y.w_qkv); g.ldo = y.nqkv; g.exclude = -1;
-        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm(dt, g, EPI_STORE, st), "qkv gemm");
+        const Layout::LayerOff& lo_ = y.lay[l];
+        // q/k/v projection: attention RMSNorm folded in, LoRA per source matrix
+        FGemmArgs g;
+        base_gemm(g, lo_.qkv, y.tiles_qkv, y.kb_qkv, y.w_xa);
+        g.sq = sq_a; g.n_sq = l == 0 ? 1 : y.tiles_d;
+        g.lora_mode = LORA_BY_TILE; g.tile_split0 = y.NQ * y.HD / 16; g.tile_split1 = (y.NQ + y.NKV) * y.HD / 16;
+        for (int i = 0; i < 3; ++i) g.la[i] = (const uint4*)(pk + lo_.la[i]);
+        g.lb = pk + lo_.lb_qkv;
+        g.out = (float*)(ws + y.w_qkv); g.ldo = y.nqkv;
+        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_STORE, st), "qkv gemm");
 
         AttnArgs at{};
         at.layer = l; at.max_batch = y.Bmax; at.n_q = y.NQ; at.n_kv = y.NKV; at.nblk = y.nblk; at.W = W; at.G = y.G;
@@ -291,81 +283,58 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         at.eps = c->cfg.rms_eps; at.scale_log2 = (float)(1.0 / sqrt((double)y.HD) * 1.4426950408889634);
         at.smem_main = attn_smem_main(dt, y.HD, y.QTmax);
         at.pos0 = pos0; at.nrows = nrows; at.qkv = (const float*)(ws + y.w_qkv);
-        at.q_norm = pk + lo.q_norm; at.k_norm = pk + lo.k_norm; at.rope = (const float2*)(pk + y.p_rope);
+        at.q_norm = pk + lo_.q_norm; at.k_norm = pk + lo_.k_norm; at.rope = (const float2*)(pk + y.p_rope);
         at.kcache = c->kv; at.vcache = c->kv + y.kv_half;
         at.part_o = (float*)(ws + y.w_attn_o); at.part_ml = (float*)(ws + y.w_attn_ml);
         PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn(dt, y.HD, y.QTmax, at, B, st), "attention");
 
         CombineArgs cb{};
-        cb.M = M; cb.MT = MT; cb.W = W; cb.n_q = y.NQ; cb.head_dim = y.HD; cb.kps = c->kps; cb.s_launch = s_launch;
-        cb.r = lora ? y.r : 0; cb.scale = scale; cb.pos0 = pos0;
-        cb.part_o = at.part_o; cb.part_ml = at.part_ml; cb.xfrag = ws + y.w_xo;
-        cb.xfrag_lo = split ? ws + y.w_xo_lo : nullptr;
-        cb.lora_a = lora ? pk + lo.a[3] : nullptr; cb.tail = ws + y.w_xo_t;
-        PBD_TIMED(c, st, PBD_KCLASS_COMBINE, launch_combine(dt, cb, st), "attention combine");
+        cb.W = W; cb.n_q = y.NQ; cb.head_dim = y.HD; cb.kps = c->kps; cb.s_launch = s_launch; cb.MT = MT;
+        cb.pos0 = pos0; cb.part_o = at.part_o; cb.part_ml = at.part_ml;
+        cb.op_hi = hi(y.w_xo); cb.op_lo = lo(y.w_xo);
+        PBD_TIMED(c, st, PBD_KCLASS_COMBINE, launch_combine(dt, cb, M, st), "attention combine");
 
-        GemmArgs go{};
-        go.w = (const uint4*)(pk + lo.o); go.n_tiles = y.tiles_o; go.ft = y.ft_o; go.kb = y.kb_o; go.ks = y.ks_o;
-        go.tail_frags = lora ? y.TF : 0; go.r = y.r; go.tail_mode = TAIL_SINGLE;
-        go.x = (const uint4*)(ws + y.w_xo); go.xt[0] = (const uint4*)(ws + y.w_xo_t);
-        go.xlo = split ? (const uint4*)(ws + y.w_xo_lo) : nullptr;
-        go.M = M; go.MT = MT; go.out = part; go.ldo = y.H; go.partial_stride = part_stride; go.exclude = -1;
-        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm(dt, go, EPI_PARTIAL, st), "o gemm");
+        // O projection + residual; writes the MLP RMSNorm operand
+        base_gemm(g, lo_.o, y.tiles_o, y.kb_o, y.w_xo);
+        g.n_sq = 0; g.lora_mode = LORA_SINGLE; g.la[0] = (const uint4*)(pk + lo_.la[3]); g.lb = pk + lo_.lb_o;
+        g.x = x; g.ldx = y.H; g.gnext = pk + lo_.mlp_norm; g.nx_hi = hi(y.w_xm); g.nx_lo = lo(y.w_xm); g.n_MT = MT;
+        g.sq_out = sq_m;
+        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "o gemm");
 
-        NormArgs nm{};
-        nm.M = M; nm.MT = MT; nm.H = y.H; nm.eps = c->cfg.rms_eps; nm.x = x;
-        nm.partials = part; nm.n_partials = y.ks_o; nm.partial_stride = part_stride;
-        nm.gain = pk + lo.mlp_norm; nm.xfrag = ws + y.w_xm; nm.xfrag_lo = split ? ws + y.w_xm_lo : nullptr;
-        nm.n_src = lora ? 2 : 0; nm.r = y.r; nm.scale = scale;
-        nm.lora_a[0] = pk + lo.a[4]; nm.lora_a[1] = pk + lo.a[5];
-        nm.tail[0] = ws + y.w_xm_t[0]; nm.tail[1] = ws + y.w_xm_t[1];
-        PBD_TIMED(c, st, PBD_KCLASS_NORM, launch_norm(dt, nm, st), "mlp norm");
+        // gate/up + SwiGLU: MLP RMSNorm folded in
+        base_gemm(g, lo_.gu, y.tiles_gu, y.kb_gu, y.w_xm);
+        g.sq = sq_m; g.n_sq = y.tiles_o;
+        g.lora_mode = LORA_ROW_HALF; g.la[0] = (const uint4*)(pk + lo_.la[4]); g.la[1] = (const uint4*)(pk + lo_.la[5]);
+        g.lb = pk + lo_.lb_gu;
+        g.nx_hi = hi(y.w_xd); g.nx_lo = lo(y.w_xd); g.n_MT = MT;
+        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_SWIGLU, st), "gate/up gemm");
 
-        GemmArgs gu{};
-        gu.w = (const uint4*)(pk + lo.gu); gu.n_tiles = y.tiles_gu; gu.ft = y.ft_gu; gu.kb = y.kb_gu; gu.ks = 1;
-        gu.tail_frags = lora ? y.TF : 0; gu.r = y.r; gu.tail_mode = TAIL_BY_ROW_HALF;
-        gu.x = (const uint4*)(ws + y.w_xm); gu.xlo = split ? (const uint4*)(ws + y.w_xm_lo) : nullptr;
-        gu.out_frag_lo = split ? ws + y.w_xd_lo : nullptr;
-        gu.xt[0] = (const uint4*)(ws + y.w_xm_t[0]); gu.xt[1] = (const uint4*)(ws + y.w_xm_t[1]);
-        gu.M = M; gu.MT = MT; gu.out_frag = ws + y.w_xd; gu.out_MT = MT; gu.exclude = -1;
-        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm(dt, gu, EPI_SWIGLU, st), "gate/up gemm");
-
-        if (lora) {
-            ShrinkArgs sh{};
-            sh.M = M; sh.MT = MT; sh.K = y.F; sh.r = y.r; sh.scale = scale;
-            sh.xfrag = ws + y.w_xd; sh.lora_a = pk + lo.a[6]; sh.tail = ws + y.w_xd_t;
-            sh.xfrag_lo = split ? ws + y.w_xd_lo : nullptr;
-            PBD_TIMED(c, st, PBD_KCLASS_NORM, launch_shrink(dt, sh, st), "down shrink");
-        }
-
-        GemmArgs gd{};
-        gd.w = (const uint4*)(pk + lo.d); gd.n_tiles = y.tiles_d; gd.ft = y.ft_d; gd.kb = y.kb_d; gd.ks = y.ks_d;
-        gd.tail_frags = lora ? y.TF : 0; gd.r = y.r; gd.tail_mode = TAIL_SINGLE;
-        gd.x = (const uint4*)(ws + y.w_xd); gd.xt[0] = (const uint4*)(ws + y.w_xd_t);
-        gd.xlo = split ? (const uint4*)(ws + y.w_xd_lo) : nullptr;
-        gd.M = M; gd.MT = MT; gd.out = part; gd.ldo = y.H; gd.partial_stride = part_stride; gd.exclude = -1;
-        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm(dt, gd, EPI_PARTIAL, st), "down gemm");
+        // down projection + residual; writes the next layer's (or the final) RMSNorm operand
+        base_gemm(g, lo_.d, y.tiles_d, y.kb_d, y.w_xd);
+        g.n_sq = 0; g.lora_mode = LORA_SINGLE; g.la[0] = (const uint4*)(pk + lo_.la[6]); g.lb = pk + lo_.lb_d;
+        g.x = x; g.ldx = y.H;
+        g.gnext = l + 1 < y.L ? pk + y.lay[l + 1].attn_norm : pk + y.p_final_norm;
+        g.nx_hi = hi(y.w_xa); g.nx_lo = lo(y.w_xa); g.n_MT = MT; g.sq_out = sq_a;
+        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "down gemm");
     }
 
-    NormArgs nf{};
-    nf.M = M; nf.MT = MT; nf.H = y.H; nf.eps = c->cfg.rms_eps; nf.x = x;
-    nf.partials = part; nf.n_partials = y.ks_d; nf.partial_stride = part_stride;
-    nf.gain = pk + y.p_final_norm; nf.xfrag = ws + y.w_xf; nf.n_src = 0;
-    nf.xfrag_lo = split ? ws + y.w_xf_lo : nullptr;
-    PBD_TIMED(c, st, PBD_KCLASS_NORM, launch_norm(dt, nf, st), "final norm");
-
-    GemmArgs ge{};
-    ge.w = (const uint4*)(pk + y.p_embed); ge.n_tiles = y.tiles_e; ge.ft = y.ft_e; ge.kb = y.kb_e; ge.ks = 1;
-    ge.tail_frags = 0; ge.r = 0; ge.tail_mode = TAIL_SINGLE;
-    ge.x = (const uint4*)(ws + y.w_xf); ge.M = M; ge.MT = MT;
-    ge.xlo = split ? (const uint4*)(ws + y.w_xf_lo) : nullptr;
+    // tied LM head with the final RMSNorm folded in, fused argmax
+    FGemmArgs ge;
+    base_gemm(ge, y.p_embed, y.tiles_e, y.kb_e, y.w_xa);
+    ge.lora = 0; ge.sq = sq_a; ge.n_sq = y.tiles_d;
     ge.logits = q.logits; ge.ldo = y.V;
     ge.arg_val = (float*)(ws + y.w_arg_val); ge.arg_idx = (int*)(ws + y.w_arg_idx);
     ge.exclude = q.mode == PASS_DRAFT ? c->cfg.mask_id : -1;
-    PBD_TIMED(c, st, PBD_KCLASS_LMHEAD, launch_gemm(dt, ge, EPI_ARGMAX, st), "lm head");
+    int n_part = y.tiles_e;
+    if (lmhead_fits(y.kb_e, MT)) {
+        n_part = std::min(y.tiles_e, LMHEAD_GRID);
+        PBD_TIMED(c, st, PBD_KCLASS_LMHEAD, launch_lmhead(dt, ge, n_part, st), "lm head");
+    } else {
+        PBD_TIMED(c, st, PBD_KCLASS_LMHEAD, launch_fgemm(dt, ge, EPI_ARGMAX, st), "lm head");
+    }
 
     ArgmaxArgs am{};
-    am.M = M; am.W = W; am.n_tiles = y.tiles_e; am.mode = q.mode; am.chunk_pos = q.chunk_pos;
+    am.M = M; am.W = W; am.n_tiles = n_part; am.mode = q.mode; am.chunk_pos = q.chunk_pos;
     am.arg_val = ge.arg_val; am.arg_idx = ge.arg_idx; am.out = q.out_tokens;
     am.lengths = q.lengths; am.nrows = nrows; am.seq_len_out = q.seq_len_out;
     PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_argmax(am, st), "argmax");
@@ -477,46 +446,59 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
     PBD_INIT_HIP(launch_fill_u32(ws, y.ws_bytes / 4, 0u, st), "clear workspace");
     PBD_INIT_HIP(launch_fill_u32(kv, y.kv_bytes / 4, 0u, st), "clear kv");
 
-    auto pack = [&](size_t off, int tiles, int ft, int kb, int K, int map, int n_src, const int* rows,
-                    const void* const* w, const void* const* b) {
+    auto pack = [&](size_t off, int tiles, int kb, int K, int map, int n_src, const int* rows, const void* const* w) {
         PackArgs p{};
-        p.n_tiles = tiles; p.ft = ft; p.kb = kb; p.K = K; p.r = y.r; p.row_map = map; p.n_src = n_src;
-        for (int i = 0; i < n_src; ++i) { p.src_rows[i] = rows[i]; p.w[i] = w[i]; p.b[i] = b ? b[i] : nullptr; }
+        p.n_tiles = tiles; p.kb = kb; p.K = K; p.row_map = map; p.n_src = n_src; p.rows_total = tiles * 16;
+        for (int i = 0; i < n_src; ++i) { p.src_rows[i] = rows[i]; p.w[i] = w[i]; }
         p.dst = c->packed + off;
         return launch_pack(dt, p, st);
+    };
+    auto pack_b = [&](size_t off, int tiles, int map, int n_src, const int* rows, const void* const* b) {
+        PackExpandArgs p{};
+        p.n_tiles = tiles; p.rt = y.RT; p.r = y.r; p.row_map = map; p.n_src = n_src;
+        for (int i = 0; i < n_src; ++i) { p.src_rows[i] = rows[i]; p.b[i] = b[i]; }
+        p.dst = c->packed + off;
+        return launch_pack_expand(dt, p, st);
     };
     {
         const int rows[1] = {y.V};
         const void* w[1] = {canon->embed};
-        PBD_INIT_HIP(pack(y.p_embed, y.tiles_e, y.ft_e, y.kb_e, y.H, MAP_CONCAT, 1, rows, w, nullptr), "pack embed");
+        PBD_INIT_HIP(pack(y.p_embed, y.tiles_e, y.kb_e, y.H, MAP_CONCAT, 1, rows, w), "pack embed");
     }
     for (int l = 0; l < y.L; ++l) {
         const pbd_layer_weights& lw = canon->layers[l];
         const Layout::LayerOff& lo = y.lay[l];
-        const void* const* B = y.r > 0 ? lw.lora_b : nullptr;
         {
             const int rows[3] = {y.NQ * y.HD, y.NKV * y.HD, y.NKV * y.HD};
             const void* w[3] = {lw.q, lw.k, lw.v};
-            const void* b[3] = {B ? B[0] : nullptr, B ? B[1] : nullptr, B ? B[2] : nullptr};
-            PBD_INIT_HIP(pack(lo.qkv, y.tiles_qkv, y.ft_qkv, y.kb_qkv, y.H, MAP_CONCAT, 3, rows, w, b), "pack qkv");
+            PBD_INIT_HIP(pack(lo.qkv, y.tiles_qkv, y.kb_qkv, y.H, MAP_CONCAT, 3, rows, w), "pack qkv");
+            if (y.r > 0) PBD_INIT_HIP(pack_b(lo.lb_qkv, y.tiles_qkv, MAP_CONCAT, 3, rows, lw.lora_b), "pack qkv B");
         }
         {
             const int rows[1] = {y.H};
             const void* w[1] = {lw.o};
-            const void* b[1] = {B ? B[3] : nullptr};
-            PBD_INIT_HIP(pack(lo.o, y.tiles_o, y.ft_o, y.kb_o, y.NQ * y.HD, MAP_CONCAT, 1, rows, w, b), "pack o");
+            PBD_INIT_HIP(pack(lo.o, y.tiles_o, y.kb_o, y.NQ * y.HD, MAP_CONCAT, 1, rows, w), "pack o");
+            if (y.r > 0) PBD_INIT_HIP(pack_b(lo.lb_o, y.tiles_o, MAP_CONCAT, 1, rows, &lw.lora_b[3]), "pack o B");
         }
         {
             const int rows[2] = {y.F, y.F};
             const void* w[2] = {lw.gate, lw.up};
-            const void* b[2] = {B ? B[4] : nullptr, B ? B[5] : nullptr};
-            PBD_INIT_HIP(pack(lo.gu, y.tiles_gu, y.ft_gu, y.kb_gu, y.H, MAP_INTERLEAVE2, 2, rows, w, b), "pack gate/up");
+            PBD_INIT_HIP(pack(lo.gu, y.tiles_gu, y.kb_gu, y.H, MAP_INTERLEAVE2, 2, rows, w), "pack gate/up");
+            if (y.r > 0) PBD_INIT_HIP(pack_b(lo.lb_gu, y.tiles_gu, MAP_INTERLEAVE2, 2, rows, &lw.lora_b[4]), "pack gate/up B");
         }
         {
             const int rows[1] = {y.H};
             const void* w[1] = {lw.down};
-            const void* b[1] = {B ? B[6] : nullptr};
-            PBD_INIT_HIP(pack(lo.d, y.tiles_d, y.ft_d, y.kb_d, y.F, MAP_CONCAT, 1, rows, w, b), "pack down");
+            PBD_INIT_HIP(pack(lo.d, y.tiles_d, y.kb_d, y.F, MAP_CONCAT, 1, rows, w), "pack down");
+            if (y.r > 0) PBD_INIT_HIP(pack_b(lo.lb_d, y.tiles_d, MAP_CONCAT, 1, rows, &lw.lora_b[6]), "pack down B");
+        }
+        if (y.r > 0) {
+            const int in_f[7] = {y.H, y.H, y.H, y.NQ * y.HD, y.H, y.H, y.F};
+            for (int i = 0; i < 7; ++i) {
+                const int rows[1] = {y.r};
+                const void* w[1] = {lw.lora_a[i]};
+                PBD_INIT_HIP(pack(lo.la[i], y.RT, in_f[i] / y.FK, in_f[i], MAP_CONCAT, 1, rows, w), "pack lora A");
+            }
         }
         PBD_INIT_HIP(hipMemcpyAsync(c->packed + lo.attn_norm, lw.attn_norm, y.H * y.esz, hipMemcpyDeviceToDevice, st), "copy norm");
         PBD_INIT_HIP(hipMemcpyAsync(c->packed + lo.mlp_norm, lw.mlp_norm, y.H * y.esz, hipMemcpyDeviceToDevice, st), "copy norm");
@@ -524,10 +506,6 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
             PBD_INIT_HIP(hipMemcpyAsync(c->packed + lo.q_norm, lw.q_norm, y.HD * y.esz, hipMemcpyDeviceToDevice, st), "copy qnorm");
             PBD_INIT_HIP(hipMemcpyAsync(c->packed + lo.k_norm, lw.k_norm, y.HD * y.esz, hipMemcpyDeviceToDevice, st), "copy knorm");
         }
-        const int in_f[7] = {y.H, y.H, y.H, y.NQ * y.HD, y.H, y.H, y.F};
-        for (int i = 0; i < 7 && y.r > 0; ++i)
-            PBD_INIT_HIP(hipMemcpyAsync(c->packed + lo.a[i], lw.lora_a[i], (size_t)y.r * in_f[i] * y.esz,
-                                        hipMemcpyDeviceToDevice, st), "copy lora A");
     }
     PBD_INIT_HIP(hipMemcpyAsync(c->packed + y.p_final_norm, canon->final_norm, y.H * y.esz, hipMemcpyDeviceToDevice, st),
                  "copy final norm");

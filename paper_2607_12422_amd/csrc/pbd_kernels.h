@@ -10,17 +10,18 @@
 namespace pbd {
 
 enum PassMode { PASS_DRAFT = 0, PASS_VERIFY = 1, PASS_PREFILL = 2 };
-enum Epilogue { EPI_STORE = 0, EPI_PARTIAL = 1, EPI_SWIGLU = 2, EPI_ARGMAX = 3 };
-enum TailMode { TAIL_SINGLE = 0, TAIL_BY_TILE = 1, TAIL_BY_ROW_HALF = 2 };
+// GEMM epilogues: raw q/k/v; residual add + next RMSNorm operand; SwiGLU; LM head argmax
+enum Epilogue { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_ARGMAX = 3 };
+// which LoRA shrink matrix a GEMM tile uses
+enum LoraMode { LORA_SINGLE = 0, LORA_BY_TILE = 1, LORA_ROW_HALF = 2 };
 enum RowMap { MAP_CONCAT = 0, MAP_INTERLEAVE2 = 1 };
 
-constexpr int MAX_NORM_DIM = 8192;     // hidden size bound for k_norm
-constexpr int MAX_SHRINK_DIM = 8192;   // ffn and n_q*head_dim bound
+constexpr int MAX_RT = 4;              // LoRA rank <= 64: up to four 16-row shrink tiles
 
 struct AssembleArgs {
     int mode;
     int W, H, vocab, mask_id, max_seq;
-    int chunk_pos, max_len;
+    int chunk_pos, max_len, MT, m_stride;
     const int* seq_len;    // draft/verify: positions
     const int* anchor;
     const int* drafts;     // verify: [B][W-1]
@@ -31,50 +32,39 @@ struct AssembleArgs {
     int* nrows;            // [B]
     int* status;
     const void* embed;     // packed [V/16][H/FK] fragments
-    float* x;              // [M][H]
+    const void* gain;      // attention RMSNorm gain of layer 0
+    float* x;              // [M][H] residual
+    void* op_hi;           // first QKV operand x*g (fragments) and its bf16 residual
+    void* op_lo;
+    float* sq;             // [1][m_stride] per-row sum of squares
 };
 
-struct NormArgs {
-    int M, MT, H;
-    float eps;
-    float* x;
-    const float* partials;
-    int n_partials;
-    size_t partial_stride;  // floats between partial slabs
-    const void* gain;
-    void* xfrag;            // operand fragments, K = H
-    void* xfrag_lo;         // bf16 residual of the operand (split operands) or null
-    int n_src, r;
-    float scale;
-    const void* lora_a[3];  // [r][H]
-    void* tail[3];          // tail operand fragments per source
-};
-
-struct ShrinkArgs {
-    int M, MT, K, r;
-    float scale;
-    const void* xfrag;
-    const void* xfrag_lo;   // or null
-    const void* lora_a;     // [r][K]
-    void* tail;
-};
-
-struct GemmArgs {
-    const uint4* w;         // packed tiles: n_tiles x ft fragments
-    int n_tiles, ft, kb, ks;
-    int tail_frags, r, tail_mode, tile_split0, tile_split1;
-    const uint4* x;         // operand fragments [kb][MT]
-    const uint4* xlo;       // residual operand fragments (split operands) or null
-    const uint4* xt[3];     // tail operand fragments [tail][MT]
+struct FGemmArgs {
+    const uint4* w;         // weight tiles: [n_tiles][kb] fragments
+    int n_tiles, kb;
+    const uint4* xhi;       // operand fragments [kb][MT]
+    const uint4* xlo;       // operand residual fragments or null
     int M, MT;
-    // epilogue
-    float* out;             // STORE / PARTIAL
-    int ldo;                // row stride of out / logits
-    size_t partial_stride;
-    void* out_frag;         // SWIGLU: down-projection operand
-    void* out_frag_lo;      // SWIGLU: its residual fragments or null
-    int out_MT;
-    float* logits;          // ARGMAX: optional [M][V]
+    // RMSNorm folded in: r_m = rsqrt(sum_p sq[p*sq_stride + m] / norm_dim + eps); n_sq = 0: r_m = 1
+    const float* sq;
+    int n_sq, sq_stride, norm_dim;
+    float eps;
+    // LoRA: shrink u = s * r_m * A x in the tile, expand B u
+    int lora, rt, lora_mode, tile_split0, tile_split1;
+    float scale;
+    const uint4* la[3];     // shrink tiles per source: [rt][kb] fragments
+    const void* lb;         // expand blocks: [n_tiles][rt] x 64 lanes x 4 elements
+    // epilogues
+    float* out;             // STORE: [M][ldo]
+    int ldo;
+    float* x;               // RESID: residual [M][ldx]
+    int ldx;
+    const void* gnext;      // RESID: gain of the next RMSNorm
+    void* nx_hi;            // RESID: next operand fragments (K = ldx) / SWIGLU: h fragments
+    void* nx_lo;
+    int n_MT;
+    float* sq_out;          // RESID: [n_tiles][sq_stride] per-tile row sums of squares
+    float* logits;          // ARGMAX: optional [M][ldo]
     float* arg_val;         // ARGMAX: [n_tiles][M]
     int* arg_idx;
     int exclude;            // ARGMAX: token id excluded (-1: none)
@@ -89,7 +79,7 @@ struct AttnArgs {
     size_t smem_main;
     const int* pos0;
     const int* nrows;
-    const float* qkv;       // [M][nqkv] raw projections
+    const float* qkv;       // [M][nqkv] projections
     const void* q_norm;
     const void* k_norm;
     const float2* rope;     // [max_seq][head_dim/2] (cos, sin)
@@ -100,15 +90,12 @@ struct AttnArgs {
 };
 
 struct CombineArgs {
-    int M, MT, W, n_q, head_dim, kps, s_launch, r;
-    float scale;
+    int W, n_q, head_dim, kps, s_launch, MT;
     const int* pos0;
     const float* part_o;
     const float* part_ml;
-    void* xfrag;
-    void* xfrag_lo;
-    const void* lora_a;     // [r][n_q*head_dim] or null
-    void* tail;
+    void* op_hi;            // O-projection operand fragments (K = n_q*head_dim)
+    void* op_lo;
 };
 
 struct ArgmaxArgs {
@@ -133,23 +120,34 @@ struct AcceptArgs {
     int* status;
 };
 
+// Repack row-major matrices into fragment tiles (W and LoRA shrink A).  Rows
+// past `rows_total` are zero.
 struct PackArgs {
-    int n_tiles, ft, kb, K, r, row_map, n_src;
+    int n_tiles, kb, K, row_map, n_src, rows_total;
     int src_rows[3];
     const void* w[3];
+    void* dst;
+};
+
+// Repack LoRA B [rows][r] into expand blocks of the GEMM output tiles.
+struct PackExpandArgs {
+    int n_tiles, rt, r, row_map, n_src;
+    int src_rows[3];
     const void* b[3];
     void* dst;
 };
 
 hipError_t launch_assemble(int dtype, const AssembleArgs& a, int batch, hipStream_t st);
-hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t st);
-hipError_t launch_shrink(int dtype, const ShrinkArgs& a, hipStream_t st);
-hipError_t launch_gemm(int dtype, const GemmArgs& a, int epi, hipStream_t st);  // split iff a.xlo
+hipError_t launch_fgemm(int dtype, const FGemmArgs& a, int epi, hipStream_t st);   // split iff a.xlo
 hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int batch, hipStream_t st);
-hipError_t launch_combine(int dtype, const CombineArgs& a, hipStream_t st);
+hipError_t launch_combine(int dtype, const CombineArgs& a, int M, hipStream_t st);
 hipError_t launch_argmax(const ArgmaxArgs& a, hipStream_t st);
+// persistent LM head: `grid` work-groups, one (max, argmax) partial each per row
+bool lmhead_fits(int kb, int MT);
+hipError_t launch_lmhead(int dtype, const FGemmArgs& a, int grid, hipStream_t st);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t st);
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st);
+hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st);
 hipError_t launch_fill_u32(void* p, size_t n_words, uint32_t v, hipStream_t st);
 size_t attn_smem_main(int dtype, int head_dim, int qt);
 size_t attn_smem_bytes(int dtype, int head_dim, int qt);

@@ -1,19 +1,27 @@
 // HIP kernels of the PEFT-BD speculative step for gfx950.
 //
-// One pass (draft or verify, Sec. 3 steps 1-3) runs, per layer:
-//   k_norm      fold split-K partials into the fp32 residual, RMSNorm, write the
-//               GEMM operand; draft: LoRA shrink u = s * A x (App. A.2)
-//   k_gemm      weight-streaming skinny GEMM on MFMA, W x (+ B u when the
-//               adapter is on) with a fused epilogue
-//   k_attn      split-KV attention partials on MFMA over the committed prefix
-//               and the block (bidirectional or causal block mask); QK-norm and
-//               RoPE of the block rows; the verify appends the block K/V
-//   k_combine   merge the split partials, write the O-projection operand;
-//               draft: LoRA shrink of the attention output
-// then the final norm, the tied LM head with a fused argmax, and the
-// longest-prefix acceptance (Sec. 3 step 4, App. A.1).
+// One pass (draft or verify, Sec. 3 steps 1-3) runs six kernels per layer:
+//   k_fgemm<STORE>   q/k/v projection; RMSNorm folded in as a per-row scale of the
+//                    accumulator; LoRA shrink A x and expand B u inside the tile
+//                    (App. A.2) when the adapter is on
+//   k_attn           split-KV attention partials on MFMA over the committed prefix
+//                    and the block (bidirectional or causal block mask); QK-norm and
+//                    RoPE of the block rows; the verify appends the block K/V
+//   k_combine        merge the split partials into the O-projection operand
+//   k_fgemm<RESID>   O projection + LoRA + residual add; writes the next RMSNorm's
+//                    operand and per-row sums of squares
+//   k_fgemm<SWIGLU>  gate/up projection + LoRA, SwiGLU epilogue
+//   k_fgemm<RESID>   down projection + LoRA + residual add
+// then the tied LM head with a fused argmax, and the longest-prefix acceptance
+// (Sec. 3 step 4, App. A.1).
+//
+// RMSNorm by linearity: W (x / rms(x) * g) = r_m * W (x * g) with r_m = 1 / rms
+// of row m, so producers write x * g and sum(x^2) partials, and consumers scale
+// their accumulators by r_m; no standalone normalisation kernel runs.
 #include "pbd_device.h"
 #include "pbd_kernels.h"
+
+#include <algorithm>
 
 namespace pbd {
 
@@ -25,291 +33,325 @@ static __device__ __forceinline__ void attn_splits(int t, int kps, int s_launch,
     chunk = ceil_div(ceil_div(max(t, 1), s_eff), 16) * 16;
 }
 
+// Write v into an operand as bf16 value (hi) plus bf16 residual (lo), or as
+// plain T when lo is null.
+template <typename T>
+static __device__ __forceinline__ void put_operand(T* hi, T* lo, size_t e, float v) {
+    const T h = from_f32<T>(v);
+    hi[e] = h;
+    if (lo) lo[e] = from_f32<T>(v - to_f32(h));
+}
+
 // ---------------------------------------------------------------------------
-// Block assembly and embedding gather (Sec. 3 steps 1 and 3)
+// Block assembly and embedding gather (Sec. 3 steps 1 and 3); writes the
+// residual x, the first q/k/v operand x * g and per-row sums of squares.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void k_assemble(AssembleArgs a) {
-    const int b = blockIdx.x;
+    const int j = blockIdx.x, b = blockIdx.y;
     const int W = a.W;
-    __shared__ int s_tok[64];
-    __shared__ int s_pos, s_nrows;
-    if (threadIdx.x == 0) {
-        int pos0 = 0, nrows = W;
-        bool ok = true;
-        if (a.mode == PASS_PREFILL) {
-            int len = a.lengths[b];
-            if (len < 1 || len > a.max_len || len + W > a.max_seq) ok = false;
-            pos0 = a.chunk_pos;
-            nrows = ok ? min(max(len - a.chunk_pos, 0), W) : 0;
-        } else {
-            pos0 = a.seq_len[b];
-            if (pos0 < 0 || pos0 + W > a.max_seq) ok = false;
-            nrows = ok ? W : 0;
-        }
-        if (!ok) {
-            atomicOr(a.status, PBD_STATUS_CAPACITY);
-            pos0 = 0;
-        }
-        s_pos = pos0;
-        s_nrows = nrows;
-        a.pos0[b] = pos0;
-        a.nrows[b] = nrows;
+    // sequence state: every row's work-group derives the same values
+    int pos0, nrows;
+    bool ok = true;
+    if (a.mode == PASS_PREFILL) {
+        const int len = a.lengths[b];
+        if (len < 1 || len > a.max_len || len + W > a.max_seq) ok = false;
+        pos0 = a.chunk_pos;
+        nrows = ok ? min(max(len - a.chunk_pos, 0), W) : 0;
+    } else {
+        pos0 = a.seq_len[b];
+        if (pos0 < 0 || pos0 + W > a.max_seq) ok = false;
+        nrows = ok ? W : 0;
     }
-    __syncthreads();
-    if (threadIdx.x < W) {
-        const int j = threadIdx.x;
-        int tok;
-        if (a.mode == PASS_PREFILL) {
-            tok = (j < s_nrows) ? a.prompt[(size_t)b * a.max_len + a.chunk_pos + j] : 0;
-        } else if (j == 0) {
-            tok = a.anchor[b];
-        } else if (a.mode == PASS_DRAFT) {
-            tok = a.mask_id;
-        } else {
-            tok = a.drafts[b * (W - 1) + j - 1];
+    if (!ok) pos0 = 0;
+    int tok;
+    if (a.mode == PASS_PREFILL) tok = (j < nrows) ? a.prompt[(size_t)b * a.max_len + a.chunk_pos + j] : 0;
+    else if (j == 0) tok = a.anchor[b];
+    else if (a.mode == PASS_DRAFT) tok = a.mask_id;
+    else tok = a.drafts[b * (W - 1) + j - 1];
+    const bool bad_tok = tok < 0 || tok >= a.vocab;
+    if (bad_tok) tok = 0;
+    if (threadIdx.x == 0) {
+        if (j == 0) {
+            a.pos0[b] = pos0;
+            a.nrows[b] = nrows;
+            if (!ok) atomicOr(a.status, PBD_STATUS_CAPACITY);
         }
-        if (tok < 0 || tok >= a.vocab) {
-            if (j < s_nrows) atomicOr(a.status, PBD_STATUS_TOKEN);
-            tok = 0;
-        }
-        s_tok[j] = tok;
+        if (bad_tok && j < nrows) atomicOr(a.status, PBD_STATUS_TOKEN);
         a.tokens[b * W + j] = tok;
     }
-    __syncthreads();
-    // Gather embedding rows from the fragment-packed table into the fp32 residual.
+    // gather the embedding row from the fragment-packed table: one 16-byte
+    // chunk of EPL consecutive features per thread and step
+    constexpr int EPL = Elt<T>::EPL;
+    constexpr int FK = Elt<T>::FK;
     const T* E = (const T*)a.embed;
-    const int FK = Elt<T>::FK;
+    const T* g = (const T*)a.gain;
+    const int m = b * W + j;
     const int ft = a.H / FK;
-    for (int idx = threadIdx.x; idx < W * a.H; idx += blockDim.x) {
-        int j = idx / a.H, k = idx % a.H;
-        int v = s_tok[j];
-        size_t off = frag_elem<T>((size_t)(v / 16) * ft + k / FK, v % 16, k % FK);
-        a.x[(size_t)(b * W + j) * a.H + k] = to_f32(E[off]);
-    }
-}
-
-// ---------------------------------------------------------------------------
-// RMSNorm with residual fold and LoRA shrink
-// ---------------------------------------------------------------------------
-template <typename T>
-__global__ __launch_bounds__(256) void k_norm(NormArgs a) {
-    const int m = blockIdx.x;
-    const int H = a.H;
-    __shared__ float s_x[MAX_NORM_DIM];
-    __shared__ float s_red[8];
-    float* xr = a.x + (size_t)m * H;
+    const int nchunk = a.H / EPL;
     float ss = 0.f;
-    for (int k = threadIdx.x; k < H; k += blockDim.x) {
-        float v = xr[k];
-        for (int p = 0; p < a.n_partials; ++p)            // fixed order: deterministic
-            v += a.partials[(size_t)p * a.partial_stride + (size_t)m * H + k];
-        if (a.n_partials > 0) xr[k] = v;
-        s_x[k] = v;
-        ss += v * v;
+    for (int c = threadIdx.x; c < nchunk; c += blockDim.x) {
+        const int k0 = c * EPL;
+        const uint4 raw = *(const uint4*)(E + frag_elem<T>((size_t)(tok / 16) * ft + k0 / FK, tok % 16, k0 % FK));
+        const T* v = (const T*)&raw;
+        float xv[EPL];
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) xv[e] = to_f32(v[e]);
+        *(float4*)(a.x + (size_t)m * a.H + k0) = float4{xv[0], xv[1], xv[2], xv[3]};
+        if (EPL == 8) *(float4*)(a.x + (size_t)m * a.H + k0 + 4) = float4{xv[4 % EPL], xv[5 % EPL], xv[6 % EPL], xv[7 % EPL]};
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+            ss += xv[e] * xv[e];
+            put_operand<T>((T*)a.op_hi, (T*)a.op_lo, xfrag_elem<T>(m, k0 + e, a.MT), xv[e] * to_f32(g[k0 + e]));
+        }
     }
+    __shared__ float s_ss[8];
     ss = wave_sum(ss);
-    const int wid = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
-    if (lane == 0) s_red[wid] = ss;
+    if (threadIdx.x % WAVE == 0) s_ss[threadIdx.x / WAVE] = ss;
     __syncthreads();
     if (threadIdx.x == 0) {
         float t = 0.f;
-        for (int w = 0; w < (int)(blockDim.x / WAVE); ++w) t += s_red[w];
-        s_red[4] = rsqrtf(t / (float)H + a.eps);
-    }
-    __syncthreads();
-    const float inv = s_red[4];
-    const T* g = (const T*)a.gain;
-    T* xf = (T*)a.xfrag;
-    T* xl = (T*)a.xfrag_lo;
-    for (int k = threadIdx.x; k < H; k += blockDim.x) {
-        const float v = s_x[k] * inv * to_f32(g[k]);
-        const T q = from_f32<T>(v);
-        const size_t e = xfrag_elem<T>(m, k, a.MT);
-        xf[e] = q;
-        if (xl) xl[e] = from_f32<T>(v - to_f32(q));
-        s_x[k] = xl ? v : to_f32(q);                       // what the GEMM sees
-    }
-    if (a.n_src == 0) return;
-    __syncthreads();
-    // u_s[j] = scale * sum_k A_s[j][k] * xn[k], one wave per (source, j).
-    const int total = a.n_src * a.r;
-    for (int job = wid; job < total; job += blockDim.x / WAVE) {
-        int src = job / a.r, j = job % a.r;
-        const T* A = (const T*)a.lora_a[src] + (size_t)j * H;
-        float acc = 0.f;
-        for (int k = lane; k < H; k += WAVE) acc += to_f32(A[k]) * s_x[k];
-        acc = wave_sum(acc);
-        if (lane == 0) ((T*)a.tail[src])[xfrag_elem<T>(m, j, a.MT)] = from_f32<T>(acc * a.scale);
-    }
-}
-
-// LoRA shrink of an operand already in fragment layout (the down projection's
-// input h): u[m][j] = scale * sum_k A[j][k] h[m][k].
-template <typename T>
-__global__ __launch_bounds__(256) void k_shrink(ShrinkArgs a) {
-    const int m = blockIdx.x;
-    __shared__ float s_h[MAX_SHRINK_DIM];
-    const T* X = (const T*)a.xfrag;
-    const T* XL = (const T*)a.xfrag_lo;
-    for (int k = threadIdx.x; k < a.K; k += blockDim.x) {
-        const size_t e = xfrag_elem<T>(m, k, a.MT);
-        s_h[k] = to_f32(X[e]) + (XL ? to_f32(XL[e]) : 0.f);
-    }
-    __syncthreads();
-    const int wid = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
-    for (int j = wid; j < a.r; j += blockDim.x / WAVE) {
-        const T* A = (const T*)a.lora_a + (size_t)j * a.K;
-        float acc = 0.f;
-        for (int k = lane; k < a.K; k += WAVE) acc += to_f32(A[k]) * s_h[k];
-        acc = wave_sum(acc);
-        if (lane == 0) ((T*)a.tail)[xfrag_elem<T>(m, j, a.MT)] = from_f32<T>(acc * a.scale);
+        for (int w = 0; w < (int)(blockDim.x / WAVE); ++w) t += s_ss[w];
+        a.sq[m] = t;
     }
 }
 
 // ---------------------------------------------------------------------------
-// Skinny weight-streaming GEMM:  Y[m][n] = sum_k W[n][k] X[m][k]  (+ LoRA tail)
+// Fused skinny weight-streaming GEMM
 //
-// A work-group owns one 16-row tile of W (and one K split); its four waves take
-// the tile's fragments round-robin, so every fragment of W is read once, as one
-// contiguous 1 KiB wavefront load, and feeds MG m-tiles of MFMA.  The LoRA
-// expand B (A x) is the same contraction over r extra k columns: the packed tile
-// carries B's rows after W's, and the operand carries u = s A x after x.
-// Cross-wave partial sums meet in LDS; the epilogue runs on the reduced tile.
+//   Y[m][n] = r_m * sum_k W[n][k] X[m][k]  +  sum_j B[n][j] u[m][j],
+//   u[m][j] = s * r_m * sum_k A[j][k] X[m][k]          (LoRA, adapter on)
+//
+// A work-group owns one 16-row tile of W; its NW waves take the tile's
+// fragments round-robin, so every weight fragment is read once, as one
+// contiguous 1 KiB wavefront load, and feeds MG m-tiles of MFMA (twice when the
+// operand is carried as bf16 value + residual).  The LoRA shrink runs on the
+// same operand fragments with the A tiles; after the cross-wave reduction the
+// expand is a 16x16x16 MFMA whose B operand is the reduced u.  r_m is 1/rms of
+// row m from the producer's sum-of-squares partials (1 when n_sq = 0).
 // ---------------------------------------------------------------------------
+template <int EPI> struct FG {
+    // waves per work-group: enough that each wave issues all its fragment loads at once
+    static constexpr int NW = (EPI == EPI_ARGMAX || EPI == EPI_SWIGLU) ? 4 : 8;
+    static constexpr int NSRC = (EPI == EPI_SWIGLU) ? 2 : 1;      // LoRA shrink sources
+    static constexpr bool LORA = EPI != EPI_ARGMAX;
+    // shrink accumulators per source (register budget of 8-wave groups)
+    static constexpr int KU = (EPI == EPI_RESID) ? 4 : 8 / NSRC;
+    // fragments in flight per wave and batch
+    template <int MG> static constexpr int unroll() { return MG >= 4 ? 2 : (EPI == EPI_STORE ? 6 : 4); }
+};
+
 template <typename T, int EPI, int MG, bool SPLIT>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
-    constexpr int FK = Elt<T>::FK;
-    constexpr int EPL = Elt<T>::EPL;
-    // fragments in flight per wave (register budget: W, X and X residual)
-    constexpr int UNR = SPLIT ? ((MG >= 8) ? 1 : (MG >= 4 ? 2 : 4)) : ((MG >= 8) ? 2 : (MG >= 4 ? 4 : 8));
-    __shared__ f32x4 s_red[4][MG][WAVE];
+__global__ __launch_bounds__(FG<EPI>::NW * 64) void k_fgemm(FGemmArgs a) {
+    constexpr int NW = FG<EPI>::NW;
+    constexpr int NSRC = FG<EPI>::NSRC;
+    constexpr int KU = FG<EPI>::KU;
+    constexpr bool LORA_OK = FG<EPI>::LORA;
+    constexpr int UNR = FG<EPI>::template unroll<MG>();
+    typedef typename K4<T>::raw braw;
+    __shared__ f32x4 s_red[NW][MG][WAVE];
     __shared__ float s_tile[MG][16][17];
+    __shared__ float s_u[16][MG * 16 + 1];
+    __shared__ float s_rm[MG * 16];
 
     const int lane = threadIdx.x % WAVE;
     const int wid = threadIdx.x / WAVE;
-    const int tile = blockIdx.x / a.ks;
-    const int split = blockIdx.x % a.ks;
-    const int fps = a.kb / a.ks;
-    const int f_begin = split * fps;
-    const int n_tail = (split == a.ks - 1) ? a.tail_frags : 0;
-    const int nf = fps + n_tail;
     const int lrow = lane % 16, lgrp = lane / 16;
-
-    // Operand sources of the LoRA tail.
-    const uint4* xt0 = a.xt[0];
-    const uint4* xt1 = a.xt[1];
-    if (a.tail_mode == TAIL_BY_TILE) {
-        xt0 = tile < a.tile_split0 ? a.xt[0] : (tile < a.tile_split1 ? a.xt[1] : a.xt[2]);
-    }
-    const uint4* wt = a.w + (size_t)tile * a.ft * WAVE;
+    const int tile = blockIdx.x;
+    const int kb = a.kb;
+    const bool lora = LORA_OK && a.lora;
+    const int rt = lora ? a.rt : 0;
+    const uint4* wt = a.w + (size_t)tile * kb * WAVE;
+    const uint4* la0 = a.la[0];
+    const uint4* la1 = a.la[1];
+    if (a.lora_mode == LORA_BY_TILE)
+        la0 = tile < a.tile_split0 ? a.la[0] : (tile < a.tile_split1 ? a.la[1] : a.la[2]);
 
     for (int mg0 = 0; mg0 < a.MT; mg0 += MG) {
         const int mgn = min(MG, a.MT - mg0);
+        // row sums of squares for r_m: every thread loads a slice of the partials
+        // now and the sum is finished after the weight loop, off the critical path
+        constexpr int NROW = MG * 16;
+        constexpr int NSLICE = NW * 64 / NROW;
+        const int sq_row = threadIdx.x % NROW, sq_slice = threadIdx.x / NROW;
+        float sq_part = 0.f;
+        {
+            const int m = mg0 * 16 + sq_row;
+            if (a.n_sq > 0 && m < a.M) {
+#pragma unroll 8
+                for (int p = sq_slice; p < a.n_sq; p += NSLICE) sq_part += a.sq[(size_t)p * a.sq_stride + m];
+            }
+        }
         f32x4 acc[MG];
+        f32x4 uacc[NSRC][KU];
 #pragma unroll
         for (int i = 0; i < MG; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NSRC; ++s)
+#pragma unroll
+            for (int i = 0; i < KU; ++i) uacc[s][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-        for (int base = wid; base < nf; base += 4 * UNR) {
+        for (int base = wid; base < kb; base += NW * UNR) {
             uint4 wv[UNR];
-            uint4 xv[UNR][MG];
-            uint4 xv2[UNR][MG];     // tail: second source; base: operand residual (SPLIT)
+            uint4 xh[UNR][MG];
+            uint4 xl[UNR][MG];
 #pragma unroll
             for (int u = 0; u < UNR; ++u) {
-                const int i = base + 4 * u;
+                const int f = base + NW * u;
                 wv[u] = uint4{0, 0, 0, 0};
 #pragma unroll
-                for (int mt = 0; mt < MG; ++mt) { xv[u][mt] = uint4{0, 0, 0, 0}; xv2[u][mt] = uint4{0, 0, 0, 0}; }
-                if (i < nf) {
-                    const bool is_tail = i >= fps;
-                    const int f = is_tail ? (a.kb + i - fps) : (f_begin + i);
-                    const int tf = i - fps;
-                    const bool lane_live = !is_tail || (tf * FK + lgrp * EPL < a.r);
-                    if (lane_live) wv[u] = wt[(size_t)f * WAVE + lane];
+                for (int mt = 0; mt < MG; ++mt) { xh[u][mt] = uint4{0, 0, 0, 0}; xl[u][mt] = uint4{0, 0, 0, 0}; }
+                if (f < kb) {
+                    wv[u] = wt[(size_t)f * WAVE + lane];
 #pragma unroll
                     for (int mt = 0; mt < MG; ++mt) {
-                        const int m = (mg0 + mt) * 16 + lrow;
-                        if (mt < mgn && m < a.M) {
-                            if (!is_tail) {
-                                xv[u][mt] = a.x[((size_t)f * a.MT + mg0 + mt) * WAVE + lane];
-                                if (SPLIT) xv2[u][mt] = a.xlo[((size_t)f * a.MT + mg0 + mt) * WAVE + lane];
-                            } else {
-                                xv[u][mt] = xt0[((size_t)tf * a.MT + mg0 + mt) * WAVE + lane];
-                                if (a.tail_mode == TAIL_BY_ROW_HALF)
-                                    xv2[u][mt] = xt1[((size_t)tf * a.MT + mg0 + mt) * WAVE + lane];
+                        if (mt < mgn && (mg0 + mt) * 16 + lrow < a.M) {
+                            const size_t xi = ((size_t)f * a.MT + mg0 + mt) * WAVE + lane;
+                            xh[u][mt] = a.xhi[xi];
+                            if (SPLIT) xl[u][mt] = a.xlo[xi];
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) {
+                const int f = base + NW * u;
+                if (f >= kb) continue;
+#pragma unroll
+                for (int mt = 0; mt < MG; ++mt) {
+                    mma_frag<T>(acc[mt], wv[u], xh[u][mt]);
+                    if (SPLIT) mma_frag<T>(acc[mt], wv[u], xl[u][mt]);
+                }
+                if (LORA_OK && rt > 0) {
+#pragma unroll
+                    for (int s = 0; s < NSRC; ++s) {
+                        const uint4* la = s == 0 ? la0 : la1;
+#pragma unroll
+                        for (int t = 0; t < MAX_RT; ++t) {
+                            if (t >= rt) break;
+                            const uint4 av = la[((size_t)t * kb + f) * WAVE + lane];
+#pragma unroll
+                            for (int mt = 0; mt < MG; ++mt) {
+                                if (t * MG + mt < KU) {
+                                    mma_frag<T>(uacc[s][t * MG + mt], av, xh[u][mt]);
+                                    if (SPLIT) mma_frag<T>(uacc[s][t * MG + mt], av, xl[u][mt]);
+                                }
                             }
                         }
                     }
                 }
             }
-#pragma unroll
-            for (int u = 0; u < UNR; ++u) {
-                const int i = base + 4 * u;
-                if (i < nf) {
-                    if (a.tail_mode == TAIL_BY_ROW_HALF && i >= fps) {
-                        // rows 0-7 of the tile use source 0, rows 8-15 source 1
-                        const uint4 zero = uint4{0, 0, 0, 0};
-                        const uint4 w_lo = lrow < 8 ? wv[u] : zero;
-                        const uint4 w_hi = lrow < 8 ? zero : wv[u];
-#pragma unroll
-                        for (int mt = 0; mt < MG; ++mt) {
-                            mma_frag<T>(acc[mt], w_lo, xv[u][mt]);
-                            mma_frag<T>(acc[mt], w_hi, xv2[u][mt]);
-                        }
-                    } else {
-#pragma unroll
-                        for (int mt = 0; mt < MG; ++mt) {
-                            mma_frag<T>(acc[mt], wv[u], xv[u][mt]);
-                            if (SPLIT && i < fps) mma_frag<T>(acc[mt], wv[u], xv2[u][mt]);
-                        }
-                    }
-                }
-            }
         }
 
-        // Reduce the four waves' partial tiles (fixed order).
+        // finish r_m = rsqrt(mean(x^2) + eps) (fixed summation order)
+        ((float*)s_red)[threadIdx.x] = sq_part;
+        __syncthreads();
+        if (threadIdx.x < NROW) {
+            float s = 0.f;
+            for (int sl = 0; sl < NSLICE; ++sl) s += ((float*)s_red)[sl * NROW + threadIdx.x];
+            s_rm[threadIdx.x] = a.n_sq > 0 ? rsqrtf(s / (float)a.norm_dim + a.eps) : 1.f;
+        }
+        __syncthreads();
+        // cross-wave reduction of the base tile (fixed order), scaled by r_m
 #pragma unroll
         for (int mt = 0; mt < MG; ++mt) s_red[wid][mt][lane] = acc[mt];
         __syncthreads();
         for (int idx = threadIdx.x; idx < MG * WAVE * 4; idx += blockDim.x) {
-            const int mt = idx / (WAVE * 4);
-            const int ln = (idx / 4) % WAVE;
-            const int e = idx % 4;
-            float v = s_red[0][mt][ln][e] + s_red[1][mt][ln][e] + s_red[2][mt][ln][e] + s_red[3][mt][ln][e];
-            s_tile[mt][(ln / 16) * 4 + e][ln % 16] = v;    // [n in tile][m in tile]
+            const int mt = idx / (WAVE * 4), ln = (idx / 4) % WAVE, e = idx % 4;
+            float v = 0.f;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) v += s_red[w][mt][ln][e];
+            s_tile[mt][(ln / 16) * 4 + e][ln % 16] = v * s_rm[mt * 16 + ln % 16];
         }
         __syncthreads();
 
-        // Epilogues.
+        // LoRA expand: B (16 rows of the tile) times u = s * r_m * (A x)
+        if (lora) {
+            f32x4 eacc[MG];
+#pragma unroll
+            for (int i = 0; i < MG; ++i) eacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < NSRC; ++s) {
+#pragma unroll
+                for (int t = 0; t < MAX_RT; ++t) {
+                    if (t >= rt) break;
+#pragma unroll
+                    for (int mt = 0; mt < MG; ++mt)
+                        s_red[wid][mt][lane] = (t * MG + mt < KU) ? uacc[s][t * MG + mt] : f32x4{0.f, 0.f, 0.f, 0.f};
+                    __syncthreads();
+                    for (int idx = threadIdx.x; idx < MG * WAVE * 4; idx += blockDim.x) {
+                        const int mt = idx / (WAVE * 4), ln = (idx / 4) % WAVE, e = idx % 4;
+                        float v = 0.f;
+#pragma unroll
+                        for (int w = 0; w < NW; ++w) v += s_red[w][mt][ln][e];
+                        s_u[(ln / 16) * 4 + e][mt * 16 + ln % 16] = v * a.scale * s_rm[mt * 16 + ln % 16];
+                    }
+                    __syncthreads();
+                    if (wid == 0) {
+                        braw bv;
+                        const T* lbp = (const T*)a.lb + (((size_t)tile * a.rt + t) * WAVE + lane) * 4;
+                        __builtin_memcpy(&bv, lbp, sizeof(braw));
+                        if (EPI == EPI_SWIGLU) {
+                            // rows 0-7 of the tile belong to source 0 (gate), rows 8-15 to source 1 (up)
+                            if ((lrow < 8) != (s == 0)) bv = braw{};
+                        }
+#pragma unroll
+                        for (int mt = 0; mt < MG; ++mt) {
+                            f32x4 p;
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) p[e] = s_u[lgrp * 4 + e][mt * 16 + lrow];
+                            mma_k4(eacc[mt], bv, p);
+                        }
+                    }
+                    __syncthreads();
+                }
+            }
+            if (wid == 0) {
+#pragma unroll
+                for (int mt = 0; mt < MG; ++mt)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) s_tile[mt][lgrp * 4 + e][lrow] += eacc[mt][e];
+            }
+            __syncthreads();
+        }
+
+        // epilogues
         if (EPI == EPI_STORE) {
-            // out[m][n0 + n] (fp32, row stride ldo), for the QKV projection
             for (int idx = threadIdx.x; idx < mgn * 256; idx += blockDim.x) {
                 const int mt = idx / 256, n = idx % 16, ml = (idx / 16) % 16;
                 const int m = (mg0 + mt) * 16 + ml;
                 if (m < a.M) a.out[(size_t)m * a.ldo + tile * 16 + n] = s_tile[mt][n][ml];
             }
-        } else if (EPI == EPI_PARTIAL) {
-            // split-K partial sums, folded in order by the next k_norm
-            float* o = a.out + (size_t)split * a.partial_stride;
-            for (int idx = threadIdx.x; idx < mgn * 256; idx += blockDim.x) {
-                const int mt = idx / 256, n = idx % 16, ml = (idx / 16) % 16;
+        } else if (EPI == EPI_RESID) {
+            // x += tile; next operand x * g_next; per-row sum of squares over the 16 columns
+            const T* gn = (const T*)a.gnext;
+            if (threadIdx.x < mgn * 16) {
+                const int mt = threadIdx.x / 16, ml = threadIdx.x % 16;
                 const int m = (mg0 + mt) * 16 + ml;
-                if (m < a.M) o[(size_t)m * a.ldo + tile * 16 + n] = s_tile[mt][n][ml];
+                if (m < a.M) {
+                    float ss = 0.f;
+                    float* xr = a.x + (size_t)m * a.ldx + tile * 16;
+#pragma unroll
+                    for (int n = 0; n < 16; ++n) {
+                        const float xv = xr[n] + s_tile[mt][n][ml];
+                        xr[n] = xv;
+                        ss += xv * xv;
+                        put_operand<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 16 + n, a.n_MT),
+                                       xv * to_f32(gn[tile * 16 + n]));
+                    }
+                    a.sq_out[(size_t)tile * a.sq_stride + m] = ss;
+                }
             }
         } else if (EPI == EPI_SWIGLU) {
-            // tile rows 0-7: gate rows 8*tile..; rows 8-15: the matching up rows.
-            T* h = (T*)a.out_frag;
+            // tile rows 0-7: gate rows 8*tile..; rows 8-15: the matching up rows
             for (int idx = threadIdx.x; idx < mgn * 128; idx += blockDim.x) {
                 const int mt = idx / 128, c = idx % 8, ml = (idx / 8) % 16;
                 const int m = (mg0 + mt) * 16 + ml;
                 if (m < a.M) {
                     const float gt = s_tile[mt][c][ml];
                     const float up = s_tile[mt][c + 8][ml];
-                    const float hv = gt / (1.f + __expf(-gt)) * up;
-                    const T hq = from_f32<T>(hv);
-                    const size_t e = xfrag_elem<T>(m, tile * 8 + c, a.out_MT);
-                    h[e] = hq;
-                    if (SPLIT) ((T*)a.out_frag_lo)[e] = from_f32<T>(hv - to_f32(hq));
+                    put_operand<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 8 + c, a.n_MT),
+                                   gt / (1.f + __expf(-gt)) * up);
                 }
             }
         } else {  // EPI_ARGMAX: tied LM head, per-tile (max, argmax) per row
@@ -342,8 +384,49 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 // keys [k_lo, k_hi) and, in the last split, the W block keys.  S^T = K Q^T is
 // computed per 16-key block (A = K fragment from the cache, B = Q^T kept in
 // registers), softmax runs online per query column in the exp2 domain, and
-// O^T += V^T P^T takes P^T directly from the score accumulators.
+// O^T += V^T P^T takes P^T directly from the score accumulators.  The four
+// waves take key blocks round-robin and merge in LDS at the end.
 // ---------------------------------------------------------------------------
+
+// Per-head RMSNorm and rotate-half RoPE of one row held by 16 lanes: lane l16
+// owns the NP pairs (i, i + HD/2) for i in [NP*l16, NP*l16 + NP), so the
+// rotation stays in the lane and the norm is a 16-lane DPP reduction.
+template <typename T, int HD>
+struct RowPrep {
+    static constexpr int HALF = HD / 2;
+    static constexpr int NP = HALF / 16;       // pairs per lane (4 or 2)
+    float lo[NP], hi[NP];
+    float2 cs[NP];
+    __device__ void load(const float* src, const float2* rope_row, int l16, bool live) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            lo[p] = live ? src[NP * l16 + p] : 0.f;
+            hi[p] = live ? src[HALF + NP * l16 + p] : 0.f;
+            cs[p] = live ? rope_row[NP * l16 + p] : float2{1.f, 0.f};
+        }
+    }
+    // normalise (if gain) and rotate; writes the row into dst[HD] as T
+    __device__ void finish(T* dst, const T* gain, bool qk_norm, float eps, int l16, T* out_lo, T* out_hi) {
+        float inv = 1.f;
+        if (qk_norm) {
+            float ss = 0.f;
+#pragma unroll
+            for (int p = 0; p < NP; ++p) ss += lo[p] * lo[p] + hi[p] * hi[p];
+            inv = rsqrtf(row16_sum(ss) / (float)HD + eps);
+        }
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            const int i = NP * l16 + p;
+            float y0 = lo[p] * inv, y1 = hi[p] * inv;
+            if (qk_norm) { y0 *= to_f32(gain[i]); y1 *= to_f32(gain[i + HALF]); }
+            out_lo[p] = from_f32<T>(y0 * cs[p].x - y1 * cs[p].y);
+            out_hi[p] = from_f32<T>(y1 * cs[p].x + y0 * cs[p].y);
+            dst[i] = out_lo[p];
+            dst[i + HALF] = out_hi[p];
+        }
+    }
+};
+
 template <typename T, int HD, int QT>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     constexpr int FK = Elt<T>::FK;
@@ -353,7 +436,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     constexpr int QROWS = QT * 16;
     constexpr int LDQ = HD + 16 / (int)sizeof(T);   // padded LDS row (bank spread)
     constexpr int KBMAX = 48;                       // block keys: W <= 33 -> 3 blocks
+    constexpr int LDO = HD + 1;                     // padded merge rows
     typedef typename K4<T>::raw vraw;
+    typedef RowPrep<T, HD> RP;
 
     const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int t = a.pos0[b];
@@ -371,40 +456,33 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     T* q_l = (T*)smem;                                   // [QROWS][LDQ]
     T* kb_l = q_l + QROWS * LDQ;                         // [KBMAX][LDQ]
     T* vb_l = kb_l + KBMAX * LDQ;                        // [KBMAX][HD]
-    float* obuf = (float*)smem;                          // [QROWS][HD] (aliases after the loop)
+    float* obuf = (float*)smem;                          // [QROWS][LDO], aliases after the key loop
     float* ml_l = (float*)(smem + a.smem_main);          // [4][QROWS][2]
 
     const int lane = threadIdx.x % WAVE, wid = threadIdx.x / WAVE;
     const int lrow = lane % 16, lgrp = lane / 16;
     const size_t row_stride = (size_t)a.nqkv;
     const float* qkv_b = a.qkv + (size_t)b * W * row_stride;
-
-    // -- Q: per-head RMSNorm, RoPE at position t + j, rounded to T (one wave per row)
-    const T* gq = (const T*)a.q_norm;
-    const T* gk = (const T*)a.k_norm;
     const float2* rope = a.rope;
-    for (int q = wid; q < QROWS; q += 4) {
-        T* dst = q_l + q * LDQ;
-        if (q >= QR) {
-            for (int i = lane; i < HD; i += WAVE) dst[i] = from_f32<T>(0.f);
-            continue;
+    constexpr int HALF = HD / 2;
+
+    // -- Q rows: wave w, lane group lgrp handles rows 16*i + 4*w + lgrp
+    {
+        constexpr int QSTEPS = QROWS / 16;
+        RP rp[QSTEPS];
+#pragma unroll
+        for (int i = 0; i < QSTEPS; ++i) {
+            const int q = 16 * i + 4 * wid + lgrp;
+            const bool live = q < QR;
+            const int qq = live ? q : 0;
+            rp[i].load(qkv_b + (size_t)(qq % W) * row_stride + (size_t)(g * G + qq / W) * HD,
+                       rope + (size_t)(t + qq % W) * HALF, lrow, live);
         }
-        const int gi = q / W, j = q % W;
-        const float* src = qkv_b + (size_t)j * row_stride + (size_t)(g * G + gi) * HD;
-        const int half = HD / 2;
-        float x0 = lane < half ? src[lane] : 0.f;
-        float x1 = lane < half ? src[lane + half] : 0.f;
-        float inv = 1.f;
-        if (a.qk_norm) {
-            float ss = wave_sum(x0 * x0 + x1 * x1);
-            inv = rsqrtf(ss / (float)HD + a.eps);
-        }
-        if (lane < half) {
-            float y0 = x0 * inv, y1 = x1 * inv;
-            if (a.qk_norm) { y0 *= to_f32(gq[lane]); y1 *= to_f32(gq[lane + half]); }
-            const float2 cs = rope[(size_t)(t + j) * half + lane];
-            dst[lane] = from_f32<T>(y0 * cs.x - y1 * cs.y);
-            dst[lane + half] = from_f32<T>(y1 * cs.x + y0 * cs.y);
+#pragma unroll
+        for (int i = 0; i < QSTEPS; ++i) {
+            const int q = 16 * i + 4 * wid + lgrp;
+            T lo[RP::NP], hi[RP::NP];
+            rp[i].finish(q_l + q * LDQ, (const T*)a.q_norm, a.qk_norm, a.eps, lrow, lo, hi);
         }
     }
     // -- block keys and values (last split only); the verify appends them to the cache
@@ -412,42 +490,48 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     T* kc = (T*)a.kcache + (((size_t)a.layer * a.max_batch + b) * a.n_kv + g) * a.nblk * 16 * HD;
     T* vc = (T*)a.vcache + (((size_t)a.layer * a.max_batch + b) * a.n_kv + g) * a.nblk * 16 * HD;
     if (last) {
-        for (int j = wid; j < nkb_blk * 16; j += 4) {
-            T* kd = kb_l + j * LDQ;
-            T* vd = vb_l + j * HD;
-            if (j >= W || j >= nrows) {
-                for (int i = lane; i < HD; i += WAVE) { kd[i] = from_f32<T>(0.f); vd[i] = from_f32<T>(0.f); }
-                continue;
-            }
-            const float* ks = qkv_b + (size_t)j * row_stride + (size_t)a.n_q * HD + (size_t)g * HD;
+        constexpr int KSTEPS = KBMAX / 16;
+        RP rk[KSTEPS];
+        float vlo[KSTEPS][RP::NP], vhi[KSTEPS][RP::NP];
+#pragma unroll
+        for (int i = 0; i < KSTEPS; ++i) {
+            const int j = 16 * i + 4 * wid + lgrp;
+            const bool live = j < nkb_blk * 16 && j < W && j < nrows;
+            const int jj = live ? j : 0;
+            const float* ks = qkv_b + (size_t)jj * row_stride + (size_t)a.n_q * HD + (size_t)g * HD;
             const float* vs = ks + (size_t)a.n_kv * HD;
-            const int half = HD / 2;
-            float x0 = lane < half ? ks[lane] : 0.f;
-            float x1 = lane < half ? ks[lane + half] : 0.f;
-            float inv = 1.f;
-            if (a.qk_norm) {
-                float ss = wave_sum(x0 * x0 + x1 * x1);
-                inv = rsqrtf(ss / (float)HD + a.eps);
+            rk[i].load(ks, rope + (size_t)(t + jj) * HALF, lrow, live);
+#pragma unroll
+            for (int p = 0; p < RP::NP; ++p) {
+                vlo[i][p] = live ? vs[RP::NP * lrow + p] : 0.f;
+                vhi[i][p] = live ? vs[HALF + RP::NP * lrow + p] : 0.f;
             }
-            const int pos = t + j;
-            if (lane < half) {
-                float y0 = x0 * inv, y1 = x1 * inv;
-                if (a.qk_norm) { y0 *= to_f32(gk[lane]); y1 *= to_f32(gk[lane + half]); }
-                const float2 cs = rope[(size_t)pos * half + lane];
-                const T k0 = from_f32<T>(y0 * cs.x - y1 * cs.y);
-                const T k1 = from_f32<T>(y1 * cs.x + y0 * cs.y);
-                kd[lane] = k0;
-                kd[lane + half] = k1;
-                if (a.write_kv) {
-                    T* blk = kc + (size_t)(pos / 16) * 16 * HD;
-                    blk[kblock_elem<T>(pos % 16, lane)] = k0;
-                    blk[kblock_elem<T>(pos % 16, lane + half)] = k1;
+        }
+#pragma unroll
+        for (int i = 0; i < KSTEPS; ++i) {
+            const int j = 16 * i + 4 * wid + lgrp;
+            if (j >= nkb_blk * 16) continue;
+            const bool live = j < W && j < nrows;
+            T klo[RP::NP], khi[RP::NP];
+            rk[i].finish(kb_l + j * LDQ, (const T*)a.k_norm, a.qk_norm, a.eps, lrow, klo, khi);
+            T* vd = vb_l + j * HD;
+#pragma unroll
+            for (int p = 0; p < RP::NP; ++p) {
+                vd[RP::NP * lrow + p] = from_f32<T>(vlo[i][p]);
+                vd[HALF + RP::NP * lrow + p] = from_f32<T>(vhi[i][p]);
+            }
+            if (live && a.write_kv) {
+                const int pos = t + j;
+                T* kblk = kc + (size_t)(pos / 16) * 16 * HD;
+                T* vblk = vc + (size_t)(pos / 16) * 16 * HD;
+#pragma unroll
+                for (int p = 0; p < RP::NP; ++p) {
+                    const int i0 = RP::NP * lrow + p;
+                    kblk[kblock_elem<T>(pos % 16, i0)] = klo[p];
+                    kblk[kblock_elem<T>(pos % 16, i0 + HALF)] = khi[p];
+                    vblk[vblock_elem(pos % 16, i0)] = from_f32<T>(vlo[i][p]);
+                    vblk[vblock_elem(pos % 16, i0 + HALF)] = from_f32<T>(vhi[i][p]);
                 }
-            }
-            for (int i = lane; i < HD; i += WAVE) {
-                const T v = from_f32<T>(vs[i]);
-                vd[i] = v;
-                if (a.write_kv) vc[(size_t)(pos / 16) * 16 * HD + vblock_elem(pos % 16, i)] = v;
             }
         }
     }
@@ -481,23 +565,16 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     const int n_items = n_pref + nkb_blk;
     const float sl2 = a.scale_log2;
 
-    for (int it = wid; it < n_items; it += 4) {
-        const bool pref = it < n_pref;
-        uint4 kf[NDS];
-        vraw vf[NDT];
-        int key0;
-        if (pref) {
-            const int kb = kb_first + it;
-            key0 = kb * 16;
-            const T* kblk = kc + (size_t)kb * 16 * HD;
-            const T* vblk = vc + (size_t)kb * 16 * HD;
+    auto load_item = [&](int it, uint4* kf, vraw* vf) {
+        if (it < n_pref) {
+            const T* kblk = kc + (size_t)(kb_first + it) * 16 * HD;
+            const T* vblk = vc + (size_t)(kb_first + it) * 16 * HD;
 #pragma unroll
             for (int ds = 0; ds < NDS; ++ds) kf[ds] = *(const uint4*)(kblk + (size_t)(ds * WAVE + lane) * EPL);
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) vf[dt] = *(const vraw*)(vblk + (size_t)(dt * WAVE + lane) * 4);
         } else {
             const int bb = it - n_pref;
-            key0 = bb * 16;
 #pragma unroll
             for (int ds = 0; ds < NDS; ++ds)
                 kf[ds] = *(const uint4*)(kb_l + (bb * 16 + lrow) * LDQ + ds * FK + lgrp * EPL);
@@ -509,6 +586,15 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 __builtin_memcpy(&vf[dt], tmp, sizeof(vraw));
             }
         }
+    };
+
+    uint4 kf[NDS], kn[NDS];
+    vraw vf[NDT], vn[NDT];
+    if (wid < n_items) load_item(wid, kf, vf);
+    for (int it = wid; it < n_items; it += 4) {
+        if (it + 4 < n_items) load_item(it + 4, kn, vn);           // next block in flight
+        const bool pref = it < n_pref;
+        const int key0 = pref ? (kb_first + it) * 16 : (it - n_pref) * 16;
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
             f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -521,15 +607,12 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int kk = key0 + lgrp * 4 + e;
-                bool ok;
-                if (pref) ok = kk < k_hi;
-                else ok = kk < nrows && (!a.causal || kk <= jq[qt]);
+                const bool ok = pref ? kk < k_hi : (kk < nrows && (!a.causal || kk <= jq[qt]));
                 valid[e] = ok;
                 sv[e] = sc[e] * sl2;
                 if (ok) mloc = fmaxf(mloc, sv[e]);
             }
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+            mloc = xrow_max(mloc);
             const float m_new = fmaxf(m_run[qt], mloc);
             const float corr = exp2f(m_run[qt] - m_new);
             f32x4 p;
@@ -539,8 +622,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 p[e] = valid[e] ? exp2f(sv[e] - m_new) : 0.f;
                 psum += p[e];
             }
-            psum += __shfl_xor(psum, 16, 64);
-            psum += __shfl_xor(psum, 32, 64);
+            psum = xrow_sum(psum);
             l_run[qt] = l_run[qt] * corr + psum;
             m_run[qt] = m_new;
 #pragma unroll
@@ -548,6 +630,12 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 o_acc[dt][qt] *= corr;
                 mma_k4(o_acc[dt][qt], vf[dt], p);
             }
+        }
+        if (it + 4 < n_items) {
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds) kf[ds] = kn[ds];
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) vf[dt] = vn[dt];
         }
     }
 
@@ -577,11 +665,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const int d = dt * 16 + lgrp * 4 + e;
-                        const int q = qt * 16 + lrow;
+                        float* o = obuf + (qt * 16 + lrow) * LDO + dt * 16 + lgrp * 4 + e;
                         const float v = o_acc[dt][qt][e] * fct[qt];
-                        if (w == 0) obuf[q * HD + d] = v;
-                        else obuf[q * HD + d] += v;
+                        *o = (w == 0) ? v : *o + v;
                     }
         }
         __syncthreads();
@@ -592,7 +678,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         const int q = idx / HD, d = idx % HD;
         const int gi = q / W, j = q % W;
         const size_t pr = (((size_t)b * a.n_q + g * G + gi) * W + j) * S + s;
-        a.part_o[pr * HD + d] = obuf[q * HD + d];
+        a.part_o[pr * HD + d] = obuf[q * LDO + d];
     }
     for (int q = threadIdx.x; q < QR; q += blockDim.x) {
         float mx = -1e30f;
@@ -606,47 +692,131 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     }
 }
 
-// Merge the split-KV partials of one block row for every query head, write the
-// O-projection operand, and (draft) its LoRA shrink.
+// ---------------------------------------------------------------------------
+// Tied LM head with the final RMSNorm folded in and a fused argmax.
+//
+// Each work-group keeps its waves' slices of the operand (all block rows) in
+// registers and walks vocabulary tiles with a grid stride; the next tile's
+// weight fragments are in flight while the current tile is reduced, so the
+// 16-row tiles of the embedding matrix stream back to back.  Each work-group
+// leaves one (max, argmax) per row; ties go to the lowest token id.
+// ---------------------------------------------------------------------------
+constexpr int LM_FPW = 8;      // weight fragments per wave and tile (hidden <= 4 * 8 * FK)
+
+template <typename T, bool SPLIT>
+__global__ __launch_bounds__(256, 2) void k_lmhead(FGemmArgs a) {
+    constexpr int NW = 4, MGH = 2;
+    __shared__ f32x4 s_red[NW][MGH][WAVE];
+    __shared__ float s_tile[MGH][16][17];
+    __shared__ float s_rm[MGH * 16];
+    __shared__ float s_sq[256];
+    const int lane = threadIdx.x % WAVE, wid = threadIdx.x / WAVE;
+    const int lrow = lane % 16;
+    const int kb = a.kb;
+    // r_m of every row from the sum-of-squares partials
+    {
+        const int row = threadIdx.x % 32, slice = threadIdx.x / 32;
+        float sp = 0.f;
+        if (row < a.M)
+            for (int p = slice; p < a.n_sq; p += 8) sp += a.sq[(size_t)p * a.sq_stride + row];
+        s_sq[threadIdx.x] = sp;
+    }
+    // operand slices in registers
+    uint4 xh[LM_FPW][MGH], xl[LM_FPW][MGH];
+#pragma unroll
+    for (int i = 0; i < LM_FPW; ++i) {
+        const int f = wid + NW * i;
+#pragma unroll
+        for (int mt = 0; mt < MGH; ++mt) {
+            xh[i][mt] = uint4{0, 0, 0, 0};
+            xl[i][mt] = uint4{0, 0, 0, 0};
+            if (f < kb && mt < a.MT && mt * 16 + lrow < a.M) {
+                const size_t xi = ((size_t)f * a.MT + mt) * WAVE + lane;
+                xh[i][mt] = a.xhi[xi];
+                if (SPLIT) xl[i][mt] = a.xlo[xi];
+            }
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < 32) {
+        float t = 0.f;
+        for (int sl = 0; sl < 8; ++sl) t += s_sq[sl * 32 + threadIdx.x];
+        s_rm[threadIdx.x] = a.n_sq > 0 ? rsqrtf(t / (float)a.norm_dim + a.eps) : 1.f;
+    }
+    float best = -INFINITY;
+    int bi = 0x7fffffff;
+    uint4 wv[LM_FPW], wn[LM_FPW];
+    auto load_tile = [&](int tile, uint4* dst) {
+        const uint4* wt = a.w + (size_t)tile * kb * WAVE;
+#pragma unroll
+        for (int i = 0; i < LM_FPW; ++i) {
+            const int f = wid + NW * i;
+            dst[i] = (f < kb) ? wt[(size_t)f * WAVE + lane] : uint4{0, 0, 0, 0};
+        }
+    };
+    int tile = blockIdx.x;
+    if (tile < a.n_tiles) load_tile(tile, wv);
+    for (; tile < a.n_tiles; tile += gridDim.x) {
+        const int next = tile + gridDim.x;
+        if (next < a.n_tiles) load_tile(next, wn);
+        f32x4 acc[MGH];
+#pragma unroll
+        for (int mt = 0; mt < MGH; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < LM_FPW; ++i)
+#pragma unroll
+            for (int mt = 0; mt < MGH; ++mt) {
+                mma_frag<T>(acc[mt], wv[i], xh[i][mt]);
+                if (SPLIT) mma_frag<T>(acc[mt], wv[i], xl[i][mt]);
+            }
+#pragma unroll
+        for (int mt = 0; mt < MGH; ++mt) s_red[wid][mt][lane] = acc[mt];
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < MGH * WAVE * 4; idx += blockDim.x) {
+            const int mt = idx / (WAVE * 4), ln = (idx / 4) % WAVE, e = idx % 4;
+            const float v = s_red[0][mt][ln][e] + s_red[1][mt][ln][e] + s_red[2][mt][ln][e] + s_red[3][mt][ln][e];
+            s_tile[mt][(ln / 16) * 4 + e][ln % 16] = v * s_rm[mt * 16 + ln % 16];
+        }
+        __syncthreads();
+        if (threadIdx.x < MGH * 16) {
+            const int m = threadIdx.x, mt = m / 16, ml = m % 16;
+            if (m < a.M) {
+                for (int n = 0; n < 16; ++n) {
+                    const int v = tile * 16 + n;
+                    const float val = s_tile[mt][n][ml];
+                    if (a.logits) a.logits[(size_t)m * a.ldo + v] = val;
+                    if (v == a.exclude) continue;
+                    if (val > best) { best = val; bi = v; }   // tiles ascend within a work-group
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < LM_FPW; ++i) wv[i] = wn[i];
+    }
+    if (threadIdx.x < a.M && threadIdx.x < MGH * 16) {
+        a.arg_val[(size_t)blockIdx.x * a.M + threadIdx.x] = best;
+        a.arg_idx[(size_t)blockIdx.x * a.M + threadIdx.x] = bi;
+    }
+}
+
+// Merge the split-KV partials of one (block row, query head) and write the
+// O-projection operand.
 template <typename T>
-__global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
-    const int m = blockIdx.x;
+__global__ void k_combine(CombineArgs a) {
+    const int m = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
     const int b = m / a.W, j = m % a.W;
-    const int HD = a.head_dim, NQ = a.n_q;
-    const int K = NQ * HD;
-    __shared__ float s_o[MAX_SHRINK_DIM];
     int s_eff, chunk;
     attn_splits(a.pos0[b], a.kps, a.s_launch, s_eff, chunk);
-    const int S = a.s_launch;
-    T* xf = (T*)a.xfrag;
-    for (int idx = threadIdx.x; idx < K; idx += blockDim.x) {
-        const int h = idx / HD, d = idx % HD;
-        const size_t pr0 = (((size_t)b * NQ + h) * a.W + j) * S;
-        float mx = -1e30f;
-        for (int s = 0; s < s_eff; ++s) mx = fmaxf(mx, a.part_ml[(pr0 + s) * 2]);
-        float L = 0.f, o = 0.f;
-        for (int s = 0; s < s_eff; ++s) {
-            const float wgt = exp2f(a.part_ml[(pr0 + s) * 2] - mx);
-            L += wgt * a.part_ml[(pr0 + s) * 2 + 1];
-            o += wgt * a.part_o[(pr0 + s) * HD + d];
-        }
-        const float val = (L > 0.f) ? o / L : 0.f;
-        const T q = from_f32<T>(val);
-        const size_t e = xfrag_elem<T>(m, idx, a.MT);
-        xf[e] = q;
-        if (a.xfrag_lo) ((T*)a.xfrag_lo)[e] = from_f32<T>(val - to_f32(q));
-        s_o[idx] = a.xfrag_lo ? val : to_f32(q);
+    const size_t pr0 = (((size_t)b * a.n_q + h) * a.W + j) * a.s_launch;
+    float mx = -1e30f;
+    for (int s = 0; s < s_eff; ++s) mx = fmaxf(mx, a.part_ml[(pr0 + s) * 2]);
+    float L = 0.f, o = 0.f;
+    for (int s = 0; s < s_eff; ++s) {
+        const float wgt = exp2f(a.part_ml[(pr0 + s) * 2] - mx);
+        L += wgt * a.part_ml[(pr0 + s) * 2 + 1];
+        o += wgt * a.part_o[(pr0 + s) * a.head_dim + d];
     }
-    if (a.r == 0 || a.lora_a == nullptr) return;
-    __syncthreads();
-    const int wid = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
-    for (int jj = wid; jj < a.r; jj += blockDim.x / WAVE) {
-        const T* A = (const T*)a.lora_a + (size_t)jj * K;
-        float acc = 0.f;
-        for (int k = lane; k < K; k += WAVE) acc += to_f32(A[k]) * s_o[k];
-        acc = wave_sum(acc);
-        if (lane == 0) ((T*)a.tail)[xfrag_elem<T>(m, jj, a.MT)] = from_f32<T>(acc * a.scale);
-    }
+    put_operand<T>((T*)a.op_hi, (T*)a.op_lo, xfrag_elem<T>(m, h * a.head_dim + d, a.MT), L > 0.f ? o / L : 0.f);
 }
 
 // ---------------------------------------------------------------------------
@@ -718,42 +888,58 @@ __global__ void k_accept(AcceptArgs a) {
 // ---------------------------------------------------------------------------
 // Initialisation helpers
 // ---------------------------------------------------------------------------
-// Repack [rows][K] weights (+ LoRA B [rows][r]) into 16-row fragment tiles.
+// Row of source matrix for row `row` of packed tile `tile`.
+static __device__ __forceinline__ void map_row(int row_map, int n_src, const int* src_rows, int tile, int row,
+                                               int& src, int& srow) {
+    if (row_map == MAP_INTERLEAVE2) {
+        src = row < 8 ? 0 : 1;
+        srow = tile * 8 + (row % 8);
+    } else {
+        const int r = tile * 16 + row;
+        src = 0;
+        srow = r;
+        if (n_src > 1 && r >= src_rows[0]) { src = 1; srow = r - src_rows[0]; }
+        if (n_src > 2 && r >= src_rows[0] + src_rows[1]) { src = 2; srow = r - src_rows[0] - src_rows[1]; }
+    }
+}
+
+// Repack [rows][K] matrices into 16-row fragment tiles.
 template <typename T>
 __global__ void k_pack(PackArgs a) {
     constexpr int EPL = Elt<T>::EPL;
     constexpr int FK = Elt<T>::FK;
-    const size_t total = (size_t)a.n_tiles * a.ft * WAVE;
+    const size_t total = (size_t)a.n_tiles * a.kb * WAVE;
     for (size_t id = blockIdx.x * (size_t)blockDim.x + threadIdx.x; id < total; id += (size_t)gridDim.x * blockDim.x) {
         const int lane = id % WAVE;
-        const int f = (id / WAVE) % a.ft;
-        const int tile = id / ((size_t)WAVE * a.ft);
+        const int f = (id / WAVE) % a.kb;
+        const int tile = id / ((size_t)WAVE * a.kb);
         const int row = lane % 16, grp = lane / 16;
         int src, srow;
-        if (a.row_map == MAP_INTERLEAVE2) {
-            src = row < 8 ? 0 : 1;
-            srow = tile * 8 + (row % 8);
-        } else {
-            const int r = tile * 16 + row;
-            src = 0;
-            srow = r;
-            if (a.n_src > 1 && r >= a.src_rows[0]) { src = 1; srow = r - a.src_rows[0]; }
-            if (a.n_src > 2 && r >= a.src_rows[0] + a.src_rows[1]) { src = 2; srow = r - a.src_rows[0] - a.src_rows[1]; }
-        }
-        T vals[EPL];
-        if (f < a.kb) {
-            const T* Wsrc = (const T*)a.w[src] + (size_t)srow * a.K + f * FK + grp * EPL;
-#pragma unroll
-            for (int e = 0; e < EPL; ++e) vals[e] = Wsrc[e];
-        } else {
-            const int kt = (f - a.kb) * FK + grp * EPL;
-#pragma unroll
-            for (int e = 0; e < EPL; ++e)
-                vals[e] = (a.b[src] && kt + e < a.r) ? ((const T*)a.b[src])[(size_t)srow * a.r + kt + e] : from_f32<T>(0.f);
-        }
+        map_row(a.row_map, a.n_src, a.src_rows, tile, row, src, srow);
         T* dst = (T*)a.dst + id * EPL;
+        const bool live = tile * 16 + row < a.rows_total && srow < a.src_rows[src];
+        const T* Wsrc = (const T*)a.w[src] + (size_t)srow * a.K + f * FK + grp * EPL;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) dst[e] = vals[e];
+        for (int e = 0; e < EPL; ++e) dst[e] = live ? Wsrc[e] : from_f32<T>(0.f);
+    }
+}
+
+// Repack LoRA B [rows][r] into expand blocks: block (tile, t), lane (row n, group g)
+// holds B[row(n)][16 t + 4 g .. +4].
+template <typename T>
+__global__ void k_pack_expand(PackExpandArgs a) {
+    const size_t total = (size_t)a.n_tiles * a.rt * WAVE;
+    for (size_t id = blockIdx.x * (size_t)blockDim.x + threadIdx.x; id < total; id += (size_t)gridDim.x * blockDim.x) {
+        const int lane = id % WAVE;
+        const int t = (id / WAVE) % a.rt;
+        const int tile = id / ((size_t)WAVE * a.rt);
+        int src, srow;
+        map_row(a.row_map, a.n_src, a.src_rows, tile, lane % 16, src, srow);
+        const int k0 = 16 * t + 4 * (lane / 16);
+        T* dst = (T*)a.dst + id * 4;
+        for (int e = 0; e < 4; ++e)
+            dst[e] = (k0 + e < a.r && srow < a.src_rows[src]) ? ((const T*)a.b[src])[(size_t)srow * a.r + k0 + e]
+                                                             : from_f32<T>(0.f);
     }
 }
 
@@ -765,33 +951,59 @@ __global__ void k_fill_u32(uint32_t* p, size_t n, uint32_t v) {
 // Host-side launchers
 // ---------------------------------------------------------------------------
 template <typename T, bool SPLIT>
-static hipError_t launch_gemm_t(const GemmArgs& a, int epi, hipStream_t st) {
-    const int mg = a.MT <= 1 ? 1 : (a.MT <= 2 ? 2 : (a.MT <= 4 ? 4 : 8));
-    dim3 grid(a.n_tiles * a.ks), block(256);
-#define PBD_GEMM_CASE(E, G)                                                     \
-    if (epi == E && mg == G) { hipLaunchKernelGGL((k_gemm<T, E, G, SPLIT>), grid, block, 0, st, a); return hipGetLastError(); }
-#define PBD_GEMM_EPI(E) PBD_GEMM_CASE(E, 1) PBD_GEMM_CASE(E, 2) PBD_GEMM_CASE(E, 4) PBD_GEMM_CASE(E, 8)
-    PBD_GEMM_EPI(EPI_STORE)
-    PBD_GEMM_EPI(EPI_PARTIAL)
-    PBD_GEMM_EPI(EPI_SWIGLU)
-    PBD_GEMM_EPI(EPI_ARGMAX)
-#undef PBD_GEMM_EPI
-#undef PBD_GEMM_CASE
+static hipError_t launch_fgemm_t(const FGemmArgs& a, int epi, hipStream_t st) {
+    // m-tiles per pass over the weights: enough for the rows, bounded by the
+    // register budget of the LoRA shrink accumulators and by LDS for 8-wave groups
+    int cap = 8;
+    if (epi == EPI_RESID) cap = 2;          // register budget of the long-K residual GEMMs
+    else if (epi != EPI_ARGMAX) cap = 4;    // LDS of the 8-wave reduction
+    if (a.lora && epi != EPI_ARGMAX) {
+        const int ku = (epi == EPI_SWIGLU || epi == EPI_RESID) ? 4 : 8;
+        cap = std::min(cap, std::max(1, ku / std::max(a.rt, 1)));
+    }
+    int mg = 1;
+    while (mg < a.MT && mg < cap) mg *= 2;
+    if (mg > cap) mg /= 2;
+    const dim3 grid(a.n_tiles);
+#define PBD_FG_CASE(E, G)                                                                            \
+    if (epi == E && mg == G) {                                                                       \
+        hipLaunchKernelGGL((k_fgemm<T, E, G, SPLIT>), grid, dim3(FG<E>::NW * 64), 0, st, a);          \
+        return hipGetLastError();                                                                    \
+    }
+#define PBD_FG_EPI(E) PBD_FG_CASE(E, 1) PBD_FG_CASE(E, 2) PBD_FG_CASE(E, 4) PBD_FG_CASE(E, 8)
+    PBD_FG_CASE(EPI_STORE, 1) PBD_FG_CASE(EPI_STORE, 2) PBD_FG_CASE(EPI_STORE, 4)
+    PBD_FG_CASE(EPI_RESID, 1) PBD_FG_CASE(EPI_RESID, 2)
+    PBD_FG_CASE(EPI_SWIGLU, 1) PBD_FG_CASE(EPI_SWIGLU, 2) PBD_FG_CASE(EPI_SWIGLU, 4)
+    PBD_FG_EPI(EPI_ARGMAX)
+#undef PBD_FG_EPI
+#undef PBD_FG_CASE
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm(int dtype, const GemmArgs& a, int epi, hipStream_t st) {
+hipError_t launch_fgemm(int dtype, const FGemmArgs& a, int epi, hipStream_t st) {
     if (dtype == PBD_DTYPE_BF16)
-        return a.xlo ? launch_gemm_t<bf16, true>(a, epi, st) : launch_gemm_t<bf16, false>(a, epi, st);
-    return launch_gemm_t<float, false>(a, epi, st);
+        return a.xlo ? launch_fgemm_t<bf16, true>(a, epi, st) : launch_fgemm_t<bf16, false>(a, epi, st);
+    return launch_fgemm_t<float, false>(a, epi, st);
+}
+
+bool lmhead_fits(int kb, int MT) { return kb <= 4 * LM_FPW && MT <= 2; }
+
+hipError_t launch_lmhead(int dtype, const FGemmArgs& a, int grid, hipStream_t st) {
+    if (dtype == PBD_DTYPE_BF16) {
+        if (a.xlo) hipLaunchKernelGGL((k_lmhead<bf16, true>), dim3(grid), dim3(256), 0, st, a);
+        else hipLaunchKernelGGL((k_lmhead<bf16, false>), dim3(grid), dim3(256), 0, st, a);
+    } else {
+        hipLaunchKernelGGL((k_lmhead<float, false>), dim3(grid), dim3(256), 0, st, a);
+    }
+    return hipGetLastError();
 }
 
 size_t attn_smem_main(int dtype, int head_dim, int qt) {
     const size_t es = dtype == PBD_DTYPE_BF16 ? 2 : 4;
     const size_t ldq = head_dim + 16 / es;
     const size_t ops = (qt * 16 * ldq + 48 * ldq + 48 * (size_t)head_dim) * es;
-    const size_t ob = (size_t)qt * 16 * head_dim * 4;
-    size_t m = ops > ob ? ops : ob;
+    const size_t ob = (size_t)qt * 16 * (head_dim + 1) * 4;
+    const size_t m = ops > ob ? ops : ob;
     return (m + 15) / 16 * 16;
 }
 
@@ -825,27 +1037,24 @@ hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int b
     return hipErrorInvalidValue;
 }
 
-#define PBD_DISPATCH(dtype, KERNEL, grid, block, st, args)                                   \
-    do {                                                                                     \
+#define PBD_DISPATCH(dtype, KERNEL, grid, block, st, args)                                        \
+    do {                                                                                          \
         if ((dtype) == PBD_DTYPE_BF16) hipLaunchKernelGGL(KERNEL<bf16>, grid, block, 0, st, args); \
-        else hipLaunchKernelGGL(KERNEL<float>, grid, block, 0, st, args);                    \
-        return hipGetLastError();                                                            \
+        else hipLaunchKernelGGL(KERNEL<float>, grid, block, 0, st, args);                         \
+        return hipGetLastError();                                                                 \
     } while (0)
 
 hipError_t launch_assemble(int dtype, const AssembleArgs& a, int batch, hipStream_t st) {
-    PBD_DISPATCH(dtype, k_assemble, dim3(batch), dim3(256), st, a);
+    PBD_DISPATCH(dtype, k_assemble, dim3(a.W, batch), dim3(256), st, a);
 }
-hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t st) {
-    PBD_DISPATCH(dtype, k_norm, dim3(a.M), dim3(256), st, a);
-}
-hipError_t launch_shrink(int dtype, const ShrinkArgs& a, hipStream_t st) {
-    PBD_DISPATCH(dtype, k_shrink, dim3(a.M), dim3(256), st, a);
-}
-hipError_t launch_combine(int dtype, const CombineArgs& a, hipStream_t st) {
-    PBD_DISPATCH(dtype, k_combine, dim3(a.M), dim3(256), st, a);
+hipError_t launch_combine(int dtype, const CombineArgs& a, int M, hipStream_t st) {
+    PBD_DISPATCH(dtype, k_combine, dim3(M, a.n_q), dim3(a.head_dim), st, a);
 }
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st) {
     PBD_DISPATCH(dtype, k_pack, dim3(1024), dim3(256), st, a);
+}
+hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st) {
+    PBD_DISPATCH(dtype, k_pack_expand, dim3(256), dim3(256), st, a);
 }
 hipError_t launch_argmax(const ArgmaxArgs& a, hipStream_t st) {
     hipLaunchKernelGGL(k_argmax, dim3(a.M), dim3(256), 0, st, a);
