@@ -21,6 +21,7 @@ thread_local std::string g_init_error;
 
 constexpr int MAX_DIM = 16384;   // bound on hidden, ffn and n_q_heads*head_dim
 constexpr int LMHEAD_GRID = 512;  // work-groups of the persistent LM head (two per CU)
+constexpr size_t MAX_LDS = 160 * 1024;   // LDS one gfx950 work-group may allocate
 
 // Every size and offset the library uses, derived from a validated config.
 struct Layout {
@@ -79,7 +80,7 @@ int validate(const pbd_config* c, std::string& err) {
     PBD_REQ(c->max_batch >= 1 && c->max_batch * W <= 4096, PBD_ERR_CAPACITY, "max_batch %d too large", c->max_batch);
     PBD_REQ(c->max_seq > W && c->max_seq <= (1 << 20), PBD_ERR_CAPACITY, "max_seq %d out of range", c->max_seq);
     const int qt = cdiv(G * W, 16);
-    PBD_REQ(attn_smem_bytes(c->dtype, c->head_dim, qt) <= 64 * 1024, PBD_ERR_SHAPE, "attention tile does not fit in LDS");
+    PBD_REQ(attn_smem_bytes(c->dtype, c->head_dim, qt) <= MAX_LDS, PBD_ERR_SHAPE, "attention tile does not fit in LDS");
 #undef PBD_REQ
     return PBD_OK;
 }
@@ -100,7 +101,7 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.nqkv = (y.NQ + 2 * y.NKV) * y.HD;
     y.kb_qkv = y.H / y.FK; y.kb_o = y.NQ * y.HD / y.FK; y.kb_gu = y.H / y.FK; y.kb_d = y.F / y.FK; y.kb_e = y.H / y.FK;
     y.tiles_qkv = y.nqkv / 16; y.tiles_o = y.H / 16; y.tiles_gu = 2 * y.F / 16; y.tiles_d = y.H / 16; y.tiles_e = y.V / 16;
-    y.S_max = std::min(64, cdiv(y.max_seq, 16));
+    y.S_max = std::min(64, cdiv(y.max_seq, 16)) + 1;   // prefix splits + the block split
 
     const size_t FR = 1024;                       // bytes per fragment
     const size_t EB = (size_t)64 * 4 * y.esz;     // bytes per LoRA expand block
@@ -256,7 +257,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     as.op_hi = hi(y.w_xa); as.op_lo = lo(y.w_xa); as.sq = sq_a;
     PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_assemble(dt, as, B, st), "assemble");
 
-    const int s_launch = std::min(y.S_max, cdiv(y.max_seq, c->kps));
+    const int s_launch = std::min(y.S_max, cdiv(y.max_seq, c->kps) + 1);
     auto base_gemm = [&](FGemmArgs& g, size_t w_off, int tiles, int kb, const size_t* xop) {
         g = FGemmArgs{};
         g.w = (const uint4*)(pk + w_off); g.n_tiles = tiles; g.kb = kb;
@@ -430,6 +431,15 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
     c->split = cfg->dtype == PBD_DTYPE_BF16;
     hipStream_t st = (hipStream_t)stream;
     const int dt = y.dtype;
+    {
+        int dev = 0, lds = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+            attn_smem_bytes(dt, y.HD, y.QTmax) > (size_t)lds) {
+            delete c;
+            return fail(nullptr, PBD_ERR_SHAPE, "attention tile exceeds the device's LDS per work-group");
+        }
+    }
 
     auto cleanup_fail = [&](hipError_t e, const char* what) {
         std::string m = std::string(what) + ": " + hipGetErrorString(e);

@@ -27,10 +27,12 @@ namespace pbd {
 
 static __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-// Split-KV schedule shared by k_attn and k_combine.
-static __device__ __forceinline__ void attn_splits(int t, int kps, int s_launch, int& s_eff, int& chunk) {
-    s_eff = min(max(ceil_div(t, kps), 1), s_launch);
-    chunk = ceil_div(ceil_div(max(t, 1), s_eff), 16) * 16;
+// Split-KV schedule shared by k_attn and k_combine: prefix splits s < s_pre
+// cover keys [0, t) in chunks of `chunk` keys (a multiple of 16); split s_pre
+// holds the W block keys.  s_launch >= 2.
+static __device__ __forceinline__ void attn_splits(int t, int kps, int s_launch, int& s_pre, int& chunk) {
+    s_pre = t > 0 ? min(ceil_div(t, kps), s_launch - 1) : 0;
+    chunk = s_pre > 0 ? ceil_div(ceil_div(t, s_pre), 16) * 16 : 16;
 }
 
 // Write v into an operand as bf16 value (hi) plus bf16 residual (lo), or as
@@ -395,34 +397,55 @@ template <typename T, int HD>
 struct RowPrep {
     static constexpr int HALF = HD / 2;
     static constexpr int NP = HALF / 16;       // pairs per lane (4 or 2)
-    float lo[NP], hi[NP];
-    float2 cs[NP];
-    __device__ void load(const float* src, const float2* rope_row, int l16, bool live) {
-#pragma unroll
-        for (int p = 0; p < NP; ++p) {
-            lo[p] = live ? src[NP * l16 + p] : 0.f;
-            hi[p] = live ? src[HALF + NP * l16 + p] : 0.f;
-            cs[p] = live ? rope_row[NP * l16 + p] : float2{1.f, 0.f};
-        }
+    typedef float __attribute__((ext_vector_type(NP))) fv;
+    typedef float __attribute__((ext_vector_type(2 * NP))) fv2;
+    fv lo, hi;
+    fv2 cs;                                    // (cos, sin) of the NP pairs
+    // vector loads from always-valid addresses; dead rows are zeroed in finish
+    __device__ void load(const float* src, const float2* rope_row, int l16) {
+        lo = *(const fv*)(src + NP * l16);
+        hi = *(const fv*)(src + HALF + NP * l16);
+        cs = *(const fv2*)(rope_row + NP * l16);
     }
-    // normalise (if gain) and rotate; writes the row into dst[HD] as T
-    __device__ void finish(T* dst, const T* gain, bool qk_norm, float eps, int l16, T* out_lo, T* out_hi) {
-        float inv = 1.f;
+    // normalise with this lane's gains and rotate; writes the row into dst[HD]
+    // as T and returns the lane's values
+    __device__ void finish(T* dst, bool live, const float* g_lo, const float* g_hi, bool qk_norm, float eps, int l16,
+                           T* out_lo, T* out_hi) {
+        float inv = live ? 1.f : 0.f;
         if (qk_norm) {
             float ss = 0.f;
 #pragma unroll
             for (int p = 0; p < NP; ++p) ss += lo[p] * lo[p] + hi[p] * hi[p];
-            inv = rsqrtf(row16_sum(ss) / (float)HD + eps);
+            inv = live ? rsqrtf(row16_sum(ss) / (float)HD + eps) : 0.f;
         }
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
             const int i = NP * l16 + p;
-            float y0 = lo[p] * inv, y1 = hi[p] * inv;
-            if (qk_norm) { y0 *= to_f32(gain[i]); y1 *= to_f32(gain[i + HALF]); }
-            out_lo[p] = from_f32<T>(y0 * cs[p].x - y1 * cs[p].y);
-            out_hi[p] = from_f32<T>(y1 * cs[p].x + y0 * cs[p].y);
+            const float y0 = lo[p] * inv * g_lo[p], y1 = hi[p] * inv * g_hi[p];
+            const float c = cs[2 * p], sn = cs[2 * p + 1];
+            out_lo[p] = from_f32<T>(y0 * c - y1 * sn);
+            out_hi[p] = from_f32<T>(y1 * c + y0 * sn);
             dst[i] = out_lo[p];
             dst[i + HALF] = out_hi[p];
+        }
+    }
+};
+
+// this lane's RMSNorm gains: raw loads now, conversion at first use
+template <typename T, int HD>
+struct Gains {
+    static constexpr int NP = RowPrep<T, HD>::NP, HALF = HD / 2;
+    typedef T __attribute__((ext_vector_type(NP))) tv;
+    tv rlo, rhi;
+    __device__ void load(const void* gain, int l16) {
+        rlo = *(const tv*)((const T*)gain + NP * l16);
+        rhi = *(const tv*)((const T*)gain + HALF + NP * l16);
+    }
+    __device__ void get(bool qk_norm, float* g_lo, float* g_hi) const {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            g_lo[p] = qk_norm ? to_f32(rlo[p]) : 1.f;
+            g_hi[p] = qk_norm ? to_f32(rhi[p]) : 1.f;
         }
     }
 };
@@ -436,19 +459,20 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     constexpr int QROWS = QT * 16;
     constexpr int LDQ = HD + 16 / (int)sizeof(T);   // padded LDS row (bank spread)
     constexpr int KBMAX = 48;                       // block keys: W <= 33 -> 3 blocks
-    constexpr int LDO = HD + 1;                     // padded merge rows
+    constexpr int LDO = HD + 4;                     // merge rows (16-byte aligned, banks spread)
+    constexpr int HALF = HD / 2;
     typedef typename K4<T>::raw vraw;
     typedef RowPrep<T, HD> RP;
 
     const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int t = a.pos0[b];
     const int nrows = a.nrows[b];
-    int s_eff, chunk;
-    attn_splits(t, a.kps, a.s_launch, s_eff, chunk);
-    if (s >= s_eff) return;
-    const int k_lo = min(s * chunk, t);
-    const int k_hi = min(t, k_lo + chunk);
-    const bool last = (s == s_eff - 1);
+    int s_pre, chunk;
+    attn_splits(t, a.kps, a.s_launch, s_pre, chunk);
+    if (s > s_pre) return;
+    const bool blk = (s == s_pre);                       // the split of the W block keys
+    const int k_lo = blk ? t : min(s * chunk, t);
+    const int k_hi = blk ? t : min(t, k_lo + chunk);
     const int W = a.W, G = a.G;
     const int QR = G * W;
 
@@ -456,7 +480,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     T* q_l = (T*)smem;                                   // [QROWS][LDQ]
     T* kb_l = q_l + QROWS * LDQ;                         // [KBMAX][LDQ]
     T* vb_l = kb_l + KBMAX * LDQ;                        // [KBMAX][HD]
-    float* obuf = (float*)smem;                          // [QROWS][LDO], aliases after the key loop
+    float* obuf = (float*)smem;                          // [2][QROWS][LDO], aliases after the key loop
     float* ml_l = (float*)(smem + a.smem_main);          // [4][QROWS][2]
 
     const int lane = threadIdx.x % WAVE, wid = threadIdx.x / WAVE;
@@ -464,61 +488,99 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     const size_t row_stride = (size_t)a.nqkv;
     const float* qkv_b = a.qkv + (size_t)b * W * row_stride;
     const float2* rope = a.rope;
-    constexpr int HALF = HD / 2;
 
-    // -- Q rows: wave w, lane group lgrp handles rows 16*i + 4*w + lgrp
-    {
-        constexpr int QSTEPS = QROWS / 16;
-        RP rp[QSTEPS];
+    T* kc = (T*)a.kcache + (((size_t)a.layer * a.max_batch + b) * a.n_kv + g) * a.nblk * 16 * HD;
+    T* vc = (T*)a.vcache + (((size_t)a.layer * a.max_batch + b) * a.n_kv + g) * a.nblk * 16 * HD;
+    const int kb_first = k_lo / 16;
+    const int n_pref = (k_hi > k_lo) ? ceil_div(k_hi, 16) - kb_first : 0;
+    const int nkb_blk = blk ? ceil_div(W, 16) : 0;
+    const int n_items = n_pref + nkb_blk;
+
+    // item it < n_pref: prefix key block kb_first + it from the cache;
+    // otherwise block keys 16*(it - n_pref) .. from LDS
+    auto load_item = [&](int it, uint4* kf, vraw* vf) {
+        if (it < n_pref) {
+            const T* kblk = kc + (size_t)(kb_first + it) * 16 * HD;
+            const T* vblk = vc + (size_t)(kb_first + it) * 16 * HD;
 #pragma unroll
-        for (int i = 0; i < QSTEPS; ++i) {
-            const int q = 16 * i + 4 * wid + lgrp;
-            const bool live = q < QR;
-            const int qq = live ? q : 0;
-            rp[i].load(qkv_b + (size_t)(qq % W) * row_stride + (size_t)(g * G + qq / W) * HD,
-                       rope + (size_t)(t + qq % W) * HALF, lrow, live);
+            for (int ds = 0; ds < NDS; ++ds) kf[ds] = *(const uint4*)(kblk + (size_t)(ds * WAVE + lane) * EPL);
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) vf[dt] = *(const vraw*)(vblk + (size_t)(dt * WAVE + lane) * 4);
+        } else {
+            const int bb = it - n_pref;
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+                kf[ds] = *(const uint4*)(kb_l + (bb * 16 + lrow) * LDQ + ds * FK + lgrp * EPL);
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                T tmp[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) tmp[e] = vb_l[(bb * 16 + lgrp * 4 + e) * HD + dt * 16 + lrow];
+                __builtin_memcpy(&vf[dt], tmp, sizeof(vraw));
+            }
         }
+    };
+
+    // the wave's first prefix key block is requested before the query
+    // preparation, which it does not depend on
+    uint4 kn[NDS];
+    vraw vn[NDT];
+    if (!blk && wid < n_items) load_item(wid, kn, vn);
+
+    // -- Q rows (and, in the block split, K/V rows): all loads first, then
+    //    norm + rotation; wave w, lane group lgrp handles rows 16*i + 4*w + lgrp
+    constexpr int QSTEPS = QROWS / 16;
+    constexpr int KSTEPS = KBMAX / 16;
+    Gains<T, HD> gq;
+    if (a.qk_norm) gq.load(a.q_norm, lrow);
+    RP rp[QSTEPS];
+#pragma unroll
+    for (int i = 0; i < QSTEPS; ++i) {
+        const int q = 16 * i + 4 * wid + lgrp;
+        const int qq = q < QR ? q : 0;
+        rp[i].load(qkv_b + (size_t)(qq % W) * row_stride + (size_t)(g * G + qq / W) * HD,
+                   rope + (size_t)(t + qq % W) * HALF, lrow);
+    }
+    float gq_lo[RP::NP], gq_hi[RP::NP];
+    if (blk) {
+        Gains<T, HD> gk;
+        if (a.qk_norm) gk.load(a.k_norm, lrow);
+        RP rk[KSTEPS];
+        typename RP::fv vlo[KSTEPS], vhi[KSTEPS];
+#pragma unroll
+        for (int i = 0; i < KSTEPS; ++i) {
+            const int j = 16 * i + 4 * wid + lgrp;
+            const int jj = (j < W && j < nrows) ? j : 0;
+            const float* ks = qkv_b + (size_t)jj * row_stride + (size_t)a.n_q * HD + (size_t)g * HD;
+            const float* vs = ks + (size_t)a.n_kv * HD;
+            rk[i].load(ks, rope + (size_t)(t + jj) * HALF, lrow);
+            vlo[i] = *(const typename RP::fv*)(vs + RP::NP * lrow);
+            vhi[i] = *(const typename RP::fv*)(vs + HALF + RP::NP * lrow);
+        }
+        gq.get(a.qk_norm, gq_lo, gq_hi);
 #pragma unroll
         for (int i = 0; i < QSTEPS; ++i) {
             const int q = 16 * i + 4 * wid + lgrp;
             T lo[RP::NP], hi[RP::NP];
-            rp[i].finish(q_l + q * LDQ, (const T*)a.q_norm, a.qk_norm, a.eps, lrow, lo, hi);
+            rp[i].finish(q_l + q * LDQ, q < QR, gq_lo, gq_hi, a.qk_norm, a.eps, lrow, lo, hi);
         }
-    }
-    // -- block keys and values (last split only); the verify appends them to the cache
-    const int nkb_blk = last ? ceil_div(W, 16) : 0;
-    T* kc = (T*)a.kcache + (((size_t)a.layer * a.max_batch + b) * a.n_kv + g) * a.nblk * 16 * HD;
-    T* vc = (T*)a.vcache + (((size_t)a.layer * a.max_batch + b) * a.n_kv + g) * a.nblk * 16 * HD;
-    if (last) {
-        constexpr int KSTEPS = KBMAX / 16;
-        RP rk[KSTEPS];
-        float vlo[KSTEPS][RP::NP], vhi[KSTEPS][RP::NP];
-#pragma unroll
-        for (int i = 0; i < KSTEPS; ++i) {
-            const int j = 16 * i + 4 * wid + lgrp;
-            const bool live = j < nkb_blk * 16 && j < W && j < nrows;
-            const int jj = live ? j : 0;
-            const float* ks = qkv_b + (size_t)jj * row_stride + (size_t)a.n_q * HD + (size_t)g * HD;
-            const float* vs = ks + (size_t)a.n_kv * HD;
-            rk[i].load(ks, rope + (size_t)(t + jj) * HALF, lrow, live);
-#pragma unroll
-            for (int p = 0; p < RP::NP; ++p) {
-                vlo[i][p] = live ? vs[RP::NP * lrow + p] : 0.f;
-                vhi[i][p] = live ? vs[HALF + RP::NP * lrow + p] : 0.f;
-            }
-        }
+        // block keys and values; the verify appends them to the cache
+        float gk_lo[RP::NP], gk_hi[RP::NP];
+        gk.get(a.qk_norm, gk_lo, gk_hi);
 #pragma unroll
         for (int i = 0; i < KSTEPS; ++i) {
             const int j = 16 * i + 4 * wid + lgrp;
             if (j >= nkb_blk * 16) continue;
             const bool live = j < W && j < nrows;
-            T klo[RP::NP], khi[RP::NP];
-            rk[i].finish(kb_l + j * LDQ, (const T*)a.k_norm, a.qk_norm, a.eps, lrow, klo, khi);
+            T klo[RP::NP], khi[RP::NP], vl[RP::NP], vh[RP::NP];
+            rk[i].finish(kb_l + j * LDQ, live, gk_lo, gk_hi, a.qk_norm, a.eps, lrow, klo, khi);
             T* vd = vb_l + j * HD;
 #pragma unroll
             for (int p = 0; p < RP::NP; ++p) {
-                vd[RP::NP * lrow + p] = from_f32<T>(vlo[i][p]);
-                vd[HALF + RP::NP * lrow + p] = from_f32<T>(vhi[i][p]);
+                vl[p] = from_f32<T>(live ? vlo[i][p] : 0.f);
+                vh[p] = from_f32<T>(live ? vhi[i][p] : 0.f);
+                vd[RP::NP * lrow + p] = vl[p];
+                vd[HALF + RP::NP * lrow + p] = vh[p];
             }
             if (live && a.write_kv) {
                 const int pos = t + j;
@@ -529,10 +591,18 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                     const int i0 = RP::NP * lrow + p;
                     kblk[kblock_elem<T>(pos % 16, i0)] = klo[p];
                     kblk[kblock_elem<T>(pos % 16, i0 + HALF)] = khi[p];
-                    vblk[vblock_elem(pos % 16, i0)] = from_f32<T>(vlo[i][p]);
-                    vblk[vblock_elem(pos % 16, i0 + HALF)] = from_f32<T>(vhi[i][p]);
+                    vblk[vblock_elem(pos % 16, i0)] = vl[p];
+                    vblk[vblock_elem(pos % 16, i0 + HALF)] = vh[p];
                 }
             }
+        }
+    } else {
+        gq.get(a.qk_norm, gq_lo, gq_hi);
+#pragma unroll
+        for (int i = 0; i < QSTEPS; ++i) {
+            const int q = 16 * i + 4 * wid + lgrp;
+            T lo[RP::NP], hi[RP::NP];
+            rp[i].finish(q_l + q * LDQ, q < QR, gq_lo, gq_hi, a.qk_norm, a.eps, lrow, lo, hi);
         }
     }
     __syncthreads();
@@ -559,40 +629,18 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) o_acc[dt][qt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-
-    const int kb_first = k_lo / 16;
-    const int n_pref = (k_hi > k_lo) ? ceil_div(k_hi, 16) - kb_first : 0;
-    const int n_items = n_pref + nkb_blk;
     const float sl2 = a.scale_log2;
 
-    auto load_item = [&](int it, uint4* kf, vraw* vf) {
-        if (it < n_pref) {
-            const T* kblk = kc + (size_t)(kb_first + it) * 16 * HD;
-            const T* vblk = vc + (size_t)(kb_first + it) * 16 * HD;
-#pragma unroll
-            for (int ds = 0; ds < NDS; ++ds) kf[ds] = *(const uint4*)(kblk + (size_t)(ds * WAVE + lane) * EPL);
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) vf[dt] = *(const vraw*)(vblk + (size_t)(dt * WAVE + lane) * 4);
-        } else {
-            const int bb = it - n_pref;
-#pragma unroll
-            for (int ds = 0; ds < NDS; ++ds)
-                kf[ds] = *(const uint4*)(kb_l + (bb * 16 + lrow) * LDQ + ds * FK + lgrp * EPL);
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) {
-                T tmp[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) tmp[e] = vb_l[(bb * 16 + lgrp * 4 + e) * HD + dt * 16 + lrow];
-                __builtin_memcpy(&vf[dt], tmp, sizeof(vraw));
-            }
-        }
-    };
-
-    uint4 kf[NDS], kn[NDS];
-    vraw vf[NDT], vn[NDT];
-    if (wid < n_items) load_item(wid, kf, vf);
+    if (blk && wid < n_items) load_item(wid, kn, vn);
     for (int it = wid; it < n_items; it += 4) {
-        if (it + 4 < n_items) load_item(it + 4, kn, vn);           // next block in flight
+        // rotate: this block's operands, then the next block's request
+        uint4 kf[NDS];
+        vraw vf[NDT];
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds) kf[ds] = kn[ds];
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) vf[dt] = vn[dt];
+        if (it + 4 < n_items) load_item(it + 4, kn, vn);
         const bool pref = it < n_pref;
         const int key0 = pref ? (kb_first + it) * 16 : (it - n_pref) * 16;
 #pragma unroll
@@ -631,15 +679,10 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 mma_k4(o_acc[dt][qt], vf[dt], p);
             }
         }
-        if (it + 4 < n_items) {
-#pragma unroll
-            for (int ds = 0; ds < NDS; ++ds) kf[ds] = kn[ds];
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) vf[dt] = vn[dt];
-        }
     }
 
-    // -- merge the four waves (fixed order) and write this split's partial
+    // -- merge the four waves: common max per query row, then a two-round tree
+    //    (waves 2,3 -> 0,1, then 1 -> 0) in LDS; wave 0 writes the partial
     __syncthreads();                                     // LDS operands dead: obuf may alias
     if (lgrp == 0) {
 #pragma unroll
@@ -649,46 +692,58 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         }
     }
     __syncthreads();
-    float fct[QT];
+    float mx[QT];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
         const int q = qt * 16 + lrow;
-        float mx = -1e30f;
-        for (int w = 0; w < 4; ++w) mx = fmaxf(mx, ml_l[(w * QROWS + q) * 2]);
-        fct[qt] = exp2f(m_run[qt] - mx);
+        mx[qt] = -1e30f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) mx[qt] = fmaxf(mx[qt], ml_l[(w * QROWS + q) * 2]);
+        const float f = exp2f(m_run[qt] - mx[qt]);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) o_acc[dt][qt] *= f;
     }
-    for (int w = 0; w < 4; ++w) {
-        if (wid == w) {
+    auto put = [&](float* reg) {
 #pragma unroll
-            for (int qt = 0; qt < QT; ++qt)
+        for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt)
+            for (int dt = 0; dt < NDT; ++dt)
+                *(f32x4*)(reg + (qt * 16 + lrow) * LDO + dt * 16 + lgrp * 4) = o_acc[dt][qt];
+    };
+    auto add = [&](const float* reg) {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        float* o = obuf + (qt * 16 + lrow) * LDO + dt * 16 + lgrp * 4 + e;
-                        const float v = o_acc[dt][qt][e] * fct[qt];
-                        *o = (w == 0) ? v : *o + v;
-                    }
-        }
-        __syncthreads();
-    }
-    // partial (max in log2 domain, sum, unnormalised output) per query row
+        for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+                o_acc[dt][qt] += *(const f32x4*)(reg + (qt * 16 + lrow) * LDO + dt * 16 + lgrp * 4);
+    };
+    if (wid >= 2) put(obuf + (wid - 2) * QROWS * LDO);
+    __syncthreads();
+    if (wid < 2) add(obuf + wid * QROWS * LDO);
+    __syncthreads();
+    if (wid == 1) put(obuf);
+    __syncthreads();
+    if (wid != 0) return;
+    add(obuf);
+
+    // partial of this split: max (log2 domain), sum, unnormalised output per query row
     const int S = a.s_launch;
-    for (int idx = threadIdx.x; idx < QR * HD; idx += blockDim.x) {
-        const int q = idx / HD, d = idx % HD;
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+        const int q = qt * 16 + lrow;
+        if (q >= QR) continue;
         const int gi = q / W, j = q % W;
         const size_t pr = (((size_t)b * a.n_q + g * G + gi) * W + j) * S + s;
-        a.part_o[pr * HD + d] = obuf[q * LDO + d];
-    }
-    for (int q = threadIdx.x; q < QR; q += blockDim.x) {
-        float mx = -1e30f;
-        for (int w = 0; w < 4; ++w) mx = fmaxf(mx, ml_l[(w * QROWS + q) * 2]);
-        float L = 0.f;
-        for (int w = 0; w < 4; ++w) L += ml_l[(w * QROWS + q) * 2 + 1] * exp2f(ml_l[(w * QROWS + q) * 2] - mx);
-        const int gi = q / W, j = q % W;
-        const size_t pr = (((size_t)b * a.n_q + g * G + gi) * W + j) * S + s;
-        a.part_ml[pr * 2 + 0] = mx;
-        a.part_ml[pr * 2 + 1] = L;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) *(f32x4*)(a.part_o + pr * HD + dt * 16 + lgrp * 4) = o_acc[dt][qt];
+        if (lgrp == 0) {
+            float L = 0.f;
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+                L += ml_l[(w * QROWS + q) * 2 + 1] * exp2f(ml_l[(w * QROWS + q) * 2] - mx[qt]);
+            a.part_ml[pr * 2 + 0] = mx[qt];
+            a.part_ml[pr * 2 + 1] = L;
+        }
     }
 }
 
@@ -805,8 +860,9 @@ template <typename T>
 __global__ void k_combine(CombineArgs a) {
     const int m = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
     const int b = m / a.W, j = m % a.W;
-    int s_eff, chunk;
-    attn_splits(a.pos0[b], a.kps, a.s_launch, s_eff, chunk);
+    int s_pre, chunk;
+    attn_splits(a.pos0[b], a.kps, a.s_launch, s_pre, chunk);
+    const int s_eff = s_pre + 1;
     const size_t pr0 = (((size_t)b * a.n_q + h) * a.W + j) * a.s_launch;
     float mx = -1e30f;
     for (int s = 0; s < s_eff; ++s) mx = fmaxf(mx, a.part_ml[(pr0 + s) * 2]);
@@ -1002,7 +1058,7 @@ size_t attn_smem_main(int dtype, int head_dim, int qt) {
     const size_t es = dtype == PBD_DTYPE_BF16 ? 2 : 4;
     const size_t ldq = head_dim + 16 / es;
     const size_t ops = (qt * 16 * ldq + 48 * ldq + 48 * (size_t)head_dim) * es;
-    const size_t ob = (size_t)qt * 16 * (head_dim + 1) * 4;
+    const size_t ob = (size_t)2 * qt * 16 * (head_dim + 4) * 4;
     const size_t m = ops > ob ? ops : ob;
     return (m + 15) / 16 * 16;
 }
