@@ -46,6 +46,8 @@ struct Layout {
     size_t w_x, w_qkv, w_sq_a, w_sq_m;
     size_t w_xa[2], w_xo[2], w_xm[2], w_xd[2];      // operand value and residual fragments
     size_t w_attn_o, w_attn_ml, w_arg_val, w_arg_idx, w_tokens, w_pos0, w_nrows, w_status, ws_bytes;
+    size_t w_kpart, w_kcnt;                          // split-K partial tiles and arrival counters
+    int ksplit;                                      // K slices of the residual GEMMs
 };
 
 int validate(const pbd_config* c, std::string& err) {
@@ -153,6 +155,9 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.w_pos0 = take((size_t)y.Bmax * 4);
     y.w_nrows = take((size_t)y.Bmax * 4);
     y.w_status = take(256);
+    y.ksplit = 4;
+    y.w_kpart = take((size_t)y.tiles_o * y.ksplit * 2 * 256 * 4);
+    y.w_kcnt = take((size_t)y.tiles_o * 4);
     y.ws_bytes = off;
 }
 
@@ -264,6 +269,16 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.xhi = (const uint4*)hi(xop); g.xlo = (const uint4*)lo(xop);
         g.M = M; g.MT = MT; g.sq_stride = y.Mmax; g.norm_dim = y.H; g.eps = c->cfg.rms_eps;
         g.lora = lora ? 1 : 0; g.rt = y.RT; g.scale = scale; g.exclude = -1;
+        g.ksplit = 1;
+    };
+    // residual GEMMs (n = hidden) have few output tiles: split K so that the
+    // whole chip streams their weights (one m-group only)
+    auto split_k = [&](FGemmArgs& g) {
+        if (g.n_tiles <= 128 && MT <= fgemm_mgroup(EPI_RESID, MT)) {
+            g.ksplit = y.ksplit;
+            g.part = (float*)(ws + y.w_kpart);
+            g.cnt = (unsigned*)(ws + y.w_kcnt);
+        }
     };
     for (int l = 0; l < y.L; ++l) {
         const Layout::LayerOff& lo_ = y.lay[l];
@@ -300,6 +315,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.n_sq = 0; g.lora_mode = LORA_SINGLE; g.la[0] = (const uint4*)(pk + lo_.la[3]); g.lb = pk + lo_.lb_o;
         g.x = x; g.ldx = y.H; g.gnext = pk + lo_.mlp_norm; g.nx_hi = hi(y.w_xm); g.nx_lo = lo(y.w_xm); g.n_MT = MT;
         g.sq_out = sq_m;
+        split_k(g);
         PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "o gemm");
 
         // gate/up + SwiGLU: MLP RMSNorm folded in
@@ -316,6 +332,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.x = x; g.ldx = y.H;
         g.gnext = l + 1 < y.L ? pk + y.lay[l + 1].attn_norm : pk + y.p_final_norm;
         g.nx_hi = hi(y.w_xa); g.nx_lo = lo(y.w_xa); g.n_MT = MT; g.sq_out = sq_a;
+        split_k(g);
         PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "down gemm");
     }
 

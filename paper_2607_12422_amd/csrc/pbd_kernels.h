@@ -17,6 +17,7 @@ enum LoraMode { LORA_SINGLE = 0, LORA_BY_TILE = 1, LORA_ROW_HALF = 2 };
 enum RowMap { MAP_CONCAT = 0, MAP_INTERLEAVE2 = 1 };
 
 constexpr int MAX_RT = 4;              // LoRA rank <= 64: up to four 16-row shrink tiles
+constexpr int KSPLIT_MAX = 4;          // K slices of a split-K GEMM
 
 struct AssembleArgs {
     int mode;
@@ -68,6 +69,11 @@ struct FGemmArgs {
     float* arg_val;         // ARGMAX: [n_tiles][M]
     int* arg_idx;
     int exclude;            // ARGMAX: token id excluded (-1: none)
+    // split-K (ksplit > 1: one m-group only): partial tiles [n_tiles][ksplit][MG*256]
+    // and per-tile arrival counters (zero between launches)
+    int ksplit;
+    float* part;
+    unsigned* cnt;
 };
 
 struct AttnArgs {
@@ -139,6 +145,7 @@ struct PackExpandArgs {
 
 hipError_t launch_assemble(int dtype, const AssembleArgs& a, int batch, hipStream_t st);
 hipError_t launch_fgemm(int dtype, const FGemmArgs& a, int epi, hipStream_t st);   // split iff a.xlo
+int fgemm_mgroup(int epi, int MT);
 hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int batch, hipStream_t st);
 hipError_t launch_combine(int dtype, const CombineArgs& a, int M, hipStream_t st);
 hipError_t launch_argmax(const ArgmaxArgs& a, hipStream_t st);

@@ -121,228 +121,286 @@ __global__ __launch_bounds__(256) void k_assemble(AssembleArgs a) {
 // ---------------------------------------------------------------------------
 // Fused skinny weight-streaming GEMM
 //
-//   Y[m][n] = r_m * sum_k W[n][k] X[m][k]  +  sum_j B[n][j] u[m][j],
-//   u[m][j] = s * r_m * sum_k A[j][k] X[m][k]          (LoRA, adapter on)
+//   Y[m][n] = r_m * ( sum_k W[n][k] X[m][k]  +  s * sum_j B[n][j] u[m][j] ),
+//   u[m][j] = sum_k A[j][k] X[m][k]                    (LoRA, adapter on)
 //
-// A work-group owns one 16-row tile of W; its NW waves take the tile's
-// fragments round-robin, so every weight fragment is read once, as one
-// contiguous 1 KiB wavefront load, and feeds MG m-tiles of MFMA (twice when the
-// operand is carried as bf16 value + residual).  The LoRA shrink runs on the
-// same operand fragments with the A tiles; after the cross-wave reduction the
-// expand is a 16x16x16 MFMA whose B operand is the reduced u.  r_m is 1/rms of
-// row m from the producer's sum-of-squares partials (1 when n_sq = 0).
+// which is the LoRA-adapted projection of the normalised row r_m * X[m] (the
+// RMSNorm gain is already inside X; r_m is 1/rms of row m from the producer's
+// sum-of-squares partials, 1 when n_sq = 0).
+//
+// A work-group owns one 16-row tile of W (and, with split-K, one of `ksplit`
+// slices of K); its NW waves take the tile's fragments round-robin, so every
+// weight fragment is read once, as one contiguous 1 KiB wavefront load, and
+// feeds MG m-tiles of MFMA (twice when the operand is carried as bf16 value +
+// residual).  Each batch of loads (W, X and the LoRA A fragments) is issued
+// before its MFMAs.  The LoRA shrink runs on the same operand fragments; each
+// wave applies the expand to its own partial u (16x16x16 MFMA, u as bf16
+// value + residual) before the single cross-wave reduction, which is valid
+// because the expand is linear.  With split-K the slices write partial tiles;
+// the last slice to arrive (device-scope counter) sums them in slice order and
+// runs the epilogue.
 // ---------------------------------------------------------------------------
 template <int EPI> struct FG {
-    // waves per work-group: enough that each wave issues all its fragment loads at once
+    // waves per work-group
     static constexpr int NW = (EPI == EPI_ARGMAX || EPI == EPI_SWIGLU) ? 4 : 8;
     static constexpr int NSRC = (EPI == EPI_SWIGLU) ? 2 : 1;      // LoRA shrink sources
-    static constexpr bool LORA = EPI != EPI_ARGMAX;
-    // shrink accumulators per source (register budget of 8-wave groups)
-    static constexpr int KU = (EPI == EPI_RESID) ? 4 : 8 / NSRC;
-    // fragments in flight per wave and batch
-    template <int MG> static constexpr int unroll() { return MG >= 4 ? 2 : (EPI == EPI_STORE ? 6 : 4); }
+    // fragments per wave and load batch: about 112 VGPRs of loads in flight
+    template <typename T, int MG, bool SPLIT, int LRT>
+    static constexpr int unroll() {
+        constexpr int per = 4 + 4 * MG * (SPLIT ? 2 : 1) + 4 * NSRC * LRT;
+        constexpr int u = 112 / per;
+        return u < 1 ? 1 : (u > 6 ? 6 : u);
+    }
 };
 
-template <typename T, int EPI, int MG, bool SPLIT>
+// acc += A(4 k per lane) * p, with p carried as bf16 value + bf16 residual
+__device__ __forceinline__ void mma_k4_split(f32x4& acc, const uint2& a, const f32x4& p) {
+    f32x4 h, l;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        h[e] = (float)(bf16)p[e];
+        l[e] = p[e] - h[e];
+    }
+    mma_k4(acc, a, h);
+    mma_k4(acc, a, l);
+}
+__device__ __forceinline__ void mma_k4_split(f32x4& acc, const uint4& a, const f32x4& p) { mma_k4(acc, a, p); }
+
+template <typename T, int EPI, int MG, bool SPLIT, int LRT>
 __global__ __launch_bounds__(FG<EPI>::NW * 64) void k_fgemm(FGemmArgs a) {
     constexpr int NW = FG<EPI>::NW;
     constexpr int NSRC = FG<EPI>::NSRC;
-    constexpr int KU = FG<EPI>::KU;
-    constexpr bool LORA_OK = FG<EPI>::LORA;
-    constexpr int UNR = FG<EPI>::template unroll<MG>();
+    constexpr int UNR = FG<EPI>::template unroll<T, MG, SPLIT, LRT>();
+    constexpr int NROW = MG * 16;
     typedef typename K4<T>::raw braw;
     __shared__ f32x4 s_red[NW][MG][WAVE];
     __shared__ float s_tile[MG][16][17];
-    __shared__ float s_u[16][MG * 16 + 1];
-    __shared__ float s_rm[MG * 16];
+    __shared__ float s_rm[NROW];
+    __shared__ float s_sq[NW * 64];
+    __shared__ int s_last;
 
     const int lane = threadIdx.x % WAVE;
     const int wid = threadIdx.x / WAVE;
     const int lrow = lane % 16, lgrp = lane / 16;
-    const int tile = blockIdx.x;
+    const int S = a.ksplit;
+    const int tile = blockIdx.x % a.n_tiles;
+    const int ks = blockIdx.x / a.n_tiles;
     const int kb = a.kb;
-    const bool lora = LORA_OK && a.lora;
-    const int rt = lora ? a.rt : 0;
+    const int kbs = ceil_div(kb, S);
+    const int f_lo = ks * kbs, f_hi = min(kb, f_lo + kbs);
     const uint4* wt = a.w + (size_t)tile * kb * WAVE;
-    const uint4* la0 = a.la[0];
-    const uint4* la1 = a.la[1];
+    const uint4* la[NSRC];
+    la[0] = a.la[0];
+    if (NSRC > 1) la[NSRC - 1] = a.la[1];
     if (a.lora_mode == LORA_BY_TILE)
-        la0 = tile < a.tile_split0 ? a.la[0] : (tile < a.tile_split1 ? a.la[1] : a.la[2]);
+        la[0] = tile < a.tile_split0 ? a.la[0] : (tile < a.tile_split1 ? a.la[1] : a.la[2]);
+    // LoRA expand blocks of this tile (lane: row lrow, r = 16 t + 4 lgrp + e),
+    // scaled by s; for SwiGLU tiles rows 0-7 take source 0 (gate), 8-15 source 1 (up)
+    braw bv[LRT > 0 ? LRT : 1];
 
     for (int mg0 = 0; mg0 < a.MT; mg0 += MG) {
         const int mgn = min(MG, a.MT - mg0);
-        // row sums of squares for r_m: every thread loads a slice of the partials
-        // now and the sum is finished after the weight loop, off the critical path
-        constexpr int NROW = MG * 16;
-        constexpr int NSLICE = NW * 64 / NROW;
-        const int sq_row = threadIdx.x % NROW, sq_slice = threadIdx.x / NROW;
-        float sq_part = 0.f;
-        {
-            const int m = mg0 * 16 + sq_row;
-            if (a.n_sq > 0 && m < a.M) {
-#pragma unroll 8
-                for (int p = sq_slice; p < a.n_sq; p += NSLICE) sq_part += a.sq[(size_t)p * a.sq_stride + m];
-            }
-        }
         f32x4 acc[MG];
-        f32x4 uacc[NSRC][KU];
+        f32x4 uacc[NSRC][LRT > 0 ? LRT * MG : 1];
 #pragma unroll
         for (int i = 0; i < MG; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < NSRC; ++s)
+        for (int sc = 0; sc < NSRC; ++sc)
 #pragma unroll
-            for (int i = 0; i < KU; ++i) uacc[s][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int i = 0; i < LRT * MG; ++i) uacc[sc][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-        for (int base = wid; base < kb; base += NW * UNR) {
-            uint4 wv[UNR];
-            uint4 xh[UNR][MG];
-            uint4 xl[UNR][MG];
+        // one batch of fragment loads: W, the operand (value and residual) and
+        // the LoRA A fragments of fragments base + NW*u
+        uint4 wv[UNR];
+        uint4 xh[UNR][MG];
+        uint4 xl[UNR][MG];
+        uint4 av[UNR][NSRC][LRT > 0 ? LRT : 1];
+        auto issue = [&](int base) {
 #pragma unroll
             for (int u = 0; u < UNR; ++u) {
                 const int f = base + NW * u;
-                wv[u] = uint4{0, 0, 0, 0};
+                const bool fl = f < f_hi;
+                const int fc = fl ? f : f_lo;               // always a valid fragment
+                wv[u] = wt[(size_t)fc * WAVE + lane];
 #pragma unroll
-                for (int mt = 0; mt < MG; ++mt) { xh[u][mt] = uint4{0, 0, 0, 0}; xl[u][mt] = uint4{0, 0, 0, 0}; }
-                if (f < kb) {
-                    wv[u] = wt[(size_t)f * WAVE + lane];
-#pragma unroll
-                    for (int mt = 0; mt < MG; ++mt) {
-                        if (mt < mgn && (mg0 + mt) * 16 + lrow < a.M) {
-                            const size_t xi = ((size_t)f * a.MT + mg0 + mt) * WAVE + lane;
-                            xh[u][mt] = a.xhi[xi];
-                            if (SPLIT) xl[u][mt] = a.xlo[xi];
-                        }
+                for (int mt = 0; mt < MG; ++mt) {
+                    xh[u][mt] = uint4{0, 0, 0, 0};
+                    xl[u][mt] = uint4{0, 0, 0, 0};
+                    if (fl && mt < mgn && (mg0 + mt) * 16 + lrow < a.M) {
+                        const size_t xi = ((size_t)f * a.MT + mg0 + mt) * WAVE + lane;
+                        xh[u][mt] = a.xhi[xi];
+                        if (SPLIT) xl[u][mt] = a.xlo[xi];
                     }
                 }
+#pragma unroll
+                for (int sc = 0; sc < NSRC; ++sc)
+#pragma unroll
+                    for (int t = 0; t < LRT; ++t) av[u][sc][t] = la[sc][((size_t)t * kb + fc) * WAVE + lane];
             }
+        };
+        auto compute = [&](int base) {
 #pragma unroll
             for (int u = 0; u < UNR; ++u) {
-                const int f = base + NW * u;
-                if (f >= kb) continue;
+                if (base + NW * u >= f_hi) continue;
 #pragma unroll
                 for (int mt = 0; mt < MG; ++mt) {
                     mma_frag<T>(acc[mt], wv[u], xh[u][mt]);
                     if (SPLIT) mma_frag<T>(acc[mt], wv[u], xl[u][mt]);
                 }
-                if (LORA_OK && rt > 0) {
 #pragma unroll
-                    for (int s = 0; s < NSRC; ++s) {
-                        const uint4* la = s == 0 ? la0 : la1;
+                for (int sc = 0; sc < NSRC; ++sc)
 #pragma unroll
-                        for (int t = 0; t < MAX_RT; ++t) {
-                            if (t >= rt) break;
-                            const uint4 av = la[((size_t)t * kb + f) * WAVE + lane];
+                    for (int t = 0; t < LRT; ++t)
 #pragma unroll
-                            for (int mt = 0; mt < MG; ++mt) {
-                                if (t * MG + mt < KU) {
-                                    mma_frag<T>(uacc[s][t * MG + mt], av, xh[u][mt]);
-                                    if (SPLIT) mma_frag<T>(uacc[s][t * MG + mt], av, xl[u][mt]);
-                                }
-                            }
+                        for (int mt = 0; mt < MG; ++mt) {
+                            mma_frag<T>(uacc[sc][t * MG + mt], av[u][sc][t], xh[u][mt]);
+                            if (SPLIT) mma_frag<T>(uacc[sc][t * MG + mt], av[u][sc][t], xl[u][mt]);
                         }
-                    }
-                }
             }
+        };
+        int base = f_lo + wid;
+        if (base < f_hi) issue(base);
+#pragma unroll
+        for (int t = 0; t < LRT; ++t)
+            __builtin_memcpy(&bv[t], (const T*)a.lb + (((size_t)tile * LRT + t) * WAVE + lane) * 4, sizeof(braw));
+
+        // requested after the first weight batch so that they do not delay it:
+        // row sums of squares for r_m (thread: row sq_row, partials sq_slice +
+        // NSLICE*i), the residual epilogue's x slice and next-norm gains
+        constexpr int NSLICE = NW * 64 / NROW;
+        constexpr int SQN = 8;
+        const int sq_row = threadIdx.x % NROW, sq_slice = threadIdx.x / NROW;
+        const int sq_m = mg0 * 16 + sq_row;
+        const bool sq_live = a.n_sq > 0 && sq_m < a.M;
+        float sqv[SQN];
+        if (a.n_sq > 0) {
+            // unconditional loads from clamped, valid indices; masked when summed
+            const int mc = min(sq_m, a.M - 1);
+#pragma unroll
+            for (int i = 0; i < SQN; ++i) sqv[i] = a.sq[(size_t)min(sq_slice + NSLICE * i, a.n_sq - 1) * a.sq_stride + mc];
+        }
+        float4 xr[4];
+        typedef T __attribute__((ext_vector_type(16))) t16;
+        t16 gq;
+        const int em = mg0 * 16 + threadIdx.x;
+        const bool e_live = EPI == EPI_RESID && threadIdx.x < mgn * 16 && em < a.M;
+        if (e_live) {
+            const float4* xs = (const float4*)(a.x + (size_t)em * a.ldx + tile * 16);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) xr[i] = xs[i];
+            gq = *(const t16*)((const T*)a.gnext + tile * 16);
         }
 
-        // finish r_m = rsqrt(mean(x^2) + eps) (fixed summation order)
-        ((float*)s_red)[threadIdx.x] = sq_part;
-        __syncthreads();
-        if (threadIdx.x < NROW) {
-            float s = 0.f;
-            for (int sl = 0; sl < NSLICE; ++sl) s += ((float*)s_red)[sl * NROW + threadIdx.x];
-            s_rm[threadIdx.x] = a.n_sq > 0 ? rsqrtf(s / (float)a.norm_dim + a.eps) : 1.f;
+        while (base < f_hi) {
+            compute(base);
+            base += NW * UNR;
+            if (base < f_hi) issue(base);
         }
-        __syncthreads();
-        // cross-wave reduction of the base tile (fixed order), scaled by r_m
+        float sq_part = 0.f;
+        if (sq_live) {
+#pragma unroll
+            for (int i = 0; i < SQN; ++i)
+                if (sq_slice + NSLICE * i < a.n_sq) sq_part += sqv[i];
+        }
+        if (sq_live)
+            for (int pidx = sq_slice + NSLICE * SQN; pidx < a.n_sq; pidx += NSLICE)
+                sq_part += a.sq[(size_t)pidx * a.sq_stride + sq_m];
+
+        // this wave's LoRA expand: acc += s * B u_wave
+#pragma unroll
+        for (int sc = 0; sc < NSRC; ++sc)
+#pragma unroll
+            for (int t = 0; t < LRT; ++t) {
+                braw b = bv[t];
+                if (EPI == EPI_SWIGLU && ((lrow < 8) != (sc == 0))) b = braw{};
+#pragma unroll
+                for (int mt = 0; mt < MG; ++mt) mma_k4_split(acc[mt], b, uacc[sc][t * MG + mt] * a.scale);
+            }
+
+        // finish r_m = rsqrt(mean(x^2) + eps) (fixed summation order)
+        s_sq[threadIdx.x] = sq_part;
 #pragma unroll
         for (int mt = 0; mt < MG; ++mt) s_red[wid][mt][lane] = acc[mt];
         __syncthreads();
+        if (threadIdx.x < NROW) {
+            float sm = 0.f;
+            for (int sl = 0; sl < NSLICE; ++sl) sm += s_sq[sl * NROW + threadIdx.x];
+            s_rm[threadIdx.x] = a.n_sq > 0 ? rsqrtf(sm / (float)a.norm_dim + a.eps) : 1.f;
+        }
+        // cross-wave reduction of the tile (fixed order)
         for (int idx = threadIdx.x; idx < MG * WAVE * 4; idx += blockDim.x) {
             const int mt = idx / (WAVE * 4), ln = (idx / 4) % WAVE, e = idx % 4;
             float v = 0.f;
 #pragma unroll
             for (int w = 0; w < NW; ++w) v += s_red[w][mt][ln][e];
-            s_tile[mt][(ln / 16) * 4 + e][ln % 16] = v * s_rm[mt * 16 + ln % 16];
+            s_tile[mt][(ln / 16) * 4 + e][ln % 16] = v;
         }
         __syncthreads();
 
-        // LoRA expand: B (16 rows of the tile) times u = s * r_m * (A x)
-        if (lora) {
-            f32x4 eacc[MG];
-#pragma unroll
-            for (int i = 0; i < MG; ++i) eacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int s = 0; s < NSRC; ++s) {
-#pragma unroll
-                for (int t = 0; t < MAX_RT; ++t) {
-                    if (t >= rt) break;
-#pragma unroll
-                    for (int mt = 0; mt < MG; ++mt)
-                        s_red[wid][mt][lane] = (t * MG + mt < KU) ? uacc[s][t * MG + mt] : f32x4{0.f, 0.f, 0.f, 0.f};
-                    __syncthreads();
-                    for (int idx = threadIdx.x; idx < MG * WAVE * 4; idx += blockDim.x) {
-                        const int mt = idx / (WAVE * 4), ln = (idx / 4) % WAVE, e = idx % 4;
-                        float v = 0.f;
-#pragma unroll
-                        for (int w = 0; w < NW; ++w) v += s_red[w][mt][ln][e];
-                        s_u[(ln / 16) * 4 + e][mt * 16 + ln % 16] = v * a.scale * s_rm[mt * 16 + ln % 16];
-                    }
-                    __syncthreads();
-                    if (wid == 0) {
-                        braw bv;
-                        const T* lbp = (const T*)a.lb + (((size_t)tile * a.rt + t) * WAVE + lane) * 4;
-                        __builtin_memcpy(&bv, lbp, sizeof(braw));
-                        if (EPI == EPI_SWIGLU) {
-                            // rows 0-7 of the tile belong to source 0 (gate), rows 8-15 to source 1 (up)
-                            if ((lrow < 8) != (s == 0)) bv = braw{};
-                        }
-#pragma unroll
-                        for (int mt = 0; mt < MG; ++mt) {
-                            f32x4 p;
-#pragma unroll
-                            for (int e = 0; e < 4; ++e) p[e] = s_u[lgrp * 4 + e][mt * 16 + lrow];
-                            mma_k4(eacc[mt], bv, p);
-                        }
-                    }
-                    __syncthreads();
-                }
+        if (S > 1) {
+            // split-K: publish this slice's tile with device-scope (L2-coherent
+            // across XCDs) atomic stores, wait for their completion, then count
+            // the arrival; the last slice reads the partials with system-scope
+            // loads (past any stale L2 line), sums them in slice order and
+            // continues with the epilogue.  No cache write-back is needed.
+            float* pp = a.part + (size_t)tile * S * (MG * 256);
+            for (int idx = threadIdx.x; idx < MG * 256; idx += blockDim.x) {
+                const int mt = idx / 256, n = (idx / 16) % 16, ml = idx % 16;
+                __hip_atomic_store(pp + (size_t)ks * (MG * 256) + idx, s_tile[mt][n][ml], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
             }
-            if (wid == 0) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            if (threadIdx.x == 0)
+                s_last = __hip_atomic_fetch_add(a.cnt + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                         (unsigned)(S - 1);
+            __syncthreads();
+            if (!s_last) return;
+            for (int idx = threadIdx.x; idx < MG * 256; idx += blockDim.x) {
+                const int mt = idx / 256, n = (idx / 16) % 16, ml = idx % 16;
+                float pv[KSPLIT_MAX];
 #pragma unroll
-                for (int mt = 0; mt < MG; ++mt)
+                for (int k2 = 0; k2 < KSPLIT_MAX; ++k2)
+                    pv[k2] = k2 < S ? __hip_atomic_load(pp + (size_t)k2 * (MG * 256) + idx, __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_SYSTEM)
+                                    : 0.f;
+                float v = 0.f;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) s_tile[mt][lgrp * 4 + e][lrow] += eacc[mt][e];
+                for (int k2 = 0; k2 < KSPLIT_MAX; ++k2) v += pv[k2];
+                s_tile[mt][n][ml] = v;
             }
+            if (threadIdx.x == 0) __hip_atomic_store(a.cnt + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __syncthreads();
         }
 
-        // epilogues
+        // epilogues (r_m applied here)
         if (EPI == EPI_STORE) {
             for (int idx = threadIdx.x; idx < mgn * 256; idx += blockDim.x) {
                 const int mt = idx / 256, n = idx % 16, ml = (idx / 16) % 16;
                 const int m = (mg0 + mt) * 16 + ml;
-                if (m < a.M) a.out[(size_t)m * a.ldo + tile * 16 + n] = s_tile[mt][n][ml];
+                if (m < a.M) a.out[(size_t)m * a.ldo + tile * 16 + n] = s_tile[mt][n][ml] * s_rm[mt * 16 + ml];
             }
         } else if (EPI == EPI_RESID) {
             // x += tile; next operand x * g_next; per-row sum of squares over the 16 columns
-            const T* gn = (const T*)a.gnext;
-            if (threadIdx.x < mgn * 16) {
+            if (e_live) {
                 const int mt = threadIdx.x / 16, ml = threadIdx.x % 16;
-                const int m = (mg0 + mt) * 16 + ml;
-                if (m < a.M) {
-                    float ss = 0.f;
-                    float* xr = a.x + (size_t)m * a.ldx + tile * 16;
+                const int m = em;
+                const float rm = s_rm[threadIdx.x];
+                float ss = 0.f;
+                float xv[16];
 #pragma unroll
-                    for (int n = 0; n < 16; ++n) {
-                        const float xv = xr[n] + s_tile[mt][n][ml];
-                        xr[n] = xv;
-                        ss += xv * xv;
-                        put_operand<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 16 + n, a.n_MT),
-                                       xv * to_f32(gn[tile * 16 + n]));
-                    }
-                    a.sq_out[(size_t)tile * a.sq_stride + m] = ss;
+                for (int n = 0; n < 16; ++n) {
+                    xv[n] = xr[n / 4][n % 4] + s_tile[mt][n][ml] * rm;
+                    ss += xv[n] * xv[n];
                 }
+                float4* xd = (float4*)(a.x + (size_t)m * a.ldx + tile * 16);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) xd[i] = float4{xv[4 * i], xv[4 * i + 1], xv[4 * i + 2], xv[4 * i + 3]};
+#pragma unroll
+                for (int n = 0; n < 16; ++n)
+                    put_operand<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 16 + n, a.n_MT),
+                                   xv[n] * to_f32(gq[n]));
+                a.sq_out[(size_t)tile * a.sq_stride + m] = ss;
             }
         } else if (EPI == EPI_SWIGLU) {
             // tile rows 0-7: gate rows 8*tile..; rows 8-15: the matching up rows
@@ -350,8 +408,9 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64) void k_fgemm(FGemmArgs a) {
                 const int mt = idx / 128, c = idx % 8, ml = (idx / 8) % 16;
                 const int m = (mg0 + mt) * 16 + ml;
                 if (m < a.M) {
-                    const float gt = s_tile[mt][c][ml];
-                    const float up = s_tile[mt][c + 8][ml];
+                    const float rm = s_rm[mt * 16 + ml];
+                    const float gt = s_tile[mt][c][ml] * rm;
+                    const float up = s_tile[mt][c + 8][ml] * rm;
                     put_operand<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 8 + c, a.n_MT),
                                    gt / (1.f + __expf(-gt)) * up);
                 }
@@ -361,11 +420,12 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64) void k_fgemm(FGemmArgs a) {
                 const int mt = idx / 16, ml = idx % 16;
                 const int m = (mg0 + mt) * 16 + ml;
                 if (m >= a.M) continue;
+                const float rm = s_rm[idx];
                 float best = -INFINITY;
                 int bi = 0x7fffffff;
                 for (int n = 0; n < 16; ++n) {
                     const int v = tile * 16 + n;
-                    const float val = s_tile[mt][n][ml];
+                    const float val = s_tile[mt][n][ml] * rm;
                     if (a.logits) a.logits[(size_t)m * a.ldo + v] = val;
                     if (v == a.exclude) continue;
                     if (val > best) { best = val; bi = v; }   // ascending v: first max wins ties
@@ -1006,40 +1066,59 @@ __global__ void k_fill_u32(uint32_t* p, size_t n, uint32_t v) {
 // ---------------------------------------------------------------------------
 // Host-side launchers
 // ---------------------------------------------------------------------------
+template <typename T, bool SPLIT, int EPI, int MG>
+static hipError_t launch_fgemm_lrt(const FGemmArgs& a, int lrt, hipStream_t st) {
+    const dim3 grid(a.n_tiles * a.ksplit), block(FG<EPI>::NW * 64);
+    switch (lrt) {
+        case 0: hipLaunchKernelGGL((k_fgemm<T, EPI, MG, SPLIT, 0>), grid, block, 0, st, a); break;
+        case 1: hipLaunchKernelGGL((k_fgemm<T, EPI, MG, SPLIT, 1>), grid, block, 0, st, a); break;
+        case 2: hipLaunchKernelGGL((k_fgemm<T, EPI, MG, SPLIT, 2>), grid, block, 0, st, a); break;
+        case 3: hipLaunchKernelGGL((k_fgemm<T, EPI, MG, SPLIT, 3>), grid, block, 0, st, a); break;
+        case 4: hipLaunchKernelGGL((k_fgemm<T, EPI, MG, SPLIT, 4>), grid, block, 0, st, a); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
 template <typename T, bool SPLIT>
-static hipError_t launch_fgemm_t(const FGemmArgs& a, int epi, hipStream_t st) {
-    // m-tiles per pass over the weights: enough for the rows, bounded by the
-    // register budget of the LoRA shrink accumulators and by LDS for 8-wave groups
-    int cap = 8;
-    if (epi == EPI_RESID) cap = 2;          // register budget of the long-K residual GEMMs
-    else if (epi != EPI_ARGMAX) cap = 4;    // LDS of the 8-wave reduction
-    if (a.lora && epi != EPI_ARGMAX) {
-        const int ku = (epi == EPI_SWIGLU || epi == EPI_RESID) ? 4 : 8;
-        cap = std::min(cap, std::max(1, ku / std::max(a.rt, 1)));
-    }
-    int mg = 1;
-    while (mg < a.MT && mg < cap) mg *= 2;
-    if (mg > cap) mg /= 2;
-    const dim3 grid(a.n_tiles);
-#define PBD_FG_CASE(E, G)                                                                            \
-    if (epi == E && mg == G) {                                                                       \
-        hipLaunchKernelGGL((k_fgemm<T, E, G, SPLIT>), grid, dim3(FG<E>::NW * 64), 0, st, a);          \
-        return hipGetLastError();                                                                    \
-    }
-#define PBD_FG_EPI(E) PBD_FG_CASE(E, 1) PBD_FG_CASE(E, 2) PBD_FG_CASE(E, 4) PBD_FG_CASE(E, 8)
+static hipError_t launch_fgemm_t(const FGemmArgs& a, int epi, int mg, hipStream_t st) {
+    const int lrt = (a.lora && epi != EPI_ARGMAX) ? a.rt : 0;
+#define PBD_FG_CASE(E, G) \
+    if (epi == E && mg == G) return launch_fgemm_lrt<T, SPLIT, E, G>(a, lrt, st);
     PBD_FG_CASE(EPI_STORE, 1) PBD_FG_CASE(EPI_STORE, 2) PBD_FG_CASE(EPI_STORE, 4)
     PBD_FG_CASE(EPI_RESID, 1) PBD_FG_CASE(EPI_RESID, 2)
     PBD_FG_CASE(EPI_SWIGLU, 1) PBD_FG_CASE(EPI_SWIGLU, 2) PBD_FG_CASE(EPI_SWIGLU, 4)
-    PBD_FG_EPI(EPI_ARGMAX)
-#undef PBD_FG_EPI
 #undef PBD_FG_CASE
+    if (epi == EPI_ARGMAX) {
+        const dim3 grid(a.n_tiles * a.ksplit), block(FG<EPI_ARGMAX>::NW * 64);
+        switch (mg) {
+            case 1: hipLaunchKernelGGL((k_fgemm<T, EPI_ARGMAX, 1, SPLIT, 0>), grid, block, 0, st, a); break;
+            case 2: hipLaunchKernelGGL((k_fgemm<T, EPI_ARGMAX, 2, SPLIT, 0>), grid, block, 0, st, a); break;
+            case 4: hipLaunchKernelGGL((k_fgemm<T, EPI_ARGMAX, 4, SPLIT, 0>), grid, block, 0, st, a); break;
+            case 8: hipLaunchKernelGGL((k_fgemm<T, EPI_ARGMAX, 8, SPLIT, 0>), grid, block, 0, st, a); break;
+            default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    }
     return hipErrorInvalidValue;
 }
 
+// m-tiles per pass over the weights: enough for the rows, bounded by the
+// register budget (residual GEMMs hold the x slice) and by LDS
+int fgemm_mgroup(int epi, int MT) {
+    const int cap = epi == EPI_ARGMAX ? 8 : (epi == EPI_RESID ? 2 : 4);
+    int mg = 1;
+    while (mg < MT && mg < cap) mg *= 2;
+    return mg;
+}
+
 hipError_t launch_fgemm(int dtype, const FGemmArgs& a, int epi, hipStream_t st) {
+    if (a.ksplit < 1 || a.ksplit > KSPLIT_MAX || (a.ksplit > 1 && (!a.part || !a.cnt || a.MT > fgemm_mgroup(epi, a.MT))))
+        return hipErrorInvalidValue;
+    const int mg = fgemm_mgroup(epi, a.MT);
     if (dtype == PBD_DTYPE_BF16)
-        return a.xlo ? launch_fgemm_t<bf16, true>(a, epi, st) : launch_fgemm_t<bf16, false>(a, epi, st);
-    return launch_fgemm_t<float, false>(a, epi, st);
+        return a.xlo ? launch_fgemm_t<bf16, true>(a, epi, mg, st) : launch_fgemm_t<bf16, false>(a, epi, mg, st);
+    return launch_fgemm_t<float, false>(a, epi, mg, st);
 }
 
 bool lmhead_fits(int kb, int MT) { return kb <= 4 * LM_FPW && MT <= 2; }
