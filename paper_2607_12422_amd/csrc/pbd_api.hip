@@ -200,25 +200,29 @@ int hip_fail(pbd_ctx* c, hipError_t e, const char* what) {
         if (_e != hipSuccess) return hip_fail(ctx, _e, what);  \
     } while (0)
 
-hipError_t prof_mark(pbd_ctx* c, hipStream_t st, int kclass, bool begin) {
+// Profiling: the launch's own start and end times, from hipExtLaunchKernel events.
+hipError_t prof_begin(pbd_ctx* c, int kclass) {
     Profiler& p = c->prof;
     if (!p.on) return hipSuccess;
-    if (p.used == p.pool.size()) {
+    while (p.used + 2 > p.pool.size()) {
         hipEvent_t e;
         hipError_t err = hipEventCreate(&e);
         if (err != hipSuccess) return err;
         p.pool.push_back(e);
     }
-    if (begin) p.recs.push_back({kclass, p.used});
-    return hipEventRecord(p.pool[p.used++], st);
+    p.recs.push_back({kclass, p.used});
+    set_launch_events(p.pool[p.used], p.pool[p.used + 1]);
+    p.used += 2;
+    return hipSuccess;
 }
 
-// Launch `expr` bracketed by profiling events of class `kc`.
+// Launch `expr` (one kernel) with its timing events when profiling is on.
 #define PBD_TIMED(ctx, st, kc, expr, what)                                   \
     do {                                                                     \
-        PBD_HIP(ctx, prof_mark(ctx, st, kc, true), "profile event");         \
-        PBD_HIP(ctx, (expr), what);                                          \
-        PBD_HIP(ctx, prof_mark(ctx, st, kc, false), "profile event");        \
+        PBD_HIP(ctx, prof_begin(ctx, kc), "profile event");                  \
+        hipError_t _le = (expr);                                             \
+        set_launch_events(nullptr, nullptr);                                 \
+        PBD_HIP(ctx, _le, what);                                             \
     } while (0)
 
 struct PassReq {
@@ -333,6 +337,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.gnext = l + 1 < y.L ? pk + y.lay[l + 1].attn_norm : pk + y.p_final_norm;
         g.nx_hi = hi(y.w_xa); g.nx_lo = lo(y.w_xa); g.n_MT = MT; g.sq_out = sq_a;
         split_k(g);
+        if (l + 1 < y.L)
         PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "down gemm");
     }
 

@@ -117,6 +117,12 @@ __device__ __host__ __forceinline__ size_t vblock_elem(int key, int dim) {
     return ((size_t)dt * 64 + (size_t)(g * 16 + dim % 16)) * 4 + e;
 }
 
+// Work-group barrier for LDS traffic: waits for this wave's LDS operations
+// only, not (as __syncthreads does) for its outstanding global loads, so loads
+// issued ahead of time stay in flight across it.  Global data shared through
+// memory needs its own wait.
+__device__ __forceinline__ void lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // ---------------------------------------------------------------------------
 // Wave reductions
 // ---------------------------------------------------------------------------

@@ -146,6 +146,7 @@ struct PackExpandArgs {
 hipError_t launch_assemble(int dtype, const AssembleArgs& a, int batch, hipStream_t st);
 hipError_t launch_fgemm(int dtype, const FGemmArgs& a, int epi, hipStream_t st);   // split iff a.xlo
 int fgemm_mgroup(int epi, int MT);
+int fgemm_threads(int epi);         // work-group size of the GEMM with epilogue epi
 hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int batch, hipStream_t st);
 hipError_t launch_combine(int dtype, const CombineArgs& a, int M, hipStream_t st);
 hipError_t launch_argmax(const ArgmaxArgs& a, hipStream_t st);
@@ -156,6 +157,8 @@ hipError_t launch_accept(const AcceptArgs& a, hipStream_t st);
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st);
 hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st);
 hipError_t launch_fill_u32(void* p, size_t n_words, uint32_t v, hipStream_t st);
+// profiling: events that the next launch records its start and end into (null: none)
+void set_launch_events(hipEvent_t start, hipEvent_t stop);
 size_t attn_smem_main(int dtype, int head_dim, int qt);
 size_t attn_smem_bytes(int dtype, int head_dim, int qt);
 

@@ -19,11 +19,29 @@
 // of row m, so producers write x * g and sum(x^2) partials, and consumers scale
 // their accumulators by r_m; no standalone normalisation kernel runs.
 #include "pbd_device.h"
+#include <hip/hip_ext.h>
+
 #include "pbd_kernels.h"
 
 #include <algorithm>
 
 namespace pbd {
+
+// Optional timing events attached to the next launch (profiling aid): with
+// events set, kernels are launched with hipExtLaunchKernel, whose events carry
+// the dispatch's own start and end times.
+static thread_local hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
+void set_launch_events(hipEvent_t start, hipEvent_t stop) {
+    g_ev_start = start;
+    g_ev_stop = stop;
+}
+#define PBD_LAUNCH(KERNEL, GRID, BLOCK, SHMEM, ST, ...)                                              \
+    do {                                                                                            \
+        if (g_ev_start)                                                                             \
+            hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, ST, g_ev_start, g_ev_stop, 0, __VA_ARGS__); \
+        else                                                                                        \
+            hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, ST, __VA_ARGS__);                        \
+    } while (0)
 
 static __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
@@ -144,6 +162,8 @@ template <int EPI> struct FG {
     // waves per work-group
     static constexpr int NW = (EPI == EPI_ARGMAX || EPI == EPI_SWIGLU) ? 4 : 8;
     static constexpr int NSRC = (EPI == EPI_SWIGLU) ? 2 : 1;      // LoRA shrink sources
+    // work-groups per CU the register budget must allow (SwiGLU: 384+ tiles on 256 CUs)
+    static constexpr int MINB = (EPI == EPI_SWIGLU) ? 2 : 1;
     // fragments per wave and load batch: about 112 VGPRs of loads in flight
     template <typename T, int MG, bool SPLIT, int LRT>
     static constexpr int unroll() {
@@ -167,7 +187,7 @@ __device__ __forceinline__ void mma_k4_split(f32x4& acc, const uint2& a, const f
 __device__ __forceinline__ void mma_k4_split(f32x4& acc, const uint4& a, const f32x4& p) { mma_k4(acc, a, p); }
 
 template <typename T, int EPI, int MG, bool SPLIT, int LRT>
-__global__ __launch_bounds__(FG<EPI>::NW * 64) void k_fgemm(FGemmArgs a) {
+__global__ __launch_bounds__(FG<EPI>::NW * 64, FG<EPI>::MINB) void k_fgemm(FGemmArgs a) {
     constexpr int NW = FG<EPI>::NW;
     constexpr int NSRC = FG<EPI>::NSRC;
     constexpr int UNR = FG<EPI>::template unroll<T, MG, SPLIT, LRT>();
@@ -321,7 +341,7 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64) void k_fgemm(FGemmArgs a) {
         s_sq[threadIdx.x] = sq_part;
 #pragma unroll
         for (int mt = 0; mt < MG; ++mt) s_red[wid][mt][lane] = acc[mt];
-        __syncthreads();
+        lds_sync();
         if (threadIdx.x < NROW) {
             float sm = 0.f;
             for (int sl = 0; sl < NSLICE; ++sl) sm += s_sq[sl * NROW + threadIdx.x];
@@ -335,7 +355,7 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64) void k_fgemm(FGemmArgs a) {
             for (int w = 0; w < NW; ++w) v += s_red[w][mt][ln][e];
             s_tile[mt][(ln / 16) * 4 + e][ln % 16] = v;
         }
-        __syncthreads();
+        lds_sync();
 
         if (S > 1) {
             // split-K: publish this slice's tile with device-scope (L2-coherent
@@ -350,11 +370,11 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64) void k_fgemm(FGemmArgs a) {
                                    __HIP_MEMORY_SCOPE_AGENT);
             }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();
+            lds_sync();
             if (threadIdx.x == 0)
                 s_last = __hip_atomic_fetch_add(a.cnt + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
                          (unsigned)(S - 1);
-            __syncthreads();
+            lds_sync();
             if (!s_last) return;
             for (int idx = threadIdx.x; idx < MG * 256; idx += blockDim.x) {
                 const int mt = idx / 256, n = (idx / 16) % 16, ml = idx % 16;
@@ -370,7 +390,7 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64) void k_fgemm(FGemmArgs a) {
                 s_tile[mt][n][ml] = v;
             }
             if (threadIdx.x == 0) __hip_atomic_store(a.cnt + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __syncthreads();
+            lds_sync();
         }
 
         // epilogues (r_m applied here)
@@ -434,7 +454,7 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64) void k_fgemm(FGemmArgs a) {
                 a.arg_idx[(size_t)tile * a.M + m] = bi;
             }
         }
-        __syncthreads();
+        lds_sync();
     }
 }
 
@@ -665,7 +685,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
             rp[i].finish(q_l + q * LDQ, q < QR, gq_lo, gq_hi, a.qk_norm, a.eps, lrow, lo, hi);
         }
     }
-    __syncthreads();
+    lds_sync();
 
     // -- Q^T fragments in registers
     uint4 qf[QT][NDS];
@@ -743,7 +763,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 
     // -- merge the four waves: common max per query row, then a two-round tree
     //    (waves 2,3 -> 0,1, then 1 -> 0) in LDS; wave 0 writes the partial
-    __syncthreads();                                     // LDS operands dead: obuf may alias
+    lds_sync();                                     // LDS operands dead: obuf may alias
     if (lgrp == 0) {
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
@@ -751,7 +771,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
             ml_l[(wid * QROWS + qt * 16 + lrow) * 2 + 1] = l_run[qt];
         }
     }
-    __syncthreads();
+    lds_sync();
     float mx[QT];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
@@ -778,11 +798,11 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 o_acc[dt][qt] += *(const f32x4*)(reg + (qt * 16 + lrow) * LDO + dt * 16 + lgrp * 4);
     };
     if (wid >= 2) put(obuf + (wid - 2) * QROWS * LDO);
-    __syncthreads();
+    lds_sync();
     if (wid < 2) add(obuf + wid * QROWS * LDO);
-    __syncthreads();
+    lds_sync();
     if (wid == 1) put(obuf);
-    __syncthreads();
+    lds_sync();
     if (wid != 0) return;
     add(obuf);
 
@@ -1070,11 +1090,11 @@ template <typename T, bool SPLIT, int EPI, int MG>
 static hipError_t launch_fgemm_lrt(const FGemmArgs& a, int lrt, hipStream_t st) {
     const dim3 grid(a.n_tiles * a.ksplit), block(FG<EPI>::NW * 64);
     switch (lrt) {
-        case 0: hipLaunchKernelGGL((k_fgemm<T, EPI, MG, SPLIT, 0>), grid, block, 0, st, a); break;
-        case 1: hipLaunchKernelGGL((k_fgemm<T, EPI, MG, SPLIT, 1>), grid, block, 0, st, a); break;
-        case 2: hipLaunchKernelGGL((k_fgemm<T, EPI, MG, SPLIT, 2>), grid, block, 0, st, a); break;
-        case 3: hipLaunchKernelGGL((k_fgemm<T, EPI, MG, SPLIT, 3>), grid, block, 0, st, a); break;
-        case 4: hipLaunchKernelGGL((k_fgemm<T, EPI, MG, SPLIT, 4>), grid, block, 0, st, a); break;
+        case 0: PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, 0>), grid, block, 0, st, a); break;
+        case 1: PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, 1>), grid, block, 0, st, a); break;
+        case 2: PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, 2>), grid, block, 0, st, a); break;
+        case 3: PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, 3>), grid, block, 0, st, a); break;
+        case 4: PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, 4>), grid, block, 0, st, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -1092,15 +1112,21 @@ static hipError_t launch_fgemm_t(const FGemmArgs& a, int epi, int mg, hipStream_
     if (epi == EPI_ARGMAX) {
         const dim3 grid(a.n_tiles * a.ksplit), block(FG<EPI_ARGMAX>::NW * 64);
         switch (mg) {
-            case 1: hipLaunchKernelGGL((k_fgemm<T, EPI_ARGMAX, 1, SPLIT, 0>), grid, block, 0, st, a); break;
-            case 2: hipLaunchKernelGGL((k_fgemm<T, EPI_ARGMAX, 2, SPLIT, 0>), grid, block, 0, st, a); break;
-            case 4: hipLaunchKernelGGL((k_fgemm<T, EPI_ARGMAX, 4, SPLIT, 0>), grid, block, 0, st, a); break;
-            case 8: hipLaunchKernelGGL((k_fgemm<T, EPI_ARGMAX, 8, SPLIT, 0>), grid, block, 0, st, a); break;
+            case 1: PBD_LAUNCH((k_fgemm<T, EPI_ARGMAX, 1, SPLIT, 0>), grid, block, 0, st, a); break;
+            case 2: PBD_LAUNCH((k_fgemm<T, EPI_ARGMAX, 2, SPLIT, 0>), grid, block, 0, st, a); break;
+            case 4: PBD_LAUNCH((k_fgemm<T, EPI_ARGMAX, 4, SPLIT, 0>), grid, block, 0, st, a); break;
+            case 8: PBD_LAUNCH((k_fgemm<T, EPI_ARGMAX, 8, SPLIT, 0>), grid, block, 0, st, a); break;
             default: return hipErrorInvalidValue;
         }
         return hipGetLastError();
     }
     return hipErrorInvalidValue;
+}
+
+int fgemm_threads(int epi) {
+    return epi == EPI_STORE ? FG<EPI_STORE>::NW * 64
+         : epi == EPI_RESID ? FG<EPI_RESID>::NW * 64
+         : epi == EPI_SWIGLU ? FG<EPI_SWIGLU>::NW * 64 : FG<EPI_ARGMAX>::NW * 64;
 }
 
 // m-tiles per pass over the weights: enough for the rows, bounded by the
@@ -1125,10 +1151,10 @@ bool lmhead_fits(int kb, int MT) { return kb <= 4 * LM_FPW && MT <= 2; }
 
 hipError_t launch_lmhead(int dtype, const FGemmArgs& a, int grid, hipStream_t st) {
     if (dtype == PBD_DTYPE_BF16) {
-        if (a.xlo) hipLaunchKernelGGL((k_lmhead<bf16, true>), dim3(grid), dim3(256), 0, st, a);
-        else hipLaunchKernelGGL((k_lmhead<bf16, false>), dim3(grid), dim3(256), 0, st, a);
+        if (a.xlo) PBD_LAUNCH((k_lmhead<bf16, true>), dim3(grid), dim3(256), 0, st, a);
+        else PBD_LAUNCH((k_lmhead<bf16, false>), dim3(grid), dim3(256), 0, st, a);
     } else {
-        hipLaunchKernelGGL((k_lmhead<float, false>), dim3(grid), dim3(256), 0, st, a);
+        PBD_LAUNCH((k_lmhead<float, false>), dim3(grid), dim3(256), 0, st, a);
     }
     return hipGetLastError();
 }
@@ -1149,11 +1175,11 @@ size_t attn_smem_bytes(int dtype, int head_dim, int qt) {
 template <typename T, int HD>
 static hipError_t launch_attn_hd(const AttnArgs& a, int qt, dim3 grid, size_t smem, hipStream_t st) {
     switch (qt) {
-        case 1: hipLaunchKernelGGL((k_attn<T, HD, 1>), grid, dim3(256), smem, st, a); break;
-        case 2: hipLaunchKernelGGL((k_attn<T, HD, 2>), grid, dim3(256), smem, st, a); break;
-        case 3: hipLaunchKernelGGL((k_attn<T, HD, 3>), grid, dim3(256), smem, st, a); break;
-        case 4: hipLaunchKernelGGL((k_attn<T, HD, 4>), grid, dim3(256), smem, st, a); break;
-        case 5: hipLaunchKernelGGL((k_attn<T, HD, 5>), grid, dim3(256), smem, st, a); break;
+        case 1: PBD_LAUNCH((k_attn<T, HD, 1>), grid, dim3(256), smem, st, a); break;
+        case 2: PBD_LAUNCH((k_attn<T, HD, 2>), grid, dim3(256), smem, st, a); break;
+        case 3: PBD_LAUNCH((k_attn<T, HD, 3>), grid, dim3(256), smem, st, a); break;
+        case 4: PBD_LAUNCH((k_attn<T, HD, 4>), grid, dim3(256), smem, st, a); break;
+        case 5: PBD_LAUNCH((k_attn<T, HD, 5>), grid, dim3(256), smem, st, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -1174,8 +1200,8 @@ hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int b
 
 #define PBD_DISPATCH(dtype, KERNEL, grid, block, st, args)                                        \
     do {                                                                                          \
-        if ((dtype) == PBD_DTYPE_BF16) hipLaunchKernelGGL(KERNEL<bf16>, grid, block, 0, st, args); \
-        else hipLaunchKernelGGL(KERNEL<float>, grid, block, 0, st, args);                         \
+        if ((dtype) == PBD_DTYPE_BF16) PBD_LAUNCH(KERNEL<bf16>, grid, block, 0, st, args); \
+        else PBD_LAUNCH(KERNEL<float>, grid, block, 0, st, args);                         \
         return hipGetLastError();                                                                 \
     } while (0)
 
@@ -1192,16 +1218,16 @@ hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st
     PBD_DISPATCH(dtype, k_pack_expand, dim3(256), dim3(256), st, a);
 }
 hipError_t launch_argmax(const ArgmaxArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL(k_argmax, dim3(a.M), dim3(256), 0, st, a);
+    PBD_LAUNCH(k_argmax, dim3(a.M), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL(k_accept, dim3((a.B + 63) / 64), dim3(64), 0, st, a);
+    PBD_LAUNCH(k_accept, dim3((a.B + 63) / 64), dim3(64), 0, st, a);
     return hipGetLastError();
 }
 hipError_t launch_fill_u32(void* p, size_t n_words, uint32_t v, hipStream_t st) {
     if (n_words == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_fill_u32, dim3(1024), dim3(256), 0, st, (uint32_t*)p, n_words, v);
+    PBD_LAUNCH(k_fill_u32, dim3(1024), dim3(256), 0, st, (uint32_t*)p, n_words, v);
     return hipGetLastError();
 }
 
