@@ -337,7 +337,6 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.gnext = l + 1 < y.L ? pk + y.lay[l + 1].attn_norm : pk + y.p_final_norm;
         g.nx_hi = hi(y.w_xa); g.nx_lo = lo(y.w_xa); g.n_MT = MT; g.sq_out = sq_a;
         split_k(g);
-        if (l + 1 < y.L)
         PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "down gemm");
     }
 
