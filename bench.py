@@ -47,6 +47,28 @@ def algorithmic_bytes(cfg, batch, prefixes):
     )
 
 
+def counter_traffic(name="k_fgemm_traffic.txt"):
+    """HBM bytes per launch of the projection GEMM from the committed rocprofv3
+    counter summary (FETCH_SIZE and WRITE_SIZE passes, scaled by a plain copy's
+    readings).  None when the summary is missing or was taken on another
+    version of the kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", name)
+    src = os.path.join(ROOT, "paper_2607_12422_amd", "csrc", "pbd_kernels.hip")
+    try:
+        kv = {}
+        for line in open(path):
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        if kv.get("kernel_source_sha256") != digest:
+            return None
+        return float(kv["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(w_, weights, prompts, reps=3):
     """The oracle (float64 NumPy) on the host: one draft + verify + accept at
     the workload's shape for the first sequence, median of `reps`; prefill
@@ -258,7 +280,7 @@ def main():
         ach = gemm_launch_bytes / (g["avg_us"] * 1e-6) / 1e9
         result["roofline"] = {"bound": "hbm", "kernel": "k_fgemm (q/k/v, o, gate/up, down projections; both passes)",
                               "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                              "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None,
+                              "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": counter_traffic(),
                               "bytes_per_launch": round(gemm_launch_bytes), "avg_launch_us": g["avg_us"]}
         lm = prof["lmhead"]
         lm_ach = byt["lmhead"] / (lm["avg_us"] * 1e-6) / 1e9 if lm["launches"] else 0.0

@@ -74,7 +74,7 @@ typedef void* pbd_stream_t;            /* hipStream_t */
 #define PBD_KCLASS_LMHEAD   1          /* tied LM head with fused argmax */
 #define PBD_KCLASS_ATTN     2          /* split-KV attention */
 #define PBD_KCLASS_COMBINE  3          /* split merge + O-projection operand */
-#define PBD_KCLASS_NORM     4          /* RMSNorm / LoRA shrink */
+#define PBD_KCLASS_NORM     4          /* unused: RMSNorm and the LoRA shrink are fused into the GEMMs */
 #define PBD_KCLASS_OTHER    5          /* block assembly, final argmax */
 #define PBD_KCLASS_COUNT    6
 
@@ -211,11 +211,12 @@ int pbd_set_attn_keys_per_split(pbd_ctx* ctx, int32_t keys);
 int pbd_set_operand_precision(pbd_ctx* ctx, int32_t mode);
 
 /*
- * Profiling aid: while enabled, every kernel launch of a pass is bracketed by a
- * pair of HIP events on the call's stream (this adds launch gaps, so time passes
- * with profiling off).  pbd_profile_enable(ctx, on) also discards earlier
+ * Profiling aid: while enabled, every kernel of a pass is launched with a pair
+ * of HIP events attached to its dispatch (hipExtLaunchKernel), which record the
+ * kernel's own start and end on the call's stream.  Use it with direct calls,
+ * not under stream capture.  pbd_profile_enable(ctx, on) also discards earlier
  * records.  pbd_profile_read waits for the last recorded event and returns the
- * summed device time and the launch count of kernel class `kclass`
+ * summed kernel time and the launch count of kernel class `kclass`
  * (PBD_KCLASS_*) since the last enable.
  */
 int pbd_profile_enable(pbd_ctx* ctx, int32_t on);
