@@ -601,11 +601,20 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         }
     };
 
-    // the wave's first prefix key block is requested before the query
-    // preparation, which it does not depend on
-    uint4 kn[NDS];
-    vraw vn[NDT];
-    if (!blk && wid < n_items) load_item(wid, kn, vn);
+    // A wave takes key blocks it, it+4, ... in chunks of CH blocks: the scores
+    // of a chunk are formed first, so the running max and the rescale of the
+    // accumulated output happen once per chunk (not at all for the first one).
+    // The wave's first chunk of prefix blocks is requested before the query
+    // preparation, which it does not depend on.
+    constexpr int CH = 2;
+    uint4 kn[CH][NDS];
+    vraw vn[CH][NDT];
+    auto load_chunk = [&](int it0) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+            if (it0 + 4 * c < n_items) load_item(it0 + 4 * c, kn[c], vn[c]);
+    };
+    if (!blk) load_chunk(wid);
 
     // -- Q rows (and, in the block split, K/V rows): all loads first, then
     //    norm + rotation; wave w, lane group lgrp handles rows 16*i + 4*w + lgrp
@@ -711,54 +720,62 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     }
     const float sl2 = a.scale_log2;
 
-    if (blk && wid < n_items) load_item(wid, kn, vn);
-    for (int it = wid; it < n_items; it += 4) {
-        // rotate: this block's operands, then the next block's request
-        uint4 kf[NDS];
-        vraw vf[NDT];
-#pragma unroll
-        for (int ds = 0; ds < NDS; ++ds) kf[ds] = kn[ds];
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) vf[dt] = vn[dt];
-        if (it + 4 < n_items) load_item(it + 4, kn, vn);
-        const bool pref = it < n_pref;
-        const int key0 = pref ? (kb_first + it) * 16 : (it - n_pref) * 16;
+    if (blk) load_chunk(wid);
+    for (int it0 = wid; it0 < n_items; it0 += 4 * CH) {
+        const bool first = it0 == wid;
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
-            f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ds = 0; ds < NDS; ++ds) mma_frag<T>(sc, kf[ds], qf[qt][ds]);
-            // lane holds keys key0 + 4*lgrp + e for query column qt*16 + lrow
-            float sv[4];
-            bool valid[4];
+            // lane holds keys key0(c) + 4*lgrp + e for query column qt*16 + lrow
+            float sv[CH][4];
+            bool valid[CH][4];
             float mloc = -1e30f;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int kk = key0 + lgrp * 4 + e;
-                const bool ok = pref ? kk < k_hi : (kk < nrows && (!a.causal || kk <= jq[qt]));
-                valid[e] = ok;
-                sv[e] = sc[e] * sl2;
-                if (ok) mloc = fmaxf(mloc, sv[e]);
+            for (int c = 0; c < CH; ++c) {
+                const int it = it0 + 4 * c;
+                f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+                if (it < n_items) {
+#pragma unroll
+                    for (int ds = 0; ds < NDS; ++ds) mma_frag<T>(sc, kn[c][ds], qf[qt][ds]);
+                }
+                const bool pref = it < n_pref;
+                const int key0 = pref ? (kb_first + it) * 16 : (it - n_pref) * 16;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int kk = key0 + lgrp * 4 + e;
+                    const bool ok = it < n_items && (pref ? kk < k_hi : (kk < nrows && (!a.causal || kk <= jq[qt])));
+                    valid[c][e] = ok;
+                    sv[c][e] = sc[e] * sl2;
+                    if (ok) mloc = fmaxf(mloc, sv[c][e]);
+                }
             }
             mloc = xrow_max(mloc);
             const float m_new = fmaxf(m_run[qt], mloc);
-            const float corr = exp2f(m_run[qt] - m_new);
-            f32x4 p;
+            if (!first) {
+                const float corr = exp2f(m_run[qt] - m_new);
+                l_run[qt] *= corr;
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) o_acc[dt][qt] *= corr;
+            }
+            f32x4 p[CH];
             float psum = 0.f;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                p[e] = valid[e] ? exp2f(sv[e] - m_new) : 0.f;
-                psum += p[e];
-            }
+            for (int c = 0; c < CH; ++c)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    p[c][e] = valid[c][e] ? exp2f(sv[c][e] - m_new) : 0.f;
+                    psum += p[c][e];
+                }
             psum = xrow_sum(psum);
-            l_run[qt] = l_run[qt] * corr + psum;
+            l_run[qt] += psum;
             m_run[qt] = m_new;
 #pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) {
-                o_acc[dt][qt] *= corr;
-                mma_k4(o_acc[dt][qt], vf[dt], p);
+            for (int c = 0; c < CH; ++c) {
+                if (it0 + 4 * c >= n_items) continue;
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) mma_k4(o_acc[dt][qt], vn[c][dt], p[c]);
             }
         }
+        if (it0 + 4 * CH < n_items) load_chunk(it0 + 4 * CH);
     }
 
     // -- merge the four waves: common max per query row, then a two-round tree
