@@ -53,6 +53,24 @@ static __device__ __forceinline__ void attn_splits(int t, int kps, int s_launch,
     chunk = s_pre > 0 ? ceil_div(ceil_div(t, s_pre), 16) * 16 : 16;
 }
 
+// Write EPL consecutive k values of one operand row (16-byte aligned run of
+// one lane's fragment slot) as value and residual, or plain T when lo is null.
+template <typename T>
+static __device__ __forceinline__ void put_operand_run(T* hi, T* lo, size_t e, const float* v) {
+    constexpr int EPL = Elt<T>::EPL;
+    T h[EPL], l[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+        h[i] = from_f32<T>(v[i]);
+        l[i] = from_f32<T>(v[i] - to_f32(h[i]));
+    }
+    uint4 hv, lv;
+    __builtin_memcpy(&hv, h, 16);
+    __builtin_memcpy(&lv, l, 16);
+    *(uint4*)(hi + e) = hv;
+    if (lo) *(uint4*)(lo + e) = lv;
+}
+
 // Write v into an operand as bf16 value (hi) plus bf16 residual (lo), or as
 // plain T when lo is null.
 template <typename T>
@@ -416,10 +434,14 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64, FG<EPI>::MINB) void k_fgemm(FGemm
                 float4* xd = (float4*)(a.x + (size_t)m * a.ldx + tile * 16);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) xd[i] = float4{xv[4 * i], xv[4 * i + 1], xv[4 * i + 2], xv[4 * i + 3]};
+                constexpr int EPL = Elt<T>::EPL;
 #pragma unroll
-                for (int n = 0; n < 16; ++n)
-                    put_operand<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 16 + n, a.n_MT),
-                                   xv[n] * to_f32(gq[n]));
+                for (int n0 = 0; n0 < 16; n0 += EPL) {
+                    float ov[EPL];
+#pragma unroll
+                    for (int i = 0; i < EPL; ++i) ov[i] = xv[n0 + i] * to_f32(gq[n0 + i]);
+                    put_operand_run<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 16 + n0, a.n_MT), ov);
+                }
                 a.sq_out[(size_t)tile * a.sq_stride + m] = ss;
             }
         } else if (EPI == EPI_SWIGLU) {
