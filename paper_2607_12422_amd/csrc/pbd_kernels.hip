@@ -137,11 +137,15 @@ __global__ __launch_bounds__(256) void k_assemble(AssembleArgs a) {
         for (int e = 0; e < EPL; ++e) xv[e] = to_f32(v[e]);
         *(float4*)(a.x + (size_t)m * a.H + k0) = float4{xv[0], xv[1], xv[2], xv[3]};
         if (EPL == 8) *(float4*)(a.x + (size_t)m * a.H + k0 + 4) = float4{xv[4 % EPL], xv[5 % EPL], xv[6 % EPL], xv[7 % EPL]};
+        typedef T __attribute__((ext_vector_type(EPL))) tv;
+        const tv gv = *(const tv*)(g + k0);
+        float ov[EPL];
 #pragma unroll
         for (int e = 0; e < EPL; ++e) {
             ss += xv[e] * xv[e];
-            put_operand<T>((T*)a.op_hi, (T*)a.op_lo, xfrag_elem<T>(m, k0 + e, a.MT), xv[e] * to_f32(g[k0 + e]));
+            ov[e] = xv[e] * to_f32(gv[e]);
         }
+        put_operand_run<T>((T*)a.op_hi, (T*)a.op_lo, xfrag_elem<T>(m, k0, a.MT), ov);
     }
     __shared__ float s_ss[8];
     ss = wave_sum(ss);
@@ -445,16 +449,23 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64, FG<EPI>::MINB) void k_fgemm(FGemm
                 a.sq_out[(size_t)tile * a.sq_stride + m] = ss;
             }
         } else if (EPI == EPI_SWIGLU) {
-            // tile rows 0-7: gate rows 8*tile..; rows 8-15: the matching up rows
-            for (int idx = threadIdx.x; idx < mgn * 128; idx += blockDim.x) {
-                const int mt = idx / 128, c = idx % 8, ml = (idx / 8) % 16;
+            // tile rows 0-7: gate rows 8*tile..; rows 8-15: the matching up rows;
+            // a thread writes one run of EPL consecutive h columns of one row
+            constexpr int EPL = Elt<T>::EPL;
+            constexpr int RUNS = 8 / EPL;
+            for (int idx = threadIdx.x; idx < mgn * 16 * RUNS; idx += blockDim.x) {
+                const int mt = idx / (16 * RUNS), ml = (idx / RUNS) % 16, c0 = (idx % RUNS) * EPL;
                 const int m = (mg0 + mt) * 16 + ml;
                 if (m < a.M) {
                     const float rm = s_rm[mt * 16 + ml];
-                    const float gt = s_tile[mt][c][ml] * rm;
-                    const float up = s_tile[mt][c + 8][ml] * rm;
-                    put_operand<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 8 + c, a.n_MT),
-                                   gt / (1.f + __expf(-gt)) * up);
+                    float hv[EPL];
+#pragma unroll
+                    for (int i = 0; i < EPL; ++i) {
+                        const float gt = s_tile[mt][c0 + i][ml] * rm;
+                        const float up = s_tile[mt][c0 + i + 8][ml] * rm;
+                        hv[i] = gt / (1.f + __expf(-gt)) * up;
+                    }
+                    put_operand_run<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 8 + c0, a.n_MT), hv);
                 }
             }
         } else {  // EPI_ARGMAX: tied LM head, per-tile (max, argmax) per row
@@ -977,7 +988,9 @@ __global__ __launch_bounds__(256, 2) void k_lmhead(FGemmArgs a) {
 // O-projection operand.
 template <typename T>
 __global__ void k_combine(CombineArgs a) {
-    const int m = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
+    // thread: EPL consecutive dims d0.. of head h for block row m
+    constexpr int EPL = Elt<T>::EPL;
+    const int m = blockIdx.x, h = blockIdx.y, d0 = threadIdx.x * EPL;
     const int b = m / a.W, j = m % a.W;
     int s_pre, chunk;
     attn_splits(a.pos0[b], a.kps, a.s_launch, s_pre, chunk);
@@ -985,13 +998,26 @@ __global__ void k_combine(CombineArgs a) {
     const size_t pr0 = (((size_t)b * a.n_q + h) * a.W + j) * a.s_launch;
     float mx = -1e30f;
     for (int s = 0; s < s_eff; ++s) mx = fmaxf(mx, a.part_ml[(pr0 + s) * 2]);
-    float L = 0.f, o = 0.f;
+    float L = 0.f, o[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) o[i] = 0.f;
     for (int s = 0; s < s_eff; ++s) {
         const float wgt = exp2f(a.part_ml[(pr0 + s) * 2] - mx);
         L += wgt * a.part_ml[(pr0 + s) * 2 + 1];
-        o += wgt * a.part_o[(pr0 + s) * a.head_dim + d];
+        const float4* src = (const float4*)(a.part_o + (pr0 + s) * a.head_dim + d0);
+#pragma unroll
+        for (int q = 0; q < EPL / 4; ++q) {
+            const float4 v = src[q];
+            o[4 * q] += wgt * v.x;
+            o[4 * q + 1] += wgt * v.y;
+            o[4 * q + 2] += wgt * v.z;
+            o[4 * q + 3] += wgt * v.w;
+        }
     }
-    put_operand<T>((T*)a.op_hi, (T*)a.op_lo, xfrag_elem<T>(m, h * a.head_dim + d, a.MT), L > 0.f ? o / L : 0.f);
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) o[i] *= inv;
+    put_operand_run<T>((T*)a.op_hi, (T*)a.op_lo, xfrag_elem<T>(m, h * a.head_dim + d0, a.MT), o);
 }
 
 // ---------------------------------------------------------------------------
@@ -1248,7 +1274,7 @@ hipError_t launch_assemble(int dtype, const AssembleArgs& a, int batch, hipStrea
     PBD_DISPATCH(dtype, k_assemble, dim3(a.W, batch), dim3(256), st, a);
 }
 hipError_t launch_combine(int dtype, const CombineArgs& a, int M, hipStream_t st) {
-    PBD_DISPATCH(dtype, k_combine, dim3(M, a.n_q), dim3(a.head_dim), st, a);
+    PBD_DISPATCH(dtype, k_combine, dim3(M, a.n_q), dim3(a.head_dim / (dtype == PBD_DTYPE_BF16 ? Elt<bf16>::EPL : Elt<float>::EPL)), st, a);
 }
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st) {
     PBD_DISPATCH(dtype, k_pack, dim3(1024), dim3(256), st, a);
