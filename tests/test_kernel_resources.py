@@ -1,0 +1,56 @@
+"""Compile-time resource check of the hot-path kernels (CPU, needs hipcc).
+
+A register array indexed with a run-time value, or a register budget that
+overflows, puts per-lane data in scratch memory, which turns every access into
+a global memory round trip.  The kernels of the Qwen3-shape passes at LoRA rank
+<= 16 (bf16 with split operands; attention with head_dim 128 and up to three
+16-row query tiles) must use no scratch at all.  (The rank-32/64 GEMM variants
+hold more shrink accumulators and do spill.)
+"""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+from paper_2607_12422_amd import build as b
+
+HOT = [
+    # projection GEMMs, bf16 value + residual operands, LoRA rank <= 16
+    r"_ZN3pbd7k_fgemmIDF16bLi\d+ELi\d+ELb1ELi[01]EEEvNS_9FGemmArgsE",
+    r"_ZN3pbd6k_attnIDF16bLi128ELi[123]EEEvNS_8AttnArgsE",            # attention, G*W <= 48 query rows
+    r"_ZN3pbd8k_lmheadIDF16bLb1EEEvNS_9FGemmArgsE",                   # LM head
+    r"_ZN3pbd9k_combineIDF16bEEvNS_11CombineArgsE",
+    r"_ZN3pbd10k_assembleIDF16bEEvNS_12AssembleArgsE",
+    r"_ZN3pbd8k_argmaxENS_10ArgmaxArgsE",
+    r"_ZN3pbd8k_acceptENS_10AcceptArgsE",
+]
+
+
+@pytest.mark.slow
+def test_hot_kernels_use_no_scratch(tmp_path):
+    cc = b.hipcc()
+    if not shutil.which(cc) and not os.path.exists(cc):
+        pytest.skip("hipcc not available")
+    cmd = [cc, *b.FLAGS, "-c", os.path.join(b.CSRC, "pbd_kernels.hip"), "-o", str(tmp_path / "k.o"),
+           "-Rpass-analysis=kernel-resource-usage"]
+    out = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True).stdout
+    usage = {}
+    name = None
+    for line in out.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and name:
+            usage[name] = int(m.group(1))
+    assert usage, out[-2000:]
+    seen = 0
+    for pat in HOT:
+        names = [n for n in usage if re.fullmatch(pat, n)]
+        assert names, f"no kernel matches {pat}"
+        for n in names:
+            seen += 1
+            assert usage[n] == 0, f"{n} uses {usage[n]} bytes of scratch per lane"
+    assert seen >= 10
