@@ -306,6 +306,17 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         at.q_norm = pk + lo_.q_norm; at.k_norm = pk + lo_.k_norm; at.rope = (const float2*)(pk + y.p_rope);
         at.kcache = c->kv; at.vcache = c->kv + y.kv_half;
         at.part_o = (float*)(ws + y.w_attn_o); at.part_ml = (float*)(ws + y.w_attn_ml);
+        // spare CUs during the attention warm the O, gate/up and down weights of
+        // this layer and the q/k/v weights of the next one
+        {
+            const size_t beg = lo_.o, end = l + 1 < y.L ? y.lay[l + 1].o : y.p_final_norm;
+            const int slots = B * y.NKV;
+            const int free_wg = 256 - s_launch * slots;
+            at.pf_x = slots > 0 && free_wg > slots ? free_wg / slots : 0;
+            at.pf = pk + beg;
+            const size_t cap = (size_t)at.pf_x * slots * 256 * 16 * 128;
+            at.pf_bytes = at.pf_x > 0 ? std::min(end - beg, cap) : 0;
+        }
         PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn(dt, y.HD, y.QTmax, at, B, st), "attention");
 
         CombineArgs cb{};

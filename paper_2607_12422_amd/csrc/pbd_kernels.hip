@@ -577,6 +577,28 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     typedef typename K4<T>::raw vraw;
     typedef RowPrep<T, HD> RP;
 
+    if ((int)blockIdx.x >= a.s_launch) {
+        // work-groups past the splits warm the memory-side cache with the
+        // weights the next kernels stream (the attention keeps few CUs busy):
+        // one word per 128-byte line of this work-group's share
+        const int n_pf = (gridDim.x - a.s_launch) * gridDim.y * gridDim.z;
+        const int ip = ((blockIdx.x - a.s_launch) * gridDim.y + blockIdx.y) * gridDim.z + blockIdx.z;
+        const size_t lines = a.pf_bytes / 128;
+        const size_t per = (lines + n_pf - 1) / n_pf;
+        const size_t l0 = (size_t)ip * per, l1 = min(l0 + per, lines);
+        constexpr int PFN = 16;
+        unsigned v[PFN];
+#pragma unroll
+        for (int i = 0; i < PFN; ++i) {
+            const size_t li = l0 + (size_t)i * blockDim.x + threadIdx.x;
+            v[i] = li < l1 ? *(const unsigned*)(a.pf + li * 128) : 0u;
+        }
+        unsigned acc = 0;
+#pragma unroll
+        for (int i = 0; i < PFN; ++i) acc ^= v[i];
+        asm volatile("" ::"v"(acc));
+        return;
+    }
     const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int t = a.pos0[b];
     const int nrows = a.nrows[b];
@@ -1251,7 +1273,7 @@ static hipError_t launch_attn_hd(const AttnArgs& a, int qt, dim3 grid, size_t sm
 }
 
 hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int batch, hipStream_t st) {
-    dim3 grid(a.s_launch, a.n_kv, batch);
+    dim3 grid(a.s_launch + a.pf_x, a.n_kv, batch);
     const size_t smem = attn_smem_bytes(dtype, head_dim, qt);
     if (dtype == PBD_DTYPE_BF16) {
         if (head_dim == 128) return launch_attn_hd<bf16, 128>(a, qt, grid, smem, st);
