@@ -105,6 +105,7 @@ def main():
     ap.add_argument("--workload", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
+    ap.add_argument("--no-draft-curve", action="store_true", help="skip the early-exit draft-cost curve")
     ap.add_argument("--kps", type=int, default=0, help="attention keys per split (0: library default)")
     ap.add_argument("--operands", choices=["bf16", "bf16x2"], default="bf16x2")
     ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of replaying HIP graphs")
@@ -257,6 +258,41 @@ def main():
                           "note": "Tab. profile; serving-runtime bound, context only"},
         "device_status": status, "setup_s": round(setup_s, 1), "timed_wall_s": round(wall, 3),
     }
+
+    if not args.no_draft_curve and not args.eager:
+        # Measured draft-cost curve (App. A.7): early-exit drafters over the
+        # first k blocks (then final norm + LM head) realise draft-cost
+        # reductions r(k) = 1 - t_draft(k) / t_draft(L); the measured iteration
+        # time t_draft(k) + t_verify + t_accept is set beside the analysis's
+        # prediction T0 (1 - r rho_d) with rho_d = t_draft / (t_draft + t_verify).
+        from paper_2607_12422_amd import costmodel
+        t0 = dmed + vmed + amed
+        rho = costmodel.draft_share(dmed, vmed)
+        curve = []
+        for k in sorted({1, cfg.n_layers // 4, cfg.n_layers // 2, 3 * cfg.n_layers // 4, cfg.n_layers}):
+            if k < 1:
+                continue
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                eng.pbd_draft_block_layers(seq, anc, draft, k)
+            g.replay()
+            torch.cuda.synchronize()
+            ks = []
+            for _ in range(max(10, args.steps // 2)):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                g.replay()
+                e1.record(stream)
+                e1.synchronize()
+                ks.append(e0.elapsed_time(e1))
+            tk = statistics.median(ks)
+            r = max(0.0, 1.0 - tk / dmed)
+            curve.append({"layers": k, "draft_ms": round(tk, 4), "r": round(r, 4),
+                          "iteration_ms": round(tk + vmed + amed, 4),
+                          "model_iteration_ms": round(costmodel.reduced_iteration_time(t0, rho, r), 4)})
+            del g
+        result["draft_cost_curve"] = {"rho_d": round(rho, 4), "T0_ms": round(t0, 4), "points": curve}
 
     if not args.no_profile:
         # Kernel durations: the same draft and verify passes launched directly

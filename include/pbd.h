@@ -176,6 +176,17 @@ int pbd_draft_block(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const i
  * [batch][D+1] receives p_0..p_D, the greedy token after each block row.
  * logits: NULL or device float [batch][D+1][vocab].
  */
+/*
+ * Early-exit draft (the drafter whose cost the draft-cost analysis of App. A.7
+ * and Tab. draft-cost-oracle varies): the same draft pass as pbd_draft_block
+ * with only the first n_layers backbone layers, followed by the final RMSNorm
+ * and the tied LM head.  n_layers in [1, cfg.n_layers]; n_layers = n_layers of
+ * the model gives exactly pbd_draft_block.  Other arguments, outputs and
+ * errors as pbd_draft_block; n_layers outside the range is PBD_ERR_INVALID_ARG.
+ */
+int pbd_draft_block_layers(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
+                           uint32_t flags, int32_t n_layers, int32_t* draft, float* logits, pbd_stream_t stream);
+
 int pbd_verify_block(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
                      const int32_t* draft, uint32_t flags, int32_t* verify, float* logits,
                      pbd_stream_t stream);

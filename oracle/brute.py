@@ -44,8 +44,9 @@ def _rotate(vec: np.ndarray, pos: int, theta: float) -> np.ndarray:
 
 
 def forward_full(w: Weights, tokens: Sequence[int], adapter_rows: Sequence[bool],
-                 visible: np.ndarray) -> np.ndarray:
-    """Logits [n, V] of a full no-cache pass; visible[i, j]: row i sees key j."""
+                 visible: np.ndarray, n_layers=None) -> np.ndarray:
+    """Logits [n, V] of a full no-cache pass; visible[i, j]: row i sees key j.
+    n_layers: only the first n_layers blocks before the final norm (None: all)."""
     cfg = w.cfg
     n = len(tokens)
     d, hq, hkv = cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
@@ -60,7 +61,7 @@ def forward_full(w: Weights, tokens: Sequence[int], adapter_rows: Sequence[bool]
             y = y + s_lora * (f(B) @ (f(A) @ row_vec))
         return y
 
-    for lw in w.layers:
+    for lw in w.layers[:n_layers]:
         Q = np.zeros((n, hq, d)); K = np.zeros((n, hkv, d)); Vv = np.zeros((n, hkv, d))
         for i in range(n):
             xn = _norm_row(x[i], f(lw.attn_norm), cfg.rms_eps)

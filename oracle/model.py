@@ -120,12 +120,15 @@ class OracleModel:
     def forward_block(self, tokens: Sequence[int], pos0: int,
                       cache_k: List[np.ndarray], cache_v: List[np.ndarray],
                       causal: bool, adapter_on: bool,
-                      logit_rows: Optional[Sequence[int]] = None):
+                      logit_rows: Optional[Sequence[int]] = None,
+                      n_layers: Optional[int] = None):
         """Run n block rows at positions pos0..pos0+n-1 over a committed prefix.
 
         cache_k[l], cache_v[l]: [pos0, h_kv, d] post-norm post-RoPE keys and
         values of the committed prefix (all visible to every block row).  Block
         key i is visible to block row j iff (not causal) or i <= j.
+        n_layers: run only the first n_layers blocks before the final norm and
+        the LM head (an early-exit drafter; None = all).
         Returns (logits [len(logit_rows), V], new_k [L][n,h_kv,d], new_v).
         """
         cfg = self.cfg
@@ -136,7 +139,7 @@ class OracleModel:
         x = self.embed[np.asarray(tokens, dtype=np.int64)]
         block_vis = np.tril(np.ones((n, n), dtype=bool)) if causal else np.ones((n, n), dtype=bool)
         new_k, new_v = [], []
-        for li, lw in enumerate(self.layers):
+        for li, lw in enumerate(self.layers[:n_layers]):
             xn = rms_norm(x, lw["attn_norm"], cfg.rms_eps)
             q = self.linear(lw, "q", xn, adapter_on).reshape(n, hq, d)
             k = self.linear(lw, "k", xn, adapter_on).reshape(n, hkv, d)
@@ -195,15 +198,19 @@ def prefill(model: OracleModel, prompt: Sequence[int]) -> SeqState:
     return SeqState(k, v, anchor, tokens=list(prompt) + [anchor], generated=[anchor])
 
 
-def draft(model: OracleModel, st: SeqState, adapter_on: bool = True, causal: bool = False):
+def draft(model: OracleModel, st: SeqState, adapter_on: bool = True, causal: bool = False,
+          n_layers: Optional[int] = None):
     """Draft pass (Sec. 3 steps 1-2): block [anchor, mask x D] at positions
     t..t+D, adapter on, bidirectional inside the block.  Returns the D draft
     tokens (argmax of rows 1..D over v != mask id) and the logits of all
-    D+1 rows.  The cache is not modified (the block K/V is scratch)."""
+    D+1 rows.  The cache is not modified (the block K/V is scratch).
+    n_layers < L gives the early-exit drafter whose cost the draft-cost
+    analysis (App. A.7) varies: the first n_layers blocks, then the final norm
+    and the LM head."""
     cfg = model.cfg
     tokens = [st.anchor] + [cfg.mask_id] * cfg.block
     lg, _, _ = model.forward_block(tokens, st.seq_len, st.cache_k, st.cache_v,
-                                   causal=causal, adapter_on=adapter_on)
+                                   causal=causal, adapter_on=adapter_on, n_layers=n_layers)
     drafts = [greedy_argmax(lg[j], exclude=cfg.mask_id) for j in range(1, cfg.block + 1)]
     return np.array(drafts, dtype=np.int32), lg
 

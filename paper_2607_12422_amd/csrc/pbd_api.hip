@@ -237,6 +237,7 @@ struct PassReq {
     int* out_tokens;
     int* seq_len_out;
     float* logits;
+    int n_layers;          // backbone layers run before the final norm and LM head (draft early exit)
 };
 
 int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
@@ -284,7 +285,8 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
             g.cnt = (unsigned*)(ws + y.w_kcnt);
         }
     };
-    for (int l = 0; l < y.L; ++l) {
+    const int L = q.n_layers > 0 ? q.n_layers : y.L;
+    for (int l = 0; l < L; ++l) {
         const Layout::LayerOff& lo_ = y.lay[l];
         // q/k/v projection: attention RMSNorm folded in, LoRA per source matrix
         FGemmArgs g;
@@ -309,7 +311,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         // spare CUs during the attention warm the O, gate/up and down weights of
         // this layer and the q/k/v weights of the next one
         {
-            const size_t beg = lo_.o, end = l + 1 < y.L ? y.lay[l + 1].o : y.p_final_norm;
+            const size_t beg = lo_.o, end = l + 1 < L ? y.lay[l + 1].o : lo_.attn_norm;
             const int slots = B * y.NKV;
             const int free_wg = 256 - s_launch * slots;
             at.pf_x = slots > 0 && free_wg > slots ? free_wg / slots : 0;
@@ -345,7 +347,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         base_gemm(g, lo_.d, y.tiles_d, y.kb_d, y.w_xd);
         g.n_sq = 0; g.lora_mode = LORA_SINGLE; g.la[0] = (const uint4*)(pk + lo_.la[6]); g.lb = pk + lo_.lb_d;
         g.x = x; g.ldx = y.H;
-        g.gnext = l + 1 < y.L ? pk + y.lay[l + 1].attn_norm : pk + y.p_final_norm;
+        g.gnext = l + 1 < L ? pk + y.lay[l + 1].attn_norm : pk + y.p_final_norm;
         g.nx_hi = hi(y.w_xa); g.nx_lo = lo(y.w_xa); g.n_MT = MT; g.sq_out = sq_a;
         split_k(g);
         PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "down gemm");
@@ -599,6 +601,22 @@ int pbd_draft_block(pbd_ctx* c, int32_t batch, const int32_t* seq_len, const int
     PassReq q{};
     q.mode = PASS_DRAFT; q.B = batch; q.seq_len = seq_len; q.anchor = anchor;
     q.adapter = adapter; q.causal = causal; q.write_kv = false; q.out_tokens = draft; q.logits = logits;
+    return run_pass(c, q, (hipStream_t)stream);
+}
+
+int pbd_draft_block_layers(pbd_ctx* c, int32_t batch, const int32_t* seq_len, const int32_t* anchor, uint32_t flags,
+                           int32_t n_layers, int32_t* draft, float* logits, pbd_stream_t stream) {
+    int rc = check_ctx(c);
+    if (rc) return rc;
+    if ((rc = check_batch(c, batch))) return rc;
+    if (!seq_len || !anchor || !draft) return fail(c, PBD_ERR_INVALID_ARG, "NULL pointer argument");
+    if (n_layers < 1 || n_layers > c->ly.L) return fail(c, PBD_ERR_INVALID_ARG, "n_layers outside [1, n_layers of the model]");
+    bool adapter, causal;
+    if ((rc = resolve_flags(c, flags, true, false, adapter, causal))) return rc;
+    PassReq q{};
+    q.mode = PASS_DRAFT; q.B = batch; q.seq_len = seq_len; q.anchor = anchor;
+    q.adapter = adapter; q.causal = causal; q.write_kv = false; q.out_tokens = draft; q.logits = logits;
+    q.n_layers = n_layers;
     return run_pass(c, q, (hipStream_t)stream);
 }
 

@@ -212,3 +212,47 @@ def test_qwen_shape_step_matches_oracle():
     _check_tokens(d.cpu().numpy()[0], dl_ref[1:], 2e-2, exclude=cfg.mask_id)
     _check_tokens(v.cpu().numpy()[0], vl_ref, 2e-2)
     g.close()
+
+
+def test_early_exit_draft_matches_oracle():
+    """pbd_draft_block_layers: the first k blocks, then the final norm and the
+    LM head; k = L is exactly pbd_draft_block."""
+    cfg, w = _tiny()
+    lengths, prompts = synth.workload_inputs(synth.WORKLOADS[0])
+    g = GpuRun(cfg, w, max_batch=1, max_seq=256)
+    g.prefill(prompts)
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompts[0])
+    B, W, V = 1, cfg.width, cfg.vocab
+    for k in range(1, cfg.n_layers + 1):
+        d = g.zeros(B, cfg.block)
+        lg = g.zeros(B, W, V, dtype=g.torch.float32)
+        g.eng.pbd_draft_block_layers(g.seq_len, g.anchor, d, k, lg)
+        _, ref = om.draft(m, st, n_layers=k)
+        assert np.abs(lg.cpu().numpy()[0] - ref).max() <= TOL32, k
+        _check_tokens(d.cpu().numpy()[0], ref[1:], TOL32, exclude=cfg.mask_id)
+    d_full, lg_full = g.draft()
+    assert g.torch.equal(lg_full, lg) and g.torch.equal(d_full, d)
+    g.close()
+
+
+def test_qwen_shape_early_exit_draft_matches_oracle():
+    """Qwen3-0.6B shape, prefix 512: the 7- and 14-layer drafters."""
+    w_ = synth.WORKLOADS[1]
+    cfg = w_.cfg
+    w = synth.make_weights(cfg, w_.seed(0))
+    lengths, prompts = synth.workload_inputs(w_)
+    g = GpuRun(cfg, w, max_batch=1, max_seq=1024)
+    g.prefill(prompts)
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompts[0])
+    for k in (7, 14):
+        d = g.zeros(1, cfg.block)
+        lg = g.zeros(1, cfg.width, cfg.vocab, dtype=g.torch.float32)
+        g.eng.pbd_draft_block_layers(g.seq_len, g.anchor, d, k, lg)
+        _, ref = om.draft(m, st, n_layers=k)
+        err = np.abs(lg.cpu().numpy()[0] - ref).max()
+        print(f"qwen early exit {k}: max-abs {err:.4f}")
+        assert err <= 2e-2
+        _check_tokens(d.cpu().numpy()[0], ref[1:], 2e-2, exclude=cfg.mask_id)
+    g.close()

@@ -76,3 +76,28 @@ def test_qk_norm_off_matches_brute_force():
     prompt = synth.make_prompts(m.cfg, [5], 2)[0]
     st = om.prefill(m, prompt)
     _check_step(w, m, st)
+
+
+@pytest.mark.parametrize("k", [1, 2])
+def test_early_exit_draft_matches_brute_force(k):
+    """The early-exit drafter (first k blocks, then final norm and LM head)
+    equals a brute-force pass truncated to the same k blocks."""
+    w, m = _model(4)
+    prompt = synth.make_prompts(m.cfg, [9], 11)[0]
+    st = om.prefill(m, prompt)
+    _, d_lg = om.draft(m, st, n_layers=k)
+    t, W = len(prompt), m.cfg.width
+    toks = list(prompt) + [st.anchor] + [m.cfg.mask_id] * m.cfg.block
+    ref = brute.forward_full(w, toks, [False] * t + [True] * W, brute.draft_mask(t, W), n_layers=k)
+    np.testing.assert_allclose(d_lg, ref[t:], atol=TOL, rtol=0)
+
+
+def test_full_depth_early_exit_is_the_draft():
+    w, m = _model(16)
+    prompt = synth.make_prompts(m.cfg, [20], 12)[0]
+    st = om.prefill(m, prompt)
+    d0, l0 = om.draft(m, st)
+    d1, l1 = om.draft(m, st, n_layers=m.cfg.n_layers)
+    assert np.array_equal(d0, d1) and np.array_equal(l0, l1)
+    _, l2 = om.draft(m, st, n_layers=1)
+    assert np.abs(l2 - l0).max() > 1e-3          # a shallower drafter is a different model
