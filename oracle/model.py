@@ -215,6 +215,80 @@ def draft(model: OracleModel, st: SeqState, adapter_on: bool = True, causal: boo
     return np.array(drafts, dtype=np.int32), lg
 
 
+# ---------------------------------------------------------------------------
+# Multi-step denoising: the one- vs two-step ablation (Sec. 4.4, Sec. 5.3;
+# the Limitations note that the adapter was trained for one step only).
+#
+# The paper names the ablation but not its remasking rule.  Readings:
+#  * k draft passes; pass s fixes n_s positions, D split as evenly as
+#    possible with the larger shares first;
+#  * every pass runs the draft pass of Sec. 3 over the current block
+#    [anchor, y_1..y_D], where y_j is the token fixed at an earlier pass or the
+#    mask id;
+#  * the candidate of a still-masked position j is the argmax of row j over
+#    v != mask id (as in the one-step draft), and its confidence is the
+#    log-probability of that candidate under the softmax of the whole row
+#    (all V ids);
+#  * the n_s still-masked positions of highest confidence are fixed (equal
+#    confidences: lower position first); the others are re-masked, and a fixed
+#    position never changes again.
+# With k = 1 this is the one-step draft.
+# ---------------------------------------------------------------------------
+
+def denoise_schedule(D: int, n_steps: int) -> List[int]:
+    """Number of positions fixed at each of the n_steps passes (1 <= n_steps <= D)."""
+    if not 1 <= n_steps <= D:
+        raise ValueError("n_steps must lie in [1, D]")
+    base, rem = divmod(D, n_steps)
+    return [base + (1 if s < rem else 0) for s in range(n_steps)]
+
+
+def draft_block_logits(model: OracleModel, st: SeqState, block: Sequence[int],
+                       adapter_on: bool = True, causal: bool = False) -> np.ndarray:
+    """Draft pass over a partly denoised block [anchor, y_1..y_D] at positions
+    t..t+D (adapter on, bidirectional inside the block); the logits of all
+    D+1 rows.  The cache is not modified."""
+    tokens = [st.anchor] + [int(t) for t in block]
+    lg, _, _ = model.forward_block(tokens, st.seq_len, st.cache_k, st.cache_v,
+                                   causal=causal, adapter_on=adapter_on)
+    return lg
+
+
+def candidate_confidence(row: np.ndarray, mask_id: int):
+    """(candidate, confidence) of one masked row: the argmax over v != mask id
+    and its log-probability under the softmax of the whole row."""
+    tok = greedy_argmax(row, exclude=mask_id)
+    mx = float(np.max(row))
+    lse = mx + float(np.log(np.sum(np.exp(row - mx))))
+    return tok, float(row[tok]) - lse
+
+
+def remask_select(conf: dict, n: int) -> List[int]:
+    """The n positions of highest confidence among conf's keys (the still-masked
+    positions); equal confidences go to the lower position."""
+    order = sorted(conf, key=lambda j: (-conf[j], j))
+    return sorted(order[:n])
+
+
+def draft_denoise(model: OracleModel, st: SeqState, n_steps: int,
+                  adapter_on: bool = True, causal: bool = False):
+    """k-step draft.  Returns the D draft tokens, the logits of the last pass,
+    the confidence at which each position was fixed and the pass (1..k) that
+    fixed it."""
+    cfg = model.cfg
+    D, mask = cfg.block, cfg.mask_id
+    block = [mask] * D
+    conf = np.full(D, np.nan)
+    fixed_at = np.zeros(D, dtype=np.int32)
+    lg = None
+    for s, n_s in enumerate(denoise_schedule(D, n_steps), start=1):
+        lg = draft_block_logits(model, st, block, adapter_on, causal)
+        cand = {j: candidate_confidence(lg[j + 1], mask) for j in range(D) if fixed_at[j] == 0}
+        for j in remask_select({j: c for j, (_, c) in cand.items()}, n_s):
+            block[j], conf[j], fixed_at[j] = cand[j][0], cand[j][1], s
+    return np.array(block, dtype=np.int32), lg, conf, fixed_at
+
+
 def verify(model: OracleModel, st: SeqState, drafts: Sequence[int],
            adapter_on: bool = False, causal: bool = True):
     """Verify pass (Sec. 3 step 3): block [anchor, x1..xD], adapter off,
