@@ -187,6 +187,34 @@ int pbd_draft_block(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const i
 int pbd_draft_block_layers(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
                            uint32_t flags, int32_t n_layers, int32_t* draft, float* logits, pbd_stream_t stream);
 
+/*
+ * Multi-step drafting for the denoising-steps ablation (Sec. 4.4, Sec. 5.3; the
+ * Limitations note that the adapter was trained for one step).  The paper gives
+ * no remasking rule; this one is low-confidence remasking:
+ *   the block starts as D masks; pass s = 1..n_steps runs the draft pass over
+ *   [anchor, y_1..y_D] (y_j = the token fixed earlier, or the mask id) and
+ *   takes, for each still-masked position j, the candidate argmax of row j
+ *   over v != mask id and its confidence, the log-probability of that
+ *   candidate under the softmax of the whole row; it then fixes the n_s
+ *   still-masked positions of highest confidence (equal confidences: lower
+ *   position first), n_s = D / n_steps, plus one for s <= D % n_steps.  Fixed
+ *   positions never change; after the last pass none is masked.
+ * n_steps = 1 gives pbd_draft_block's tokens and logits.
+ *
+ * n_steps: in [1, D], else PBD_ERR_INVALID_ARG.
+ * draft: device int32 [batch][D]; holds the block state between passes and the
+ *   final draft at the end (its previous contents are ignored).
+ * conf: NULL or device float [batch][D]: confidence at which each position was
+ *   fixed.  fixed_at: NULL or device int32 [batch][D]: the pass (1-based) that
+ *   fixed it.  logits: NULL or device float [batch][D+1][V], the last pass's.
+ * seq_len, anchor, flags, stream, errors: as pbd_draft_block.  The KV cache is
+ * not modified.  Work per call: n_steps draft passes, each followed by one
+ * small remasking kernel.
+ */
+int pbd_draft_block_denoise(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
+                            uint32_t flags, int32_t n_steps, int32_t* draft, float* conf, int32_t* fixed_at,
+                            float* logits, pbd_stream_t stream);
+
 int pbd_verify_block(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
                      const int32_t* draft, uint32_t flags, int32_t* verify, float* logits,
                      pbd_stream_t stream);

@@ -42,7 +42,8 @@ PBD_STATUS_FORCED_N = 4
 
 EXPORTED = (
     "pbd_packed_weight_bytes", "pbd_kv_bytes", "pbd_workspace_bytes", "pbd_init_weights",
-    "pbd_prefill", "pbd_draft_block", "pbd_draft_block_layers", "pbd_verify_block", "pbd_accept_commit",
+    "pbd_prefill", "pbd_draft_block", "pbd_draft_block_layers", "pbd_draft_block_denoise",
+    "pbd_verify_block", "pbd_accept_commit",
     "pbd_sync_status", "pbd_set_attn_keys_per_split", "pbd_set_operand_precision",
     "pbd_profile_enable", "pbd_profile_read", "pbd_last_error", "pbd_destroy",
 )
@@ -94,6 +95,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         "pbd_prefill": (ctypes.c_int, [vp, i32, vp, vp, i32, vp, vp, vp]),
         "pbd_draft_block": (ctypes.c_int, [vp, i32, vp, vp, u32, vp, vp, vp]),
         "pbd_draft_block_layers": (ctypes.c_int, [vp, i32, vp, vp, u32, i32, vp, vp, vp]),
+        "pbd_draft_block_denoise": (ctypes.c_int, [vp, i32, vp, vp, u32, i32, vp, vp, vp, vp, vp]),
         "pbd_verify_block": (ctypes.c_int, [vp, i32, vp, vp, vp, u32, vp, vp, vp]),
         "pbd_accept_commit": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
         "pbd_sync_status": (ctypes.c_int, [vp, vp, ctypes.POINTER(i32)]),
@@ -228,6 +230,15 @@ class Engine:
         B = int(seq_len.shape[0]) if batch is None else batch
         rc = self.lib.pbd_draft_block_layers(self.ctx, B, _ptr(seq_len), _ptr(anchor), flags, int(n_layers),
                                              _ptr(draft), _ptr(logits), _stream(stream))
+        _check(rc, self.ctx)
+
+    def pbd_draft_block_denoise(self, seq_len, anchor, draft, n_steps: int, conf=None, fixed_at=None,
+                                logits=None, flags: int = PBD_PASS_DEFAULT, batch: Optional[int] = None,
+                                stream=None):
+        B = int(seq_len.shape[0]) if batch is None else batch
+        rc = self.lib.pbd_draft_block_denoise(self.ctx, B, _ptr(seq_len), _ptr(anchor), flags, int(n_steps),
+                                              _ptr(draft), _ptr(conf), _ptr(fixed_at), _ptr(logits),
+                                              _stream(stream))
         _check(rc, self.ctx)
 
     def pbd_verify_block(self, seq_len, anchor, draft, verify, logits=None, flags: int = PBD_PASS_DEFAULT,

@@ -47,6 +47,8 @@ struct Layout {
     size_t w_xa[2], w_xo[2], w_xm[2], w_xd[2];      // operand value and residual fragments
     size_t w_attn_o, w_attn_ml, w_arg_val, w_arg_idx, w_tokens, w_pos0, w_nrows, w_status, ws_bytes;
     size_t w_kpart, w_kcnt;                          // split-K partial tiles and arrival counters
+    size_t w_arg_mx, w_arg_sum;                      // LM-head softmax partials (draft confidence)
+    size_t w_dn_tok, w_dn_conf;                      // one denoising pass's candidates and confidences
     int ksplit;                                      // K slices of the residual GEMMs
 };
 
@@ -158,6 +160,10 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.ksplit = 4;
     y.w_kpart = take((size_t)y.tiles_o * y.ksplit * 2 * 256 * 4);
     y.w_kcnt = take((size_t)y.tiles_o * 4);
+    y.w_arg_mx = take((size_t)y.tiles_e * y.Mmax * 4);
+    y.w_arg_sum = take((size_t)y.tiles_e * y.Mmax * 4);
+    y.w_dn_tok = take((size_t)y.Bmax * y.D * 4);
+    y.w_dn_conf = take((size_t)y.Bmax * y.D * 4);
     y.ws_bytes = off;
 }
 
@@ -238,6 +244,7 @@ struct PassReq {
     int* seq_len_out;
     float* logits;
     int n_layers;          // backbone layers run before the final norm and LM head (draft early exit)
+    float* conf;           // draft: per-row confidence of the argmax (null: not computed)
 };
 
 int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
@@ -360,6 +367,10 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     ge.logits = q.logits; ge.ldo = y.V;
     ge.arg_val = (float*)(ws + y.w_arg_val); ge.arg_idx = (int*)(ws + y.w_arg_idx);
     ge.exclude = q.mode == PASS_DRAFT ? c->cfg.mask_id : -1;
+    if (q.conf) {
+        ge.arg_mx = (float*)(ws + y.w_arg_mx);
+        ge.arg_sum = (float*)(ws + y.w_arg_sum);
+    }
     int n_part = y.tiles_e;
     if (lmhead_fits(y.kb_e, MT)) {
         n_part = std::min(y.tiles_e, LMHEAD_GRID);
@@ -372,6 +383,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     am.M = M; am.W = W; am.n_tiles = n_part; am.mode = q.mode; am.chunk_pos = q.chunk_pos;
     am.arg_val = ge.arg_val; am.arg_idx = ge.arg_idx; am.out = q.out_tokens;
     am.lengths = q.lengths; am.nrows = nrows; am.seq_len_out = q.seq_len_out;
+    am.arg_mx = ge.arg_mx; am.arg_sum = ge.arg_sum; am.conf = q.conf;
     PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_argmax(am, st), "argmax");
     return PBD_OK;
 }
@@ -618,6 +630,38 @@ int pbd_draft_block_layers(pbd_ctx* c, int32_t batch, const int32_t* seq_len, co
     q.adapter = adapter; q.causal = causal; q.write_kv = false; q.out_tokens = draft; q.logits = logits;
     q.n_layers = n_layers;
     return run_pass(c, q, (hipStream_t)stream);
+}
+
+int pbd_draft_block_denoise(pbd_ctx* c, int32_t batch, const int32_t* seq_len, const int32_t* anchor, uint32_t flags,
+                            int32_t n_steps, int32_t* draft, float* conf, int32_t* fixed_at, float* logits,
+                            pbd_stream_t stream) {
+    int rc = check_ctx(c);
+    if (rc) return rc;
+    if ((rc = check_batch(c, batch))) return rc;
+    if (!seq_len || !anchor || !draft) return fail(c, PBD_ERR_INVALID_ARG, "NULL pointer argument");
+    const int D = c->ly.D;
+    if (n_steps < 1 || n_steps > D) return fail(c, PBD_ERR_INVALID_ARG, "n_steps outside [1, block]");
+    bool adapter, causal;
+    if ((rc = resolve_flags(c, flags, true, false, adapter, causal))) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    int* cand = (int*)(c->ws + c->ly.w_dn_tok);
+    float* cand_conf = (float*)(c->ws + c->ly.w_dn_conf);
+    // the block starts fully masked; `draft` holds its state between passes
+    PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_fill_u32(draft, (size_t)batch * D, (uint32_t)c->cfg.mask_id, st),
+              "denoise init");
+    const int base = D / n_steps, rem = D % n_steps;
+    for (int s = 1; s <= n_steps; ++s) {
+        PassReq q{};
+        q.mode = PASS_DRAFT; q.B = batch; q.seq_len = seq_len; q.anchor = anchor; q.drafts = draft;
+        q.adapter = adapter; q.causal = causal; q.write_kv = false;
+        q.out_tokens = cand; q.conf = cand_conf; q.logits = s == n_steps ? logits : nullptr;
+        if ((rc = run_pass(c, q, st))) return rc;
+        RemaskArgs r{};
+        r.D = D; r.mask_id = c->cfg.mask_id; r.n_fix = base + (s <= rem ? 1 : 0); r.step = s;
+        r.cand = cand; r.cand_conf = cand_conf; r.block = draft; r.conf = conf; r.fixed_at = fixed_at;
+        PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_remask(r, batch, st), "remask");
+    }
+    return PBD_OK;
 }
 
 int pbd_verify_block(pbd_ctx* c, int32_t batch, const int32_t* seq_len, const int32_t* anchor, const int32_t* draft,

@@ -25,7 +25,7 @@ struct AssembleArgs {
     int chunk_pos, max_len, MT, m_stride;
     const int* seq_len;    // draft/verify: positions
     const int* anchor;
-    const int* drafts;     // verify: [B][W-1]
+    const int* drafts;     // verify: [B][W-1]; draft: null (all masks) or the partly denoised block
     const int* prompt;     // prefill: [B][max_len]
     const int* lengths;    // prefill: [B]
     int* tokens;           // [B][W]
@@ -69,6 +69,10 @@ struct FGemmArgs {
     float* arg_val;         // ARGMAX: [n_tiles][M]
     int* arg_idx;
     int exclude;            // ARGMAX: token id excluded (-1: none)
+    // ARGMAX with confidence (null: none): per partial, the row's maximum over
+    // all columns and the sum of exp(value - that maximum), same layout as arg_val
+    float* arg_mx;
+    float* arg_sum;
     // split-K (ksplit > 1: one m-group only): partial tiles [n_tiles][ksplit][MG*256]
     // and per-tile arrival counters (zero between launches)
     int ksplit;
@@ -118,6 +122,23 @@ struct ArgmaxArgs {
     const int* lengths;
     const int* nrows;
     int* seq_len_out;
+    // draft with confidence (null: none): the log-probability of each row's
+    // argmax under the softmax of the whole row, [B][W-1] like out
+    const float* arg_mx;
+    const float* arg_sum;
+    float* conf;
+};
+
+// One remasking pass of multi-step denoising: among the still-masked positions
+// of each sequence (block entry == mask id), fix the n_fix whose candidate has
+// the highest confidence (equal confidences: lower position first).
+struct RemaskArgs {
+    int D, mask_id, n_fix, step;
+    const int* cand;        // [B][D] candidates of this pass
+    const float* cand_conf; // [B][D] their confidences
+    int* block;             // [B][D] block state, updated in place
+    float* conf;            // optional [B][D]: confidence at which a position was fixed
+    int* fixed_at;          // optional [B][D]: pass (1-based) that fixed it
 };
 
 struct AcceptArgs {
@@ -157,9 +178,11 @@ hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int b
 hipError_t launch_combine(int dtype, const CombineArgs& a, int M, hipStream_t st);
 hipError_t launch_argmax(const ArgmaxArgs& a, hipStream_t st);
 // persistent LM head: `grid` work-groups, one (max, argmax) partial each per row
+// (and one softmax partial when a.arg_sum is set)
 bool lmhead_fits(int kb, int MT);
 hipError_t launch_lmhead(int dtype, const FGemmArgs& a, int grid, hipStream_t st);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t st);
+hipError_t launch_remask(const RemaskArgs& a, int batch, hipStream_t st);
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st);
 hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st);
 hipError_t launch_fill_u32(void* p, size_t n_words, uint32_t v, hipStream_t st);

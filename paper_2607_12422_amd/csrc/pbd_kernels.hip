@@ -105,7 +105,7 @@ __global__ __launch_bounds__(256) void k_assemble(AssembleArgs a) {
     int tok;
     if (a.mode == PASS_PREFILL) tok = (j < nrows) ? a.prompt[(size_t)b * a.max_len + a.chunk_pos + j] : 0;
     else if (j == 0) tok = a.anchor[b];
-    else if (a.mode == PASS_DRAFT) tok = a.mask_id;
+    else if (a.mode == PASS_DRAFT) tok = a.drafts ? a.drafts[b * (W - 1) + j - 1] : a.mask_id;
     else tok = a.drafts[b * (W - 1) + j - 1];
     const bool bad_tok = tok < 0 || tok >= a.vocab;
     if (bad_tok) tok = 0;
@@ -485,6 +485,15 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64, FG<EPI>::MINB) void k_fgemm(FGemm
                 }
                 a.arg_val[(size_t)tile * a.M + m] = best;
                 a.arg_idx[(size_t)tile * a.M + m] = bi;
+                if (a.arg_sum) {     // softmax partial over all 16 columns
+                    float mx = -INFINITY;
+                    for (int n = 0; n < 16; ++n) mx = fmaxf(mx, s_tile[mt][n][ml] * rm);
+                    float sm = 0.f;
+                    if (mx > -INFINITY)
+                        for (int n = 0; n < 16; ++n) sm += expf(s_tile[mt][n][ml] * rm - mx);
+                    a.arg_mx[(size_t)tile * a.M + m] = mx;
+                    a.arg_sum[(size_t)tile * a.M + m] = sm;
+                }
             }
         }
         lds_sync();
@@ -906,11 +915,14 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 // registers and walks vocabulary tiles with a grid stride; the next tile's
 // weight fragments are in flight while the current tile is reduced, so the
 // 16-row tiles of the embedding matrix stream back to back.  Each work-group
-// leaves one (max, argmax) per row; ties go to the lowest token id.
+// leaves one (max, argmax) per row; ties go to the lowest token id.  With
+// CONF it also leaves the row's softmax partial over its tiles (maximum and
+// sum of exp(value - maximum)), kept online by all 256 threads, two columns
+// of each tile per thread.
 // ---------------------------------------------------------------------------
 constexpr int LM_FPW = 8;      // weight fragments per wave and tile (hidden <= 4 * 8 * FK)
 
-template <typename T, bool SPLIT>
+template <typename T, bool SPLIT, bool CONF>
 __global__ __launch_bounds__(256, 2) void k_lmhead(FGemmArgs a) {
     constexpr int NW = 4, MGH = 2;
     __shared__ f32x4 s_red[NW][MGH][WAVE];
@@ -952,6 +964,8 @@ __global__ __launch_bounds__(256, 2) void k_lmhead(FGemmArgs a) {
     }
     float best = -INFINITY;
     int bi = 0x7fffffff;
+    float cmx = -INFINITY, csum = 0.f;     // CONF: running softmax partial of (row, column pair)
+    const int crow = threadIdx.x % 32, ccol = (threadIdx.x / 32) * 2;
     uint4 wv[LM_FPW], wn[LM_FPW];
     auto load_tile = [&](int tile, uint4* dst) {
         const uint4* wt = a.w + (size_t)tile * kb * WAVE;
@@ -997,12 +1011,43 @@ __global__ __launch_bounds__(256, 2) void k_lmhead(FGemmArgs a) {
                 }
             }
         }
+        if (CONF && crow < a.M) {
+            const float v0 = s_tile[crow / 16][ccol][crow % 16];
+            const float v1 = s_tile[crow / 16][ccol + 1][crow % 16];
+            const float nm = fmaxf(cmx, fmaxf(v0, v1));
+            if (nm > -INFINITY) {
+                csum = csum * expf(cmx - nm) + expf(v0 - nm) + expf(v1 - nm);
+                cmx = nm;
+            }
+        }
 #pragma unroll
         for (int i = 0; i < LM_FPW; ++i) wv[i] = wn[i];
     }
     if (threadIdx.x < a.M && threadIdx.x < MGH * 16) {
         a.arg_val[(size_t)blockIdx.x * a.M + threadIdx.x] = best;
         a.arg_idx[(size_t)blockIdx.x * a.M + threadIdx.x] = bi;
+    }
+    if (CONF) {
+        // merge the eight column-pair partials of each row
+        __syncthreads();
+        float* s_mx = s_sq;
+        float* s_sm = &s_tile[0][0][0];
+        static_assert(MGH * 16 * 17 >= 256, "LDS reuse");
+        s_mx[threadIdx.x] = cmx;
+        s_sm[threadIdx.x] = csum;
+        __syncthreads();
+        if (threadIdx.x < 32 && (int)threadIdx.x < a.M) {
+            float mx = -INFINITY;
+            for (int k = 0; k < 8; ++k) mx = fmaxf(mx, s_mx[k * 32 + threadIdx.x]);
+            float sm = 0.f;
+            if (mx > -INFINITY)
+                for (int k = 0; k < 8; ++k) {
+                    const float pm = s_mx[k * 32 + threadIdx.x];
+                    if (pm > -INFINITY) sm += s_sm[k * 32 + threadIdx.x] * expf(pm - mx);
+                }
+            a.arg_mx[(size_t)blockIdx.x * a.M + threadIdx.x] = mx;
+            a.arg_sum[(size_t)blockIdx.x * a.M + threadIdx.x] = sm;
+        }
     }
 }
 
@@ -1050,17 +1095,29 @@ __global__ void k_combine(CombineArgs a) {
 __global__ __launch_bounds__(256) void k_argmax(ArgmaxArgs a) {
     const int m = blockIdx.x;
     const int b = m / a.W, j = m % a.W;
+    const bool conf = a.conf != nullptr;
     float best = -INFINITY;
     int bi = 0x7fffffff;
+    float mx = -INFINITY, sm = 0.f;      // softmax partial of the whole row (conf only)
+    auto merge = [](float& m1, float& s1, float m2, float s2) {
+        const float nm = fmaxf(m1, m2);
+        if (nm == -INFINITY) return;
+        s1 = (m1 > -INFINITY ? s1 * expf(m1 - nm) : 0.f) + (m2 > -INFINITY ? s2 * expf(m2 - nm) : 0.f);
+        m1 = nm;
+    };
     for (int tI = threadIdx.x; tI < a.n_tiles; tI += blockDim.x) {
         const float v = a.arg_val[(size_t)tI * a.M + m];
         const int i = a.arg_idx[(size_t)tI * a.M + m];
         if (v > best || (v == best && i < bi)) { best = v; bi = i; }
+        if (conf) merge(mx, sm, a.arg_mx[(size_t)tI * a.M + m], a.arg_sum[(size_t)tI * a.M + m]);
     }
     __shared__ float s_v[256];
     __shared__ int s_i[256];
+    __shared__ float s_m[256], s_s[256];
     s_v[threadIdx.x] = best;
     s_i[threadIdx.x] = bi;
+    s_m[threadIdx.x] = mx;
+    s_s[threadIdx.x] = sm;
     __syncthreads();
     for (int st = blockDim.x / 2; st > 0; st >>= 1) {
         if ((int)threadIdx.x < st) {
@@ -1070,6 +1127,12 @@ __global__ __launch_bounds__(256) void k_argmax(ArgmaxArgs a) {
                 s_v[threadIdx.x] = v2;
                 s_i[threadIdx.x] = i2;
             }
+            if (conf) {
+                float m1 = s_m[threadIdx.x], s1 = s_s[threadIdx.x];
+                merge(m1, s1, s_m[threadIdx.x + st], s_s[threadIdx.x + st]);
+                s_m[threadIdx.x] = m1;
+                s_s[threadIdx.x] = s1;
+            }
         }
         __syncthreads();
     }
@@ -1077,6 +1140,8 @@ __global__ __launch_bounds__(256) void k_argmax(ArgmaxArgs a) {
     const int tok = s_i[0];
     if (a.mode == PASS_DRAFT) {
         if (j >= 1) a.out[b * (a.W - 1) + j - 1] = tok;
+        // log-probability of the argmax under the softmax of the whole row
+        if (conf && j >= 1) a.conf[b * (a.W - 1) + j - 1] = s_v[0] - (s_m[0] + logf(s_s[0]));
     } else if (a.mode == PASS_VERIFY) {
         a.out[b * a.W + j] = tok;
     } else {
@@ -1084,6 +1149,34 @@ __global__ __launch_bounds__(256) void k_argmax(ArgmaxArgs a) {
             a.out[b] = tok;                     // anchor
             a.seq_len_out[b] = a.lengths[b];
         }
+    }
+}
+
+// One remasking pass of multi-step denoising (the denoising-steps ablation of
+// Sec. 4.4 / Sec. 5.3; the remasking rule is a reading: the paper gives none).
+// One wave per sequence, one lane per block position: a still-masked position
+// is fixed when fewer than n_fix other still-masked positions beat it (higher
+// confidence, or equal confidence and a lower position).  All lanes read the
+// block state before any lane writes it.
+__global__ __launch_bounds__(64) void k_remask(RemaskArgs a) {
+    __shared__ float s_c[64];
+    __shared__ int s_open[64];
+    const int b = blockIdx.x, j = threadIdx.x;
+    const size_t idx = (size_t)b * a.D + j;
+    const bool open = j < a.D && a.block[idx] == a.mask_id;
+    float c = open ? a.cand_conf[idx] : -INFINITY;
+    if (c != c) c = -INFINITY;            // a NaN confidence ranks last
+    s_c[j] = c;
+    s_open[j] = open ? 1 : 0;
+    __syncthreads();
+    if (!open) return;
+    int rank = 0;
+    for (int i = 0; i < a.D; ++i)
+        if (s_open[i] && (s_c[i] > c || (s_c[i] == c && i < j))) ++rank;
+    if (rank < a.n_fix) {
+        a.block[idx] = a.cand[idx];
+        if (a.conf) a.conf[idx] = a.cand_conf[idx];
+        if (a.fixed_at) a.fixed_at[idx] = a.step;
     }
 }
 
@@ -1237,11 +1330,19 @@ hipError_t launch_fgemm(int dtype, const FGemmArgs& a, int epi, hipStream_t st) 
 bool lmhead_fits(int kb, int MT) { return kb <= 4 * LM_FPW && MT <= 2; }
 
 hipError_t launch_lmhead(int dtype, const FGemmArgs& a, int grid, hipStream_t st) {
+    const bool conf = a.arg_sum != nullptr;
+    if (conf && !a.arg_mx) return hipErrorInvalidValue;
     if (dtype == PBD_DTYPE_BF16) {
-        if (a.xlo) PBD_LAUNCH((k_lmhead<bf16, true>), dim3(grid), dim3(256), 0, st, a);
-        else PBD_LAUNCH((k_lmhead<bf16, false>), dim3(grid), dim3(256), 0, st, a);
+        if (a.xlo) {
+            if (conf) PBD_LAUNCH((k_lmhead<bf16, true, true>), dim3(grid), dim3(256), 0, st, a);
+            else PBD_LAUNCH((k_lmhead<bf16, true, false>), dim3(grid), dim3(256), 0, st, a);
+        } else {
+            if (conf) PBD_LAUNCH((k_lmhead<bf16, false, true>), dim3(grid), dim3(256), 0, st, a);
+            else PBD_LAUNCH((k_lmhead<bf16, false, false>), dim3(grid), dim3(256), 0, st, a);
+        }
     } else {
-        PBD_LAUNCH((k_lmhead<float, false>), dim3(grid), dim3(256), 0, st, a);
+        if (conf) PBD_LAUNCH((k_lmhead<float, false, true>), dim3(grid), dim3(256), 0, st, a);
+        else PBD_LAUNCH((k_lmhead<float, false, false>), dim3(grid), dim3(256), 0, st, a);
     }
     return hipGetLastError();
 }
@@ -1306,6 +1407,11 @@ hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st
 }
 hipError_t launch_argmax(const ArgmaxArgs& a, hipStream_t st) {
     PBD_LAUNCH(k_argmax, dim3(a.M), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+hipError_t launch_remask(const RemaskArgs& a, int batch, hipStream_t st) {
+    if (a.D < 1 || a.D > 64 || batch < 1) return hipErrorInvalidValue;
+    PBD_LAUNCH(k_remask, dim3(batch), dim3(64), 0, st, a);
     return hipGetLastError();
 }
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t st) {

@@ -52,6 +52,16 @@ class GpuRun:
         self.eng.pbd_draft_block(self.seq_len, self.anchor, d, lg, flags=flags)
         return d, lg
 
+    def denoise(self, n_steps, flags=0, logits=True):
+        """k-step draft: (draft, confidence, pass that fixed each position, last pass's logits)."""
+        B, W, V, D = self.seq_len.shape[0], self.cfg.width, self.cfg.vocab, self.cfg.block
+        d = self.zeros(B, D)
+        conf = self.zeros(B, D, dtype=self.torch.float32)
+        fixed = self.zeros(B, D)
+        lg = self.zeros(B, W, V, dtype=self.torch.float32) if logits else None
+        self.eng.pbd_draft_block_denoise(self.seq_len, self.anchor, d, n_steps, conf, fixed, lg, flags=flags)
+        return d, conf, fixed, lg
+
     def verify(self, drafts, flags=0, logits=True):
         B, W, V = self.seq_len.shape[0], self.cfg.width, self.cfg.vocab
         v = self.zeros(B, W)
@@ -72,3 +82,51 @@ class GpuRun:
 
     def close(self):
         self.eng.close()
+
+
+def check_denoise(m, st, tok, conf, fixed_at, last_logits, n_steps, tol, what=""):
+    """Follow the GPU's k-step draft with the oracle, pass by pass.
+
+    At each pass the oracle runs on the block state the GPU had (the tokens it
+    fixed at earlier passes) and checks: the GPU's confidences of the positions
+    it fixed (within 2 tol: a candidate's log-probability is the row maximum
+    minus the row's log-sum-exp, each off by at most tol); its tokens at
+    decisive rows; its choice of positions, exactly when the oracle's
+    confidence gap at the cut exceeds 4 tol, else that no unchosen position
+    beats a chosen one by more than 4 tol.  The last pass's logits are compared
+    within tol.  Returns the worst confidence error."""
+    cfg = m.cfg
+    D, mask = cfg.block, cfg.mask_id
+    sched = om.denoise_schedule(D, n_steps)
+    assert [int((fixed_at == s).sum()) for s in range(1, n_steps + 1)] == sched, (what, fixed_at)
+    assert not np.any(tok == mask)
+    block = [mask] * D
+    worst = 0.0
+    for s in range(1, n_steps + 1):
+        lg = om.draft_block_logits(m, st, block)
+        open_ = [j for j in range(D) if block[j] == mask]
+        cand = {j: om.candidate_confidence(lg[j + 1], mask) for j in open_}
+        chosen = [j for j in open_ if fixed_at[j] == s]
+        assert all(fixed_at[j] >= s for j in open_), what
+        for j in chosen:
+            err = abs(float(conf[j]) - cand[j][1])
+            worst = max(worst, err)
+            assert err <= 2 * tol, (what, s, j, float(conf[j]), cand[j][1])
+            if decisive(lg[j + 1][None], tol, mask)[0]:
+                assert int(tok[j]) == cand[j][0], (what, s, j)
+        ref = om.remask_select({j: c for j, (_, c) in cand.items()}, sched[s - 1])
+        cs = sorted((c for _, c in cand.values()), reverse=True)
+        n_s = sched[s - 1]
+        gap = cs[n_s - 1] - cs[n_s] if n_s < len(cs) else np.inf
+        if gap > 4 * tol:
+            assert chosen == ref, (what, s, chosen, ref)
+        else:
+            lo = min(cand[j][1] for j in chosen)
+            hi = max((cand[j][1] for j in open_ if j not in chosen), default=-np.inf)
+            assert hi <= lo + 4 * tol, (what, s, chosen, ref)
+        for j in chosen:
+            block[j] = int(tok[j])
+        if s == n_steps:
+            err = float(np.abs(last_logits - lg).max())
+            assert err <= tol, (what, err)
+    return worst
