@@ -301,6 +301,61 @@ def verify(model: OracleModel, st: SeqState, drafts: Sequence[int],
     return p, lg, k, v
 
 
+# ---------------------------------------------------------------------------
+# Unanchored drafting: the anchored-vs-unanchored ablation (Sec. 4.4, Sec. 5.3).
+#
+# The paper does not define the anchor.  Reading: the anchored draft puts the
+# anchor (the last committed token, position t) into the block, with the
+# adapter on, attending bidirectionally with the masks; the unanchored draft's
+# block is the D masks alone at t+1..t+D, and the anchor is context already in
+# the cache, computed as the verifier computes it (adapter off, seeing the
+# prefix and itself).  The anchor's verifier row also yields p_0, so the
+# verify that follows covers the D drafts alone; together they give the same
+# K/V and predictions p_0..p_D as the anchored verify of [anchor, drafts].
+# ---------------------------------------------------------------------------
+
+def draft_unanchored(model: OracleModel, st: SeqState, adapter_on: bool = True, causal: bool = False):
+    """Unanchored draft.  Returns the D draft tokens, p_0 (the verifier's
+    prediction after the anchor), the logits of the anchor row and the D mask
+    rows ([D+1, V]) and the anchor's K/V (per layer [1, h_kv, d])."""
+    cfg = model.cfg
+    lg0, k0, v0 = model.forward_block([st.anchor], st.seq_len, st.cache_k, st.cache_v,
+                                      causal=True, adapter_on=False)
+    ck = [np.concatenate([a, b], axis=0) for a, b in zip(st.cache_k, k0)]
+    cv = [np.concatenate([a, b], axis=0) for a, b in zip(st.cache_v, v0)]
+    lg, _, _ = model.forward_block([cfg.mask_id] * cfg.block, st.seq_len + 1, ck, cv,
+                                   causal=causal, adapter_on=adapter_on)
+    drafts = [greedy_argmax(lg[j], exclude=cfg.mask_id) for j in range(cfg.block)]
+    return (np.array(drafts, dtype=np.int32), greedy_argmax(lg0[0]),
+            np.concatenate([lg0, lg], axis=0), (k0, v0))
+
+
+def verify_unanchored(model: OracleModel, st: SeqState, anchor_kv, drafts: Sequence[int],
+                      adapter_on: bool = False, causal: bool = True):
+    """Verify of the D drafts alone at t+1..t+D over the prefix plus the
+    anchor's K/V.  Returns p_1..p_D, their logits ([D, V]) and the K/V of rows
+    t..t+D (the anchor's first) to be committed."""
+    k0, v0 = anchor_kv
+    ck = [np.concatenate([a, b], axis=0) for a, b in zip(st.cache_k, k0)]
+    cv = [np.concatenate([a, b], axis=0) for a, b in zip(st.cache_v, v0)]
+    lg, k, v = model.forward_block([int(t) for t in drafts], st.seq_len + 1, ck, cv,
+                                   causal=causal, adapter_on=adapter_on)
+    p = np.array([greedy_argmax(lg[j]) for j in range(len(drafts))], dtype=np.int32)
+    kk = [np.concatenate([a, b], axis=0) for a, b in zip(k0, k)]
+    vv = [np.concatenate([a, b], axis=0) for a, b in zip(v0, v)]
+    return p, lg, kk, vv
+
+
+def step_unanchored(model: OracleModel, st: SeqState, forced_n: Optional[int] = None):
+    """One unanchored speculative step: draft, verify, accept, commit."""
+    drafts, p0, dlg, akv = draft_unanchored(model, st)
+    p_rest, vlg, k, v = verify_unanchored(model, st, akv, drafts)
+    p = np.concatenate([[p0], p_rest]).astype(np.int32)
+    n, out = accept(drafts, p, forced_n)
+    commit(st, n, out, k, v)
+    return dict(drafts=drafts, draft_logits=dlg, p=p, verify_logits=vlg, n=n, out=out)
+
+
 def accept(drafts: Sequence[int], p: Sequence[int], forced_n: Optional[int] = None):
     """Longest-prefix acceptance (Sec. 3 step 4, App. A.1).
 
