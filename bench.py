@@ -107,6 +107,7 @@ def main():
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-draft-curve", action="store_true", help="skip the early-exit draft-cost curve")
     ap.add_argument("--no-denoise", action="store_true", help="skip the denoising-steps ablation timings")
+    ap.add_argument("--no-unanchored", action="store_true", help="skip the unanchored-drafting ablation timings")
     ap.add_argument("--kps", type=int, default=0, help="attention keys per split (0: library default)")
     ap.add_argument("--operands", choices=["bf16", "bf16x2"], default="bf16x2")
     ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of replaying HIP graphs")
@@ -316,6 +317,21 @@ def main():
             "paper_context": {"note": "Sec. 5.3: two-step denoising lowers throughput 34.05 -> 7.29 tokens/s and the "
                                       "accepted prefix 2.881 -> 1.021 with the trained adapter; acceptance needs "
                                       "trained weights and is not measured here"}}
+
+    if not args.no_unanchored and not args.eager:
+        # Anchored-vs-unanchored ablation (Sec. 4.4, Sec. 5.3): the unanchored
+        # draft (D masks; the anchor row computed as a verifier row and cached)
+        # and the verify of the D drafts alone, each timed as a graph.
+        vbuf = torch.zeros(B, cfg.width, **i32)
+        reps = max(10, args.steps // 2)
+        tdu = time_graph(lambda: eng.pbd_draft_block_unanchored(seq, anc, draft, vbuf), reps)
+        tvu = time_graph(lambda: eng.pbd_verify_block_unanchored(seq, draft, vbuf), reps)
+        result["unanchored_ablation"] = {
+            "draft_ms": round(tdu, 4), "verify_ms": round(tvu, 4), "iteration_ms": round(tdu + tvu + amed, 4),
+            "anchored_iteration_ms": round(dmed + vmed + amed, 4),
+            "rows_per_sequence": {"draft": cfg.width, "verify": cfg.block},
+            "paper_context": {"note": "Sec. 5.3 (HF loop): anchoring raises the accepted prefix 2.826 -> 3.046 at "
+                                      "15.4-15.6 tokens/s; acceptance needs trained weights and is not measured here"}}
 
     if not args.no_profile:
         # Kernel durations: the same draft and verify passes launched directly

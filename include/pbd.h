@@ -220,6 +220,41 @@ int pbd_verify_block(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const 
                      pbd_stream_t stream);
 
 /*
+ * Unanchored drafting, the anchored-vs-unanchored ablation (Sec. 4.4, Sec. 5.3).
+ * The paper does not define the anchor.  Reading: in the anchored step the
+ * draft block is [anchor, mask x D] with the adapter on for every row; in the
+ * unanchored step the block is the D masks alone at t+1..t+D, and the anchor
+ * (the last committed token, position t) is context already in the cache,
+ * computed as the verifier computes it.
+ *
+ * pbd_draft_block_unanchored runs rows [anchor, mask x D] at t..t+D in one pass:
+ * the anchor row without the adapter, seeing the prefix and itself (exactly the
+ * verifier's row for position t), its K/V appended to the cache at t; the mask
+ * rows with the adapter (per flags), seeing the prefix, the anchor and the
+ * whole block.  draft[b][j-1] = argmax of mask row j over v != mask id;
+ * verify[b][0] = argmax of the anchor row over all V (the verifier's p_0).
+ * verify: device int32 [batch][D+1]; only column 0 is written.  logits: NULL
+ * or device float [batch][D+1][V] (row 0: the anchor row).
+ *
+ * pbd_verify_block_unanchored runs the D drafts alone at t+1..t+D, without the
+ * adapter, causal, over the prefix including the anchor; it appends their K/V
+ * at t+1..t+D and writes verify[b][j] = argmax of row j-1 over all V for
+ * j = 1..D (the verifier's p_1..p_D).  logits: NULL or device float
+ * [batch][D][V].  With the anchor's K/V from the draft, the pair computes the
+ * same K/V and predictions p_0..p_D as pbd_verify_block over [anchor, draft];
+ * pbd_accept_commit then applies unchanged.
+ *
+ * Flags, stream, capacity (t + D + 1 <= max_seq) and errors as
+ * pbd_draft_block / pbd_verify_block.  The unanchored draft writes the cache
+ * row t; call it only on a state whose anchor is not yet committed (after a
+ * prefill or an accept).
+ */
+int pbd_draft_block_unanchored(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
+                               uint32_t flags, int32_t* draft, int32_t* verify, float* logits, pbd_stream_t stream);
+int pbd_verify_block_unanchored(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* draft,
+                                uint32_t flags, int32_t* verify, float* logits, pbd_stream_t stream);
+
+/*
  * Acceptance and commit (Sec. 3 steps 4-5; App. A.1).  For each sequence:
  * n = largest k <= D with draft[i-1] == verify[i-1] for all i <= k (or
  * forced_n[b] if forced_n != NULL, device int32 [batch], each in [0, D]);

@@ -43,7 +43,7 @@ PBD_STATUS_FORCED_N = 4
 EXPORTED = (
     "pbd_packed_weight_bytes", "pbd_kv_bytes", "pbd_workspace_bytes", "pbd_init_weights",
     "pbd_prefill", "pbd_draft_block", "pbd_draft_block_layers", "pbd_draft_block_denoise",
-    "pbd_verify_block", "pbd_accept_commit",
+    "pbd_verify_block", "pbd_draft_block_unanchored", "pbd_verify_block_unanchored", "pbd_accept_commit",
     "pbd_sync_status", "pbd_set_attn_keys_per_split", "pbd_set_operand_precision",
     "pbd_profile_enable", "pbd_profile_read", "pbd_last_error", "pbd_destroy",
 )
@@ -96,6 +96,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         "pbd_draft_block": (ctypes.c_int, [vp, i32, vp, vp, u32, vp, vp, vp]),
         "pbd_draft_block_layers": (ctypes.c_int, [vp, i32, vp, vp, u32, i32, vp, vp, vp]),
         "pbd_draft_block_denoise": (ctypes.c_int, [vp, i32, vp, vp, u32, i32, vp, vp, vp, vp, vp]),
+        "pbd_draft_block_unanchored": (ctypes.c_int, [vp, i32, vp, vp, u32, vp, vp, vp, vp]),
+        "pbd_verify_block_unanchored": (ctypes.c_int, [vp, i32, vp, vp, u32, vp, vp, vp]),
         "pbd_verify_block": (ctypes.c_int, [vp, i32, vp, vp, vp, u32, vp, vp, vp]),
         "pbd_accept_commit": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
         "pbd_sync_status": (ctypes.c_int, [vp, vp, ctypes.POINTER(i32)]),
@@ -246,6 +248,20 @@ class Engine:
         B = int(seq_len.shape[0]) if batch is None else batch
         rc = self.lib.pbd_verify_block(self.ctx, B, _ptr(seq_len), _ptr(anchor), _ptr(draft), flags,
                                        _ptr(verify), _ptr(logits), _stream(stream))
+        _check(rc, self.ctx)
+
+    def pbd_draft_block_unanchored(self, seq_len, anchor, draft, verify, logits=None,
+                                   flags: int = PBD_PASS_DEFAULT, batch: Optional[int] = None, stream=None):
+        B = int(seq_len.shape[0]) if batch is None else batch
+        rc = self.lib.pbd_draft_block_unanchored(self.ctx, B, _ptr(seq_len), _ptr(anchor), flags, _ptr(draft),
+                                                 _ptr(verify), _ptr(logits), _stream(stream))
+        _check(rc, self.ctx)
+
+    def pbd_verify_block_unanchored(self, seq_len, draft, verify, logits=None, flags: int = PBD_PASS_DEFAULT,
+                                    batch: Optional[int] = None, stream=None):
+        B = int(seq_len.shape[0]) if batch is None else batch
+        rc = self.lib.pbd_verify_block_unanchored(self.ctx, B, _ptr(seq_len), _ptr(draft), flags, _ptr(verify),
+                                                  _ptr(logits), _stream(stream))
         _check(rc, self.ctx)
 
     def pbd_accept_commit(self, draft, verify, seq_len, anchor, n_accepted, out_tokens, forced_n=None,

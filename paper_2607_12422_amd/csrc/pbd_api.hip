@@ -245,6 +245,12 @@ struct PassReq {
     float* logits;
     int n_layers;          // backbone layers run before the final norm and LM head (draft early exit)
     float* conf;           // draft: per-row confidence of the argmax (null: not computed)
+    // unanchored drafting (both false: the anchored passes [anchor, D rows] at seq_len)
+    bool anchor_cached;    // draft: the anchor row runs as a verifier row (no adapter, causal,
+                           // K/V appended); its argmax goes to out0[b * (D + 1)]
+    bool no_anchor;        // verify of the D drafts alone at seq_len + 1 (anchor already cached);
+                           // predictions to out_tokens[b * (D + 1) + 1 + j]
+    int* out0;
 };
 
 int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
@@ -252,7 +258,9 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     char* ws = c->ws;
     char* pk = c->packed;
     const int dt = y.dtype;
-    const int W = y.W, B = q.B, M = B * W, MT = cdiv(M, 16);
+    const int W = q.no_anchor ? y.D : y.W, B = q.B, M = B * W, MT = cdiv(M, 16);
+    const int lead = (q.mode == PASS_PREFILL || q.no_anchor) ? 0 : 1;
+    const int QT = cdiv(y.G * W, 16);
     const float scale = y.r > 0 ? c->cfg.lora_alpha / (float)y.r : 0.f;
     const bool lora = q.adapter && y.r > 0;
     const bool split = c->split && dt == PBD_DTYPE_BF16;
@@ -268,6 +276,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     AssembleArgs as{};
     as.mode = q.mode; as.W = W; as.H = y.H; as.vocab = y.V; as.mask_id = c->cfg.mask_id; as.max_seq = y.max_seq;
     as.chunk_pos = q.chunk_pos; as.max_len = q.max_len; as.MT = MT; as.m_stride = y.Mmax;
+    as.lead = lead; as.pos_add = q.no_anchor ? 1 : 0;
     as.seq_len = q.seq_len; as.anchor = q.anchor; as.drafts = q.drafts; as.prompt = q.prompt; as.lengths = q.lengths;
     as.tokens = (int*)(ws + y.w_tokens); as.pos0 = pos0; as.nrows = nrows; as.status = status;
     as.embed = pk + y.p_embed; as.gain = pk + y.lay[0].attn_norm; as.x = x;
@@ -281,6 +290,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.xhi = (const uint4*)hi(xop); g.xlo = (const uint4*)lo(xop);
         g.M = M; g.MT = MT; g.sq_stride = y.Mmax; g.norm_dim = y.H; g.eps = c->cfg.rms_eps;
         g.lora = lora ? 1 : 0; g.rt = y.RT; g.scale = scale; g.exclude = -1;
+        g.W = W; g.adapter_from = q.anchor_cached ? 1 : 0; g.excl_from = lead;
         g.ksplit = 1;
     };
     // residual GEMMs (n = hidden) have few output tiles: split K so that the
@@ -308,9 +318,11 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         AttnArgs at{};
         at.layer = l; at.max_batch = y.Bmax; at.n_q = y.NQ; at.n_kv = y.NKV; at.nblk = y.nblk; at.W = W; at.G = y.G;
         at.nqkv = y.nqkv; at.kps = c->kps; at.s_launch = s_launch;
-        at.causal = q.causal ? 1 : 0; at.write_kv = q.write_kv ? 1 : 0; at.qk_norm = c->cfg.qk_norm ? 1 : 0;
+        at.full_from = q.causal ? W : (q.anchor_cached ? 1 : 0);
+        at.kv_rows = q.write_kv ? W : (q.anchor_cached ? 1 : 0);
+        at.qk_norm = c->cfg.qk_norm ? 1 : 0;
         at.eps = c->cfg.rms_eps; at.scale_log2 = (float)(1.0 / sqrt((double)y.HD) * 1.4426950408889634);
-        at.smem_main = attn_smem_main(dt, y.HD, y.QTmax);
+        at.smem_main = attn_smem_main(dt, y.HD, QT);
         at.pos0 = pos0; at.nrows = nrows; at.qkv = (const float*)(ws + y.w_qkv);
         at.q_norm = pk + lo_.q_norm; at.k_norm = pk + lo_.k_norm; at.rope = (const float2*)(pk + y.p_rope);
         at.kcache = c->kv; at.vcache = c->kv + y.kv_half;
@@ -326,7 +338,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
             const size_t cap = (size_t)at.pf_x * slots * 256 * 16 * 128;
             at.pf_bytes = at.pf_x > 0 ? std::min(end - beg, cap) : 0;
         }
-        PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn(dt, y.HD, y.QTmax, at, B, st), "attention");
+        PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn(dt, y.HD, QT, at, B, st), "attention");
 
         CombineArgs cb{};
         cb.W = W; cb.n_q = y.NQ; cb.head_dim = y.HD; cb.kps = c->kps; cb.s_launch = s_launch; cb.MT = MT;
@@ -384,6 +396,8 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     am.arg_val = ge.arg_val; am.arg_idx = ge.arg_idx; am.out = q.out_tokens;
     am.lengths = q.lengths; am.nrows = nrows; am.seq_len_out = q.seq_len_out;
     am.arg_mx = ge.arg_mx; am.arg_sum = ge.arg_sum; am.conf = q.conf;
+    am.lead = lead; am.out0 = q.out0; am.out0_stride = y.D + 1;
+    am.out_stride = q.no_anchor ? y.D + 1 : W; am.out_off = q.no_anchor ? 1 : 0;
     PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_argmax(am, st), "argmax");
     return PBD_OK;
 }
@@ -674,6 +688,35 @@ int pbd_verify_block(pbd_ctx* c, int32_t batch, const int32_t* seq_len, const in
     if ((rc = resolve_flags(c, flags, false, true, adapter, causal))) return rc;
     PassReq q{};
     q.mode = PASS_VERIFY; q.B = batch; q.seq_len = seq_len; q.anchor = anchor; q.drafts = draft;
+    q.adapter = adapter; q.causal = causal; q.write_kv = true; q.out_tokens = verify; q.logits = logits;
+    return run_pass(c, q, (hipStream_t)stream);
+}
+
+int pbd_draft_block_unanchored(pbd_ctx* c, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
+                               uint32_t flags, int32_t* draft, int32_t* verify, float* logits, pbd_stream_t stream) {
+    int rc = check_ctx(c);
+    if (rc) return rc;
+    if ((rc = check_batch(c, batch))) return rc;
+    if (!seq_len || !anchor || !draft || !verify) return fail(c, PBD_ERR_INVALID_ARG, "NULL pointer argument");
+    bool adapter, causal;
+    if ((rc = resolve_flags(c, flags, true, false, adapter, causal))) return rc;
+    PassReq q{};
+    q.mode = PASS_DRAFT; q.B = batch; q.seq_len = seq_len; q.anchor = anchor;
+    q.adapter = adapter; q.causal = causal; q.write_kv = false; q.anchor_cached = true;
+    q.out_tokens = draft; q.out0 = verify; q.logits = logits;
+    return run_pass(c, q, (hipStream_t)stream);
+}
+
+int pbd_verify_block_unanchored(pbd_ctx* c, int32_t batch, const int32_t* seq_len, const int32_t* draft,
+                                uint32_t flags, int32_t* verify, float* logits, pbd_stream_t stream) {
+    int rc = check_ctx(c);
+    if (rc) return rc;
+    if ((rc = check_batch(c, batch))) return rc;
+    if (!seq_len || !draft || !verify) return fail(c, PBD_ERR_INVALID_ARG, "NULL pointer argument");
+    bool adapter, causal;
+    if ((rc = resolve_flags(c, flags, false, true, adapter, causal))) return rc;
+    PassReq q{};
+    q.mode = PASS_VERIFY; q.B = batch; q.seq_len = seq_len; q.drafts = draft; q.no_anchor = true;
     q.adapter = adapter; q.causal = causal; q.write_kv = true; q.out_tokens = verify; q.logits = logits;
     return run_pass(c, q, (hipStream_t)stream);
 }

@@ -23,9 +23,11 @@ struct AssembleArgs {
     int mode;
     int W, H, vocab, mask_id, max_seq;
     int chunk_pos, max_len, MT, m_stride;
+    int lead;              // draft/verify: leading anchor rows (1, or 0 for a block of drafts only)
+    int pos_add;           // draft/verify: the block starts at seq_len + pos_add
     const int* seq_len;    // draft/verify: positions
     const int* anchor;
-    const int* drafts;     // verify: [B][W-1]; draft: null (all masks) or the partly denoised block
+    const int* drafts;     // verify: [B][W-lead]; draft: null (all masks) or the partly denoised block
     const int* prompt;     // prefill: [B][max_len]
     const int* lengths;    // prefill: [B]
     int* tokens;           // [B][W]
@@ -50,6 +52,9 @@ struct FGemmArgs {
     const float* sq;
     int n_sq, sq_stride, norm_dim;
     float eps;
+    // rows per sequence; block rows j = m % W below adapter_from run without
+    // the adapter, and below excl_from without the argmax exclusion
+    int W, adapter_from, excl_from;
     // LoRA: shrink u = s * r_m * A x in the tile, expand B u
     int lora, rt, lora_mode, tile_split0, tile_split1;
     float scale;
@@ -84,7 +89,9 @@ struct AttnArgs {
     int layer, max_batch, n_q, n_kv, nblk, W, G;
     int nqkv;
     int kps, s_launch;
-    int causal, write_kv, qk_norm;
+    // block key i is visible to block row j iff i <= j or j >= full_from
+    // (full_from = W: causal; 0: bidirectional); rows j < kv_rows append their K/V
+    int full_from, kv_rows, qk_norm;
     float eps, scale_log2;
     size_t smem_main;
     const int* pos0;
@@ -116,6 +123,10 @@ struct CombineArgs {
 
 struct ArgmaxArgs {
     int M, W, n_tiles, mode, chunk_pos;
+    int lead;               // draft: rows j >= lead are draft rows, out[b][j - lead]
+    int* out0;              // draft: argmax of row 0 when lead = 1 (null: dropped), at out0[b * out0_stride]
+    int out0_stride;
+    int out_stride, out_off;  // verify: out[b * out_stride + out_off + j]
     const float* arg_val;
     const int* arg_idx;
     int* out;

@@ -97,16 +97,17 @@ __global__ __launch_bounds__(256) void k_assemble(AssembleArgs a) {
         pos0 = a.chunk_pos;
         nrows = ok ? min(max(len - a.chunk_pos, 0), W) : 0;
     } else {
-        pos0 = a.seq_len[b];
+        pos0 = a.seq_len[b] + a.pos_add;
         if (pos0 < 0 || pos0 + W > a.max_seq) ok = false;
         nrows = ok ? W : 0;
     }
     if (!ok) pos0 = 0;
     int tok;
+    const int nd = W - a.lead;
     if (a.mode == PASS_PREFILL) tok = (j < nrows) ? a.prompt[(size_t)b * a.max_len + a.chunk_pos + j] : 0;
-    else if (j == 0) tok = a.anchor[b];
-    else if (a.mode == PASS_DRAFT) tok = a.drafts ? a.drafts[b * (W - 1) + j - 1] : a.mask_id;
-    else tok = a.drafts[b * (W - 1) + j - 1];
+    else if (j < a.lead) tok = a.anchor[b];
+    else if (a.mode == PASS_DRAFT) tok = a.drafts ? a.drafts[b * nd + j - a.lead] : a.mask_id;
+    else tok = a.drafts[b * nd + j - a.lead];
     const bool bad_tok = tok < 0 || tok >= a.vocab;
     if (bad_tok) tok = 0;
     if (threadIdx.x == 0) {
@@ -305,6 +306,14 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64, FG<EPI>::MINB) void k_fgemm(FGemm
 #pragma unroll
         for (int t = 0; t < LRT; ++t)
             __builtin_memcpy(&bv[t], (const T*)a.lb + (((size_t)tile * LRT + t) * WAVE + lane) * 4, sizeof(braw));
+        // LoRA scale per m-tile (0 for rows without the adapter: the lane's u
+        // column is block row lrow of the m-tile), formed while the loads fly
+        float lsc[MG];
+#pragma unroll
+        for (int mt = 0; mt < MG; ++mt) {
+            lsc[mt] = a.scale;
+            if (LRT > 0 && a.adapter_from > 0 && ((mg0 + mt) * 16 + lrow) % a.W < a.adapter_from) lsc[mt] = 0.f;
+        }
 
         // requested after the first weight batch so that they do not delay it:
         // row sums of squares for r_m (thread: row sq_row, partials sq_slice +
@@ -356,7 +365,7 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64, FG<EPI>::MINB) void k_fgemm(FGemm
                 braw b = bv[t];
                 if (EPI == EPI_SWIGLU && ((lrow < 8) != (sc == 0))) b = braw{};
 #pragma unroll
-                for (int mt = 0; mt < MG; ++mt) mma_k4_split(acc[mt], b, uacc[sc][t * MG + mt] * a.scale);
+                for (int mt = 0; mt < MG; ++mt) mma_k4_split(acc[mt], b, uacc[sc][t * MG + mt] * lsc[mt]);
             }
 
         // finish r_m = rsqrt(mean(x^2) + eps) (fixed summation order)
@@ -476,11 +485,12 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64, FG<EPI>::MINB) void k_fgemm(FGemm
                 const float rm = s_rm[idx];
                 float best = -INFINITY;
                 int bi = 0x7fffffff;
+                const int excl = m % a.W >= a.excl_from ? a.exclude : -1;
                 for (int n = 0; n < 16; ++n) {
                     const int v = tile * 16 + n;
                     const float val = s_tile[mt][n][ml] * rm;
                     if (a.logits) a.logits[(size_t)m * a.ldo + v] = val;
-                    if (v == a.exclude) continue;
+                    if (v == excl) continue;
                     if (val > best) { best = val; bi = v; }   // ascending v: first max wins ties
                 }
                 a.arg_val[(size_t)tile * a.M + m] = best;
@@ -735,7 +745,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 vd[RP::NP * lrow + p] = vl[p];
                 vd[HALF + RP::NP * lrow + p] = vh[p];
             }
-            if (live && a.write_kv) {
+            if (live && j < a.kv_rows) {
                 const int pos = t + j;
                 T* kblk = kc + (size_t)(pos / 16) * 16 * HD;
                 T* vblk = vc + (size_t)(pos / 16) * 16 * HD;
@@ -806,7 +816,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int kk = key0 + lgrp * 4 + e;
-                    const bool ok = it < n_items && (pref ? kk < k_hi : (kk < nrows && (!a.causal || kk <= jq[qt])));
+                    const bool ok = it < n_items && (pref ? kk < k_hi : (kk < nrows && (kk <= jq[qt] || jq[qt] >= a.full_from)));
                     valid[c][e] = ok;
                     sv[c][e] = sc[e] * sl2;
                     if (ok) mloc = fmaxf(mloc, sv[c][e]);
@@ -964,6 +974,8 @@ __global__ __launch_bounds__(256, 2) void k_lmhead(FGemmArgs a) {
     }
     float best = -INFINITY;
     int bi = 0x7fffffff;
+    // the token id this thread's row excludes from its argmax (-1: none)
+    const int excl = (int)threadIdx.x % a.W >= a.excl_from ? a.exclude : -1;
     float cmx = -INFINITY, csum = 0.f;     // CONF: running softmax partial of (row, column pair)
     const int crow = threadIdx.x % 32, ccol = (threadIdx.x / 32) * 2;
     uint4 wv[LM_FPW], wn[LM_FPW];
@@ -1006,7 +1018,7 @@ __global__ __launch_bounds__(256, 2) void k_lmhead(FGemmArgs a) {
                     const int v = tile * 16 + n;
                     const float val = s_tile[mt][n][ml];
                     if (a.logits) a.logits[(size_t)m * a.ldo + v] = val;
-                    if (v == a.exclude) continue;
+                    if (v == excl) continue;
                     if (val > best) { best = val; bi = v; }   // tiles ascend within a work-group
                 }
             }
@@ -1139,11 +1151,16 @@ __global__ __launch_bounds__(256) void k_argmax(ArgmaxArgs a) {
     if (threadIdx.x != 0) return;
     const int tok = s_i[0];
     if (a.mode == PASS_DRAFT) {
-        if (j >= 1) a.out[b * (a.W - 1) + j - 1] = tok;
-        // log-probability of the argmax under the softmax of the whole row
-        if (conf && j >= 1) a.conf[b * (a.W - 1) + j - 1] = s_v[0] - (s_m[0] + logf(s_s[0]));
+        const int nd = a.W - a.lead;
+        if (j >= a.lead) {
+            a.out[b * nd + j - a.lead] = tok;
+            // log-probability of the argmax under the softmax of the whole row
+            if (conf) a.conf[b * nd + j - a.lead] = s_v[0] - (s_m[0] + logf(s_s[0]));
+        } else if (a.out0) {
+            a.out0[(size_t)b * a.out0_stride] = tok;
+        }
     } else if (a.mode == PASS_VERIFY) {
-        a.out[b * a.W + j] = tok;
+        a.out[b * a.out_stride + a.out_off + j] = tok;
     } else {
         if (a.chunk_pos + j == a.lengths[b] - 1 && j < a.nrows[b]) {
             a.out[b] = tok;                     // anchor

@@ -62,6 +62,22 @@ class GpuRun:
         self.eng.pbd_draft_block_denoise(self.seq_len, self.anchor, d, n_steps, conf, fixed, lg, flags=flags)
         return d, conf, fixed, lg
 
+    def draft_unanchored(self, flags=0, logits=True):
+        """Unanchored draft: (draft, verify buffer holding p_0 in column 0, logits [B][D+1][V])."""
+        B, W, V = self.seq_len.shape[0], self.cfg.width, self.cfg.vocab
+        d = self.zeros(B, self.cfg.block)
+        v = self.zeros(B, W)
+        lg = self.zeros(B, W, V, dtype=self.torch.float32) if logits else None
+        self.eng.pbd_draft_block_unanchored(self.seq_len, self.anchor, d, v, lg, flags=flags)
+        return d, v, lg
+
+    def verify_unanchored(self, drafts, verify, flags=0, logits=True):
+        """Unanchored verify: fills verify[:, 1:]; logits [B][D][V]."""
+        B, D, V = self.seq_len.shape[0], self.cfg.block, self.cfg.vocab
+        lg = self.zeros(B, D, V, dtype=self.torch.float32) if logits else None
+        self.eng.pbd_verify_block_unanchored(self.seq_len, drafts, verify, lg, flags=flags)
+        return verify, lg
+
     def verify(self, drafts, flags=0, logits=True):
         B, W, V = self.seq_len.shape[0], self.cfg.width, self.cfg.vocab
         v = self.zeros(B, W)

@@ -82,6 +82,8 @@ def test_calls_reject_null_context(lib):
     assert lib.pbd_draft_block_layers(None, 1, None, None, 0, 1, None, None, None) == b.PBD_ERR_INVALID_ARG
     assert lib.pbd_draft_block_denoise(None, 1, None, None, 0, 1, None, None, None, None, None) == b.PBD_ERR_INVALID_ARG
     assert lib.pbd_verify_block(None, 1, None, None, None, 0, None, None, None) == b.PBD_ERR_INVALID_ARG
+    assert lib.pbd_draft_block_unanchored(None, 1, None, None, 0, None, None, None, None) == b.PBD_ERR_INVALID_ARG
+    assert lib.pbd_verify_block_unanchored(None, 1, None, None, 0, None, None, None) == b.PBD_ERR_INVALID_ARG
     assert lib.pbd_accept_commit(None, 1, None, None, None, None, None, None, None, None) == b.PBD_ERR_INVALID_ARG
     assert lib.pbd_prefill(None, 1, None, None, 1, None, None, None) == b.PBD_ERR_INVALID_ARG
     st = ctypes.c_int32()

@@ -1,0 +1,171 @@
+"""GPU parity of unanchored drafting (pbd_draft_block_unanchored and
+pbd_verify_block_unanchored) against the oracle.
+
+Reading: the draft block is the D masks alone at t+1..t+D; the anchor at t is
+cache context computed as the verifier computes it, in the draft pass (a
+verifier row: no adapter, causal, K/V appended), which also yields p_0; the
+verify covers the D drafts alone.  Tolerances: logits 1e-4 (tiny fp32) and
+2e-2 (Qwen3-0.6B shape, bf16); token ids and counts exact at decisive rows.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import model as om
+
+from gpu_harness import GpuRun, decisive
+
+pytestmark = pytest.mark.gpu
+
+TOL32 = 1e-4
+
+
+def _tiny(D=16):
+    cfg = synth.TINY.with_(block=D)
+    return cfg, synth.make_weights(cfg, synth.WORKLOADS[0].seed(0))
+
+
+def _check_ids(got, ref_logits, tol, exclude=None):
+    lg = ref_logits.copy()
+    dec = decisive(lg, tol, exclude)
+    if exclude is not None:
+        lg[..., exclude] = -np.inf
+    ref = np.argmax(lg, axis=-1)
+    assert np.all(np.asarray(got)[dec] == ref[dec]), (got, ref, dec)
+
+
+def _round(g, m, st, b, d, v, dlg, vlg, tol, forced=None, what=""):
+    """Compare one sequence's unanchored draft and verify with the oracle;
+    returns the oracle's (n, out, K, V) for the commit."""
+    cfg = m.cfg
+    d_np, v_np = d.cpu().numpy()[b], v.cpu().numpy()[b]
+    d_ref, p0_ref, dl_ref, akv = om.draft_unanchored(m, st)
+    e = float(np.abs(dlg.cpu().numpy()[b] - dl_ref).max())
+    assert e <= tol, (what, "draft", e)
+    _check_ids(d_np, dl_ref[1:], tol, cfg.mask_id)
+    _check_ids(v_np[:1], dl_ref[:1], tol)
+    p_ref, vl_ref, k, vv = om.verify_unanchored(m, st, akv, d_np)
+    e = float(np.abs(vlg.cpu().numpy()[b] - vl_ref).max())
+    assert e <= tol, (what, "verify", e)
+    _check_ids(v_np[1:], vl_ref, tol)
+    nn, oo = om.accept(d_np, v_np, forced_n=forced)
+    return nn, oo, k, vv
+
+
+def test_tiny_unanchored_step_matches_oracle():
+    cfg, w = _tiny()
+    lengths, prompts = synth.workload_inputs(synth.WORKLOADS[0])
+    g = GpuRun(cfg, w, max_batch=1, max_seq=256)
+    g.prefill(prompts)
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompts[0])
+    d, v, dlg = g.draft_unanchored()
+    v, vlg = g.verify_unanchored(d, v)
+    nn, oo, _, _ = _round(g, m, st, 0, d, v, dlg, vlg, TOL32)
+    n, out = g.accept(d, v)
+    assert int(n[0]) == nn and list(out.cpu().numpy()[0][:nn + 1]) == oo
+    assert int(g.seq_len[0]) == len(prompts[0]) + nn + 1
+    assert g.status() == 0
+    g.close()
+
+
+def test_unanchored_pair_equals_anchored_verify():
+    """The anchor row of the unanchored draft is the anchored verify's row 0
+    (bit for bit: same kernels and widths, adapter contribution zero), and the
+    unanchored verify's rows are its rows 1..D (to fp32 rounding: the anchor is
+    a cached key instead of a block key)."""
+    cfg, w = _tiny()
+    lengths, prompts = synth.workload_inputs(synth.WORKLOADS[0])
+    g = GpuRun(cfg, w, max_batch=1, max_seq=256)
+    g.prefill(prompts)
+    d, v, dlg = g.draft_unanchored()
+    v, vlg = g.verify_unanchored(d, v)
+    va, vla = g.verify(d)
+    assert g.torch.equal(dlg[:, 0], vla[:, 0])
+    assert float((vlg - vla[:, 1:]).abs().max()) <= 1e-5
+    assert g.torch.equal(v[:, 0], va[:, 0])
+    dec = decisive(vla.cpu().numpy()[0, 1:], 1e-5)
+    assert np.array_equal(v.cpu().numpy()[0, 1:][dec], va.cpu().numpy()[0, 1:][dec])
+    g.close()
+
+
+def test_tiny_unanchored_loop_matches_oracle():
+    """Rounds with forced and then real acceptance: every pass, count, commit
+    and length follows the oracle (the oracle takes the GPU's committed tokens,
+    equal to its own at decisive rows); the anchored passes that follow still
+    match, so the cache bookkeeping is right."""
+    cfg, w = _tiny(4)
+    prompt = synth.make_prompts(cfg, [9], 3)[0]
+    forced = synth.make_forced_accepts(6, 1, cfg.block, 5)[:, 0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=128)
+    g.prefill([prompt])
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompt)
+    for r in range(10):
+        fn = int(forced[r]) if r < 6 else None
+        d, v, dlg = g.draft_unanchored()
+        v, vlg = g.verify_unanchored(d, v)
+        nn, oo, k, vv = _round(g, m, st, 0, d, v, dlg, vlg, TOL32, forced=fn, what=f"round {r}")
+        n, out = g.accept(d, v, forced=None if fn is None else [fn])
+        assert int(n[0]) == nn and list(out.cpu().numpy()[0][:nn + 1]) == oo
+        om.commit(st, nn, oo, k, vv)
+        assert int(g.seq_len[0]) == st.seq_len and int(g.anchor[0]) == st.anchor
+    d, dlg = g.draft()
+    _, dl_ref = om.draft(m, st)
+    assert np.abs(dlg.cpu().numpy()[0] - dl_ref).max() <= TOL32
+    v, vlg = g.verify(d)
+    _, vl_ref, _, _ = om.verify(m, st, d.cpu().numpy()[0])
+    assert np.abs(vlg.cpu().numpy()[0] - vl_ref).max() <= TOL32
+    assert g.status() == 0
+    g.close()
+
+
+def test_tiny_ragged_batch_unanchored():
+    """Three sequences: the draft has 51 rows (the LM head runs as the tiled
+    GEMM with a per-row mask-id exclusion), the verify 48."""
+    cfg, w = _tiny()
+    lens = [5, 40, 129]
+    prompts = synth.make_prompts(cfg, lens, 7)
+    g = GpuRun(cfg, w, max_batch=4, max_seq=192)
+    g.prefill(prompts)
+    d, v, dlg = g.draft_unanchored()
+    v, vlg = g.verify_unanchored(d, v)
+    m = om.OracleModel(w)
+    for b, p in enumerate(prompts):
+        _round(g, m, om.prefill(m, p), b, d, v, dlg, vlg, TOL32, what=f"seq {b}")
+    n, out = g.accept(d, v)
+    assert g.status() == 0
+    g.close()
+
+
+def test_unanchored_capacity_overflow_sets_status():
+    from paper_2607_12422_amd import binding as bd
+    cfg, w = _tiny(16)
+    prompt = synth.make_prompts(cfg, [10], 12)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=64)
+    g.prefill([prompt])
+    g.seq_len.fill_(64 - 16)            # t + D + 1 = max_seq + 1
+    d, v, _ = g.draft_unanchored(logits=False)
+    assert g.status() & bd.PBD_STATUS_CAPACITY
+    g.verify_unanchored(d, v, logits=False)
+    assert g.status() & bd.PBD_STATUS_CAPACITY
+    g.close()
+
+
+def test_qwen_shape_unanchored_step_matches_oracle():
+    """Qwen3-0.6B shape, bf16, prefix 512: one unanchored step."""
+    w_ = synth.WORKLOADS[1]
+    cfg = w_.cfg
+    w = synth.make_weights(cfg, w_.seed(0))
+    lengths, prompts = synth.workload_inputs(w_)
+    g = GpuRun(cfg, w, max_batch=1, max_seq=1024)
+    g.prefill(prompts)
+    d, v, dlg = g.draft_unanchored()
+    v, vlg = g.verify_unanchored(d, v)
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompts[0])
+    nn, oo, _, _ = _round(g, m, st, 0, d, v, dlg, vlg, 2e-2, what="qwen")
+    n, out = g.accept(d, v)
+    assert int(n[0]) == nn
+    assert g.status() == 0
+    g.close()
