@@ -110,6 +110,8 @@ def main():
     ap.add_argument("--no-unanchored", action="store_true", help="skip the unanchored-drafting ablation timings")
     ap.add_argument("--kps", type=int, default=0, help="attention keys per split (0: library default)")
     ap.add_argument("--operands", choices=["bf16", "bf16x2"], default="bf16x2")
+    ap.add_argument("--attn-qsplit", type=int, default=-2,
+                    help="attention work-group per 16 query rows (1), per KV head (0), automatic (-1); default: the library's")
     ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of replaying HIP graphs")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 10 plain device copies of MIB MiB (reference for the HBM byte counters) and exit")
@@ -150,6 +152,8 @@ def main():
                                   else binding.PBD_OPERANDS_BF16)
     if args.kps:
         eng.pbd_set_attn_keys_per_split(args.kps)
+    if args.attn_qsplit >= -1:
+        eng.pbd_set_attn_query_split(args.attn_qsplit)
     i32 = dict(dtype=torch.int32, device=dev)
     L = max(lengths)
     buf = np.zeros((B, L), dtype=np.int32)

@@ -274,8 +274,18 @@ int pbd_accept_commit(pbd_ctx* ctx, int32_t batch, const int32_t* draft, const i
  */
 int pbd_sync_status(pbd_ctx* ctx, pbd_stream_t stream, int32_t* status);
 
-/* Attention split tuning: prefix keys per split-KV work item (multiple of 16). */
+/* Attention split tuning: prefix keys per split-KV work item (multiple of 16; default 256). */
 int pbd_set_attn_keys_per_split(pbd_ctx* ctx, int32_t keys);
+
+/*
+ * Attention layout tuning.  mode 1: each split-KV work item runs as one
+ * work-group per 16 query rows (shorter per-wave instruction chains, more
+ * work-groups, K/V read once per group); 0: one work-group takes all G*W query
+ * rows of a KV head; -1 (default): 1 when batch * n_kv_heads * (splits at
+ * max_seq) < 256, else 0.  Results are identical up to fp32 rounding.
+ * Other modes: PBD_ERR_INVALID_ARG.
+ */
+int pbd_set_attn_query_split(pbd_ctx* ctx, int32_t mode);
 
 /*
  * Precision of the GEMM activation operands of bf16 models: PBD_OPERANDS_BF16 or

@@ -44,7 +44,7 @@ EXPORTED = (
     "pbd_packed_weight_bytes", "pbd_kv_bytes", "pbd_workspace_bytes", "pbd_init_weights",
     "pbd_prefill", "pbd_draft_block", "pbd_draft_block_layers", "pbd_draft_block_denoise",
     "pbd_verify_block", "pbd_draft_block_unanchored", "pbd_verify_block_unanchored", "pbd_accept_commit",
-    "pbd_sync_status", "pbd_set_attn_keys_per_split", "pbd_set_operand_precision",
+    "pbd_sync_status", "pbd_set_attn_keys_per_split", "pbd_set_attn_query_split", "pbd_set_operand_precision",
     "pbd_profile_enable", "pbd_profile_read", "pbd_last_error", "pbd_destroy",
 )
 
@@ -102,6 +102,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         "pbd_accept_commit": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
         "pbd_sync_status": (ctypes.c_int, [vp, vp, ctypes.POINTER(i32)]),
         "pbd_set_attn_keys_per_split": (ctypes.c_int, [vp, i32]),
+        "pbd_set_attn_query_split": (ctypes.c_int, [vp, i32]),
         "pbd_set_operand_precision": (ctypes.c_int, [vp, i32]),
         "pbd_profile_enable": (ctypes.c_int, [vp, i32]),
         "pbd_profile_read": (ctypes.c_int, [vp, i32, ctypes.POINTER(ctypes.c_double),
@@ -279,6 +280,9 @@ class Engine:
 
     def pbd_set_attn_keys_per_split(self, keys: int):
         _check(self.lib.pbd_set_attn_keys_per_split(self.ctx, int(keys)), self.ctx)
+
+    def pbd_set_attn_query_split(self, mode: int):
+        _check(self.lib.pbd_set_attn_query_split(self.ctx, int(mode)), self.ctx)
 
     def pbd_set_operand_precision(self, mode: int):
         _check(self.lib.pbd_set_operand_precision(self.ctx, int(mode)), self.ctx)

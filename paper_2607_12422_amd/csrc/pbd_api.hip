@@ -184,6 +184,8 @@ struct pbd_ctx {
     char* kv;
     char* ws;
     int kps;
+    int qsplit;          // attention: one work-group per 16 query rows (1), per KV head (0), or
+                         // automatic (-1: split when the split-KV grid leaves most CUs idle)
     bool split;          // GEMM activation operands as bf16 hi + bf16 residual
     Profiler prof;
     std::string err;
@@ -260,7 +262,10 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     const int dt = y.dtype;
     const int W = q.no_anchor ? y.D : y.W, B = q.B, M = B * W, MT = cdiv(M, 16);
     const int lead = (q.mode == PASS_PREFILL || q.no_anchor) ? 0 : 1;
-    const int QT = cdiv(y.G * W, 16);
+    const int QT = cdiv(y.G * W, 16);              // query tiles per (KV head, sequence)
+    const int s_launch = std::min(y.S_max, cdiv(y.max_seq, c->kps) + 1);   // split-KV grid columns
+    const bool qsplit = c->qsplit > 0 || (c->qsplit < 0 && B * y.NKV * s_launch < 256);
+    const int QTw = qsplit ? 1 : QT;                // ... per attention work-group
     const float scale = y.r > 0 ? c->cfg.lora_alpha / (float)y.r : 0.f;
     const bool lora = q.adapter && y.r > 0;
     const bool split = c->split && dt == PBD_DTYPE_BF16;
@@ -283,7 +288,6 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     as.op_hi = hi(y.w_xa); as.op_lo = lo(y.w_xa); as.sq = sq_a;
     PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_assemble(dt, as, B, st), "assemble");
 
-    const int s_launch = std::min(y.S_max, cdiv(y.max_seq, c->kps) + 1);
     auto base_gemm = [&](FGemmArgs& g, size_t w_off, int tiles, int kb, const size_t* xop) {
         g = FGemmArgs{};
         g.w = (const uint4*)(pk + w_off); g.n_tiles = tiles; g.kb = kb;
@@ -317,12 +321,12 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
 
         AttnArgs at{};
         at.layer = l; at.max_batch = y.Bmax; at.n_q = y.NQ; at.n_kv = y.NKV; at.nblk = y.nblk; at.W = W; at.G = y.G;
-        at.nqkv = y.nqkv; at.kps = c->kps; at.s_launch = s_launch;
+        at.nqkv = y.nqkv; at.kps = c->kps; at.s_launch = s_launch; at.n_qgrp = QT / QTw;
         at.full_from = q.causal ? W : (q.anchor_cached ? 1 : 0);
         at.kv_rows = q.write_kv ? W : (q.anchor_cached ? 1 : 0);
         at.qk_norm = c->cfg.qk_norm ? 1 : 0;
         at.eps = c->cfg.rms_eps; at.scale_log2 = (float)(1.0 / sqrt((double)y.HD) * 1.4426950408889634);
-        at.smem_main = attn_smem_main(dt, y.HD, QT);
+        at.smem_main = attn_smem_main(dt, y.HD, QTw);
         at.pos0 = pos0; at.nrows = nrows; at.qkv = (const float*)(ws + y.w_qkv);
         at.q_norm = pk + lo_.q_norm; at.k_norm = pk + lo_.k_norm; at.rope = (const float2*)(pk + y.p_rope);
         at.kcache = c->kv; at.vcache = c->kv + y.kv_half;
@@ -331,14 +335,14 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         // this layer and the q/k/v weights of the next one
         {
             const size_t beg = lo_.o, end = l + 1 < L ? y.lay[l + 1].o : lo_.attn_norm;
-            const int slots = B * y.NKV;
+            const int slots = B * y.NKV * at.n_qgrp;
             const int free_wg = 256 - s_launch * slots;
             at.pf_x = slots > 0 && free_wg > slots ? free_wg / slots : 0;
             at.pf = pk + beg;
             const size_t cap = (size_t)at.pf_x * slots * 256 * 16 * 128;
             at.pf_bytes = at.pf_x > 0 ? std::min(end - beg, cap) : 0;
         }
-        PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn(dt, y.HD, QT, at, B, st), "attention");
+        PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn(dt, y.HD, QTw, at, B, st), "attention");
 
         CombineArgs cb{};
         cb.W = W; cb.n_q = y.NQ; cb.head_dim = y.HD; cb.kps = c->kps; cb.s_launch = s_launch; cb.MT = MT;
@@ -487,7 +491,8 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
     c->packed = (char*)packed;
     c->kv = (char*)kv;
     c->ws = (char*)ws;
-    c->kps = 128;
+    c->kps = 256;
+    c->qsplit = -1;
     c->split = cfg->dtype == PBD_DTYPE_BF16;
     hipStream_t st = (hipStream_t)stream;
     const int dt = y.dtype;
@@ -758,6 +763,14 @@ int pbd_set_attn_keys_per_split(pbd_ctx* c, int32_t keys) {
     if (rc) return rc;
     if (keys < 16 || keys % 16 != 0) return fail(c, PBD_ERR_INVALID_ARG, "keys per split must be a positive multiple of 16");
     c->kps = keys;
+    return PBD_OK;
+}
+
+int pbd_set_attn_query_split(pbd_ctx* c, int32_t mode) {
+    int rc = check_ctx(c);
+    if (rc) return rc;
+    if (mode < -1 || mode > 1) return fail(c, PBD_ERR_INVALID_ARG, "query split mode must be -1, 0 or 1");
+    c->qsplit = mode;
     return PBD_OK;
 }
 

@@ -89,6 +89,7 @@ struct AttnArgs {
     int layer, max_batch, n_q, n_kv, nblk, W, G;
     int nqkv;
     int kps, s_launch;
+    int n_qgrp;             // work-groups per (split, KV head, sequence), each over QT query tiles
     // block key i is visible to block row j iff i <= j or j >= full_from
     // (full_from = W: causal; 0: bidirectional); rows j < kv_rows append their K/V
     int full_from, kv_rows, qk_norm;

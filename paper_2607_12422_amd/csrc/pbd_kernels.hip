@@ -618,7 +618,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         asm volatile("" ::"v"(acc));
         return;
     }
-    const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    const int s = blockIdx.x, g = blockIdx.y;
+    const int b = blockIdx.z / a.n_qgrp;
+    const int q0 = (blockIdx.z % a.n_qgrp) * QROWS;      // first query row of this work-group
     const int t = a.pos0[b];
     const int nrows = a.nrows[b];
     int s_pre, chunk;
@@ -699,7 +701,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     RP rp[QSTEPS];
 #pragma unroll
     for (int i = 0; i < QSTEPS; ++i) {
-        const int q = 16 * i + 4 * wid + lgrp;
+        const int q = q0 + 16 * i + 4 * wid + lgrp;
         const int qq = q < QR ? q : 0;
         rp[i].load(qkv_b + (size_t)(qq % W) * row_stride + (size_t)(g * G + qq / W) * HD,
                    rope + (size_t)(t + qq % W) * HALF, lrow);
@@ -723,9 +725,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         gq.get(a.qk_norm, gq_lo, gq_hi);
 #pragma unroll
         for (int i = 0; i < QSTEPS; ++i) {
-            const int q = 16 * i + 4 * wid + lgrp;
+            const int ql = 16 * i + 4 * wid + lgrp;
             T lo[RP::NP], hi[RP::NP];
-            rp[i].finish(q_l + q * LDQ, q < QR, gq_lo, gq_hi, a.qk_norm, a.eps, lrow, lo, hi);
+            rp[i].finish(q_l + ql * LDQ, q0 + ql < QR, gq_lo, gq_hi, a.qk_norm, a.eps, lrow, lo, hi);
         }
         // block keys and values; the verify appends them to the cache
         float gk_lo[RP::NP], gk_hi[RP::NP];
@@ -745,7 +747,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 vd[RP::NP * lrow + p] = vl[p];
                 vd[HALF + RP::NP * lrow + p] = vh[p];
             }
-            if (live && j < a.kv_rows) {
+            if (live && j < a.kv_rows && q0 == 0) {
                 const int pos = t + j;
                 T* kblk = kc + (size_t)(pos / 16) * 16 * HD;
                 T* vblk = vc + (size_t)(pos / 16) * 16 * HD;
@@ -763,9 +765,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         gq.get(a.qk_norm, gq_lo, gq_hi);
 #pragma unroll
         for (int i = 0; i < QSTEPS; ++i) {
-            const int q = 16 * i + 4 * wid + lgrp;
+            const int ql = 16 * i + 4 * wid + lgrp;
             T lo[RP::NP], hi[RP::NP];
-            rp[i].finish(q_l + q * LDQ, q < QR, gq_lo, gq_hi, a.qk_norm, a.eps, lrow, lo, hi);
+            rp[i].finish(q_l + ql * LDQ, q0 + ql < QR, gq_lo, gq_hi, a.qk_norm, a.eps, lrow, lo, hi);
         }
     }
     lds_sync();
@@ -781,7 +783,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     // block row of each of this lane's query columns (for the causal mask)
     int jq[QT];
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) jq[qt] = (qt * 16 + lrow) % W;
+    for (int qt = 0; qt < QT; ++qt) jq[qt] = (q0 + qt * 16 + lrow) % W;
 
     f32x4 o_acc[NDT][QT];
     float m_run[QT], l_run[QT];
@@ -901,7 +903,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     const int S = a.s_launch;
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
-        const int q = qt * 16 + lrow;
+        const int ql = qt * 16 + lrow, q = q0 + ql;     // local and global query row
         if (q >= QR) continue;
         const int gi = q / W, j = q % W;
         const size_t pr = (((size_t)b * a.n_q + g * G + gi) * W + j) * S + s;
@@ -911,7 +913,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
             float L = 0.f;
 #pragma unroll
             for (int w = 0; w < 4; ++w)
-                L += ml_l[(w * QROWS + q) * 2 + 1] * exp2f(ml_l[(w * QROWS + q) * 2] - mx[qt]);
+                L += ml_l[(w * QROWS + ql) * 2 + 1] * exp2f(ml_l[(w * QROWS + ql) * 2] - mx[qt]);
             a.part_ml[pr * 2 + 0] = mx[qt];
             a.part_ml[pr * 2 + 1] = L;
         }
@@ -1391,7 +1393,7 @@ static hipError_t launch_attn_hd(const AttnArgs& a, int qt, dim3 grid, size_t sm
 }
 
 hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int batch, hipStream_t st) {
-    dim3 grid(a.s_launch + a.pf_x, a.n_kv, batch);
+    dim3 grid(a.s_launch + a.pf_x, a.n_kv, batch * a.n_qgrp);
     const size_t smem = attn_smem_bytes(dtype, head_dim, qt);
     if (dtype == PBD_DTYPE_BF16) {
         if (head_dim == 128) return launch_attn_hd<bf16, 128>(a, qt, grid, smem, st);

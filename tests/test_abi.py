@@ -89,6 +89,7 @@ def test_calls_reject_null_context(lib):
     st = ctypes.c_int32()
     assert lib.pbd_sync_status(None, None, ctypes.byref(st)) == b.PBD_ERR_INVALID_ARG
     assert lib.pbd_set_attn_keys_per_split(None, 64) == b.PBD_ERR_INVALID_ARG
+    assert lib.pbd_set_attn_query_split(None, 1) == b.PBD_ERR_INVALID_ARG
     lib.pbd_destroy(None)
 
 

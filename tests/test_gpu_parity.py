@@ -256,3 +256,35 @@ def test_qwen_shape_early_exit_draft_matches_oracle():
         assert err <= 2e-2
         _check_tokens(d.cpu().numpy()[0], ref[1:], 2e-2, exclude=cfg.mask_id)
     g.close()
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("D,t,B", [(16, 40, 1), (3, 33, 1), (16, 100, 3)])
+def test_attention_query_split_matches_oracle(D, t, B, mode):
+    """Attention work-groups over all query rows of a KV head (0) or over 16
+    query rows each (1) give the same passes."""
+    cfg, w = _tiny(D)
+    prompts = synth.make_prompts(cfg, [t + 7 * b for b in range(B)], 200 + t)
+    g = GpuRun(cfg, w, max_batch=B, max_seq=192)
+    g.eng.pbd_set_attn_query_split(mode)
+    g.prefill(prompts)
+    m = om.OracleModel(w)
+    d, dlg = g.draft()
+    v, vlg = g.verify(d)
+    for b, p in enumerate(prompts):
+        st = om.prefill(m, p)
+        _, dl_ref = om.draft(m, st)
+        assert np.abs(dlg.cpu().numpy()[b] - dl_ref).max() <= TOL32
+        _, vl_ref, _, _ = om.verify(m, st, d.cpu().numpy()[b])
+        assert np.abs(vlg.cpu().numpy()[b] - vl_ref).max() <= TOL32
+    # the verify's block K/V reached the cache: the next draft still matches
+    n, out = g.accept(d, v)
+    d2, dlg2 = g.draft()
+    for b, p in enumerate(prompts):
+        st = om.prefill(m, p)
+        _, _, k, vv = om.verify(m, st, d.cpu().numpy()[b])
+        nn, oo = om.accept(d.cpu().numpy()[b], v.cpu().numpy()[b], forced_n=int(n.cpu().numpy()[b]))
+        om.commit(st, nn, oo, k, vv)
+        _, dl_ref = om.draft(m, st)
+        assert np.abs(dlg2.cpu().numpy()[b] - dl_ref).max() <= TOL32
+    g.close()
