@@ -332,15 +332,25 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         at.kcache = c->kv; at.vcache = c->kv + y.kv_half;
         at.part_o = (float*)(ws + y.w_attn_o); at.part_ml = (float*)(ws + y.w_attn_ml);
         // spare CUs during the attention warm the O, gate/up and down weights of
-        // this layer and the q/k/v weights of the next one
+        // this layer and the q/k/v weights of the next one, then the next
+        // layer's K/V of the batch's sequences when that slab is small
         {
             const size_t beg = lo_.o, end = l + 1 < L ? y.lay[l + 1].o : lo_.attn_norm;
             const int slots = B * y.NKV * at.n_qgrp;
             const int free_wg = 256 - s_launch * slots;
             at.pf_x = slots > 0 && free_wg > slots ? free_wg / slots : 0;
-            at.pf = pk + beg;
-            const size_t cap = (size_t)at.pf_x * slots * 256 * 16 * 128;
-            at.pf_bytes = at.pf_x > 0 ? std::min(end - beg, cap) : 0;
+            size_t cap = (size_t)at.pf_x * slots * 256 * 16 * 128;
+            at.pf[0] = pk + beg;
+            at.pf_bytes[0] = std::min(end - beg, cap);
+            cap -= at.pf_bytes[0];
+            const size_t kv_seq = (size_t)y.NKV * y.nblk * 16 * y.HD * y.esz;   // one sequence's K (or V) of a layer
+            const size_t kv_b = (size_t)B * kv_seq;
+            if (l + 1 < L && kv_b <= ((size_t)16 << 20) && 2 * kv_b <= cap) {
+                const size_t off = (size_t)(l + 1) * y.Bmax * kv_seq;
+                at.pf[1] = c->kv + off;
+                at.pf[2] = c->kv + y.kv_half + off;
+                at.pf_bytes[1] = at.pf_bytes[2] = kv_b;
+            }
         }
         PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn(dt, y.HD, QTw, at, B, st), "attention");
 

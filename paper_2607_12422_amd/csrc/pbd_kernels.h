@@ -105,12 +105,12 @@ struct AttnArgs {
     void* vcache;
     float* part_o;          // [B][n_q][W][s_launch][head_dim]
     float* part_ml;         // [B][n_q][W][s_launch][2]
-    // pf_x extra grid columns of work-groups touch [pf, pf + pf_bytes) once per
-    // 128-byte line (at most 16 lines per thread), warming the memory-side
-    // cache for the kernels that follow
+    // pf_x extra grid columns of work-groups touch the ranges [pf[i],
+    // pf[i] + pf_bytes[i]) once per 128-byte line (at most 16 lines per
+    // thread), warming the memory-side cache for the kernels that follow
     int pf_x;
-    const char* pf;
-    size_t pf_bytes;
+    const char* pf[3];
+    size_t pf_bytes[3];
 };
 
 struct CombineArgs {

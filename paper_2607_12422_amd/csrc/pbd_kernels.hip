@@ -597,12 +597,13 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     typedef RowPrep<T, HD> RP;
 
     if ((int)blockIdx.x >= a.s_launch) {
-        // work-groups past the splits warm the memory-side cache with the
-        // weights the next kernels stream (the attention keeps few CUs busy):
-        // one word per 128-byte line of this work-group's share
+        // work-groups past the splits warm the memory-side cache with what
+        // the next kernels read (the attention keeps few CUs busy): one word
+        // per 128-byte line of this work-group's share of the three ranges
         const int n_pf = (gridDim.x - a.s_launch) * gridDim.y * gridDim.z;
         const int ip = ((blockIdx.x - a.s_launch) * gridDim.y + blockIdx.y) * gridDim.z + blockIdx.z;
-        const size_t lines = a.pf_bytes / 128;
+        const size_t n0 = a.pf_bytes[0] / 128, n1 = a.pf_bytes[1] / 128, n2 = a.pf_bytes[2] / 128;
+        const size_t lines = n0 + n1 + n2;
         const size_t per = (lines + n_pf - 1) / n_pf;
         const size_t l0 = (size_t)ip * per, l1 = min(l0 + per, lines);
         constexpr int PFN = 16;
@@ -610,7 +611,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < PFN; ++i) {
             const size_t li = l0 + (size_t)i * blockDim.x + threadIdx.x;
-            v[i] = li < l1 ? *(const unsigned*)(a.pf + li * 128) : 0u;
+            const char* p = li < n0 ? a.pf[0] + li * 128
+                          : li < n0 + n1 ? a.pf[1] + (li - n0) * 128 : a.pf[2] + (li - n0 - n1) * 128;
+            v[i] = li < l1 ? *(const unsigned*)p : 0u;
         }
         unsigned acc = 0;
 #pragma unroll
@@ -682,7 +685,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     // accumulated output happen once per chunk (not at all for the first one).
     // The wave's first chunk of prefix blocks is requested before the query
     // preparation, which it does not depend on.
-    constexpr int CH = 2;
+    constexpr int CH = QT == 1 ? 4 : 2;     // key blocks per chunk (a 16-row work-group has the registers for 4)
     uint4 kn[CH][NDS];
     vraw vn[CH][NDT];
     auto load_chunk = [&](int it0) {
