@@ -628,12 +628,22 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     const int nrows = a.nrows[b];
     int s_pre, chunk;
     attn_splits(t, a.kps, a.s_launch, s_pre, chunk);
-    if (s > s_pre) return;
+    const int W = a.W, G = a.G;
+    const int QR = G * W;
+    if (s > s_pre) {
+        // unused split: mark its partials empty (max -inf, sum 0), so that the
+        // merge can read every split without the sequence's position
+        const int q = q0 + (int)threadIdx.x;
+        if ((int)threadIdx.x < QROWS && q < QR) {
+            const size_t pr = (((size_t)b * a.n_q + g * G + q / W) * W + q % W) * a.s_launch + s;
+            a.part_ml[pr * 2 + 0] = -INFINITY;
+            a.part_ml[pr * 2 + 1] = 0.f;
+        }
+        return;
+    }
     const bool blk = (s == s_pre);                       // the split of the W block keys
     const int k_lo = blk ? t : min(s * chunk, t);
     const int k_hi = blk ? t : min(t, k_lo + chunk);
-    const int W = a.W, G = a.G;
-    const int QR = G * W;
 
     extern __shared__ __align__(16) unsigned char smem[];
     T* q_l = (T*)smem;                                   // [QROWS][LDQ]
@@ -1069,26 +1079,20 @@ __global__ __launch_bounds__(256, 2) void k_lmhead(FGemmArgs a) {
 }
 
 // Merge the split-KV partials of one (block row, query head) and write the
-// O-projection operand.
-template <typename T>
+// O-projection operand.  SMAX > 0: all s_launch <= SMAX splits are read at
+// once (unused ones carry max -inf and contribute nothing), so no load waits
+// for the sequence's position; SMAX = 0: the active splits only.
+template <typename T, int SMAX>
 __global__ void k_combine(CombineArgs a) {
     // thread: EPL consecutive dims d0.. of head h for block row m
     constexpr int EPL = Elt<T>::EPL;
     const int m = blockIdx.x, h = blockIdx.y, d0 = threadIdx.x * EPL;
     const int b = m / a.W, j = m % a.W;
-    int s_pre, chunk;
-    attn_splits(a.pos0[b], a.kps, a.s_launch, s_pre, chunk);
-    const int s_eff = s_pre + 1;
     const size_t pr0 = (((size_t)b * a.n_q + h) * a.W + j) * a.s_launch;
-    float mx = -1e30f;
-    for (int s = 0; s < s_eff; ++s) mx = fmaxf(mx, a.part_ml[(pr0 + s) * 2]);
     float L = 0.f, o[EPL];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) o[i] = 0.f;
-    for (int s = 0; s < s_eff; ++s) {
-        const float wgt = exp2f(a.part_ml[(pr0 + s) * 2] - mx);
-        L += wgt * a.part_ml[(pr0 + s) * 2 + 1];
-        const float4* src = (const float4*)(a.part_o + (pr0 + s) * a.head_dim + d0);
+    auto add = [&](float wgt, const float4* src) {
 #pragma unroll
         for (int q = 0; q < EPL / 4; ++q) {
             const float4 v = src[q];
@@ -1096,6 +1100,40 @@ __global__ void k_combine(CombineArgs a) {
             o[4 * q + 1] += wgt * v.y;
             o[4 * q + 2] += wgt * v.z;
             o[4 * q + 3] += wgt * v.w;
+        }
+    };
+    if (SMAX > 0) {
+        float ms[SMAX > 0 ? SMAX : 1], ls[SMAX > 0 ? SMAX : 1];
+        float4 ov[SMAX > 0 ? SMAX : 1][EPL / 4];
+#pragma unroll
+        for (int s = 0; s < SMAX; ++s) {
+            const int sc = s < a.s_launch ? s : 0;        // valid index; weight 0 below
+            ms[s] = a.part_ml[(pr0 + sc) * 2];
+            ls[s] = a.part_ml[(pr0 + sc) * 2 + 1];
+#pragma unroll
+            for (int q = 0; q < EPL / 4; ++q) ov[s][q] = ((const float4*)(a.part_o + (pr0 + sc) * a.head_dim + d0))[q];
+        }
+        float mx = -1e30f;
+#pragma unroll
+        for (int s = 0; s < SMAX; ++s)
+            if (s < a.s_launch) mx = fmaxf(mx, ms[s]);
+#pragma unroll
+        for (int s = 0; s < SMAX; ++s) {
+            if (s >= a.s_launch || !(ms[s] > -INFINITY)) continue;
+            const float wgt = exp2f(ms[s] - mx);
+            L += wgt * ls[s];
+            add(wgt, ov[s]);
+        }
+    } else {
+        int s_pre, chunk;
+        attn_splits(a.pos0[b], a.kps, a.s_launch, s_pre, chunk);
+        const int s_eff = s_pre + 1;
+        float mx = -1e30f;
+        for (int s = 0; s < s_eff; ++s) mx = fmaxf(mx, a.part_ml[(pr0 + s) * 2]);
+        for (int s = 0; s < s_eff; ++s) {
+            const float wgt = exp2f(a.part_ml[(pr0 + s) * 2] - mx);
+            L += wgt * a.part_ml[(pr0 + s) * 2 + 1];
+            add(wgt, (const float4*)(a.part_o + (pr0 + s) * a.head_dim + d0));
         }
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
@@ -1418,8 +1456,16 @@ hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int b
 hipError_t launch_assemble(int dtype, const AssembleArgs& a, int batch, hipStream_t st) {
     PBD_DISPATCH(dtype, k_assemble, dim3(a.W, batch), dim3(256), st, a);
 }
+template <typename T>
+static hipError_t launch_combine_t(const CombineArgs& a, int M, hipStream_t st) {
+    const dim3 grid(M, a.n_q), block(a.head_dim / Elt<T>::EPL);
+    if (a.s_launch <= 4) PBD_LAUNCH((k_combine<T, 4>), grid, block, 0, st, a);
+    else if (a.s_launch <= 8) PBD_LAUNCH((k_combine<T, 8>), grid, block, 0, st, a);
+    else PBD_LAUNCH((k_combine<T, 0>), grid, block, 0, st, a);
+    return hipGetLastError();
+}
 hipError_t launch_combine(int dtype, const CombineArgs& a, int M, hipStream_t st) {
-    PBD_DISPATCH(dtype, k_combine, dim3(M, a.n_q), dim3(a.head_dim / (dtype == PBD_DTYPE_BF16 ? Elt<bf16>::EPL : Elt<float>::EPL)), st, a);
+    return dtype == PBD_DTYPE_BF16 ? launch_combine_t<bf16>(a, M, st) : launch_combine_t<float>(a, M, st);
 }
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st) {
     PBD_DISPATCH(dtype, k_pack, dim3(1024), dim3(256), st, a);

@@ -21,7 +21,7 @@ HOT = [
     r"_ZN3pbd7k_fgemmIDF16bLi\d+ELi\d+ELb1ELi[01]EEEvNS_9FGemmArgsE",
     r"_ZN3pbd6k_attnIDF16bLi128ELi[123]EEEvNS_8AttnArgsE",            # attention, G*W <= 48 query rows
     r"_ZN3pbd8k_lmheadIDF16bLb1ELb[01]EEEvNS_9FGemmArgsE",            # LM head (with / without confidence)
-    r"_ZN3pbd9k_combineIDF16bEEvNS_11CombineArgsE",
+    r"_ZN3pbd9k_combineIDF16bLi\d+EEEvNS_11CombineArgsE",
     r"_ZN3pbd10k_assembleIDF16bEEvNS_12AssembleArgsE",
     r"_ZN3pbd8k_argmaxENS_10ArgmaxArgsE",
     r"_ZN3pbd8k_acceptENS_10AcceptArgsE",
