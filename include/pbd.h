@@ -110,6 +110,9 @@ typedef struct pbd_config {
     int32_t dtype;          /* PBD_DTYPE_F32 or PBD_DTYPE_BF16 */
     int32_t max_batch;      /* sequences per call */
     int32_t max_seq;        /* KV capacity per sequence (positions) */
+    int32_t prefill_chunk;  /* prompt rows per sequence per prefill pass: 0 (= D + 1) or
+                               in [1, 1024]; max_batch * max(D + 1, prefill_chunk) <= 4096.
+                               The workspace grows with it. */
 } pbd_config;
 
 /*
@@ -154,6 +157,10 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon,
  * [1, max_len] and with lengths[b] + D + 1 <= max_seq.  Writes the prompt K/V to
  * the cache, seq_len[b] = lengths[b] and anchor[b] = greedy next token (device
  * int32 [batch] each), which is the first generated token.
+ * The prompt runs in chunks of cfg.prefill_chunk rows per sequence (D + 1 if
+ * 0): per chunk, the projections run as one GEMM over batch * chunk rows, the
+ * chunk's K/V are appended to the cache first, and attention reads every key
+ * from the cache with a causal mask inside the chunk.
  */
 int pbd_prefill(pbd_ctx* ctx, int32_t batch, const int32_t* tokens, const int32_t* lengths,
                 int32_t max_len, int32_t* seq_len, int32_t* anchor, pbd_stream_t stream);

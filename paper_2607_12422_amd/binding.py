@@ -56,7 +56,7 @@ class PbdConfig(ctypes.Structure):
         ("vocab", ctypes.c_int32), ("lora_rank", ctypes.c_int32), ("lora_alpha", ctypes.c_float),
         ("block", ctypes.c_int32), ("mask_id", ctypes.c_int32), ("rms_eps", ctypes.c_float),
         ("rope_theta", ctypes.c_float), ("qk_norm", ctypes.c_int32), ("dtype", ctypes.c_int32),
-        ("max_batch", ctypes.c_int32), ("max_seq", ctypes.c_int32),
+        ("max_batch", ctypes.c_int32), ("max_seq", ctypes.c_int32), ("prefill_chunk", ctypes.c_int32),
     ]
 
 
@@ -125,7 +125,7 @@ class PbdError(RuntimeError):
         self.code = code
 
 
-def make_config(cfg, max_batch: int, max_seq: int) -> PbdConfig:
+def make_config(cfg, max_batch: int, max_seq: int, prefill_chunk: int = 0) -> PbdConfig:
     """pbd_config from a model description with the attribute names of pbd_config."""
     return PbdConfig(
         n_layers=cfg.n_layers, hidden=cfg.hidden, n_q_heads=cfg.n_q_heads, n_kv_heads=cfg.n_kv_heads,
@@ -133,7 +133,7 @@ def make_config(cfg, max_batch: int, max_seq: int) -> PbdConfig:
         lora_alpha=cfg.lora_alpha, block=cfg.block, mask_id=cfg.mask_id, rms_eps=cfg.rms_eps,
         rope_theta=cfg.rope_theta, qk_norm=1 if cfg.qk_norm else 0,
         dtype=PBD_DTYPE_BF16 if cfg.dtype == "bf16" else PBD_DTYPE_F32,
-        max_batch=max_batch, max_seq=max_seq)
+        max_batch=max_batch, max_seq=max_seq, prefill_chunk=prefill_chunk)
 
 
 def _ptr(t) -> Optional[int]:
@@ -181,11 +181,12 @@ class Engine:
     library itself never allocates device memory.
     """
 
-    def __init__(self, cfg, dev_weights, max_batch: int, max_seq: int, device="cuda:0", stream=None):
+    def __init__(self, cfg, dev_weights, max_batch: int, max_seq: int, device="cuda:0", stream=None,
+                 prefill_chunk: int = 0):
         import torch
         self.lib = load_library()
         self.cfg = cfg
-        self.pcfg = make_config(cfg, max_batch, max_seq)
+        self.pcfg = make_config(cfg, max_batch, max_seq, prefill_chunk)
         self.device = torch.device(device)
         nb = self.lib.pbd_packed_weight_bytes(ctypes.byref(self.pcfg))
         if nb == 0:

@@ -21,17 +21,18 @@ thread_local std::string g_init_error;
 
 constexpr int MAX_DIM = 16384;   // bound on hidden, ffn and n_q_heads*head_dim
 constexpr int LMHEAD_GRID = 512;  // work-groups of the persistent LM head (two per CU)
+constexpr int PREFILL_KPS = 1024; // keys per attention split in prefill chunks (many query groups)
 constexpr size_t MAX_LDS = 160 * 1024;   // LDS one gfx950 work-group may allocate
 
 // Every size and offset the library uses, derived from a validated config.
 struct Layout {
-    int L, H, NQ, NKV, HD, F, V, r, D, W, Bmax, max_seq, dtype;
+    int L, H, NQ, NKV, HD, F, V, r, D, W, Wp, Bmax, max_seq, dtype;   // Wp: prefill rows per pass
     size_t esz;
     int FK, EPL;
     int Mmax, MTmax, RT, nblk, G, QTmax;
     int kb_qkv, kb_o, kb_gu, kb_d, kb_e;
     int tiles_qkv, tiles_o, tiles_gu, tiles_d, tiles_e;
-    int nqkv, S_max;
+    int nqkv, S_max, S_pre;   // attention splits: step passes, prefill chunks
     // packed weights (bytes)
     struct LayerOff {
         size_t qkv, o, gu, d, attn_norm, mlp_norm, q_norm, k_norm;
@@ -81,7 +82,11 @@ int validate(const pbd_config* c, std::string& err) {
             "lora_rank %d must be a multiple of 8 in [0, 64]", c->lora_rank);
     PBD_REQ(c->lora_rank == 0 || c->lora_alpha > 0.f, PBD_ERR_INVALID_ARG, "lora_alpha must be positive");
     PBD_REQ(c->rms_eps > 0.f && c->rope_theta > 0.f, PBD_ERR_INVALID_ARG, "rms_eps and rope_theta must be positive");
-    PBD_REQ(c->max_batch >= 1 && c->max_batch * W <= 4096, PBD_ERR_CAPACITY, "max_batch %d too large", c->max_batch);
+    PBD_REQ(c->prefill_chunk >= 0 && c->prefill_chunk <= 1024, PBD_ERR_SHAPE,
+            "prefill_chunk %d outside [0, 1024]", c->prefill_chunk);
+    const int Wp = c->prefill_chunk > 0 ? c->prefill_chunk : W;
+    PBD_REQ(c->max_batch >= 1 && c->max_batch * std::max(W, Wp) <= 4096, PBD_ERR_CAPACITY,
+            "max_batch %d too large for the pass widths", c->max_batch);
     PBD_REQ(c->max_seq > W && c->max_seq <= (1 << 20), PBD_ERR_CAPACITY, "max_seq %d out of range", c->max_seq);
     const int qt = cdiv(G * W, 16);
     PBD_REQ(attn_smem_bytes(c->dtype, c->head_dim, qt) <= MAX_LDS, PBD_ERR_SHAPE, "attention tile does not fit in LDS");
@@ -92,11 +97,12 @@ int validate(const pbd_config* c, std::string& err) {
 void make_layout(const pbd_config* c, Layout& y) {
     y.L = c->n_layers; y.H = c->hidden; y.NQ = c->n_q_heads; y.NKV = c->n_kv_heads; y.HD = c->head_dim;
     y.F = c->ffn; y.V = c->vocab; y.r = c->lora_rank; y.D = c->block; y.W = c->block + 1;
+    y.Wp = c->prefill_chunk > 0 ? c->prefill_chunk : y.W;
     y.Bmax = c->max_batch; y.max_seq = c->max_seq; y.dtype = c->dtype;
     y.esz = c->dtype == PBD_DTYPE_BF16 ? 2 : 4;
     y.EPL = (int)(16 / y.esz);
     y.FK = 4 * y.EPL;
-    y.Mmax = y.Bmax * y.W;
+    y.Mmax = y.Bmax * std::max(y.W, y.Wp);
     y.MTmax = cdiv(y.Mmax, 16);
     y.RT = cdiv(y.r, 16);
     y.nblk = cdiv(y.max_seq, 16);
@@ -106,6 +112,7 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.kb_qkv = y.H / y.FK; y.kb_o = y.NQ * y.HD / y.FK; y.kb_gu = y.H / y.FK; y.kb_d = y.F / y.FK; y.kb_e = y.H / y.FK;
     y.tiles_qkv = y.nqkv / 16; y.tiles_o = y.H / 16; y.tiles_gu = 2 * y.F / 16; y.tiles_d = y.H / 16; y.tiles_e = y.V / 16;
     y.S_max = std::min(64, cdiv(y.max_seq, 16)) + 1;   // prefix splits + the block split
+    y.S_pre = std::min(y.S_max, cdiv(y.max_seq, PREFILL_KPS) + 1);
 
     const size_t FR = 1024;                       // bytes per fragment
     const size_t EB = (size_t)64 * 4 * y.esz;     // bytes per LoRA expand block
@@ -148,7 +155,7 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.w_xo[0] = take(y.kb_o * xfr);   y.w_xo[1] = take(nlo * y.kb_o * xfr);
     y.w_xm[0] = take(y.kb_gu * xfr);  y.w_xm[1] = take(nlo * y.kb_gu * xfr);
     y.w_xd[0] = take(y.kb_d * xfr);   y.w_xd[1] = take(nlo * y.kb_d * xfr);
-    const size_t nrow_part = (size_t)y.Bmax * y.NQ * y.W * y.S_max;
+    const size_t nrow_part = (size_t)y.Bmax * y.NQ * std::max((size_t)y.W * y.S_max, (size_t)y.Wp * y.S_pre);
     y.w_attn_o = take(nrow_part * y.HD * 4);
     y.w_attn_ml = take(nrow_part * 2 * 4);
     y.w_arg_val = take((size_t)y.tiles_e * y.Mmax * 4);
@@ -260,11 +267,13 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     char* ws = c->ws;
     char* pk = c->packed;
     const int dt = y.dtype;
-    const int W = q.no_anchor ? y.D : y.W, B = q.B, M = B * W, MT = cdiv(M, 16);
-    const int lead = (q.mode == PASS_PREFILL || q.no_anchor) ? 0 : 1;
+    const bool pre = q.mode == PASS_PREFILL;         // prefill chunk: K/V appended first, chunk-mode attention
+    const int W = pre ? y.Wp : (q.no_anchor ? y.D : y.W), B = q.B, M = B * W, MT = cdiv(M, 16);
+    const int lead = (pre || q.no_anchor) ? 0 : 1;
     const int QT = cdiv(y.G * W, 16);              // query tiles per (KV head, sequence)
-    const int s_launch = std::min(y.S_max, cdiv(y.max_seq, c->kps) + 1);   // split-KV grid columns
-    const bool qsplit = c->qsplit > 0 || (c->qsplit < 0 && B * y.NKV * s_launch < 256);
+    const int kps = pre ? std::max(c->kps, PREFILL_KPS) : c->kps;
+    const int s_launch = pre ? y.S_pre : std::min(y.S_max, cdiv(y.max_seq, kps) + 1);   // split-KV grid columns
+    const bool qsplit = pre || c->qsplit > 0 || (c->qsplit < 0 && B * y.NKV * s_launch < 256);
     const int QTw = qsplit ? 1 : QT;                // ... per attention work-group
     const float scale = y.r > 0 ? c->cfg.lora_alpha / (float)y.r : 0.f;
     const bool lora = q.adapter && y.r > 0;
@@ -281,7 +290,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     AssembleArgs as{};
     as.mode = q.mode; as.W = W; as.H = y.H; as.vocab = y.V; as.mask_id = c->cfg.mask_id; as.max_seq = y.max_seq;
     as.chunk_pos = q.chunk_pos; as.max_len = q.max_len; as.MT = MT; as.m_stride = y.Mmax;
-    as.lead = lead; as.pos_add = q.no_anchor ? 1 : 0;
+    as.lead = lead; as.pos_add = q.no_anchor ? 1 : 0; as.room = y.W;
     as.seq_len = q.seq_len; as.anchor = q.anchor; as.drafts = q.drafts; as.prompt = q.prompt; as.lengths = q.lengths;
     as.tokens = (int*)(ws + y.w_tokens); as.pos0 = pos0; as.nrows = nrows; as.status = status;
     as.embed = pk + y.p_embed; as.gain = pk + y.lay[0].attn_norm; as.x = x;
@@ -321,9 +330,10 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
 
         AttnArgs at{};
         at.layer = l; at.max_batch = y.Bmax; at.n_q = y.NQ; at.n_kv = y.NKV; at.nblk = y.nblk; at.W = W; at.G = y.G;
-        at.nqkv = y.nqkv; at.kps = c->kps; at.s_launch = s_launch; at.n_qgrp = QT / QTw;
+        at.nqkv = y.nqkv; at.kps = kps; at.s_launch = s_launch; at.n_qgrp = QT / QTw;
         at.full_from = q.causal ? W : (q.anchor_cached ? 1 : 0);
-        at.kv_rows = q.write_kv ? W : (q.anchor_cached ? 1 : 0);
+        at.kv_rows = pre ? 0 : q.write_kv ? W : (q.anchor_cached ? 1 : 0);
+        at.chunk = pre ? 1 : 0;
         at.qk_norm = c->cfg.qk_norm ? 1 : 0;
         at.eps = c->cfg.rms_eps; at.scale_log2 = (float)(1.0 / sqrt((double)y.HD) * 1.4426950408889634);
         at.smem_main = attn_smem_main(dt, y.HD, QTw);
@@ -352,10 +362,18 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
                 at.pf_bytes[1] = at.pf_bytes[2] = kv_b;
             }
         }
+        if (pre) {
+            KVWriteArgs kw{};
+            kw.layer = l; kw.max_batch = y.Bmax; kw.n_q = y.NQ; kw.n_kv = y.NKV; kw.nblk = y.nblk; kw.W = W;
+            kw.nqkv = y.nqkv; kw.qk_norm = c->cfg.qk_norm ? 1 : 0; kw.eps = c->cfg.rms_eps;
+            kw.pos0 = pos0; kw.nrows = nrows; kw.qkv = at.qkv; kw.k_norm = at.k_norm; kw.rope = at.rope;
+            kw.kcache = at.kcache; kw.vcache = at.vcache;
+            PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_kvwrite(dt, y.HD, kw, B, st), "prefill K/V");
+        }
         PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn(dt, y.HD, QTw, at, B, st), "attention");
 
         CombineArgs cb{};
-        cb.W = W; cb.n_q = y.NQ; cb.head_dim = y.HD; cb.kps = c->kps; cb.s_launch = s_launch; cb.MT = MT;
+        cb.W = W; cb.n_q = y.NQ; cb.head_dim = y.HD; cb.kps = kps; cb.s_launch = s_launch; cb.MT = MT;
         cb.pos0 = pos0; cb.part_o = at.part_o; cb.part_ml = at.part_ml;
         cb.op_hi = hi(y.w_xo); cb.op_lo = lo(y.w_xo);
         PBD_TIMED(c, st, PBD_KCLASS_COMBINE, launch_combine(dt, cb, M, st), "attention combine");
@@ -620,7 +638,7 @@ int pbd_prefill(pbd_ctx* c, int32_t batch, const int32_t* tokens, const int32_t*
     if (!tokens || !lengths || !seq_len || !anchor) return fail(c, PBD_ERR_INVALID_ARG, "NULL pointer argument");
     if (max_len < 1) return fail(c, PBD_ERR_INVALID_ARG, "max_len must be >= 1");
     if (max_len + c->ly.W > c->cfg.max_seq) return fail(c, PBD_ERR_CAPACITY, "max_len + D + 1 exceeds max_seq");
-    const int W = c->ly.W;
+    const int W = c->ly.Wp;                 // prompt rows per pass
     for (int cp = 0; cp < max_len; cp += W) {
         PassReq q{};
         q.mode = PASS_PREFILL; q.B = batch; q.prompt = tokens; q.lengths = lengths; q.max_len = max_len;

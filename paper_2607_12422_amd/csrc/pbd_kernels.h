@@ -24,6 +24,7 @@ struct AssembleArgs {
     int W, H, vocab, mask_id, max_seq;
     int chunk_pos, max_len, MT, m_stride;
     int lead;              // draft/verify: leading anchor rows (1, or 0 for a block of drafts only)
+    int room;              // prefill: rows a prompt must leave free in the cache (D + 1)
     int pos_add;           // draft/verify: the block starts at seq_len + pos_add
     const int* seq_len;    // draft/verify: positions
     const int* anchor;
@@ -111,6 +112,23 @@ struct AttnArgs {
     int pf_x;
     const char* pf[3];
     size_t pf_bytes[3];
+    // chunk mode (prefill): the W block rows' K/V are already in the cache at
+    // positions t..t+nrows-1; every key is read from the cache, causal inside
+    // the chunk; no block split and no K/V writes
+    int chunk;
+};
+
+// Prefill chunk K/V: norm + RoPE of the W rows' keys, appended with the values.
+struct KVWriteArgs {
+    int layer, max_batch, n_q, n_kv, nblk, W, nqkv, qk_norm;
+    float eps;
+    const int* pos0;
+    const int* nrows;
+    const float* qkv;       // [M][nqkv] projections
+    const void* k_norm;
+    const float2* rope;
+    void* kcache;
+    void* vcache;
 };
 
 struct CombineArgs {
@@ -194,6 +212,7 @@ hipError_t launch_argmax(const ArgmaxArgs& a, hipStream_t st);
 bool lmhead_fits(int kb, int MT);
 hipError_t launch_lmhead(int dtype, const FGemmArgs& a, int grid, hipStream_t st);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t st);
+hipError_t launch_kvwrite(int dtype, int head_dim, const KVWriteArgs& a, int batch, hipStream_t st);
 hipError_t launch_remask(const RemaskArgs& a, int batch, hipStream_t st);
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st);
 hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st);

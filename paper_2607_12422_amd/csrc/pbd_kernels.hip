@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256) void k_assemble(AssembleArgs a) {
     bool ok = true;
     if (a.mode == PASS_PREFILL) {
         const int len = a.lengths[b];
-        if (len < 1 || len > a.max_len || len + W > a.max_seq) ok = false;
+        if (len < 1 || len > a.max_len || len + a.room > a.max_seq) ok = false;
         pos0 = a.chunk_pos;
         nrows = ok ? min(max(len - a.chunk_pos, 0), W) : 0;
     } else {
@@ -582,6 +582,49 @@ struct Gains {
     }
 };
 
+// Prefill chunk: per-head RMSNorm and RoPE of the chunk's keys, appended to
+// the cache with the values before the chunk's attention reads them.  One
+// work-group per (16 rows, KV head, sequence); 16 lanes per row.
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void k_kvwrite(KVWriteArgs a) {
+    typedef RowPrep<T, HD> RP;
+    constexpr int NP = RP::NP, HALF = RP::HALF;
+    __shared__ T s_row[16][HD];
+    const int g = blockIdx.y, b = blockIdx.z;
+    const int lane = threadIdx.x % WAVE, wid = threadIdx.x / WAVE;
+    const int lrow = lane % 16, lgrp = lane / 16;
+    const int r = 4 * wid + lgrp;
+    const int j = blockIdx.x * 16 + r;
+    const int t = a.pos0[b], nrows = a.nrows[b];
+    const bool live = j < a.W && j < nrows;
+    const int jj = live ? j : 0;                        // dead rows read a valid row
+    const float* ks = a.qkv + ((size_t)b * a.W + jj) * a.nqkv + (size_t)a.n_q * HD + (size_t)g * HD;
+    const float* vs = ks + (size_t)a.n_kv * HD;
+    RP rk;
+    rk.load(ks, a.rope + (size_t)(t + jj) * HALF, lrow);
+    const typename RP::fv vlo = *(const typename RP::fv*)(vs + NP * lrow);
+    const typename RP::fv vhi = *(const typename RP::fv*)(vs + HALF + NP * lrow);
+    Gains<T, HD> gk;
+    if (a.qk_norm) gk.load(a.k_norm, lrow);
+    float g_lo[NP], g_hi[NP];
+    gk.get(a.qk_norm, g_lo, g_hi);
+    T klo[NP], khi[NP];
+    rk.finish(s_row[r], live, g_lo, g_hi, a.qk_norm, a.eps, lrow, klo, khi);
+    if (!live) return;
+    const int pos = t + j;
+    const size_t head = (((size_t)a.layer * a.max_batch + b) * a.n_kv + g) * a.nblk * 16 * HD;
+    T* kblk = (T*)a.kcache + head + (size_t)(pos / 16) * 16 * HD;
+    T* vblk = (T*)a.vcache + head + (size_t)(pos / 16) * 16 * HD;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        const int i0 = NP * lrow + p;
+        kblk[kblock_elem<T>(pos % 16, i0)] = klo[p];
+        kblk[kblock_elem<T>(pos % 16, i0 + HALF)] = khi[p];
+        vblk[vblock_elem(pos % 16, i0)] = from_f32<T>(vlo[p]);
+        vblk[vblock_elem(pos % 16, i0 + HALF)] = from_f32<T>(vhi[p]);
+    }
+}
+
 template <typename T, int HD, int QT>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     constexpr int FK = Elt<T>::FK;
@@ -626,11 +669,14 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     const int q0 = (blockIdx.z % a.n_qgrp) * QROWS;      // first query row of this work-group
     const int t = a.pos0[b];
     const int nrows = a.nrows[b];
+    // chunk mode (prefill): the chunk's keys are already in the cache; splits
+    // s < s_pre cover keys [0, t + nrows) and there is no block split
+    const int T_keys = a.chunk ? t + nrows : t;
     int s_pre, chunk;
-    attn_splits(t, a.kps, a.s_launch, s_pre, chunk);
+    attn_splits(T_keys, a.kps, a.chunk ? a.s_launch + 1 : a.s_launch, s_pre, chunk);
     const int W = a.W, G = a.G;
     const int QR = G * W;
-    if (s > s_pre) {
+    if (a.chunk ? s >= s_pre : s > s_pre) {
         // unused split: mark its partials empty (max -inf, sum 0), so that the
         // merge can read every split without the sequence's position
         const int q = q0 + (int)threadIdx.x;
@@ -641,9 +687,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         }
         return;
     }
-    const bool blk = (s == s_pre);                       // the split of the W block keys
-    const int k_lo = blk ? t : min(s * chunk, t);
-    const int k_hi = blk ? t : min(t, k_lo + chunk);
+    const bool blk = !a.chunk && s == s_pre;             // the split of the W block keys
+    const int k_lo = blk ? t : min(s * chunk, T_keys);
+    const int k_hi = blk ? t : min(T_keys, k_lo + chunk);
 
     extern __shared__ __align__(16) unsigned char smem[];
     T* q_l = (T*)smem;                                   // [QROWS][LDQ]
@@ -715,7 +761,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < QSTEPS; ++i) {
         const int q = q0 + 16 * i + 4 * wid + lgrp;
-        const int qq = q < QR ? q : 0;
+        const int qq = (q < QR && (q % W) < nrows) ? q : 0;   // dead rows read a valid row
         rp[i].load(qkv_b + (size_t)(qq % W) * row_stride + (size_t)(g * G + qq / W) * HD,
                    rope + (size_t)(t + qq % W) * HALF, lrow);
     }
@@ -831,7 +877,8 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int kk = key0 + lgrp * 4 + e;
-                    const bool ok = it < n_items && (pref ? kk < k_hi : (kk < nrows && (kk <= jq[qt] || jq[qt] >= a.full_from)));
+                    const bool ok = it < n_items && (pref ? (kk < k_hi && (!a.chunk || kk < t || kk - t <= jq[qt]))
+                                                       : (kk < nrows && (kk <= jq[qt] || jq[qt] >= a.full_from)));
                     valid[c][e] = ok;
                     sv[c][e] = sc[e] * sl2;
                     if (ok) mloc = fmaxf(mloc, sv[c][e]);
@@ -1079,9 +1126,9 @@ __global__ __launch_bounds__(256, 2) void k_lmhead(FGemmArgs a) {
 }
 
 // Merge the split-KV partials of one (block row, query head) and write the
-// O-projection operand.  SMAX > 0: all s_launch <= SMAX splits are read at
-// once (unused ones carry max -inf and contribute nothing), so no load waits
-// for the sequence's position; SMAX = 0: the active splits only.
+// O-projection operand.  Every one of the s_launch splits is read (unused ones
+// carry max -inf and contribute nothing), so no load waits for the sequence's
+// position; SMAX > 0: all loads issued at once.
 template <typename T, int SMAX>
 __global__ void k_combine(CombineArgs a) {
     // thread: EPL consecutive dims d0.. of head h for block row m
@@ -1125,13 +1172,12 @@ __global__ void k_combine(CombineArgs a) {
             add(wgt, ov[s]);
         }
     } else {
-        int s_pre, chunk;
-        attn_splits(a.pos0[b], a.kps, a.s_launch, s_pre, chunk);
-        const int s_eff = s_pre + 1;
         float mx = -1e30f;
-        for (int s = 0; s < s_eff; ++s) mx = fmaxf(mx, a.part_ml[(pr0 + s) * 2]);
-        for (int s = 0; s < s_eff; ++s) {
-            const float wgt = exp2f(a.part_ml[(pr0 + s) * 2] - mx);
+        for (int s = 0; s < a.s_launch; ++s) mx = fmaxf(mx, a.part_ml[(pr0 + s) * 2]);
+        for (int s = 0; s < a.s_launch; ++s) {
+            const float ms = a.part_ml[(pr0 + s) * 2];
+            if (!(ms > -INFINITY)) continue;
+            const float wgt = exp2f(ms - mx);
             L += wgt * a.part_ml[(pr0 + s) * 2 + 1];
             add(wgt, (const float4*)(a.part_o + (pr0 + s) * a.head_dim + d0));
         }
@@ -1480,6 +1526,19 @@ hipError_t launch_argmax(const ArgmaxArgs& a, hipStream_t st) {
 hipError_t launch_remask(const RemaskArgs& a, int batch, hipStream_t st) {
     if (a.D < 1 || a.D > 64 || batch < 1) return hipErrorInvalidValue;
     PBD_LAUNCH(k_remask, dim3(batch), dim3(64), 0, st, a);
+    return hipGetLastError();
+}
+hipError_t launch_kvwrite(int dtype, int head_dim, const KVWriteArgs& a, int batch, hipStream_t st) {
+    const dim3 grid((a.W + 15) / 16, a.n_kv, batch), block(256);
+    if (dtype == PBD_DTYPE_BF16) {
+        if (head_dim == 128) PBD_LAUNCH((k_kvwrite<bf16, 128>), grid, block, 0, st, a);
+        else if (head_dim == 64) PBD_LAUNCH((k_kvwrite<bf16, 64>), grid, block, 0, st, a);
+        else return hipErrorInvalidValue;
+    } else {
+        if (head_dim == 128) PBD_LAUNCH((k_kvwrite<float, 128>), grid, block, 0, st, a);
+        else if (head_dim == 64) PBD_LAUNCH((k_kvwrite<float, 64>), grid, block, 0, st, a);
+        else return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t st) {

@@ -19,14 +19,15 @@ def decisive(logits: np.ndarray, tol: float, exclude=None) -> np.ndarray:
 class GpuRun:
     """One engine plus int32 state tensors for B sequences."""
 
-    def __init__(self, cfg, weights, max_batch, max_seq, dev_weights=None):
+    def __init__(self, cfg, weights, max_batch, max_seq, dev_weights=None, prefill_chunk=0):
         import torch
         from paper_2607_12422_amd import Engine, upload_weights
         self.torch = torch
         self.cfg = cfg
         self.dev = torch.device("cuda:0")
         self.dw = dev_weights or upload_weights(weights, cfg.dtype, self.dev)
-        self.eng = Engine(cfg, self.dw, max_batch=max_batch, max_seq=max_seq, device=self.dev)
+        self.eng = Engine(cfg, self.dw, max_batch=max_batch, max_seq=max_seq, device=self.dev,
+                          prefill_chunk=prefill_chunk)
 
     def i32(self, a):
         return self.torch.tensor(np.asarray(a), dtype=self.torch.int32, device=self.dev)

@@ -37,8 +37,8 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_struct_layout_matches_header():
-    # pbd_config: 17 four-byte fields; layer weights: 11 + 14 pointers.
-    assert ctypes.sizeof(b.PbdConfig) == 17 * 4
+    # pbd_config: 18 four-byte fields; layer weights: 11 + 14 pointers.
+    assert ctypes.sizeof(b.PbdConfig) == 18 * 4
     assert ctypes.sizeof(b.PbdLayerWeights) == 25 * ctypes.sizeof(ctypes.c_void_p)
 
 
@@ -57,6 +57,7 @@ def test_buffer_sizes(lib):
 @pytest.mark.parametrize("field,value", [
     ("head_dim", 96), ("hidden", 100), ("vocab", 4095), ("block", 0), ("block", 40),
     ("lora_rank", 12), ("n_kv_heads", 3), ("mask_id", 4096), ("dtype", 7), ("max_seq", 5),
+    ("prefill_chunk", -1), ("prefill_chunk", 1025), ("prefill_chunk", 4096),
 ])
 def test_invalid_config_sizes_are_zero(lib, field, value):
     cfg = b.make_config(synth.TINY, 1, 256)
