@@ -108,6 +108,7 @@ def main():
     ap.add_argument("--no-draft-curve", action="store_true", help="skip the early-exit draft-cost curve")
     ap.add_argument("--no-denoise", action="store_true", help="skip the denoising-steps ablation timings")
     ap.add_argument("--no-unanchored", action="store_true", help="skip the unanchored-drafting ablation timings")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the prefill timings")
     ap.add_argument("--kps", type=int, default=0, help="attention keys per split (0: library default)")
     ap.add_argument("--operands", choices=["bf16", "bf16x2"], default="bf16x2")
     ap.add_argument("--attn-qsplit", type=int, default=-2,
@@ -147,7 +148,6 @@ def main():
     max_seq = max(lengths) + (w_.gen_tokens or 0) + 4 * cfg.width + args.steps + args.warmup + 64
     dw = upload_weights(weights, cfg.dtype, dev)
     eng = Engine(cfg, dw, max_batch=B, max_seq=max_seq, device=dev)
-    del dw
     eng.pbd_set_operand_precision(binding.PBD_OPERANDS_BF16X2 if args.operands == "bf16x2"
                                   else binding.PBD_OPERANDS_BF16)
     if args.kps:
@@ -336,6 +336,53 @@ def main():
             "rows_per_sequence": {"draft": cfg.width, "verify": cfg.block},
             "paper_context": {"note": "Sec. 5.3 (HF loop): anchoring raises the accepted prefix 2.826 -> 3.046 at "
                                       "15.4-15.6 tokens/s; acceptance needs trained weights and is not measured here"}}
+
+    if not args.no_prefill:
+        # Prefill (builds the prefix the steps start from): prompt chunks of
+        # prefill_chunk rows per pass (D + 1 by default), each pass one GEMM
+        # over the chunk's rows per projection.  Timed with HIP events around
+        # the whole call, launches included (prefill is not graph-captured).
+        lin_params = cfg.n_layers * sum(o * i for _, o, i in cfg.linear_shapes())
+
+        def time_prefill(chunk, prm, reps):
+            Lp, Bp = max(len(p) for p in prm), len(prm)
+            e = Engine(cfg, dw, max_batch=Bp, max_seq=Lp + 4 * cfg.width + 64, device=dev, prefill_chunk=chunk)
+            e.pbd_set_operand_precision(binding.PBD_OPERANDS_BF16X2 if args.operands == "bf16x2"
+                                        else binding.PBD_OPERANDS_BF16)
+            pb = np.zeros((Bp, Lp), dtype=np.int32)
+            for bb, p in enumerate(prm):
+                pb[bb, :len(p)] = p
+            tok = torch.tensor(pb, **i32)
+            ln = torch.tensor([len(p) for p in prm], **i32)
+            sl, an = torch.zeros(Bp, **i32), torch.zeros(Bp, **i32)
+            e.pbd_prefill(tok, ln, Lp, sl, an)
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(reps):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                e.pbd_prefill(tok, ln, Lp, sl, an)
+                e1.record(stream)
+                e1.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            e.close()
+            del e
+            return statistics.median(ts)
+
+        def point(chunk, prm, reps):
+            t_ms = time_prefill(chunk, prm, reps)
+            ntok = sum(len(p) for p in prm)
+            return {"chunk": chunk or cfg.width, "ms": round(t_ms, 3), "tokens_per_s": round(ntok / t_ms * 1e3, 1),
+                    "projection_tflops": round(2 * lin_params * ntok / (t_ms * 1e-3) / 1e12, 2)}
+        long_prompt = synth.make_prompts(cfg, [4096], w_.seed(7))
+        result["prefill"] = {
+            "prompt_tokens": sum(lengths),
+            "points": [point(ch, prompts, 5) for ch in (0, 128, 256, 512)],
+            "long_prompt": [point(ch, long_prompt, 3) for ch in (0, 512, 1024)],
+            "note": "projection_tflops counts 2 x linear parameters x prompt tokens (the bf16 value+residual "
+                    "operands run two MFMAs per product; dense bf16 peak 2500 TFLOP/s)"}
+    del dw
 
     if not args.no_profile:
         # Kernel durations: the same draft and verify passes launched directly

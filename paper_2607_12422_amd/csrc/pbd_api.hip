@@ -22,6 +22,7 @@ thread_local std::string g_init_error;
 constexpr int MAX_DIM = 16384;   // bound on hidden, ffn and n_q_heads*head_dim
 constexpr int LMHEAD_GRID = 512;  // work-groups of the persistent LM head (two per CU)
 constexpr int PREFILL_KPS = 1024; // keys per attention split in prefill chunks (many query groups)
+constexpr int BIG_MIN_MT = 16;    // prefill chunks of >= 256 rows use the large-M projection
 constexpr size_t MAX_LDS = 160 * 1024;   // LDS one gfx950 work-group may allocate
 
 // Every size and offset the library uses, derived from a validated config.
@@ -49,6 +50,8 @@ struct Layout {
     size_t w_attn_o, w_attn_ml, w_arg_val, w_arg_idx, w_tokens, w_pos0, w_nrows, w_status, ws_bytes;
     size_t w_kpart, w_kcnt;                          // split-K partial tiles and arrival counters
     size_t w_arg_mx, w_arg_sum;                      // LM-head softmax partials (draft confidence)
+    size_t w_xc[2], w_sqc;                           // prefill: gathered last rows (LM-head operand, Σx² partials)
+    size_t w_big;                                    // prefill: fp32 output of a large-M projection
     size_t w_dn_tok, w_dn_conf;                      // one denoising pass's candidates and confidences
     int ksplit;                                      // K slices of the residual GEMMs
 };
@@ -170,6 +173,10 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.w_arg_mx = take((size_t)y.tiles_e * y.Mmax * 4);
     y.w_arg_sum = take((size_t)y.tiles_e * y.Mmax * 4);
     y.w_dn_tok = take((size_t)y.Bmax * y.D * 4);
+    const size_t xfc = (size_t)cdiv(y.Bmax, 16) * FR;
+    y.w_xc[0] = take(y.kb_e * xfc); y.w_xc[1] = take(nlo * y.kb_e * xfc);
+    y.w_sqc = take((size_t)std::max(y.tiles_d, 1) * y.Bmax * 4);
+    y.w_big = y.Wp > y.W ? take((size_t)y.Mmax * std::max(y.H, 2 * y.F) * 4) : 0;
     y.w_dn_conf = take((size_t)y.Bmax * y.D * 4);
     y.ws_bytes = off;
 }
@@ -315,6 +322,26 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
             g.cnt = (unsigned*)(ws + y.w_kcnt);
         }
     };
+    // prefill chunks of many rows (adapter off): large-M projections, with the
+    // residual / SwiGLU epilogues as row kernels on their fp32 output
+    const bool big = pre && !lora && MT >= BIG_MIN_MT && y.w_big != 0;
+    float* ybig = (float*)(ws + y.w_big);
+    auto big_args = [&](const FGemmArgs& g) {
+        BigGemmArgs b{};
+        b.w = g.w; b.n_tiles = g.n_tiles; b.kb = g.kb; b.xhi = g.xhi; b.xlo = g.xlo; b.M = g.M; b.MT = g.MT;
+        b.sq = g.sq; b.n_sq = g.n_sq; b.sq_stride = g.sq_stride; b.norm_dim = g.norm_dim; b.eps = g.eps;
+        const bool direct = g.out != nullptr;       // q/k/v: straight to the projection buffer
+        b.out = direct ? g.out : ybig;
+        b.ldo = direct ? g.ldo : g.n_tiles * 16;
+        return b;
+    };
+    auto resid_args = [&](const FGemmArgs& g) {
+        ResidRowsArgs r{};
+        r.M = M; r.n_tiles = g.n_tiles; r.ldx = g.ldx; r.ldy = g.n_tiles * 16; r.n_MT = g.n_MT;
+        r.sq_stride = g.sq_stride; r.x = g.x; r.y = ybig; r.gnext = g.gnext;
+        r.nx_hi = g.nx_hi; r.nx_lo = g.nx_lo; r.sq_out = g.sq_out;
+        return r;
+    };
     const int L = q.n_layers > 0 ? q.n_layers : y.L;
     for (int l = 0; l < L; ++l) {
         const Layout::LayerOff& lo_ = y.lay[l];
@@ -326,7 +353,8 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         for (int i = 0; i < 3; ++i) g.la[i] = (const uint4*)(pk + lo_.la[i]);
         g.lb = pk + lo_.lb_qkv;
         g.out = (float*)(ws + y.w_qkv); g.ldo = y.nqkv;
-        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_STORE, st), "qkv gemm");
+        if (big) PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm_big(dt, big_args(g), st), "qkv gemm");
+        else PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_STORE, st), "qkv gemm");
 
         AttnArgs at{};
         at.layer = l; at.max_batch = y.Bmax; at.n_q = y.NQ; at.n_kv = y.NKV; at.nblk = y.nblk; at.W = W; at.G = y.G;
@@ -384,7 +412,12 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.x = x; g.ldx = y.H; g.gnext = pk + lo_.mlp_norm; g.nx_hi = hi(y.w_xm); g.nx_lo = lo(y.w_xm); g.n_MT = MT;
         g.sq_out = sq_m;
         split_k(g);
-        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "o gemm");
+        if (big) {
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm_big(dt, big_args(g), st), "o gemm");
+            PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_resid_rows(dt, resid_args(g), st), "o residual");
+        } else {
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "o gemm");
+        }
 
         // gate/up + SwiGLU: MLP RMSNorm folded in
         base_gemm(g, lo_.gu, y.tiles_gu, y.kb_gu, y.w_xm);
@@ -392,7 +425,15 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.lora_mode = LORA_ROW_HALF; g.la[0] = (const uint4*)(pk + lo_.la[4]); g.la[1] = (const uint4*)(pk + lo_.la[5]);
         g.lb = pk + lo_.lb_gu;
         g.nx_hi = hi(y.w_xd); g.nx_lo = lo(y.w_xd); g.n_MT = MT;
-        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_SWIGLU, st), "gate/up gemm");
+        if (big) {
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm_big(dt, big_args(g), st), "gate/up gemm");
+            SwigluRowsArgs sw{};
+            sw.M = M; sw.n_tiles = g.n_tiles; sw.ldy = 2 * y.F; sw.n_MT = MT;
+            sw.y = (const float*)(ws + y.w_big); sw.nx_hi = g.nx_hi; sw.nx_lo = g.nx_lo;
+            PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_swiglu_rows(dt, sw, st), "swiglu");
+        } else {
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_SWIGLU, st), "gate/up gemm");
+        }
 
         // down projection + residual; writes the next layer's (or the final) RMSNorm operand
         base_gemm(g, lo_.d, y.tiles_d, y.kb_d, y.w_xd);
@@ -401,13 +442,31 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.gnext = l + 1 < L ? pk + y.lay[l + 1].attn_norm : pk + y.p_final_norm;
         g.nx_hi = hi(y.w_xa); g.nx_lo = lo(y.w_xa); g.n_MT = MT; g.sq_out = sq_a;
         split_k(g);
-        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "down gemm");
+        if (big) {
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm_big(dt, big_args(g), st), "down gemm");
+            PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_resid_rows(dt, resid_args(g), st), "down residual");
+        } else {
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "down gemm");
+        }
     }
 
-    // tied LM head with the final RMSNorm folded in, fused argmax
+    // tied LM head with the final RMSNorm folded in, fused argmax (prefill:
+    // on each sequence's last prompt row only, gathered into a compact operand)
     FGemmArgs ge;
     base_gemm(ge, y.p_embed, y.tiles_e, y.kb_e, y.w_xa);
     ge.lora = 0; ge.sq = sq_a; ge.n_sq = y.tiles_d;
+    int lm_MT = MT;
+    if (pre) {
+        GatherArgs ga{};
+        ga.W = W; ga.MT = MT; ga.MTc = cdiv(B, 16); ga.kb = y.kb_e; ga.n_sq = y.tiles_d; ga.sq_stride = y.Mmax;
+        ga.sqc_stride = y.Bmax; ga.chunk_pos = q.chunk_pos; ga.lengths = q.lengths; ga.nrows = nrows;
+        ga.x_hi = hi(y.w_xa); ga.x_lo = lo(y.w_xa); ga.sq = sq_a;
+        ga.c_hi = hi(y.w_xc); ga.c_lo = lo(y.w_xc); ga.c_sq = (float*)(ws + y.w_sqc);
+        PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_gather_last(dt, ga, B, st), "gather last rows");
+        lm_MT = ga.MTc;
+        ge.M = B; ge.MT = lm_MT; ge.xhi = (const uint4*)ga.c_hi; ge.xlo = (const uint4*)ga.c_lo;
+        ge.sq = ga.c_sq; ge.sq_stride = y.Bmax; ge.W = 1; ge.excl_from = 1;
+    }
     ge.logits = q.logits; ge.ldo = y.V;
     ge.arg_val = (float*)(ws + y.w_arg_val); ge.arg_idx = (int*)(ws + y.w_arg_idx);
     ge.exclude = q.mode == PASS_DRAFT ? c->cfg.mask_id : -1;
@@ -416,7 +475,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         ge.arg_sum = (float*)(ws + y.w_arg_sum);
     }
     int n_part = y.tiles_e;
-    if (lmhead_fits(y.kb_e, MT)) {
+    if (lmhead_fits(y.kb_e, lm_MT)) {
         n_part = std::min(y.tiles_e, LMHEAD_GRID);
         PBD_TIMED(c, st, PBD_KCLASS_LMHEAD, launch_lmhead(dt, ge, n_part, st), "lm head");
     } else {
@@ -424,7 +483,8 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     }
 
     ArgmaxArgs am{};
-    am.M = M; am.W = W; am.n_tiles = n_part; am.mode = q.mode; am.chunk_pos = q.chunk_pos;
+    am.M = pre ? B : M; am.W = pre ? 1 : W; am.n_tiles = n_part; am.mode = q.mode; am.chunk_pos = q.chunk_pos;
+    am.compact = pre ? 1 : 0;
     am.arg_val = ge.arg_val; am.arg_idx = ge.arg_idx; am.out = q.out_tokens;
     am.lengths = q.lengths; am.nrows = nrows; am.seq_len_out = q.seq_len_out;
     am.arg_mx = ge.arg_mx; am.arg_sum = ge.arg_sum; am.conf = q.conf;

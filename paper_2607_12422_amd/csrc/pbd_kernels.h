@@ -131,6 +131,56 @@ struct KVWriteArgs {
     void* vcache;
 };
 
+// Prefill: each sequence's last prompt row of the chunk (final-norm operand
+// fragments and row sum-of-squares partials) gathered into row b of a compact
+// operand, so the LM head runs on batch rows only.
+struct GatherArgs {
+    int W, MT, MTc, kb, n_sq, sq_stride, sqc_stride, chunk_pos;
+    const int* lengths;
+    const int* nrows;
+    const void* x_hi;       // operand fragments [kb][MT]
+    const void* x_lo;
+    const float* sq;        // [n_sq][sq_stride]
+    void* c_hi;             // compact operand fragments [kb][MTc]
+    void* c_lo;
+    float* c_sq;            // [n_sq][sqc_stride]
+};
+
+// Large-M projection (prefill chunks): out[m][16 t + r] = r_m * (W x_m)[16 t + r]
+// for every row m and weight tile t, on the same packed operands as FGemmArgs.
+struct BigGemmArgs {
+    const uint4* w;         // weight tiles [n_tiles][kb] fragments
+    int n_tiles, kb;
+    const uint4* xhi;       // operand fragments [kb][MT]
+    const uint4* xlo;       // residual fragments or null
+    int M, MT;
+    const float* sq;        // RMSNorm partials [n_sq][sq_stride]; n_sq = 0: r_m = 1
+    int n_sq, sq_stride, norm_dim;
+    float eps;
+    float* out;             // [M][ldo] fp32
+    int ldo;
+};
+
+// Residual epilogue of a large-M projection: x += y over 16-column tiles, the
+// next operand x * g_next and the per-tile row sums of squares.
+struct ResidRowsArgs {
+    int M, n_tiles, ldx, ldy, n_MT, sq_stride;
+    float* x;
+    const float* y;
+    const void* gnext;
+    void* nx_hi;
+    void* nx_lo;
+    float* sq_out;
+};
+
+// SwiGLU epilogue of a large-M gate/up projection (tile rows 0-7 gate, 8-15 up).
+struct SwigluRowsArgs {
+    int M, n_tiles, ldy, n_MT;
+    const float* y;
+    void* nx_hi;
+    void* nx_lo;
+};
+
 struct CombineArgs {
     int W, n_q, head_dim, kps, s_launch, MT;
     const int* pos0;
@@ -146,6 +196,7 @@ struct ArgmaxArgs {
     int* out0;              // draft: argmax of row 0 when lead = 1 (null: dropped), at out0[b * out0_stride]
     int out0_stride;
     int out_stride, out_off;  // verify: out[b * out_stride + out_off + j]
+    int compact;            // prefill: row m is sequence m's last prompt row (gathered), if in this chunk
     const float* arg_val;
     const int* arg_idx;
     int* out;
@@ -213,6 +264,10 @@ bool lmhead_fits(int kb, int MT);
 hipError_t launch_lmhead(int dtype, const FGemmArgs& a, int grid, hipStream_t st);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t st);
 hipError_t launch_kvwrite(int dtype, int head_dim, const KVWriteArgs& a, int batch, hipStream_t st);
+hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStream_t st);
+hipError_t launch_gemm_big(int dtype, const BigGemmArgs& a, hipStream_t st);   // split iff a.xlo
+hipError_t launch_resid_rows(int dtype, const ResidRowsArgs& a, hipStream_t st);
+hipError_t launch_swiglu_rows(int dtype, const SwigluRowsArgs& a, hipStream_t st);
 hipError_t launch_remask(const RemaskArgs& a, int batch, hipStream_t st);
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st);
 hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st);

@@ -1250,6 +1250,12 @@ __global__ __launch_bounds__(256) void k_argmax(ArgmaxArgs a) {
         }
     } else if (a.mode == PASS_VERIFY) {
         a.out[b * a.out_stride + a.out_off + j] = tok;
+    } else if (a.compact) {
+        const int r = a.lengths[m] - 1 - a.chunk_pos;  // row m: sequence m's gathered last row
+        if (r >= 0 && r < a.nrows[m]) {
+            a.out[m] = tok;                     // anchor
+            a.seq_len_out[m] = a.lengths[m];
+        }
     } else {
         if (a.chunk_pos + j == a.lengths[b] - 1 && j < a.nrows[b]) {
             a.out[b] = tok;                     // anchor
@@ -1541,6 +1547,191 @@ hipError_t launch_kvwrite(int dtype, int head_dim, const KVWriteArgs& a, int bat
     }
     return hipGetLastError();
 }
+template <typename T>
+__global__ __launch_bounds__(256) void k_gather_last(GatherArgs a) {
+    constexpr int EPL = Elt<T>::EPL, FK = Elt<T>::FK;
+    const int b = blockIdx.x;
+    const int r = a.lengths[b] - 1 - a.chunk_pos;
+    const int row = (r >= 0 && r < a.nrows[b]) ? r : 0;  // out of this chunk: any valid row (unused)
+    const int m = b * a.W + row;
+    for (int idx = threadIdx.x; idx < a.kb * (FK / EPL); idx += blockDim.x) {
+        const int f = idx / (FK / EPL), k = (idx % (FK / EPL)) * EPL;
+        const size_t src = frag_elem<T>((size_t)f * a.MT + m / 16, m % 16, k);
+        const size_t dst = frag_elem<T>((size_t)f * a.MTc + b / 16, b % 16, k);
+        *(uint4*)((T*)a.c_hi + dst) = *(const uint4*)((const T*)a.x_hi + src);
+        if (a.x_lo) *(uint4*)((T*)a.c_lo + dst) = *(const uint4*)((const T*)a.x_lo + src);
+    }
+    for (int p = threadIdx.x; p < a.n_sq; p += blockDim.x) a.c_sq[(size_t)p * a.sqc_stride + b] = a.sq[(size_t)p * a.sq_stride + m];
+}
+
+hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStream_t st) {
+    if (dtype == PBD_DTYPE_BF16) PBD_LAUNCH(k_gather_last<bf16>, dim3(batch), dim3(256), 0, st, a);
+    else PBD_LAUNCH(k_gather_last<float>, dim3(batch), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Large-M projection for prefill chunks.  The skinny GEMM above streams each
+// weight tile once against every row; with hundreds of rows it would re-read
+// the operand per weight tile and wait a full load latency per 64-row group.
+// Here a work-group owns a 64-row x 64-column output block (4 x 4 MFMA tiles,
+// a 2 x 2 tile quadrant per wave) and walks K with BG_P fragment steps of
+// loads in flight; r_m (the folded RMSNorm) scales rows in the epilogue and
+// the fp32 result goes to out.  Residual and SwiGLU epilogues run after it as
+// row kernels.
+// ---------------------------------------------------------------------------
+constexpr int BG_MT = 4, BG_NT = 4, BG_P = 4;
+
+template <typename T, bool SPLIT>
+__global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
+    const int lane = threadIdx.x % WAVE, wid = threadIdx.x / WAVE;
+    const int lrow = lane % 16, lgrp = lane / 16;
+    const int mt0 = blockIdx.y * BG_MT + (wid / 2) * 2, nt0 = blockIdx.x * BG_NT + (wid % 2) * 2;
+    __shared__ float s_part[4][BG_MT * 16];
+    __shared__ float s_rm[BG_MT * 16];
+    const uint4 zero{0, 0, 0, 0};
+    uint4 wv[BG_P][2], xh[BG_P][2], xl[BG_P][2];
+    auto issue = [&](int f, int st) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int nt = nt0 + i;
+            wv[st][i] = (f < a.kb && nt < a.n_tiles) ? a.w[((size_t)nt * a.kb + f) * WAVE + lane] : zero;
+        }
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int mt = mt0 + j;
+            const bool ok = f < a.kb && mt < a.MT && mt * 16 + lrow < a.M;
+            const size_t xi = ((size_t)f * a.MT + mt) * WAVE + lane;
+            xh[st][j] = ok ? a.xhi[xi] : zero;
+            if (SPLIT) xl[st][j] = ok ? a.xlo[xi] : zero;
+        }
+    };
+#pragma unroll
+    for (int st = 0; st < BG_P; ++st) issue(st, st);
+    // RMSNorm partials of the block's rows: four slices per row, summed in LDS
+    {
+        const int r = threadIdx.x % (BG_MT * 16), sl = threadIdx.x / (BG_MT * 16);
+        const int m = blockIdx.y * BG_MT * 16 + r;
+        float sm = 0.f;
+        if (m < a.M)
+            for (int p = sl; p < a.n_sq; p += 4) sm += a.sq[(size_t)p * a.sq_stride + m];
+        s_part[sl][r] = sm;
+    }
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int f0 = 0; f0 < a.kb; f0 += BG_P) {
+#pragma unroll
+        for (int st = 0; st < BG_P; ++st) {
+            if (f0 + st < a.kb) {
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) {
+                        mma_frag<T>(acc[j][i], wv[st][i], xh[st][j]);
+                        if (SPLIT) mma_frag<T>(acc[j][i], wv[st][i], xl[st][j]);
+                    }
+            }
+            issue(f0 + st + BG_P, st);
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < BG_MT * 16) {
+        const float sm = s_part[0][threadIdx.x] + s_part[1][threadIdx.x] + s_part[2][threadIdx.x] + s_part[3][threadIdx.x];
+        s_rm[threadIdx.x] = a.n_sq > 0 ? rsqrtf(sm / (float)a.norm_dim + a.eps) : 1.f;
+    }
+    __syncthreads();
+    // lane: row lrow of the m-tile, columns 4 lgrp .. 4 lgrp + 3 of the n-tile
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int mt = mt0 + j, nt = nt0 + i, m = mt * 16 + lrow;
+            if (mt >= a.MT || m >= a.M || nt >= a.n_tiles) continue;
+            const float rm = s_rm[m - blockIdx.y * BG_MT * 16];
+            const f32x4 v = acc[j][i] * rm;
+            *(float4*)(a.out + (size_t)m * a.ldo + nt * 16 + lgrp * 4) = float4{v[0], v[1], v[2], v[3]};
+        }
+}
+
+// thread: one row, one 16-column tile
+template <typename T>
+__global__ __launch_bounds__(256) void k_resid_rows(ResidRowsArgs a) {
+    constexpr int EPL = Elt<T>::EPL;
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    const int m = idx / a.n_tiles, tile = idx % a.n_tiles;
+    if (m >= a.M) return;
+    float4* xp = (float4*)(a.x + (size_t)m * a.ldx + tile * 16);
+    const float4* yp = (const float4*)(a.y + (size_t)m * a.ldy + tile * 16);
+    const T* g = (const T*)a.gnext + tile * 16;
+    float xv[16];
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float4 xo = xp[i], yo = yp[i];
+        xv[4 * i] = xo.x + yo.x;
+        xv[4 * i + 1] = xo.y + yo.y;
+        xv[4 * i + 2] = xo.z + yo.z;
+        xv[4 * i + 3] = xo.w + yo.w;
+    }
+#pragma unroll
+    for (int n = 0; n < 16; ++n) ss += xv[n] * xv[n];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) xp[i] = float4{xv[4 * i], xv[4 * i + 1], xv[4 * i + 2], xv[4 * i + 3]};
+#pragma unroll
+    for (int n0 = 0; n0 < 16; n0 += EPL) {
+        float ov[EPL];
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) ov[i] = xv[n0 + i] * to_f32(g[n0 + i]);
+        put_operand_run<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 16 + n0, a.n_MT), ov);
+    }
+    a.sq_out[(size_t)tile * a.sq_stride + m] = ss;
+}
+
+// thread: one row, one run of EPL outputs of one gate/up tile
+template <typename T>
+__global__ __launch_bounds__(256) void k_swiglu_rows(SwigluRowsArgs a) {
+    constexpr int EPL = Elt<T>::EPL, RUNS = 8 / EPL;
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    const int m = idx / (a.n_tiles * RUNS), rem = idx % (a.n_tiles * RUNS);
+    const int tile = rem / RUNS, c0 = (rem % RUNS) * EPL;
+    if (m >= a.M) return;
+    const float* y = a.y + (size_t)m * a.ldy + tile * 16;
+    float hv[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+        const float gt = y[c0 + i], up = y[c0 + i + 8];
+        hv[i] = gt / (1.f + __expf(-gt)) * up;
+    }
+    put_operand_run<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 8 + c0, a.n_MT), hv);
+}
+
+hipError_t launch_gemm_big(int dtype, const BigGemmArgs& a, hipStream_t st) {
+    const dim3 grid((a.n_tiles + BG_NT - 1) / BG_NT, (a.MT + BG_MT - 1) / BG_MT), block(256);
+    if (dtype == PBD_DTYPE_BF16) {
+        if (a.xlo) PBD_LAUNCH((k_gemm_big<bf16, true>), grid, block, 0, st, a);
+        else PBD_LAUNCH((k_gemm_big<bf16, false>), grid, block, 0, st, a);
+    } else {
+        PBD_LAUNCH((k_gemm_big<float, false>), grid, block, 0, st, a);
+    }
+    return hipGetLastError();
+}
+hipError_t launch_resid_rows(int dtype, const ResidRowsArgs& a, hipStream_t st) {
+    const int n = a.M * a.n_tiles;
+    if (dtype == PBD_DTYPE_BF16) PBD_LAUNCH(k_resid_rows<bf16>, dim3((n + 255) / 256), dim3(256), 0, st, a);
+    else PBD_LAUNCH(k_resid_rows<float>, dim3((n + 255) / 256), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+hipError_t launch_swiglu_rows(int dtype, const SwigluRowsArgs& a, hipStream_t st) {
+    const int runs = dtype == PBD_DTYPE_BF16 ? 8 / Elt<bf16>::EPL : 8 / Elt<float>::EPL;
+    const int n = a.M * a.n_tiles * runs;
+    if (dtype == PBD_DTYPE_BF16) PBD_LAUNCH(k_swiglu_rows<bf16>, dim3((n + 255) / 256), dim3(256), 0, st, a);
+    else PBD_LAUNCH(k_swiglu_rows<float>, dim3((n + 255) / 256), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t st) {
     PBD_LAUNCH(k_accept, dim3((a.B + 63) / 64), dim3(64), 0, st, a);
     return hipGetLastError();
