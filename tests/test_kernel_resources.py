@@ -26,6 +26,12 @@ HOT = [
     r"_ZN3pbd8k_argmaxENS_10ArgmaxArgsE",
     r"_ZN3pbd8k_acceptENS_10AcceptArgsE",
     r"_ZN3pbd8k_remaskENS_10RemaskArgsE",
+    # prefill chunks
+    r"_ZN3pbd10k_gemm_bigIDF16bLb[01]EEEvNS_11BigGemmArgsE",
+    r"_ZN3pbd9k_kvwriteIDF16bLi128EEEvNS_11KVWriteArgsE",
+    r"_ZN3pbd12k_resid_rowsIDF16bEEvNS_13ResidRowsArgsE",
+    r"_ZN3pbd13k_swiglu_rowsIDF16bEEvNS_14SwigluRowsArgsE",
+    r"_ZN3pbd13k_gather_lastIDF16bEEvNS_10GatherArgsE",
 ]
 
 
@@ -54,4 +60,4 @@ def test_hot_kernels_use_no_scratch(tmp_path):
         for n in names:
             seen += 1
             assert usage[n] == 0, f"{n} uses {usage[n]} bytes of scratch per lane"
-    assert seen >= 10
+    assert seen >= 15
