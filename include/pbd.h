@@ -90,7 +90,11 @@ typedef void* pbd_stream_t;            /* hipStream_t */
  * Qwen3-0.6B (Sec. 4.1) and does not print the architecture.
  * Supported: head_dim 64 or 128; n_q_heads a multiple of n_kv_heads;
  * hidden, ffn, n_q_heads*head_dim multiples of 64; vocab a multiple of 16;
- * 1 <= block <= 32; lora_rank in [0, 64] and a multiple of 8; mask_id in [0, vocab).
+ * 0 <= block <= 32 (block = 0: width-1 passes, so that pbd_verify_block over
+ * [anchor] followed by pbd_accept_commit is one plain autoregressive greedy
+ * step, the baseline speculation is measured against; the unanchored verify
+ * then fails with PBD_ERR_SHAPE); lora_rank in [0, 64] and a multiple of 8;
+ * mask_id in [0, vocab).
  */
 typedef struct pbd_config {
     int32_t n_layers;
@@ -102,7 +106,7 @@ typedef struct pbd_config {
     int32_t vocab;
     int32_t lora_rank;      /* r */
     float   lora_alpha;     /* scale s = alpha / r (App. A.2: r = 16, alpha = 32) */
-    int32_t block;          /* D, masked positions per draft (Sec. 3: D = 16) */
+    int32_t block;          /* D, masked positions per draft (Sec. 3: D = 16); 0: autoregressive steps */
     int32_t mask_id;        /* token id of the diffusion mask */
     float   rms_eps;
     float   rope_theta;

@@ -77,7 +77,7 @@ int validate(const pbd_config* c, std::string& err) {
             "ffn %d must be a multiple of 64 and <= %d", c->ffn, MAX_DIM);
     PBD_REQ(c->vocab >= 16 && c->vocab % 16 == 0, PBD_ERR_SHAPE, "vocab %d must be a positive multiple of 16", c->vocab);
     PBD_REQ(c->mask_id >= 0 && c->mask_id < c->vocab, PBD_ERR_INVALID_ARG, "mask_id %d outside [0, vocab)", c->mask_id);
-    PBD_REQ(c->block >= 1 && c->block <= 32, PBD_ERR_SHAPE, "block %d must lie in [1, 32]", c->block);
+    PBD_REQ(c->block >= 0 && c->block <= 32, PBD_ERR_SHAPE, "block %d must lie in [0, 32]", c->block);
     const int W = c->block + 1;
     const int G = c->n_q_heads / c->n_kv_heads;
     PBD_REQ(G * W <= 80, PBD_ERR_SHAPE, "query rows per KV head (%d) exceed 80", G * W);
@@ -806,6 +806,7 @@ int pbd_verify_block_unanchored(pbd_ctx* c, int32_t batch, const int32_t* seq_le
     if (rc) return rc;
     if ((rc = check_batch(c, batch))) return rc;
     if (!seq_len || !draft || !verify) return fail(c, PBD_ERR_INVALID_ARG, "NULL pointer argument");
+    if (c->ly.D < 1) return fail(c, PBD_ERR_SHAPE, "the unanchored verify needs block >= 1");
     bool adapter, causal;
     if ((rc = resolve_flags(c, flags, false, true, adapter, causal))) return rc;
     PassReq q{};

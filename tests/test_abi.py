@@ -55,7 +55,7 @@ def test_buffer_sizes(lib):
 
 
 @pytest.mark.parametrize("field,value", [
-    ("head_dim", 96), ("hidden", 100), ("vocab", 4095), ("block", 0), ("block", 40),
+    ("head_dim", 96), ("hidden", 100), ("vocab", 4095), ("block", -1), ("block", 40),
     ("lora_rank", 12), ("n_kv_heads", 3), ("mask_id", 4096), ("dtype", 7), ("max_seq", 5),
     ("prefill_chunk", -1), ("prefill_chunk", 1025), ("prefill_chunk", 4096),
 ])

@@ -288,3 +288,29 @@ def test_attention_query_split_matches_oracle(D, t, B, mode):
         _, dl_ref = om.draft(m, st)
         assert np.abs(dlg2.cpu().numpy()[b] - dl_ref).max() <= TOL32
     g.close()
+
+
+def test_block_zero_is_greedy_autoregressive_decoding():
+    """D = 0: the verify of [anchor] plus the commit is one greedy decode step;
+    twelve of them reproduce the oracle's greedy continuation (at every step
+    whose top-1/top-2 margin is decisive; the oracle follows the GPU)."""
+    cfg, w = _tiny(0)
+    prompt = synth.make_prompts(cfg, [23], 31)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=64)
+    g.prefill([prompt])
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompt)
+    assert int(g.anchor[0]) == st.anchor
+    empty = g.zeros(1, 1)
+    for _ in range(12):
+        v, vlg = g.verify(empty)
+        p_ref, vl_ref, k, vv = om.verify(m, st, [])
+        assert np.abs(vlg.cpu().numpy()[0] - vl_ref).max() <= TOL32
+        _check_tokens(v.cpu().numpy()[0], vl_ref, TOL32)
+        n, out = g.accept(empty, v)
+        assert int(n[0]) == 0
+        nn, oo = om.accept([], v.cpu().numpy()[0])
+        om.commit(st, nn, oo, k, vv)
+        assert int(g.seq_len[0]) == st.seq_len and int(g.anchor[0]) == st.anchor
+    assert g.status() == 0
+    g.close()
