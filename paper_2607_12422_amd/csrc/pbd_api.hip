@@ -176,7 +176,7 @@ void make_layout(const pbd_config* c, Layout& y) {
     const size_t xfc = (size_t)cdiv(y.Bmax, 16) * FR;
     y.w_xc[0] = take(y.kb_e * xfc); y.w_xc[1] = take(nlo * y.kb_e * xfc);
     y.w_sqc = take((size_t)std::max(y.tiles_d, 1) * y.Bmax * 4);
-    y.w_big = y.Wp > y.W ? take((size_t)y.Mmax * std::max(y.H, 2 * y.F) * 4) : 0;
+    y.w_big = y.Mmax >= BIG_MIN_MT * 16 ? take((size_t)y.Mmax * std::max(y.H, 2 * y.F) * 4) : 0;
     y.w_dn_conf = take((size_t)y.Bmax * y.D * 4);
     y.ws_bytes = off;
 }
@@ -322,9 +322,10 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
             g.cnt = (unsigned*)(ws + y.w_kcnt);
         }
     };
-    // prefill chunks of many rows (adapter off): large-M projections, with the
-    // residual / SwiGLU epilogues as row kernels on their fp32 output
-    const bool big = pre && !lora && MT >= BIG_MIN_MT && y.w_big != 0;
+    // passes of many rows without the adapter (prefill chunks, large-batch
+    // verify): large-M projections, with the residual / SwiGLU epilogues as
+    // row kernels on their fp32 output
+    const bool big = !lora && MT >= BIG_MIN_MT && y.w_big != 0;
     float* ybig = (float*)(ws + y.w_big);
     auto big_args = [&](const FGemmArgs& g) {
         BigGemmArgs b{};
@@ -358,7 +359,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
 
         AttnArgs at{};
         at.layer = l; at.max_batch = y.Bmax; at.n_q = y.NQ; at.n_kv = y.NKV; at.nblk = y.nblk; at.W = W; at.G = y.G;
-        at.nqkv = y.nqkv; at.kps = kps; at.s_launch = s_launch; at.n_qgrp = QT / QTw;
+        at.nqkv = y.nqkv; at.kps = kps; at.s_launch = s_launch; at.n_qgrp = cdiv(QT, QTw);
         at.full_from = q.causal ? W : (q.anchor_cached ? 1 : 0);
         at.kv_rows = pre ? 0 : q.write_kv ? W : (q.anchor_cached ? 1 : 0);
         at.chunk = pre ? 1 : 0;

@@ -6,9 +6,12 @@ Sequences are independent, so the oracle checks sampled sequences of a batch
 one by one.  Where a full-size oracle sequence would cost minutes, properties
 that hold at any size are checked on the whole batch instead:
 
-* a sequence's logits do not depend on the rest of the batch (to fp32
-  rounding: the LM head's row-norm partials are summed in an order that
-  depends on the batch's row count);
+* a sequence's logits do not depend on the rest of the batch, to within
+  1e-2 (half the oracle tolerance): the batch's row count selects the GEMM
+  (a batch of 32 runs its prefill and verify projections as the large-M GEMM,
+  one sequence alone the skinny one), whose different accumulation orders can
+  round the bf16 K/V cache differently; a row of another sequence leaking in
+  would show as an O(1) error;
 * with the adapter off and a causal mask override, the draft pass over
   [anchor, mask x D] equals the verify pass over the same block (bitwise).
 
@@ -180,8 +183,8 @@ def test_config5_full_batch_properties_and_sampled_sequence():
     for alone, batched, what in ((dlg1.cpu().numpy()[0], dlg_np[0], "draft"), (vlg1.cpu().numpy()[0], vlg_np[0], "verify")):
         err = float(np.abs(alone - batched).max())
         print(f"config 5 sequence 0 alone vs in the batch ({what}): max-abs {err:.2e}")
-        assert err <= 1e-3
-    dec = decisive(dlg_np[0][1:], 1e-3, cfg.mask_id)
+        assert err <= 1e-2
+    dec = decisive(dlg_np[0][1:], 2e-2, cfg.mask_id)
     assert np.array_equal(d1.cpu().numpy()[0][dec], d_np[0][dec])
     g1.close()
     g.close()
