@@ -22,6 +22,8 @@ thread_local std::string g_init_error;
 constexpr int MAX_DIM = 16384;   // bound on hidden, ffn and n_q_heads*head_dim
 constexpr int LMHEAD_GRID = 512;  // work-groups of the persistent LM head (two per CU)
 constexpr int PREFILL_KPS = 1024; // keys per attention split in prefill chunks (many query groups)
+constexpr int ATTN_KPS = 256;     // keys per attention split of a step pass, unless the grid is too large
+constexpr int ATTN_GRID_CAP = 2560; // ... then doubled while batch x KV heads x splits exceeds this (10 per CU)
 constexpr int BIG_MIN_MT = 16;    // prefill chunks of >= 256 rows use the large-M projection
 constexpr size_t MAX_LDS = 160 * 1024;   // LDS one gfx950 work-group may allocate
 
@@ -278,7 +280,12 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     const int W = pre ? y.Wp : (q.no_anchor ? y.D : y.W), B = q.B, M = B * W, MT = cdiv(M, 16);
     const int lead = (pre || q.no_anchor) ? 0 : 1;
     const int QT = cdiv(y.G * W, 16);              // query tiles per (KV head, sequence)
-    const int kps = pre ? std::max(c->kps, PREFILL_KPS) : c->kps;
+    int kps = c->kps;
+    if (kps == 0) {       // automatic: long prefixes at large batch take fewer, longer splits
+        kps = ATTN_KPS;
+        while (kps < y.max_seq && (size_t)B * y.NKV * cdiv(y.max_seq, kps) > (size_t)ATTN_GRID_CAP) kps *= 2;
+    }
+    if (pre) kps = std::max(kps, PREFILL_KPS);
     const int s_launch = pre ? y.S_pre : std::min(y.S_max, cdiv(y.max_seq, kps) + 1);   // split-KV grid columns
     const bool qsplit = pre || c->qsplit > 0 || (c->qsplit < 0 && B * y.NKV * s_launch < 256);
     const int QTw = qsplit ? 1 : QT;                // ... per attention work-group
@@ -580,7 +587,7 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
     c->packed = (char*)packed;
     c->kv = (char*)kv;
     c->ws = (char*)ws;
-    c->kps = 256;
+    c->kps = 0;
     c->qsplit = -1;
     c->split = cfg->dtype == PBD_DTYPE_BF16;
     hipStream_t st = (hipStream_t)stream;
@@ -851,7 +858,7 @@ int pbd_sync_status(pbd_ctx* c, pbd_stream_t stream, int32_t* status) {
 int pbd_set_attn_keys_per_split(pbd_ctx* c, int32_t keys) {
     int rc = check_ctx(c);
     if (rc) return rc;
-    if (keys < 16 || keys % 16 != 0) return fail(c, PBD_ERR_INVALID_ARG, "keys per split must be a positive multiple of 16");
+    if (keys < 0 || keys % 16 != 0) return fail(c, PBD_ERR_INVALID_ARG, "keys per split must be 0 (automatic) or a positive multiple of 16");
     c->kps = keys;
     return PBD_OK;
 }

@@ -740,8 +740,13 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     // of a chunk are formed first, so the running max and the rescale of the
     // accumulated output happen once per chunk (not at all for the first one).
     // The wave's first chunk of prefix blocks is requested before the query
-    // preparation, which it does not depend on.
-    constexpr int CH = QT == 1 ? 4 : 2;     // key blocks per chunk (a 16-row work-group has the registers for 4)
+    // preparation, which it does not depend on.  Splits of cache keys hold two
+    // chunks in registers (the next one loading), so CH is the largest of
+    // 4, 2, 1 for which those, the output accumulators and the Q fragments
+    // fit a budget of 304 registers per lane (beyond it the compiler spills).
+    constexpr int R_BLK = NDS * 4 + NDT * (int)(sizeof(vraw) / 4);    // one key block's K and V
+    constexpr int R_FIX = QT * (NDT * 4 + NDS * 4);
+    constexpr int CH = 8 * R_BLK + R_FIX <= 304 ? 4 : 4 * R_BLK + R_FIX <= 304 ? 2 : 1;
     uint4 kn[CH][NDS];
     vraw vn[CH][NDT];
     auto load_chunk = [&](int it0) {
@@ -749,7 +754,25 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         for (int c = 0; c < CH; ++c)
             if (it0 + 4 * c < n_items) load_item(it0 + 4 * c, kn[c], vn[c]);
     };
-    if (!blk) load_chunk(wid);
+    // prefix block it from the cache (it clamped into range by the caller)
+    auto load_pref = [&](int it, uint4* kf, vraw* vf) {
+        const T* kblk = kc + (size_t)(kb_first + it) * 16 * HD;
+        const T* vblk = vc + (size_t)(kb_first + it) * 16 * HD;
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds) kf[ds] = *(const uint4*)(kblk + (size_t)(ds * WAVE + lane) * EPL);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) vf[dt] = *(const vraw*)(vblk + (size_t)(dt * WAVE + lane) * 4);
+    };
+    // splits of prefix keys only: every load is unconditional (indexes past the
+    // wave's last block repeat that block), so that the compiler's wait before
+    // a chunk's products covers that chunk's loads and not the next chunk's
+    const bool pipe = !blk && n_items > 0;
+    if (pipe) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) load_pref(min(wid + 4 * c, n_items - 1), kn[c], vn[c]);
+    } else if (!blk) {
+        load_chunk(wid);
+    }
 
     // -- Q rows (and, in the block split, K/V rows): all loads first, then
     //    norm + rotation; wave w, lane group lgrp handles rows 16*i + 4*w + lgrp
@@ -855,8 +878,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     }
     const float sl2 = a.scale_log2;
 
-    if (blk) load_chunk(wid);
-    for (int it0 = wid; it0 < n_items; it0 += 4 * CH) {
+    auto step = [&](int it0, const uint4 (&kcur)[CH][NDS], const vraw (&vcur)[CH][NDT]) {
         const bool first = it0 == wid;
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
@@ -870,7 +892,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
                 if (it < n_items) {
 #pragma unroll
-                    for (int ds = 0; ds < NDS; ++ds) mma_frag<T>(sc, kn[c][ds], qf[qt][ds]);
+                    for (int ds = 0; ds < NDS; ++ds) mma_frag<T>(sc, kcur[c][ds], qf[qt][ds]);
                 }
                 const bool pref = it < n_pref;
                 const int key0 = pref ? (kb_first + it) * 16 : (it - n_pref) * 16;
@@ -908,10 +930,35 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
             for (int c = 0; c < CH; ++c) {
                 if (it0 + 4 * c >= n_items) continue;
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) mma_k4(o_acc[dt][qt], vn[c][dt], p[c]);
+                for (int dt = 0; dt < NDT; ++dt) mma_k4(o_acc[dt][qt], vcur[c][dt], p[c]);
             }
         }
-        if (it0 + 4 * CH < n_items) load_chunk(it0 + 4 * CH);
+    };
+    if (pipe) {
+        // the next chunk's loads are in flight while the current one is reduced;
+        // the last chunk is peeled off so that no load is issued past the end
+        uint4 kx[CH][NDS];
+        vraw vx[CH][NDT];
+        int it0 = wid;
+        for (; it0 + 4 * CH < n_items; it0 += 4 * CH) {
+#pragma unroll
+            for (int c = 0; c < CH; ++c) load_pref(min(it0 + 4 * CH + 4 * c, n_items - 1), kx[c], vx[c]);
+            step(it0, kn, vn);
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+#pragma unroll
+                for (int ds = 0; ds < NDS; ++ds) kn[c][ds] = kx[c][ds];
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) vn[c][dt] = vx[c][dt];
+            }
+        }
+        if (it0 < n_items) step(it0, kn, vn);
+    } else {
+        if (blk) load_chunk(wid);
+        for (int it0 = wid; it0 < n_items; it0 += 4 * CH) {
+            step(it0, kn, vn);
+            if (it0 + 4 * CH < n_items) load_chunk(it0 + 4 * CH);
+        }
     }
 
     // -- merge the four waves: common max per query row, then a two-round tree
@@ -1578,9 +1625,12 @@ hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStre
 // a 2 x 2 tile quadrant per wave) and walks K with BG_P fragment steps of
 // loads in flight; r_m (the folded RMSNorm) scales rows in the epilogue and
 // the fp32 result goes to out.  Residual and SwiGLU epilogues run after it as
-// row kernels.
+// row kernels.  Loads are unconditional from clamped addresses (a guarded
+// load would make the compiler wait for every load at each loop turn): tiles
+// past the ends only feed outputs that are not stored, steps past K are not
+// computed.
 // ---------------------------------------------------------------------------
-constexpr int BG_MT = 4, BG_NT = 4, BG_P = 4;
+constexpr int BG_MT = 4, BG_NT = 4, BG_P = 8;
 
 template <typename T, bool SPLIT>
 __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
@@ -1589,21 +1639,18 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
     const int mt0 = blockIdx.y * BG_MT + (wid / 2) * 2, nt0 = blockIdx.x * BG_NT + (wid % 2) * 2;
     __shared__ float s_part[4][BG_MT * 16];
     __shared__ float s_rm[BG_MT * 16];
-    const uint4 zero{0, 0, 0, 0};
     uint4 wv[BG_P][2], xh[BG_P][2], xl[BG_P][2];
+    const int ntc[2] = {min(nt0, a.n_tiles - 1), min(nt0 + 1, a.n_tiles - 1)};
+    const int mtc[2] = {min(mt0, a.MT - 1), min(mt0 + 1, a.MT - 1)};
     auto issue = [&](int f, int st) {
+        const int fc = min(f, a.kb - 1);
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int nt = nt0 + i;
-            wv[st][i] = (f < a.kb && nt < a.n_tiles) ? a.w[((size_t)nt * a.kb + f) * WAVE + lane] : zero;
-        }
+        for (int i = 0; i < 2; ++i) wv[st][i] = a.w[((size_t)ntc[i] * a.kb + fc) * WAVE + lane];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            const int mt = mt0 + j;
-            const bool ok = f < a.kb && mt < a.MT && mt * 16 + lrow < a.M;
-            const size_t xi = ((size_t)f * a.MT + mt) * WAVE + lane;
-            xh[st][j] = ok ? a.xhi[xi] : zero;
-            if (SPLIT) xl[st][j] = ok ? a.xlo[xi] : zero;
+            const size_t xi = ((size_t)fc * a.MT + mtc[j]) * WAVE + lane;
+            xh[st][j] = a.xhi[xi];
+            if (SPLIT) xl[st][j] = a.xlo[xi];
         }
     };
 #pragma unroll

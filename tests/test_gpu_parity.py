@@ -290,6 +290,36 @@ def test_attention_query_split_matches_oracle(D, t, B, mode):
     g.close()
 
 
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("kps", [16, 512, 0])
+def test_attention_key_splits_match_oracle(kps, mode):
+    """Long prefixes (1000 and 1013 keys) in splits of 16 keys (one block per
+    work-group), of 512 (several chunks per wave, each wave's next chunk
+    loading while the current one is reduced, a ragged last chunk) and the
+    automatic size, for both query layouts."""
+    cfg, w = _tiny(16)
+    prompts = synth.make_prompts(cfg, [1000, 1013], 321)
+    g = GpuRun(cfg, w, max_batch=2, max_seq=1100)
+    g.eng.pbd_set_attn_query_split(mode)
+    from paper_2607_12422_amd.binding import PbdError
+    for bad in (-16, 8, 24):
+        with pytest.raises(PbdError):
+            g.eng.pbd_set_attn_keys_per_split(bad)
+    g.eng.pbd_set_attn_keys_per_split(kps)
+    g.prefill(prompts)
+    m = om.OracleModel(w)
+    d, dlg = g.draft()
+    v, vlg = g.verify(d)
+    for b, p in enumerate(prompts):
+        st = om.prefill(m, p)
+        _, dl_ref = om.draft(m, st)
+        assert np.abs(dlg.cpu().numpy()[b] - dl_ref).max() <= TOL32
+        _, vl_ref, _, _ = om.verify(m, st, d.cpu().numpy()[b])
+        assert np.abs(vlg.cpu().numpy()[b] - vl_ref).max() <= TOL32
+    assert g.status() == 0
+    g.close()
+
+
 def test_block_zero_is_greedy_autoregressive_decoding():
     """D = 0: the verify of [anchor] plus the commit is one greedy decode step;
     twelve of them reproduce the oracle's greedy continuation (at every step
