@@ -53,7 +53,8 @@ struct Layout {
     size_t w_kpart, w_kcnt;                          // split-K partial tiles and arrival counters
     size_t w_arg_mx, w_arg_sum;                      // LM-head softmax partials (draft confidence)
     size_t w_xc[2], w_sqc;                           // prefill: gathered last rows (LM-head operand, Σx² partials)
-    size_t w_big;                                    // prefill: fp32 output of a large-M projection
+    size_t w_big;                                    // fp32 output of a large-M projection
+    size_t w_u;                                      // its LoRA shrink u = A x, [M][sources * RT * 16] fp32
     size_t w_dn_tok, w_dn_conf;                      // one denoising pass's candidates and confidences
     int ksplit;                                      // K slices of the residual GEMMs
 };
@@ -179,6 +180,7 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.w_xc[0] = take(y.kb_e * xfc); y.w_xc[1] = take(nlo * y.kb_e * xfc);
     y.w_sqc = take((size_t)std::max(y.tiles_d, 1) * y.Bmax * 4);
     y.w_big = y.Mmax >= BIG_MIN_MT * 16 ? take((size_t)y.Mmax * std::max(y.H, 2 * y.F) * 4) : 0;
+    y.w_u = y.w_big && y.r > 0 ? take((size_t)y.Mmax * 3 * y.RT * 16 * 4) : 0;   // LoRA shrink, large-M path
     y.w_dn_conf = take((size_t)y.Bmax * y.D * 4);
     y.ws_bytes = off;
 }
@@ -329,11 +331,12 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
             g.cnt = (unsigned*)(ws + y.w_kcnt);
         }
     };
-    // passes of many rows without the adapter (prefill chunks, large-batch
-    // verify): large-M projections, with the residual / SwiGLU epilogues as
-    // row kernels on their fp32 output
-    const bool big = !lora && MT >= BIG_MIN_MT && y.w_big != 0;
+    // passes of many rows (prefill chunks, large-batch steps): large-M
+    // projections, with the residual / SwiGLU epilogues as row kernels on
+    // their fp32 output
+    const bool big = MT >= BIG_MIN_MT && y.w_big != 0 && (!lora || y.w_u != 0);
     float* ybig = (float*)(ws + y.w_big);
+    float* ubig = (float*)(ws + y.w_u);
     auto big_args = [&](const FGemmArgs& g) {
         BigGemmArgs b{};
         b.w = g.w; b.n_tiles = g.n_tiles; b.kb = g.kb; b.xhi = g.xhi; b.xlo = g.xlo; b.M = g.M; b.MT = g.MT;
@@ -342,6 +345,26 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         b.out = direct ? g.out : ybig;
         b.ldo = direct ? g.ldo : g.n_tiles * 16;
         return b;
+    };
+    // with the adapter: the shrink of the projection's nsrc LoRA A matrices,
+    // stacked in the packed layout as one [nsrc RT][kb] tile matrix, then the
+    // projection with the expand
+    auto launch_big = [&](const FGemmArgs& g, int nsrc) -> hipError_t {
+        BigGemmArgs b = big_args(g);
+        if (lora) {
+            const size_t src_frags = (size_t)y.RT * g.kb * 64;          // uint4 per source matrix
+            for (int i = 1; i < nsrc; ++i)
+                if (g.la[i] != g.la[0] + i * src_frags) return hipErrorInvalidValue;
+            BigGemmArgs sh{};
+            sh.w = g.la[0]; sh.n_tiles = nsrc * y.RT; sh.kb = g.kb; sh.xhi = g.xhi; sh.xlo = g.xlo;
+            sh.M = g.M; sh.MT = g.MT; sh.n_sq = 0; sh.out = ubig; sh.ldo = nsrc * y.RT * 16;
+            const hipError_t e = launch_gemm_big(dt, sh, st);
+            if (e != hipSuccess) return e;
+            b.u = ubig; b.ldu = sh.ldo; b.lrt = y.RT; b.lora_mode = g.lora_mode;
+            b.tile_split0 = g.tile_split0; b.tile_split1 = g.tile_split1;
+            b.W = g.W; b.adapter_from = g.adapter_from; b.scale = g.scale; b.lb = g.lb;
+        }
+        return launch_gemm_big(dt, b, st);
     };
     auto resid_args = [&](const FGemmArgs& g) {
         ResidRowsArgs r{};
@@ -361,7 +384,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         for (int i = 0; i < 3; ++i) g.la[i] = (const uint4*)(pk + lo_.la[i]);
         g.lb = pk + lo_.lb_qkv;
         g.out = (float*)(ws + y.w_qkv); g.ldo = y.nqkv;
-        if (big) PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm_big(dt, big_args(g), st), "qkv gemm");
+        if (big) PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 3), "qkv gemm");
         else PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_STORE, st), "qkv gemm");
 
         AttnArgs at{};
@@ -421,7 +444,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.sq_out = sq_m;
         split_k(g);
         if (big) {
-            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm_big(dt, big_args(g), st), "o gemm");
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 1), "o gemm");
             PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_resid_rows(dt, resid_args(g), st), "o residual");
         } else {
             PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "o gemm");
@@ -434,7 +457,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.lb = pk + lo_.lb_gu;
         g.nx_hi = hi(y.w_xd); g.nx_lo = lo(y.w_xd); g.n_MT = MT;
         if (big) {
-            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm_big(dt, big_args(g), st), "gate/up gemm");
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 2), "gate/up gemm");
             SwigluRowsArgs sw{};
             sw.M = M; sw.n_tiles = g.n_tiles; sw.ldy = 2 * y.F; sw.n_MT = MT;
             sw.y = (const float*)(ws + y.w_big); sw.nx_hi = g.nx_hi; sw.nx_lo = g.nx_lo;
@@ -451,7 +474,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.nx_hi = hi(y.w_xa); g.nx_lo = lo(y.w_xa); g.n_MT = MT; g.sq_out = sq_a;
         split_k(g);
         if (big) {
-            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_gemm_big(dt, big_args(g), st), "down gemm");
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 1), "down gemm");
             PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_resid_rows(dt, resid_args(g), st), "down residual");
         } else {
             PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "down gemm");

@@ -159,6 +159,15 @@ struct BigGemmArgs {
     float eps;
     float* out;             // [M][ldo] fp32
     int ldo;
+    // LoRA expand (lrt > 0), added before the r_m scaling: acc += s * B u, with
+    // u [M][ldu] fp32 the shrink A x of source sc at columns sc * lrt * 16, B
+    // blocks [n_tiles][lrt] x 64 lanes x 4 elements; the source of a tile is
+    // chosen as in the small-M GEMM (lora_mode, tile_split0/1); block rows
+    // m % W < adapter_from take no adapter
+    const float* u;
+    int ldu, lrt, lora_mode, tile_split0, tile_split1, W, adapter_from;
+    float scale;
+    const void* lb;
 };
 
 // Residual epilogue of a large-M projection: x += y over 16-column tiles, the

@@ -1618,9 +1618,10 @@ hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStre
 }
 
 // ---------------------------------------------------------------------------
-// Large-M projection for prefill chunks.  The skinny GEMM above streams each
-// weight tile once against every row; with hundreds of rows it would re-read
-// the operand per weight tile and wait a full load latency per 64-row group.
+// Large-M projection (prefill chunks, passes of many block rows).  The skinny
+// GEMM above streams each weight tile once against every row; with hundreds of
+// rows it would re-read the operand per weight tile and wait a full load
+// latency per 64-row group.
 // Here a work-group owns a 64-row x 64-column output block (4 x 4 MFMA tiles,
 // a 2 x 2 tile quadrant per wave) and walks K with BG_P fragment steps of
 // loads in flight; r_m (the folded RMSNorm) scales rows in the epilogue and
@@ -1628,7 +1629,10 @@ hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStre
 // row kernels.  Loads are unconditional from clamped addresses (a guarded
 // load would make the compiler wait for every load at each loop turn): tiles
 // past the ends only feed outputs that are not stored, steps past K are not
-// computed.
+// computed.  With the adapter, a first launch of this kernel on the stacked
+// LoRA A tiles leaves the shrink u = A x in fp32, and the projection adds
+// s * B u per tile before the r_m scaling (r_m (W x + s B A x), the same sum
+// the skinny GEMM forms in-tile).
 // ---------------------------------------------------------------------------
 constexpr int BG_MT = 4, BG_NT = 4, BG_P = 8;
 
@@ -1682,6 +1686,38 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
                     }
             }
             issue(f0 + st + BG_P, st);
+        }
+    }
+    if (a.lrt > 0) {
+        // LoRA expand: lane operand u[m = tile row lrow][r = 16 t + 4 lgrp + e],
+        // the layout the shrink's epilogue stored it in
+        typedef typename K4<T>::raw braw;
+        float lsc[2];
+        int mc[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int m = (mt0 + j) * 16 + lrow;
+            mc[j] = min(m, a.M - 1);
+            lsc[j] = (m < a.M && m % a.W >= a.adapter_from) ? a.scale : 0.f;
+        }
+        const int nsrc = a.lora_mode == LORA_ROW_HALF ? 2 : 1;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int nt = ntc[i];
+            const int s0 = a.lora_mode == LORA_BY_TILE ? (nt < a.tile_split0 ? 0 : nt < a.tile_split1 ? 1 : 2) : 0;
+            for (int t = 0; t < a.lrt; ++t) {
+                braw b;
+                __builtin_memcpy(&b, (const T*)a.lb + (((size_t)nt * a.lrt + t) * WAVE + lane) * 4, sizeof(braw));
+                for (int sc = 0; sc < nsrc; ++sc) {
+                    // gate/up tiles: rows 0-7 take source 0 (gate), 8-15 source 1 (up)
+                    const braw bb = (nsrc == 2 && ((lrow < 8) != (sc == 0))) ? braw{} : b;
+#pragma unroll
+                    for (int j = 0; j < 2; ++j) {
+                        const float4 uv = *(const float4*)(a.u + (size_t)mc[j] * a.ldu + ((s0 + sc) * a.lrt + t) * 16 + lgrp * 4);
+                        mma_k4_split(acc[j][i], bb, f32x4{uv.x, uv.y, uv.z, uv.w} * lsc[j]);
+                    }
+                }
+            }
         }
     }
     __syncthreads();

@@ -69,6 +69,23 @@ def test_tiny_unanchored_step_matches_oracle():
     g.close()
 
 
+def test_large_batch_unanchored_matches_oracle():
+    """16 sequences: the unanchored draft's mask block has 16 x 16 = 256 rows,
+    so its adapter-on projections run on the large-M GEMM with the LoRA
+    shrink and expand; every sequence's passes match the oracle."""
+    cfg, w = _tiny()
+    prompts = synth.make_prompts(cfg, [4 + 9 * b for b in range(16)], 17)
+    g = GpuRun(cfg, w, max_batch=16, max_seq=256)
+    g.prefill(prompts)
+    m = om.OracleModel(w)
+    d, v, dlg = g.draft_unanchored()
+    v, vlg = g.verify_unanchored(d, v)
+    for b, p in enumerate(prompts):
+        _round(g, m, om.prefill(m, p), b, d, v, dlg, vlg, TOL32, what=f"seq {b}")
+    assert g.status() == 0
+    g.close()
+
+
 def test_unanchored_pair_equals_anchored_verify():
     """The anchor row of the unanchored draft is the anchored verify's row 0
     (bit for bit: same kernels and widths, adapter contribution zero), and the
