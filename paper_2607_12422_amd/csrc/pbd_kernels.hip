@@ -625,6 +625,8 @@ __global__ __launch_bounds__(256) void k_kvwrite(KVWriteArgs a) {
     }
 }
 
+constexpr float RESCALE_SLACK = 8.f;
+
 template <typename T, int HD, int QT>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     constexpr int FK = Elt<T>::FK;
@@ -896,23 +898,33 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 }
                 const bool pref = it < n_pref;
                 const int key0 = pref ? (kb_first + it) * 16 : (it - n_pref) * 16;
+                // key masks with bitwise operators: no branches per element
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int kk = key0 + lgrp * 4 + e;
-                    const bool ok = it < n_items && (pref ? (kk < k_hi && (!a.chunk || kk < t || kk - t <= jq[qt]))
-                                                       : (kk < nrows && (kk <= jq[qt] || jq[qt] >= a.full_from)));
+                    const bool in_pref = (kk < k_hi) & (!a.chunk | (kk < t) | (kk - t <= jq[qt]));
+                    const bool in_blk = (kk < nrows) & ((kk <= jq[qt]) | (jq[qt] >= a.full_from));
+                    const bool ok = (it < n_items) & (pref ? in_pref : in_blk);
                     valid[c][e] = ok;
                     sv[c][e] = sc[e] * sl2;
-                    if (ok) mloc = fmaxf(mloc, sv[c][e]);
+                    mloc = fmaxf(mloc, ok ? sv[c][e] : -1e30f);
                 }
             }
             mloc = xrow_max(mloc);
+            // The reference maximum m_run is raised (and the output and sum
+            // rescaled) only when some row's maximum exceeds it by more than
+            // RESCALE_SLACK (log2 units, a vote of the wave): the weights
+            // exp2(s - m_run) stay below 2^RESCALE_SLACK and the ratio of sums
+            // is the same for any reference, so only rounding differs.
             const float m_new = fmaxf(m_run[qt], mloc);
-            if (!first) {
+            if (first) {
+                m_run[qt] = m_new;
+            } else if (__any(m_new > m_run[qt] + RESCALE_SLACK)) {
                 const float corr = exp2f(m_run[qt] - m_new);
                 l_run[qt] *= corr;
 #pragma unroll
                 for (int dt = 0; dt < NDT; ++dt) o_acc[dt][qt] *= corr;
+                m_run[qt] = m_new;
             }
             f32x4 p[CH];
             float psum = 0.f;
@@ -920,12 +932,11 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
             for (int c = 0; c < CH; ++c)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    p[c][e] = valid[c][e] ? exp2f(sv[c][e] - m_new) : 0.f;
+                    p[c][e] = valid[c][e] ? exp2f(sv[c][e] - m_run[qt]) : 0.f;
                     psum += p[c][e];
                 }
             psum = xrow_sum(psum);
             l_run[qt] += psum;
-            m_run[qt] = m_new;
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
                 if (it0 + 4 * c >= n_items) continue;
