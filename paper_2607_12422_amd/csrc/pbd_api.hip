@@ -24,7 +24,7 @@ constexpr int LMHEAD_GRID = 512;  // work-groups of the persistent LM head (two 
 constexpr int PREFILL_KPS = 1024; // keys per attention split in prefill chunks (many query groups)
 constexpr int ATTN_KPS = 256;     // keys per attention split of a step pass, unless the grid is too large
 constexpr int ATTN_GRID_CAP = 2560; // ... then doubled while batch x KV heads x splits exceeds this (10 per CU)
-constexpr int BIG_MIN_MT = 16;    // prefill chunks of >= 256 rows use the large-M projection
+constexpr int BIG_MIN_MT = 8;    // passes of >= 128 rows (prefill chunks, batches of 8+) use the large-M projection
 constexpr size_t MAX_LDS = 160 * 1024;   // LDS one gfx950 work-group may allocate
 
 // Every size and offset the library uses, derived from a validated config.

@@ -8,7 +8,7 @@ that hold at any size are checked on the whole batch instead:
 
 * a sequence's logits do not depend on the rest of the batch, to within
   1e-2 (half the oracle tolerance): the batch's row count selects the GEMM
-  (a batch of 32 runs its prefill and verify projections as the large-M GEMM,
+  (a batch of 32 runs its prefill and step projections as the large-M GEMM,
   one sequence alone the skinny one), whose different accumulation orders can
   round the bf16 K/V cache differently; a row of another sequence leaking in
   would show as an O(1) error;
