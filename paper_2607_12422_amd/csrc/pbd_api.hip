@@ -509,6 +509,14 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     if (lmhead_fits(y.kb_e, lm_MT)) {
         n_part = std::min(y.tiles_e, LMHEAD_GRID);
         PBD_TIMED(c, st, PBD_KCLASS_LMHEAD, launch_lmhead(dt, ge, n_part, st), "lm head");
+    } else if (big && !pre) {
+        // many rows: the large-M GEMM with the argmax epilogue, m-blocks
+        // fastest so that the row blocks sharing an embedding tile run together
+        BigGemmArgs b = big_args(ge);
+        b.out = nullptr; b.logits = ge.logits; b.ldo = y.V;
+        b.arg_val = ge.arg_val; b.arg_idx = ge.arg_idx; b.arg_mx = ge.arg_mx; b.arg_sum = ge.arg_sum;
+        b.exclude = ge.exclude; b.excl_from = ge.excl_from; b.W = ge.W; b.m_fast = 1;
+        PBD_TIMED(c, st, PBD_KCLASS_LMHEAD, launch_gemm_big(dt, b, st), "lm head");
     } else {
         PBD_TIMED(c, st, PBD_KCLASS_LMHEAD, launch_fgemm(dt, ge, EPI_ARGMAX, st), "lm head");
     }

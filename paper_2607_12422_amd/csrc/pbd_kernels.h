@@ -168,6 +168,20 @@ struct BigGemmArgs {
     int ldu, lrt, lora_mode, tile_split0, tile_split1, W, adapter_from;
     float scale;
     const void* lb;
+    // argmax epilogue (arg_val set; tied LM head): per 16-column tile and row
+    // the (max, argmax) with column `exclude` skipped on block rows m % W >=
+    // excl_from, ties to the lowest column, into arg_val/arg_idx [n_tiles][M];
+    // optional logits [M][ldo] and softmax partials arg_mx/arg_sum (maximum
+    // over the tile and sum of exp(value - maximum)); out is not written
+    float* logits;
+    float* arg_val;
+    int* arg_idx;
+    float* arg_mx;
+    float* arg_sum;
+    int exclude, excl_from;
+    // grid order: m-blocks fastest (the blocks that share weight tiles run
+    // together; for weights larger than the memory-side cache)
+    int m_fast;
 };
 
 // Residual epilogue of a large-M projection: x += y over 16-column tiles, the

@@ -1651,7 +1651,8 @@ template <typename T, bool SPLIT>
 __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
     const int lane = threadIdx.x % WAVE, wid = threadIdx.x / WAVE;
     const int lrow = lane % 16, lgrp = lane / 16;
-    const int mt0 = blockIdx.y * BG_MT + (wid / 2) * 2, nt0 = blockIdx.x * BG_NT + (wid % 2) * 2;
+    const int bm = a.m_fast ? blockIdx.x : blockIdx.y, bn = a.m_fast ? blockIdx.y : blockIdx.x;
+    const int mt0 = bm * BG_MT + (wid / 2) * 2, nt0 = bn * BG_NT + (wid % 2) * 2;
     __shared__ float s_part[4][BG_MT * 16];
     __shared__ float s_rm[BG_MT * 16];
     uint4 wv[BG_P][2], xh[BG_P][2], xl[BG_P][2];
@@ -1673,7 +1674,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
     // RMSNorm partials of the block's rows: four slices per row, summed in LDS
     {
         const int r = threadIdx.x % (BG_MT * 16), sl = threadIdx.x / (BG_MT * 16);
-        const int m = blockIdx.y * BG_MT * 16 + r;
+        const int m = bm * BG_MT * 16 + r;
         float sm = 0.f;
         if (m < a.M)
             for (int p = sl; p < a.n_sq; p += 4) sm += a.sq[(size_t)p * a.sq_stride + m];
@@ -1738,13 +1739,55 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
     }
     __syncthreads();
     // lane: row lrow of the m-tile, columns 4 lgrp .. 4 lgrp + 3 of the n-tile
+    if (a.arg_val) {
+        // every lane takes part in the cross-lane steps; only live rows store
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int mt = mt0 + j, nt = nt0 + i, m = mt * 16 + lrow;
+                const bool live = mt < a.MT && m < a.M && nt < a.n_tiles;
+                const f32x4 v = acc[j][i] * s_rm[m - bm * BG_MT * 16];
+                const int col0 = nt * 16 + lgrp * 4;
+                if (live && a.logits) *(float4*)(a.logits + (size_t)m * a.ldo + col0) = float4{v[0], v[1], v[2], v[3]};
+                const int excl = m % a.W >= a.excl_from ? a.exclude : -1;
+                float best = -INFINITY;
+                int bi = 0x7fffffff;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (col0 + e != excl && v[e] > best) { best = v[e]; bi = col0 + e; }   // ascending: first max wins
+#pragma unroll
+                for (int off = 16; off <= 32; off *= 2) {       // the row's four lane groups
+                    const float ob = __shfl_xor(best, off);
+                    const int oi = __shfl_xor(bi, off);
+                    if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+                }
+                if (a.arg_mx) {      // softmax partial over all 16 columns
+                    float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+                    mx = fmaxf(mx, __shfl_xor(mx, 16));
+                    mx = fmaxf(mx, __shfl_xor(mx, 32));
+                    float sm = expf(v[0] - mx) + expf(v[1] - mx) + expf(v[2] - mx) + expf(v[3] - mx);
+                    sm += __shfl_xor(sm, 16);
+                    sm += __shfl_xor(sm, 32);
+                    if (live && lgrp == 0) {
+                        a.arg_mx[(size_t)nt * a.M + m] = mx;
+                        a.arg_sum[(size_t)nt * a.M + m] = sm;
+                    }
+                }
+                if (live && lgrp == 0) {
+                    a.arg_val[(size_t)nt * a.M + m] = best;
+                    a.arg_idx[(size_t)nt * a.M + m] = bi;
+                }
+            }
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int mt = mt0 + j, nt = nt0 + i, m = mt * 16 + lrow;
             if (mt >= a.MT || m >= a.M || nt >= a.n_tiles) continue;
-            const float rm = s_rm[m - blockIdx.y * BG_MT * 16];
+            const float rm = s_rm[m - bm * BG_MT * 16];
             const f32x4 v = acc[j][i] * rm;
             *(float4*)(a.out + (size_t)m * a.ldo + nt * 16 + lgrp * 4) = float4{v[0], v[1], v[2], v[3]};
         }
@@ -1803,7 +1846,9 @@ __global__ __launch_bounds__(256) void k_swiglu_rows(SwigluRowsArgs a) {
 }
 
 hipError_t launch_gemm_big(int dtype, const BigGemmArgs& a, hipStream_t st) {
-    const dim3 grid((a.n_tiles + BG_NT - 1) / BG_NT, (a.MT + BG_MT - 1) / BG_MT), block(256);
+    const int gn = (a.n_tiles + BG_NT - 1) / BG_NT, gm = (a.MT + BG_MT - 1) / BG_MT;
+    if ((a.m_fast ? gn : gm) > 65535) return hipErrorInvalidValue;     // grid y limit
+    const dim3 grid(a.m_fast ? gm : gn, a.m_fast ? gn : gm), block(256);
     if (dtype == PBD_DTYPE_BF16) {
         if (a.xlo) PBD_LAUNCH((k_gemm_big<bf16, true>), grid, block, 0, st, a);
         else PBD_LAUNCH((k_gemm_big<bf16, false>), grid, block, 0, st, a);
