@@ -746,9 +746,12 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     // chunks in registers (the next one loading), so CH is the largest of
     // 4, 2, 1 for which those, the output accumulators and the Q fragments
     // fit a budget of 304 registers per lane (beyond it the compiler spills).
+    // With four or more query tiles the Q fragments are read from LDS at each
+    // use instead of being held in registers.
+    constexpr bool QF_LDS = QT >= 4;
     constexpr int R_BLK = NDS * 4 + NDT * (int)(sizeof(vraw) / 4);    // one key block's K and V
-    constexpr int R_FIX = QT * (NDT * 4 + NDS * 4);
-    constexpr int CH = 8 * R_BLK + R_FIX <= 304 ? 4 : 4 * R_BLK + R_FIX <= 304 ? 2 : 1;
+    constexpr int R_FIX = QT * (NDT * 4 + (QF_LDS ? 0 : NDS * 4));
+    constexpr int CH = QF_LDS ? 1 : 8 * R_BLK + R_FIX <= 304 ? 4 : 4 * R_BLK + R_FIX <= 304 ? 2 : 1;
     uint4 kn[CH][NDS];
     vraw vn[CH][NDT];
     auto load_chunk = [&](int it0) {
@@ -856,13 +859,21 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     }
     lds_sync();
 
-    // -- Q^T fragments in registers
-    uint4 qf[QT][NDS];
+    // -- Q^T fragments in registers (or read from LDS at each use, QF_LDS)
+    uint4 qf[QF_LDS ? 1 : QT][NDS];
+    if (!QF_LDS) {
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
+        for (int qt = 0; qt < (QF_LDS ? 1 : QT); ++qt)
 #pragma unroll
-        for (int ds = 0; ds < NDS; ++ds)
-            qf[qt][ds] = *(const uint4*)(q_l + (qt * 16 + lrow) * LDQ + ds * FK + lgrp * EPL);
+            for (int ds = 0; ds < NDS; ++ds)
+                qf[qt][ds] = *(const uint4*)(q_l + (qt * 16 + lrow) * LDQ + ds * FK + lgrp * EPL);
+    }
+    // z0: a zero the compiler cannot see through, so that the LDS reads stay
+    // inside the key loop instead of being hoisted into registers
+    auto qfrag = [&](int qt, int ds, int z0) -> uint4 {
+        if (QF_LDS) return *(const uint4*)(q_l + z0 + (qt * 16 + lrow) * LDQ + ds * FK + lgrp * EPL);
+        return qf[QF_LDS ? 0 : qt][ds];
+    };
 
     // block row of each of this lane's query columns (for the causal mask)
     int jq[QT];
@@ -882,61 +893,80 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 
     auto step = [&](int it0, const uint4 (&kcur)[CH][NDS], const vraw (&vcur)[CH][NDT]) {
         const bool first = it0 == wid;
+        int z0 = 0;
+        if (QF_LDS) asm volatile("s_mov_b32 %0, 0" : "=s"(z0));
+        // a chunk whose blocks all lie inside the split's cache keys (below
+        // the chunk rows in chunk mode) needs no key mask (wave-uniform)
+        bool full = true;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int it = it0 + 4 * c;
+            full = full && it < n_items && it < n_pref && (kb_first + it) * 16 + 16 <= (a.chunk ? min(k_hi, t) : k_hi);
+        }
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
-            // lane holds keys key0(c) + 4*lgrp + e for query column qt*16 + lrow
+            // lane holds keys key0(c) + 4*lgrp + e for query column qt*16 + lrow;
+            // masked keys score -inf (weight exp2(-inf) = 0)
             float sv[CH][4];
-            bool valid[CH][4];
-            float mloc = -1e30f;
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
                 const int it = it0 + 4 * c;
                 f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
                 if (it < n_items) {
 #pragma unroll
-                    for (int ds = 0; ds < NDS; ++ds) mma_frag<T>(sc, kcur[c][ds], qf[qt][ds]);
+                    for (int ds = 0; ds < NDS; ++ds) mma_frag<T>(sc, kcur[c][ds], qfrag(qt, ds, z0));
                 }
-                const bool pref = it < n_pref;
-                const int key0 = pref ? (kb_first + it) * 16 : (it - n_pref) * 16;
-                // key masks with bitwise operators: no branches per element
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int kk = key0 + lgrp * 4 + e;
-                    const bool in_pref = (kk < k_hi) & (!a.chunk | (kk < t) | (kk - t <= jq[qt]));
-                    const bool in_blk = (kk < nrows) & ((kk <= jq[qt]) | (jq[qt] >= a.full_from));
-                    const bool ok = (it < n_items) & (pref ? in_pref : in_blk);
-                    valid[c][e] = ok;
-                    sv[c][e] = sc[e] * sl2;
-                    mloc = fmaxf(mloc, ok ? sv[c][e] : -1e30f);
+                for (int e = 0; e < 4; ++e) sv[c][e] = sc[e] * sl2;
+                if (!full) {
+                    const bool pref = it < n_pref;
+                    const int key0 = pref ? (kb_first + it) * 16 : (it - n_pref) * 16;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int kk = key0 + lgrp * 4 + e;
+                        const bool in_pref = (kk < k_hi) & (!a.chunk | (kk < t) | (kk - t <= jq[qt]));
+                        const bool in_blk = (kk < nrows) & ((kk <= jq[qt]) | (jq[qt] >= a.full_from));
+                        const bool ok = (it < n_items) & (pref ? in_pref : in_blk);
+                        if (!ok) sv[c][e] = -INFINITY;
+                    }
                 }
             }
-            mloc = xrow_max(mloc);
-            // The reference maximum m_run is raised (and the output and sum
-            // rescaled) only when some row's maximum exceeds it by more than
-            // RESCALE_SLACK (log2 units, a vote of the wave): the weights
-            // exp2(s - m_run) stay below 2^RESCALE_SLACK and the ratio of sums
-            // is the same for any reference, so only rounding differs.
-            const float m_new = fmaxf(m_run[qt], mloc);
-            if (first) {
-                m_run[qt] = m_new;
-            } else if (__any(m_new > m_run[qt] + RESCALE_SLACK)) {
-                const float corr = exp2f(m_run[qt] - m_new);
-                l_run[qt] *= corr;
+            // The reference maximum m_run is set from the wave's first chunk
+            // and raised (the output and sum rescaled) only when a score
+            // exceeds it by more than RESCALE_SLACK (log2 units, a vote of the
+            // wave): the weights exp2(s - m_run) stay below 2^RESCALE_SLACK
+            // and the ratio of sums is the same for any reference, so only
+            // rounding differs.  Otherwise no row maximum is formed.
+            bool over = false;
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) o_acc[dt][qt] *= corr;
+            for (int c = 0; c < CH; ++c)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) over = over | (sv[c][e] > m_run[qt] + RESCALE_SLACK);
+            if (first || __any(over)) {
+                float mloc = -1e30f;
+#pragma unroll
+                for (int c = 0; c < CH; ++c)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) mloc = fmaxf(mloc, sv[c][e]);
+                const float m_new = fmaxf(m_run[qt], xrow_max(mloc));
+                if (!first) {
+                    const float corr = exp2f(m_run[qt] - m_new);
+                    l_run[qt] *= corr;
+#pragma unroll
+                    for (int dt = 0; dt < NDT; ++dt) o_acc[dt][qt] *= corr;
+                }
                 m_run[qt] = m_new;
             }
+            // l_run holds this lane's share of the row sum; the four lane
+            // groups of a query column are added after the key loop
             f32x4 p[CH];
-            float psum = 0.f;
 #pragma unroll
             for (int c = 0; c < CH; ++c)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    p[c][e] = valid[c][e] ? exp2f(sv[c][e] - m_run[qt]) : 0.f;
-                    psum += p[c][e];
+                    p[c][e] = exp2f(sv[c][e] - m_run[qt]);
+                    l_run[qt] += p[c][e];
                 }
-            psum = xrow_sum(psum);
-            l_run[qt] += psum;
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
                 if (it0 + 4 * c >= n_items) continue;
@@ -971,6 +1001,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
             if (it0 + 4 * CH < n_items) load_chunk(it0 + 4 * CH);
         }
     }
+
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) l_run[qt] = xrow_sum(l_run[qt]);
 
     // -- merge the four waves: common max per query row, then a two-round tree
     //    (waves 2,3 -> 0,1, then 1 -> 0) in LDS; wave 0 writes the partial
