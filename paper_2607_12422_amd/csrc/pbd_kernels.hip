@@ -891,6 +891,10 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     }
     const float sl2 = a.scale_log2;
 
+    // One chunk in phases, each straight-line over all query tiles so that
+    // the tiles' independent MFMA chains interleave: scores, key masks (only
+    // on chunks that reach past the split), one vote on the reference
+    // maximum, weights and P.V.
     auto step = [&](int it0, const uint4 (&kcur)[CH][NDS], const vraw (&vcur)[CH][NDT]) {
         const bool first = it0 == wid;
         int z0 = 0;
@@ -903,51 +907,64 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
             const int it = it0 + 4 * c;
             full = full && it < n_items && it < n_pref && (kb_first + it) * 16 + 16 <= (a.chunk ? min(k_hi, t) : k_hi);
         }
+        // lane holds keys key0(c) + 4*lgrp + e for query column qt*16 + lrow;
+        // masked keys score -inf (weight exp2(-inf) = 0)
+        float sv[QT][CH][4];
 #pragma unroll
-        for (int qt = 0; qt < QT; ++qt) {
-            // lane holds keys key0(c) + 4*lgrp + e for query column qt*16 + lrow;
-            // masked keys score -inf (weight exp2(-inf) = 0)
-            float sv[CH][4];
+        for (int c = 0; c < CH; ++c) {
+            f32x4 sc[QT];
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) sc[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (it0 + 4 * c < n_items) {
+#pragma unroll
+                for (int ds = 0; ds < NDS; ++ds)
+#pragma unroll
+                    for (int qt = 0; qt < QT; ++qt) mma_frag<T>(sc[qt], kcur[c][ds], qfrag(qt, ds, z0));
+            }
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) sv[qt][c][e] = sc[qt][e] * sl2;
+        }
+        if (!full) {
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
                 const int it = it0 + 4 * c;
-                f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
-                if (it < n_items) {
+                const bool pref = it < n_pref;
+                const int key0 = pref ? (kb_first + it) * 16 : (it - n_pref) * 16;
 #pragma unroll
-                    for (int ds = 0; ds < NDS; ++ds) mma_frag<T>(sc, kcur[c][ds], qfrag(qt, ds, z0));
-                }
-#pragma unroll
-                for (int e = 0; e < 4; ++e) sv[c][e] = sc[e] * sl2;
-                if (!full) {
-                    const bool pref = it < n_pref;
-                    const int key0 = pref ? (kb_first + it) * 16 : (it - n_pref) * 16;
+                for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const int kk = key0 + lgrp * 4 + e;
                         const bool in_pref = (kk < k_hi) & (!a.chunk | (kk < t) | (kk - t <= jq[qt]));
                         const bool in_blk = (kk < nrows) & ((kk <= jq[qt]) | (jq[qt] >= a.full_from));
                         const bool ok = (it < n_items) & (pref ? in_pref : in_blk);
-                        if (!ok) sv[c][e] = -INFINITY;
+                        if (!ok) sv[qt][c][e] = -INFINITY;
                     }
-                }
             }
-            // The reference maximum m_run is set from the wave's first chunk
-            // and raised (the output and sum rescaled) only when a score
-            // exceeds it by more than RESCALE_SLACK (log2 units, a vote of the
-            // wave): the weights exp2(s - m_run) stay below 2^RESCALE_SLACK
-            // and the ratio of sums is the same for any reference, so only
-            // rounding differs.  Otherwise no row maximum is formed.
-            bool over = false;
+        }
+        // The reference maximum m_run is set from the wave's first chunk and
+        // raised (the output and sum rescaled) only when a score exceeds it by
+        // more than RESCALE_SLACK (log2 units, one vote of the wave over all
+        // tiles): the weights exp2(s - m_run) stay below 2^RESCALE_SLACK and
+        // the ratio of sums is the same for any reference, so only rounding
+        // differs.  Otherwise no row maximum is formed.
+        bool over = false;
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
             for (int c = 0; c < CH; ++c)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) over = over | (sv[c][e] > m_run[qt] + RESCALE_SLACK);
-            if (first || __any(over)) {
+                for (int e = 0; e < 4; ++e) over = over | (sv[qt][c][e] > m_run[qt] + RESCALE_SLACK);
+        if (first || __any(over)) {
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) {
                 float mloc = -1e30f;
 #pragma unroll
                 for (int c = 0; c < CH; ++c)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) mloc = fmaxf(mloc, sv[c][e]);
+                    for (int e = 0; e < 4; ++e) mloc = fmaxf(mloc, sv[qt][c][e]);
                 const float m_new = fmaxf(m_run[qt], xrow_max(mloc));
                 if (!first) {
                     const float corr = exp2f(m_run[qt] - m_new);
@@ -957,22 +974,26 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                 }
                 m_run[qt] = m_new;
             }
-            // l_run holds this lane's share of the row sum; the four lane
-            // groups of a query column are added after the key loop
-            f32x4 p[CH];
+        }
+        // l_run holds this lane's share of the row sum; the four lane groups
+        // of a query column are added after the key loop
+        f32x4 p[QT][CH];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
             for (int c = 0; c < CH; ++c)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    p[c][e] = exp2f(sv[c][e] - m_run[qt]);
-                    l_run[qt] += p[c][e];
+                    p[qt][c][e] = exp2f(sv[qt][c][e] - m_run[qt]);
+                    l_run[qt] += p[qt][c][e];
                 }
 #pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                if (it0 + 4 * c >= n_items) continue;
+        for (int c = 0; c < CH; ++c) {
+            if (it0 + 4 * c >= n_items) continue;
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) mma_k4(o_acc[dt][qt], vcur[c][dt], p[c]);
-            }
+            for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+                for (int qt = 0; qt < QT; ++qt) mma_k4(o_acc[dt][qt], vcur[c][dt], p[qt][c]);
         }
     };
     if (pipe) {
