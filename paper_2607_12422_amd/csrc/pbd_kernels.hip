@@ -1688,18 +1688,20 @@ hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStre
 // rows it would re-read the operand per weight tile and wait a full load
 // latency per 64-row group.
 // Here a work-group owns a 64-row x 64-column output block (4 x 4 MFMA tiles,
-// a 2 x 2 tile quadrant per wave) and walks K with BG_P fragment steps of
-// loads in flight; r_m (the folded RMSNorm) scales rows in the epilogue and
-// the fp32 result goes to out.  Residual and SwiGLU epilogues run after it as
-// row kernels.  Loads are unconditional from clamped addresses (a guarded
-// load would make the compiler wait for every load at each loop turn): tiles
-// past the ends only feed outputs that are not stored, steps past K are not
-// computed.  With the adapter, a first launch of this kernel on the stacked
+// a 2 x 2 tile quadrant per wave) and walks K through a double buffer in LDS:
+// each K step's 4 W and 4 (+4 residual) operand fragments are loaded once by
+// the work-group, four steps ahead, and every wave reads its quadrant's
+// fragments from LDS.  r_m (the folded RMSNorm) scales rows in the epilogue
+// and the fp32 result goes to out.  Residual and SwiGLU epilogues run after
+// it as row kernels.  Loads are unconditional from clamped addresses (a
+// guarded load would make the compiler wait for every load at each loop
+// turn): tiles past the ends only feed outputs that are not stored, steps
+// past K are not computed.  With the adapter, a first launch of this kernel on the stacked
 // LoRA A tiles leaves the shrink u = A x in fp32, and the projection adds
 // s * B u per tile before the r_m scaling (r_m (W x + s B A x), the same sum
 // the skinny GEMM forms in-tile).
 // ---------------------------------------------------------------------------
-constexpr int BG_MT = 4, BG_NT = 4, BG_P = 8;
+constexpr int BG_MT = 4, BG_NT = 4;
 
 template <typename T, bool SPLIT>
 __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
@@ -1709,22 +1711,30 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
     const int mt0 = bm * BG_MT + (wid / 2) * 2, nt0 = bn * BG_NT + (wid % 2) * 2;
     __shared__ float s_part[4][BG_MT * 16];
     __shared__ float s_rm[BG_MT * 16];
-    uint4 wv[BG_P][2], xh[BG_P][2], xl[BG_P][2];
     const int ntc[2] = {min(nt0, a.n_tiles - 1), min(nt0 + 1, a.n_tiles - 1)};
-    const int mtc[2] = {min(mt0, a.MT - 1), min(mt0 + 1, a.MT - 1)};
-    auto issue = [&](int f, int st) {
+    // wave w loads fragment w of each kind (W tile, value and residual
+    // m-tile) GS steps ahead and writes it to one of two LDS step buffers;
+    // all waves read their operands from there, so each fragment leaves the
+    // cache once per work-group (native vectors keep the slots in registers)
+    constexpr int GS = 4;
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    __shared__ u32x4 s_op[2][12][WAVE];
+    const int ntw = min(bn * BG_NT + wid, a.n_tiles - 1), mtw = min(bm * BG_MT + wid, a.MT - 1);
+    u32x4 gv[GS][3];                      // W, value, residual fragments of a step
+    auto gload = [&](int f, int st) {
         const int fc = min(f, a.kb - 1);
-#pragma unroll
-        for (int i = 0; i < 2; ++i) wv[st][i] = a.w[((size_t)ntc[i] * a.kb + fc) * WAVE + lane];
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const size_t xi = ((size_t)fc * a.MT + mtc[j]) * WAVE + lane;
-            xh[st][j] = a.xhi[xi];
-            if (SPLIT) xl[st][j] = a.xlo[xi];
-        }
+        gv[st][0] = *(const u32x4*)(a.w + ((size_t)ntw * a.kb + fc) * WAVE + lane);
+        const size_t xi = ((size_t)fc * a.MT + mtw) * WAVE + lane;
+        gv[st][1] = *(const u32x4*)(a.xhi + xi);
+        if (SPLIT) gv[st][2] = *(const u32x4*)(a.xlo + xi);
+    };
+    auto swrite = [&](int st, int buf) {
+        s_op[buf][wid][lane] = gv[st][0];
+        s_op[buf][4 + wid][lane] = gv[st][1];
+        if (SPLIT) s_op[buf][8 + wid][lane] = gv[st][2];
     };
 #pragma unroll
-    for (int st = 0; st < BG_P; ++st) issue(st, st);
+    for (int st = 0; st < GS; ++st) gload(st, st);
     // RMSNorm partials of the block's rows: four slices per row, summed in LDS
     {
         const int r = threadIdx.x % (BG_MT * 16), sl = threadIdx.x / (BG_MT * 16);
@@ -1739,19 +1749,36 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
     for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int i = 0; i < 2; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int f0 = 0; f0 < a.kb; f0 += BG_P) {
+    // step f sits in LDS buffer f & 1 (GS is even, so that is u & 1); each
+    // turn writes step f + 1 into the other buffer, reloads the register slot
+    // of step f (already in LDS) with step f + GS, and ends with a barrier.
+    // Loads past K repeat the last step; their products are not formed.
+    swrite(0, 0);
+    lds_sync();
+    for (int f0 = 0; f0 < a.kb; f0 += GS) {
 #pragma unroll
-        for (int st = 0; st < BG_P; ++st) {
-            if (f0 + st < a.kb) {
+        for (int u = 0; u < GS; ++u) {
+            const int buf = u & 1;
+            uint4 w2[2], h2[2], l2[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) w2[i] = __builtin_bit_cast(uint4, s_op[buf][(wid % 2) * 2 + i][lane]);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                h2[j] = __builtin_bit_cast(uint4, s_op[buf][4 + (wid / 2) * 2 + j][lane]);
+                if (SPLIT) l2[j] = __builtin_bit_cast(uint4, s_op[buf][8 + (wid / 2) * 2 + j][lane]);
+            }
+            swrite((u + 1) % GS, buf ^ 1);
+            gload(f0 + u + GS, u);
+            if (f0 + u < a.kb) {
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
 #pragma unroll
                     for (int i = 0; i < 2; ++i) {
-                        mma_frag<T>(acc[j][i], wv[st][i], xh[st][j]);
-                        if (SPLIT) mma_frag<T>(acc[j][i], wv[st][i], xl[st][j]);
+                        mma_frag<T>(acc[j][i], w2[i], h2[j]);
+                        if (SPLIT) mma_frag<T>(acc[j][i], w2[i], l2[j]);
                     }
             }
-            issue(f0 + st + BG_P, st);
+            lds_sync();
         }
     }
     if (a.lrt > 0) {
