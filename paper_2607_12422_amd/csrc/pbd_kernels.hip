@@ -1701,54 +1701,70 @@ hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStre
 // s * B u per tile before the r_m scaling (r_m (W x + s B A x), the same sum
 // the skinny GEMM forms in-tile).
 // ---------------------------------------------------------------------------
-constexpr int BG_MT = 4, BG_NT = 4;
-
-template <typename T, bool SPLIT>
+// WT: tiles per wave in each direction (2: 64x64 blocks, 4: 128x128 blocks)
+template <typename T, bool SPLIT, int WT>
 __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
+    constexpr int BT = 2 * WT;                  // m- and n-tiles per block
+    constexpr int FPW = BT / 4;                 // fragments of each kind a wave stages per step
+    constexpr int NSL = 256 / (BT * 16);        // RMSNorm partial slices per row
     const int lane = threadIdx.x % WAVE, wid = threadIdx.x / WAVE;
     const int lrow = lane % 16, lgrp = lane / 16;
     const int bm = a.m_fast ? blockIdx.x : blockIdx.y, bn = a.m_fast ? blockIdx.y : blockIdx.x;
-    const int mt0 = bm * BG_MT + (wid / 2) * 2, nt0 = bn * BG_NT + (wid % 2) * 2;
-    __shared__ float s_part[4][BG_MT * 16];
-    __shared__ float s_rm[BG_MT * 16];
-    const int ntc[2] = {min(nt0, a.n_tiles - 1), min(nt0 + 1, a.n_tiles - 1)};
-    // wave w loads fragment w of each kind (W tile, value and residual
-    // m-tile) GS steps ahead and writes it to one of two LDS step buffers;
-    // all waves read their operands from there, so each fragment leaves the
-    // cache once per work-group (native vectors keep the slots in registers)
+    const int mt0 = bm * BT + (wid / 2) * WT, nt0 = bn * BT + (wid % 2) * WT;
+    __shared__ float s_part[NSL][BT * 16];
+    __shared__ float s_rm[BT * 16];
+    int ntc[WT];
+#pragma unroll
+    for (int i = 0; i < WT; ++i) ntc[i] = min(nt0 + i, a.n_tiles - 1);
+    // wave w loads fragments w FPW .. w FPW + FPW - 1 of each kind (W tile,
+    // value and residual m-tile) GS steps ahead and writes them to one of two
+    // LDS step buffers; all waves read their operands from there, so each
+    // fragment leaves the cache once per work-group (native vectors keep the
+    // slots in registers)
     constexpr int GS = 4;
     typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-    __shared__ u32x4 s_op[2][12][WAVE];
-    const int ntw = min(bn * BG_NT + wid, a.n_tiles - 1), mtw = min(bm * BG_MT + wid, a.MT - 1);
-    u32x4 gv[GS][3];                      // W, value, residual fragments of a step
+    __shared__ u32x4 s_op[2][3 * BT][WAVE];     // [W tiles | value m-tiles | residual m-tiles]
+    int ntw[FPW], mtw[FPW];
+#pragma unroll
+    for (int k = 0; k < FPW; ++k) {
+        ntw[k] = min(bn * BT + wid * FPW + k, a.n_tiles - 1);
+        mtw[k] = min(bm * BT + wid * FPW + k, a.MT - 1);
+    }
+    u32x4 gv[GS][3][FPW];                 // W, value, residual fragments of a step
     auto gload = [&](int f, int st) {
         const int fc = min(f, a.kb - 1);
-        gv[st][0] = *(const u32x4*)(a.w + ((size_t)ntw * a.kb + fc) * WAVE + lane);
-        const size_t xi = ((size_t)fc * a.MT + mtw) * WAVE + lane;
-        gv[st][1] = *(const u32x4*)(a.xhi + xi);
-        if (SPLIT) gv[st][2] = *(const u32x4*)(a.xlo + xi);
+#pragma unroll
+        for (int k = 0; k < FPW; ++k) {
+            gv[st][0][k] = *(const u32x4*)(a.w + ((size_t)ntw[k] * a.kb + fc) * WAVE + lane);
+            const size_t xi = ((size_t)fc * a.MT + mtw[k]) * WAVE + lane;
+            gv[st][1][k] = *(const u32x4*)(a.xhi + xi);
+            if (SPLIT) gv[st][2][k] = *(const u32x4*)(a.xlo + xi);
+        }
     };
     auto swrite = [&](int st, int buf) {
-        s_op[buf][wid][lane] = gv[st][0];
-        s_op[buf][4 + wid][lane] = gv[st][1];
-        if (SPLIT) s_op[buf][8 + wid][lane] = gv[st][2];
+#pragma unroll
+        for (int k = 0; k < FPW; ++k) {
+            s_op[buf][wid * FPW + k][lane] = gv[st][0][k];
+            s_op[buf][BT + wid * FPW + k][lane] = gv[st][1][k];
+            if (SPLIT) s_op[buf][2 * BT + wid * FPW + k][lane] = gv[st][2][k];
+        }
     };
 #pragma unroll
     for (int st = 0; st < GS; ++st) gload(st, st);
-    // RMSNorm partials of the block's rows: four slices per row, summed in LDS
+    // RMSNorm partials of the block's rows: NSL slices per row, summed in LDS
     {
-        const int r = threadIdx.x % (BG_MT * 16), sl = threadIdx.x / (BG_MT * 16);
-        const int m = bm * BG_MT * 16 + r;
+        const int r = threadIdx.x % (BT * 16), sl = threadIdx.x / (BT * 16);
+        const int m = bm * BT * 16 + r;
         float sm = 0.f;
         if (m < a.M)
-            for (int p = sl; p < a.n_sq; p += 4) sm += a.sq[(size_t)p * a.sq_stride + m];
+            for (int p = sl; p < a.n_sq; p += NSL) sm += a.sq[(size_t)p * a.sq_stride + m];
         s_part[sl][r] = sm;
     }
-    f32x4 acc[2][2];
+    f32x4 acc[WT][WT];
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < WT; ++j)
 #pragma unroll
-        for (int i = 0; i < 2; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < WT; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
     // step f sits in LDS buffer f & 1 (GS is even, so that is u & 1); each
     // turn writes step f + 1 into the other buffer, reloads the register slot
     // of step f (already in LDS) with step f + GS, and ends with a barrier.
@@ -1759,21 +1775,21 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
 #pragma unroll
         for (int u = 0; u < GS; ++u) {
             const int buf = u & 1;
-            uint4 w2[2], h2[2], l2[2];
+            uint4 w2[WT], h2[WT], l2[WT];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) w2[i] = __builtin_bit_cast(uint4, s_op[buf][(wid % 2) * 2 + i][lane]);
+            for (int i = 0; i < WT; ++i) w2[i] = __builtin_bit_cast(uint4, s_op[buf][(wid % 2) * WT + i][lane]);
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                h2[j] = __builtin_bit_cast(uint4, s_op[buf][4 + (wid / 2) * 2 + j][lane]);
-                if (SPLIT) l2[j] = __builtin_bit_cast(uint4, s_op[buf][8 + (wid / 2) * 2 + j][lane]);
+            for (int j = 0; j < WT; ++j) {
+                h2[j] = __builtin_bit_cast(uint4, s_op[buf][BT + (wid / 2) * WT + j][lane]);
+                if (SPLIT) l2[j] = __builtin_bit_cast(uint4, s_op[buf][2 * BT + (wid / 2) * WT + j][lane]);
             }
             swrite((u + 1) % GS, buf ^ 1);
             gload(f0 + u + GS, u);
             if (f0 + u < a.kb) {
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < WT; ++j)
 #pragma unroll
-                    for (int i = 0; i < 2; ++i) {
+                    for (int i = 0; i < WT; ++i) {
                         mma_frag<T>(acc[j][i], w2[i], h2[j]);
                         if (SPLIT) mma_frag<T>(acc[j][i], w2[i], l2[j]);
                     }
@@ -1785,17 +1801,17 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
         // LoRA expand: lane operand u[m = tile row lrow][r = 16 t + 4 lgrp + e],
         // the layout the shrink's epilogue stored it in
         typedef typename K4<T>::raw braw;
-        float lsc[2];
-        int mc[2];
+        float lsc[WT];
+        int mc[WT];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < WT; ++j) {
             const int m = (mt0 + j) * 16 + lrow;
             mc[j] = min(m, a.M - 1);
             lsc[j] = (m < a.M && m % a.W >= a.adapter_from) ? a.scale : 0.f;
         }
         const int nsrc = a.lora_mode == LORA_ROW_HALF ? 2 : 1;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < WT; ++i) {
             const int nt = ntc[i];
             const int s0 = a.lora_mode == LORA_BY_TILE ? (nt < a.tile_split0 ? 0 : nt < a.tile_split1 ? 1 : 2) : 0;
             for (int t = 0; t < a.lrt; ++t) {
@@ -1805,7 +1821,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
                     // gate/up tiles: rows 0-7 take source 0 (gate), 8-15 source 1 (up)
                     const braw bb = (nsrc == 2 && ((lrow < 8) != (sc == 0))) ? braw{} : b;
 #pragma unroll
-                    for (int j = 0; j < 2; ++j) {
+                    for (int j = 0; j < WT; ++j) {
                         const float4 uv = *(const float4*)(a.u + (size_t)mc[j] * a.ldu + ((s0 + sc) * a.lrt + t) * 16 + lgrp * 4);
                         mma_k4_split(acc[j][i], bb, f32x4{uv.x, uv.y, uv.z, uv.w} * lsc[j]);
                     }
@@ -1814,8 +1830,10 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
         }
     }
     __syncthreads();
-    if (threadIdx.x < BG_MT * 16) {
-        const float sm = s_part[0][threadIdx.x] + s_part[1][threadIdx.x] + s_part[2][threadIdx.x] + s_part[3][threadIdx.x];
+    if (threadIdx.x < BT * 16) {
+        float sm = 0.f;
+#pragma unroll
+        for (int sl = 0; sl < NSL; ++sl) sm += s_part[sl][threadIdx.x];
         s_rm[threadIdx.x] = a.n_sq > 0 ? rsqrtf(sm / (float)a.norm_dim + a.eps) : 1.f;
     }
     __syncthreads();
@@ -1823,12 +1841,12 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
     if (a.arg_val) {
         // every lane takes part in the cross-lane steps; only live rows store
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < WT; ++j)
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
+            for (int i = 0; i < WT; ++i) {
                 const int mt = mt0 + j, nt = nt0 + i, m = mt * 16 + lrow;
                 const bool live = mt < a.MT && m < a.M && nt < a.n_tiles;
-                const f32x4 v = acc[j][i] * s_rm[m - bm * BG_MT * 16];
+                const f32x4 v = acc[j][i] * s_rm[m - bm * BT * 16];
                 const int col0 = nt * 16 + lgrp * 4;
                 if (live && a.logits) *(float4*)(a.logits + (size_t)m * a.ldo + col0) = float4{v[0], v[1], v[2], v[3]};
                 const int excl = m % a.W >= a.excl_from ? a.exclude : -1;
@@ -1863,12 +1881,12 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
         return;
     }
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < WT; ++j)
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < WT; ++i) {
             const int mt = mt0 + j, nt = nt0 + i, m = mt * 16 + lrow;
             if (mt >= a.MT || m >= a.M || nt >= a.n_tiles) continue;
-            const float rm = s_rm[m - bm * BG_MT * 16];
+            const float rm = s_rm[m - bm * BT * 16];
             const f32x4 v = acc[j][i] * rm;
             *(float4*)(a.out + (size_t)m * a.ldo + nt * 16 + lgrp * 4) = float4{v[0], v[1], v[2], v[3]};
         }
@@ -1926,17 +1944,30 @@ __global__ __launch_bounds__(256) void k_swiglu_rows(SwigluRowsArgs a) {
     put_operand_run<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 8 + c0, a.n_MT), hv);
 }
 
-hipError_t launch_gemm_big(int dtype, const BigGemmArgs& a, hipStream_t st) {
-    const int gn = (a.n_tiles + BG_NT - 1) / BG_NT, gm = (a.MT + BG_MT - 1) / BG_MT;
+template <int WT>
+static hipError_t launch_gemm_big_wt(int dtype, const BigGemmArgs& a, hipStream_t st) {
+    const int gn = (a.n_tiles + 2 * WT - 1) / (2 * WT), gm = (a.MT + 2 * WT - 1) / (2 * WT);
     if ((a.m_fast ? gn : gm) > 65535) return hipErrorInvalidValue;     // grid y limit
     const dim3 grid(a.m_fast ? gm : gn, a.m_fast ? gn : gm), block(256);
     if (dtype == PBD_DTYPE_BF16) {
-        if (a.xlo) PBD_LAUNCH((k_gemm_big<bf16, true>), grid, block, 0, st, a);
-        else PBD_LAUNCH((k_gemm_big<bf16, false>), grid, block, 0, st, a);
+        if (a.xlo) PBD_LAUNCH((k_gemm_big<bf16, true, WT>), grid, block, 0, st, a);
+        else PBD_LAUNCH((k_gemm_big<bf16, false, WT>), grid, block, 0, st, a);
     } else {
-        PBD_LAUNCH((k_gemm_big<float, false>), grid, block, 0, st, a);
+        PBD_LAUNCH((k_gemm_big<float, false, WT>), grid, block, 0, st, a);
     }
     return hipGetLastError();
+}
+
+// The tied LM head (argmax epilogue) takes 128 x 128 blocks (twice the MFMA
+// work per byte of LDS traffic) when they still give every CU four
+// work-groups and pad at most one row in eight; everything else takes
+// 64 x 64, whose extra work-groups hide more latency (measured faster for
+// the projections at up to 1056 rows)
+hipError_t launch_gemm_big(int dtype, const BigGemmArgs& a, hipStream_t st) {
+    const int bm8 = (a.MT + 7) / 8;
+    const long big_blocks = (long)bm8 * ((a.n_tiles + 7) / 8);
+    if (a.arg_val && big_blocks >= 4 * 256 && (bm8 * 8 - a.MT) * 8 <= a.MT) return launch_gemm_big_wt<4>(dtype, a, st);
+    return launch_gemm_big_wt<2>(dtype, a, st);
 }
 hipError_t launch_resid_rows(int dtype, const ResidRowsArgs& a, hipStream_t st) {
     const int n = a.M * a.n_tiles;

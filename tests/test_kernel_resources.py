@@ -27,7 +27,7 @@ HOT = [
     r"_ZN3pbd8k_acceptENS_10AcceptArgsE",
     r"_ZN3pbd8k_remaskENS_10RemaskArgsE",
     # prefill chunks
-    r"_ZN3pbd10k_gemm_bigIDF16bLb[01]EEEvNS_11BigGemmArgsE",
+    r"_ZN3pbd10k_gemm_bigIDF16bLb[01]ELi[24]EEEvNS_11BigGemmArgsE",
     r"_ZN3pbd9k_kvwriteIDF16bLi128EEEvNS_11KVWriteArgsE",
     r"_ZN3pbd12k_resid_rowsIDF16bEEvNS_13ResidRowsArgsE",
     r"_ZN3pbd13k_swiglu_rowsIDF16bEEvNS_14SwigluRowsArgsE",
