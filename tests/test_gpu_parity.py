@@ -350,6 +350,39 @@ def test_large_batch_adapter_passes_match_oracle():
     g.close()
 
 
+def test_full_width_batch_lm_head_blocks_match_oracle():
+    """256 sequences x 16 block rows = 4096 rows (the largest batch x width):
+    the LM head runs as 128 x 128 blocks of the large-M GEMM (32 x 32 blocks
+    against the 4096-word vocabulary, no padded rows), with and without the
+    softmax partials of the denoising confidence; sampled sequences match
+    the oracle row by row, and every sequence's drafts are valid ids."""
+    from gpu_harness import check_denoise
+    cfg, w = _tiny(15)
+    B = 256
+    prompts = synth.make_prompts(cfg, [3 + (b * 7) % 13 for b in range(B)], 5)
+    g = GpuRun(cfg, w, max_batch=B, max_seq=48)
+    g.prefill(prompts)
+    m = om.OracleModel(w)
+    d, dlg = g.draft()
+    v, vlg = g.verify(d)
+    d, dlg, v, vlg = (x.cpu().numpy() for x in (d, dlg, v, vlg))
+    assert d.min() >= 0 and d.max() < cfg.vocab and not np.any(d == cfg.mask_id)
+    for b in (0, 1, 77, 128, 200, 255):
+        st = om.prefill(m, prompts[b])
+        _, dl_ref = om.draft(m, st)
+        assert np.abs(dlg[b] - dl_ref).max() <= TOL32, b
+        _check_tokens(d[b], dl_ref[1:], TOL32, exclude=cfg.mask_id)
+        _, vl_ref, _, _ = om.verify(m, st, d[b])
+        assert np.abs(vlg[b] - vl_ref).max() <= TOL32, b
+        _check_tokens(v[b], vl_ref, TOL32)
+    dd, conf, fixed, lg = (x.cpu().numpy() for x in g.denoise(2))
+    for b in (3, 250):
+        st = om.prefill(m, prompts[b])
+        check_denoise(m, st, dd[b], conf[b], fixed[b], lg[b], 2, TOL32, what=f"seq {b}")
+    assert g.status() == 0
+    g.close()
+
+
 def test_block_zero_is_greedy_autoregressive_decoding():
     """D = 0: the verify of [anchor] plus the commit is one greedy decode step;
     twelve of them reproduce the oracle's greedy continuation (at every step
