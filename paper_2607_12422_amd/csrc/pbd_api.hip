@@ -349,8 +349,9 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     // with the adapter: the shrink of the projection's nsrc LoRA A matrices,
     // stacked in the packed layout as one [nsrc RT][kb] tile matrix, then the
     // projection with the expand
-    auto launch_big = [&](const FGemmArgs& g, int nsrc) -> hipError_t {
+    auto launch_big = [&](const FGemmArgs& g, int nsrc, bool swiglu = false) -> hipError_t {
         BigGemmArgs b = big_args(g);
+        if (swiglu) { b.sw_hi = g.nx_hi; b.sw_lo = g.nx_lo; b.sw_MT = g.n_MT; }
         if (lora) {
             const size_t src_frags = (size_t)y.RT * g.kb * 64;          // uint4 per source matrix
             for (int i = 1; i < nsrc; ++i)
@@ -457,11 +458,8 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.lb = pk + lo_.lb_gu;
         g.nx_hi = hi(y.w_xd); g.nx_lo = lo(y.w_xd); g.n_MT = MT;
         if (big) {
-            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 2), "gate/up gemm");
-            SwigluRowsArgs sw{};
-            sw.M = M; sw.n_tiles = g.n_tiles; sw.ldy = 2 * y.F; sw.n_MT = MT;
-            sw.y = (const float*)(ws + y.w_big); sw.nx_hi = g.nx_hi; sw.nx_lo = g.nx_lo;
-            PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_swiglu_rows(dt, sw, st), "swiglu");
+            // SwiGLU in the GEMM epilogue: the down projection's operand directly
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 2, true), "gate/up gemm");
         } else {
             PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_SWIGLU, st), "gate/up gemm");
         }

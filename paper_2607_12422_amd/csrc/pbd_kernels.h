@@ -182,6 +182,13 @@ struct BigGemmArgs {
     // grid order: m-blocks fastest (the blocks that share weight tiles run
     // together; for weights larger than the memory-side cache)
     int m_fast;
+    // SwiGLU epilogue (sw_hi set; gate/up tiles with rows 0-7 gate and 8-15
+    // up of the same FFN columns): h = silu(gate) * up written as the down
+    // projection's operand fragments (K = n_tiles * 8, sw_MT m-tiles); out is
+    // not written
+    void* sw_hi;
+    void* sw_lo;
+    int sw_MT;
 };
 
 // Residual epilogue of a large-M projection: x += y over 16-column tiles, the
@@ -194,14 +201,6 @@ struct ResidRowsArgs {
     void* nx_hi;
     void* nx_lo;
     float* sq_out;
-};
-
-// SwiGLU epilogue of a large-M gate/up projection (tile rows 0-7 gate, 8-15 up).
-struct SwigluRowsArgs {
-    int M, n_tiles, ldy, n_MT;
-    const float* y;
-    void* nx_hi;
-    void* nx_lo;
 };
 
 struct CombineArgs {
@@ -290,7 +289,6 @@ hipError_t launch_kvwrite(int dtype, int head_dim, const KVWriteArgs& a, int bat
 hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStream_t st);
 hipError_t launch_gemm_big(int dtype, const BigGemmArgs& a, hipStream_t st);   // split iff a.xlo
 hipError_t launch_resid_rows(int dtype, const ResidRowsArgs& a, hipStream_t st);
-hipError_t launch_swiglu_rows(int dtype, const SwigluRowsArgs& a, hipStream_t st);
 hipError_t launch_remask(const RemaskArgs& a, int batch, hipStream_t st);
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st);
 hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st);

@@ -1880,6 +1880,33 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
             }
         return;
     }
+    if (a.sw_hi) {
+        // SwiGLU: the lane's up values sit 32 lanes away (column + 8); lane
+        // groups 0 and 1 form h for FFN columns 8 nt + 4 lgrp + e and one
+        // lane writes each run of EPL consecutive columns, as the row kernel
+        // does (same values, same arithmetic)
+        constexpr int EPL = Elt<T>::EPL;
+#pragma unroll
+        for (int j = 0; j < WT; ++j)
+#pragma unroll
+            for (int i = 0; i < WT; ++i) {
+                const int mt = mt0 + j, nt = nt0 + i, m = mt * 16 + lrow;
+                const bool live = mt < a.MT && m < a.M && nt < a.n_tiles;
+                const f32x4 v = acc[j][i] * s_rm[m - bm * BT * 16];
+                float h[8];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float gt = v[e], up = __shfl_xor(v[e], 32);
+                    h[e] = gt / (1.f + __expf(-gt)) * up;
+                }
+#pragma unroll
+                for (int e = 0; e < 4; ++e) h[4 + e] = __shfl_xor(h[e], 16);   // lane group 0 gets columns 4..7
+                const bool writer = EPL == 8 ? lgrp == 0 : lgrp < 2;
+                if (live && writer)
+                    put_operand_run<T>((T*)a.sw_hi, (T*)a.sw_lo, xfrag_elem<T>(m, nt * 8 + lgrp * 4, a.sw_MT), h);
+            }
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < WT; ++j)
 #pragma unroll
@@ -1926,23 +1953,6 @@ __global__ __launch_bounds__(256) void k_resid_rows(ResidRowsArgs a) {
     a.sq_out[(size_t)tile * a.sq_stride + m] = ss;
 }
 
-// thread: one row, one run of EPL outputs of one gate/up tile
-template <typename T>
-__global__ __launch_bounds__(256) void k_swiglu_rows(SwigluRowsArgs a) {
-    constexpr int EPL = Elt<T>::EPL, RUNS = 8 / EPL;
-    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-    const int m = idx / (a.n_tiles * RUNS), rem = idx % (a.n_tiles * RUNS);
-    const int tile = rem / RUNS, c0 = (rem % RUNS) * EPL;
-    if (m >= a.M) return;
-    const float* y = a.y + (size_t)m * a.ldy + tile * 16;
-    float hv[EPL];
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-        const float gt = y[c0 + i], up = y[c0 + i + 8];
-        hv[i] = gt / (1.f + __expf(-gt)) * up;
-    }
-    put_operand_run<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 8 + c0, a.n_MT), hv);
-}
 
 template <int WT>
 static hipError_t launch_gemm_big_wt(int dtype, const BigGemmArgs& a, hipStream_t st) {
@@ -1973,13 +1983,6 @@ hipError_t launch_resid_rows(int dtype, const ResidRowsArgs& a, hipStream_t st) 
     const int n = a.M * a.n_tiles;
     if (dtype == PBD_DTYPE_BF16) PBD_LAUNCH(k_resid_rows<bf16>, dim3((n + 255) / 256), dim3(256), 0, st, a);
     else PBD_LAUNCH(k_resid_rows<float>, dim3((n + 255) / 256), dim3(256), 0, st, a);
-    return hipGetLastError();
-}
-hipError_t launch_swiglu_rows(int dtype, const SwigluRowsArgs& a, hipStream_t st) {
-    const int runs = dtype == PBD_DTYPE_BF16 ? 8 / Elt<bf16>::EPL : 8 / Elt<float>::EPL;
-    const int n = a.M * a.n_tiles * runs;
-    if (dtype == PBD_DTYPE_BF16) PBD_LAUNCH(k_swiglu_rows<bf16>, dim3((n + 255) / 256), dim3(256), 0, st, a);
-    else PBD_LAUNCH(k_swiglu_rows<float>, dim3((n + 255) / 256), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
