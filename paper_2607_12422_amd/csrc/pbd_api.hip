@@ -53,7 +53,7 @@ struct Layout {
     size_t w_kpart, w_kcnt;                          // split-K partial tiles and arrival counters
     size_t w_arg_mx, w_arg_sum;                      // LM-head softmax partials (draft confidence)
     size_t w_xc[2], w_sqc;                           // prefill: gathered last rows (LM-head operand, Σx² partials)
-    size_t w_big;                                    // fp32 output of a large-M projection
+    bool big;                                        // passes of >= BIG_MIN_MT m-tiles can use the large-M GEMM
     size_t w_u;                                      // its LoRA shrink u = A x, [M][sources * RT * 16] fp32
     size_t w_dn_tok, w_dn_conf;                      // one denoising pass's candidates and confidences
     int ksplit;                                      // K slices of the residual GEMMs
@@ -179,8 +179,8 @@ void make_layout(const pbd_config* c, Layout& y) {
     const size_t xfc = (size_t)cdiv(y.Bmax, 16) * FR;
     y.w_xc[0] = take(y.kb_e * xfc); y.w_xc[1] = take(nlo * y.kb_e * xfc);
     y.w_sqc = take((size_t)std::max(y.tiles_d, 1) * y.Bmax * 4);
-    y.w_big = y.Mmax >= BIG_MIN_MT * 16 ? take((size_t)y.Mmax * std::max(y.H, 2 * y.F) * 4) : 0;
-    y.w_u = y.w_big && y.r > 0 ? take((size_t)y.Mmax * 3 * y.RT * 16 * 4) : 0;   // LoRA shrink, large-M path
+    y.big = y.Mmax >= BIG_MIN_MT * 16;
+    y.w_u = y.big && y.r > 0 ? take((size_t)y.Mmax * 3 * y.RT * 16 * 4) : 0;   // LoRA shrink, large-M path
     y.w_dn_conf = take((size_t)y.Bmax * y.D * 4);
     y.ws_bytes = off;
 }
@@ -334,24 +334,25 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     // passes of many rows (prefill chunks, large-batch steps): large-M
     // projections, with the residual / SwiGLU epilogues as row kernels on
     // their fp32 output
-    const bool big = MT >= BIG_MIN_MT && y.w_big != 0 && (!lora || y.w_u != 0);
-    float* ybig = (float*)(ws + y.w_big);
+    const bool big = MT >= BIG_MIN_MT && y.big && (!lora || y.w_u != 0);
     float* ubig = (float*)(ws + y.w_u);
     auto big_args = [&](const FGemmArgs& g) {
         BigGemmArgs b{};
         b.w = g.w; b.n_tiles = g.n_tiles; b.kb = g.kb; b.xhi = g.xhi; b.xlo = g.xlo; b.M = g.M; b.MT = g.MT;
         b.sq = g.sq; b.n_sq = g.n_sq; b.sq_stride = g.sq_stride; b.norm_dim = g.norm_dim; b.eps = g.eps;
-        const bool direct = g.out != nullptr;       // q/k/v: straight to the projection buffer
-        b.out = direct ? g.out : ybig;
-        b.ldo = direct ? g.ldo : g.n_tiles * 16;
+        b.out = g.out; b.ldo = g.ldo;                // STORE (q/k/v); the other projections use epilogues
         return b;
     };
     // with the adapter: the shrink of the projection's nsrc LoRA A matrices,
     // stacked in the packed layout as one [nsrc RT][kb] tile matrix, then the
     // projection with the expand
-    auto launch_big = [&](const FGemmArgs& g, int nsrc, bool swiglu = false) -> hipError_t {
+    auto launch_big = [&](const FGemmArgs& g, int nsrc, int epi = EPI_STORE) -> hipError_t {
         BigGemmArgs b = big_args(g);
-        if (swiglu) { b.sw_hi = g.nx_hi; b.sw_lo = g.nx_lo; b.sw_MT = g.n_MT; }
+        if (epi == EPI_SWIGLU) { b.sw_hi = g.nx_hi; b.sw_lo = g.nx_lo; b.sw_MT = g.n_MT; }
+        if (epi == EPI_RESID) {
+            b.rx = g.x; b.ldx = g.ldx; b.rgain = g.gnext; b.rn_hi = g.nx_hi; b.rn_lo = g.nx_lo;
+            b.rn_MT = g.n_MT; b.rsq = g.sq_out; b.rsq_stride = g.sq_stride;
+        }
         if (lora) {
             const size_t src_frags = (size_t)y.RT * g.kb * 64;          // uint4 per source matrix
             for (int i = 1; i < nsrc; ++i)
@@ -366,13 +367,6 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
             b.W = g.W; b.adapter_from = g.adapter_from; b.scale = g.scale; b.lb = g.lb;
         }
         return launch_gemm_big(dt, b, st);
-    };
-    auto resid_args = [&](const FGemmArgs& g) {
-        ResidRowsArgs r{};
-        r.M = M; r.n_tiles = g.n_tiles; r.ldx = g.ldx; r.ldy = g.n_tiles * 16; r.n_MT = g.n_MT;
-        r.sq_stride = g.sq_stride; r.x = g.x; r.y = ybig; r.gnext = g.gnext;
-        r.nx_hi = g.nx_hi; r.nx_lo = g.nx_lo; r.sq_out = g.sq_out;
-        return r;
     };
     const int L = q.n_layers > 0 ? q.n_layers : y.L;
     for (int l = 0; l < L; ++l) {
@@ -445,8 +439,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.sq_out = sq_m;
         split_k(g);
         if (big) {
-            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 1), "o gemm");
-            PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_resid_rows(dt, resid_args(g), st), "o residual");
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 1, EPI_RESID), "o gemm");
         } else {
             PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "o gemm");
         }
@@ -459,7 +452,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.nx_hi = hi(y.w_xd); g.nx_lo = lo(y.w_xd); g.n_MT = MT;
         if (big) {
             // SwiGLU in the GEMM epilogue: the down projection's operand directly
-            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 2, true), "gate/up gemm");
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 2, EPI_SWIGLU), "gate/up gemm");
         } else {
             PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_SWIGLU, st), "gate/up gemm");
         }
@@ -472,8 +465,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.nx_hi = hi(y.w_xa); g.nx_lo = lo(y.w_xa); g.n_MT = MT; g.sq_out = sq_a;
         split_k(g);
         if (big) {
-            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 1), "down gemm");
-            PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_resid_rows(dt, resid_args(g), st), "down residual");
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 1, EPI_RESID), "down gemm");
         } else {
             PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "down gemm");
         }

@@ -189,18 +189,18 @@ struct BigGemmArgs {
     void* sw_hi;
     void* sw_lo;
     int sw_MT;
-};
-
-// Residual epilogue of a large-M projection: x += y over 16-column tiles, the
-// next operand x * g_next and the per-tile row sums of squares.
-struct ResidRowsArgs {
-    int M, n_tiles, ldx, ldy, n_MT, sq_stride;
-    float* x;
-    const float* y;
-    const void* gnext;
-    void* nx_hi;
-    void* nx_lo;
-    float* sq_out;
+    // residual epilogue (rx set; n = hidden): x += y in place ([M][ldx]
+    // fp32), the next RMSNorm operand x * rgain as fragments (rn_MT m-tiles)
+    // and the tile's row sums of squares rsq[tile * rsq_stride + m]; out is
+    // not written
+    float* rx;
+    int ldx;
+    const void* rgain;
+    void* rn_hi;
+    void* rn_lo;
+    int rn_MT;
+    float* rsq;
+    int rsq_stride;
 };
 
 struct CombineArgs {
@@ -288,7 +288,6 @@ hipError_t launch_accept(const AcceptArgs& a, hipStream_t st);
 hipError_t launch_kvwrite(int dtype, int head_dim, const KVWriteArgs& a, int batch, hipStream_t st);
 hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStream_t st);
 hipError_t launch_gemm_big(int dtype, const BigGemmArgs& a, hipStream_t st);   // split iff a.xlo
-hipError_t launch_resid_rows(int dtype, const ResidRowsArgs& a, hipStream_t st);
 hipError_t launch_remask(const RemaskArgs& a, int batch, hipStream_t st);
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st);
 hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st);

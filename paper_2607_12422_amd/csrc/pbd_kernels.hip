@@ -1880,6 +1880,44 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
             }
         return;
     }
+    if (a.rx) {
+        // residual: the lane's 4 columns of the row; the tile's sum of squares
+        // over its four lane groups; runs of EPL operand values gathered from
+        // the neighbouring lane group for bf16
+        constexpr int EPL = Elt<T>::EPL;
+#pragma unroll
+        for (int j = 0; j < WT; ++j)
+#pragma unroll
+            for (int i = 0; i < WT; ++i) {
+                const int mt = mt0 + j, nt = nt0 + i, m = mt * 16 + lrow;
+                const bool live = mt < a.MT && m < a.M && nt < a.n_tiles;
+                const f32x4 v = acc[j][i] * s_rm[m - bm * BT * 16];
+                const int col0 = nt * 16 + lgrp * 4;
+                float xv[4] = {0.f, 0.f, 0.f, 0.f}, gv4[4] = {0.f, 0.f, 0.f, 0.f};
+                if (live) {
+                    float4* xp = (float4*)(a.rx + (size_t)m * a.ldx + col0);
+                    const float4 xo = *xp;
+                    xv[0] = xo.x + v[0]; xv[1] = xo.y + v[1]; xv[2] = xo.z + v[2]; xv[3] = xo.w + v[3];
+                    *xp = float4{xv[0], xv[1], xv[2], xv[3]};
+                    const T* g = (const T*)a.rgain + col0;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) gv4[e] = to_f32(g[e]);
+                }
+                float ss = xv[0] * xv[0] + xv[1] * xv[1] + xv[2] * xv[2] + xv[3] * xv[3];
+                ss += __shfl_xor(ss, 16);
+                ss += __shfl_xor(ss, 32);
+                float ov[8];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) ov[e] = xv[e] * gv4[e];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) ov[4 + e] = __shfl_xor(ov[e], 16);   // next 4 columns (even lane groups)
+                const bool writer = EPL == 8 ? (lgrp % 2) == 0 : true;
+                if (live && writer)
+                    put_operand_run<T>((T*)a.rn_hi, (T*)a.rn_lo, xfrag_elem<T>(m, col0, a.rn_MT), ov);
+                if (live && lgrp == 0) a.rsq[(size_t)nt * a.rsq_stride + m] = ss;
+            }
+        return;
+    }
     if (a.sw_hi) {
         // SwiGLU: the lane's up values sit 32 lanes away (column + 8); lane
         // groups 0 and 1 form h for FFN columns 8 nt + 4 lgrp + e and one
@@ -1919,39 +1957,6 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
         }
 }
 
-// thread: one row, one 16-column tile
-template <typename T>
-__global__ __launch_bounds__(256) void k_resid_rows(ResidRowsArgs a) {
-    constexpr int EPL = Elt<T>::EPL;
-    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-    const int m = idx / a.n_tiles, tile = idx % a.n_tiles;
-    if (m >= a.M) return;
-    float4* xp = (float4*)(a.x + (size_t)m * a.ldx + tile * 16);
-    const float4* yp = (const float4*)(a.y + (size_t)m * a.ldy + tile * 16);
-    const T* g = (const T*)a.gnext + tile * 16;
-    float xv[16];
-    float ss = 0.f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const float4 xo = xp[i], yo = yp[i];
-        xv[4 * i] = xo.x + yo.x;
-        xv[4 * i + 1] = xo.y + yo.y;
-        xv[4 * i + 2] = xo.z + yo.z;
-        xv[4 * i + 3] = xo.w + yo.w;
-    }
-#pragma unroll
-    for (int n = 0; n < 16; ++n) ss += xv[n] * xv[n];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) xp[i] = float4{xv[4 * i], xv[4 * i + 1], xv[4 * i + 2], xv[4 * i + 3]};
-#pragma unroll
-    for (int n0 = 0; n0 < 16; n0 += EPL) {
-        float ov[EPL];
-#pragma unroll
-        for (int i = 0; i < EPL; ++i) ov[i] = xv[n0 + i] * to_f32(g[n0 + i]);
-        put_operand_run<T>((T*)a.nx_hi, (T*)a.nx_lo, xfrag_elem<T>(m, tile * 16 + n0, a.n_MT), ov);
-    }
-    a.sq_out[(size_t)tile * a.sq_stride + m] = ss;
-}
 
 
 template <int WT>
@@ -1974,16 +1979,11 @@ static hipError_t launch_gemm_big_wt(int dtype, const BigGemmArgs& a, hipStream_
 // 64 x 64, whose extra work-groups hide more latency (measured faster for
 // the projections at up to 1056 rows)
 hipError_t launch_gemm_big(int dtype, const BigGemmArgs& a, hipStream_t st) {
+    if (!a.arg_val && !a.sw_hi && !a.rx && !a.out) return hipErrorInvalidValue;   // no destination
     const int bm8 = (a.MT + 7) / 8;
     const long big_blocks = (long)bm8 * ((a.n_tiles + 7) / 8);
     if (a.arg_val && big_blocks >= 4 * 256 && (bm8 * 8 - a.MT) * 8 <= a.MT) return launch_gemm_big_wt<4>(dtype, a, st);
     return launch_gemm_big_wt<2>(dtype, a, st);
-}
-hipError_t launch_resid_rows(int dtype, const ResidRowsArgs& a, hipStream_t st) {
-    const int n = a.M * a.n_tiles;
-    if (dtype == PBD_DTYPE_BF16) PBD_LAUNCH(k_resid_rows<bf16>, dim3((n + 255) / 256), dim3(256), 0, st, a);
-    else PBD_LAUNCH(k_resid_rows<float>, dim3((n + 255) / 256), dim3(256), 0, st, a);
-    return hipGetLastError();
 }
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t st) {

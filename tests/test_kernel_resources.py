@@ -29,7 +29,6 @@ HOT = [
     # prefill chunks
     r"_ZN3pbd10k_gemm_bigIDF16bLb[01]ELi[24]EEEvNS_11BigGemmArgsE",
     r"_ZN3pbd9k_kvwriteIDF16bLi128EEEvNS_11KVWriteArgsE",
-    r"_ZN3pbd12k_resid_rowsIDF16bEEvNS_13ResidRowsArgsE",
     r"_ZN3pbd13k_gather_lastIDF16bEEvNS_10GatherArgsE",
 ]
 
