@@ -746,12 +746,15 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     // chunks in registers (the next one loading), so CH is the largest of
     // 4, 2, 1 for which those, the output accumulators and the Q fragments
     // fit a budget of 304 registers per lane (beyond it the compiler spills).
+    // A single query tile takes one block per chunk: the work-group then fits
+    // in 256 registers per lane, two waves per SIMD, which hides more of the
+    // chain than larger chunks do (measured on the batch-1 step).
     // With four or more query tiles the Q fragments are read from LDS at each
     // use instead of being held in registers.
     constexpr bool QF_LDS = QT >= 4;
     constexpr int R_BLK = NDS * 4 + NDT * (int)(sizeof(vraw) / 4);    // one key block's K and V
     constexpr int R_FIX = QT * (NDT * 4 + (QF_LDS ? 0 : NDS * 4));
-    constexpr int CH = QF_LDS ? 1 : 8 * R_BLK + R_FIX <= 304 ? 4 : 4 * R_BLK + R_FIX <= 304 ? 2 : 1;
+    constexpr int CH = (QT == 1 || QF_LDS) ? 1 : 8 * R_BLK + R_FIX <= 304 ? 4 : 4 * R_BLK + R_FIX <= 304 ? 2 : 1;
     uint4 kn[CH][NDS];
     vraw vn[CH][NDT];
     auto load_chunk = [&](int it0) {
