@@ -297,8 +297,9 @@ int pbd_set_attn_keys_per_split(pbd_ctx* ctx, int32_t keys);
  * Attention layout tuning.  mode 1: each split-KV work item runs as one
  * work-group per 16 query rows (shorter per-wave instruction chains, more
  * work-groups, K/V read once per group); 0: one work-group takes all G*W query
- * rows of a KV head; -1 (default): 1 when batch * n_kv_heads * (splits at
- * max_seq) < 256, else 0.  Results are identical up to fp32 rounding.
+ * rows of a KV head; -1 (default): 1 when G*W needs at most three 16-row
+ * tiles or batch * n_kv_heads * (splits at max_seq) < 256, else 0.  Results
+ * are identical up to fp32 rounding.
  * Other modes: PBD_ERR_INVALID_ARG.
  */
 int pbd_set_attn_query_split(pbd_ctx* ctx, int32_t mode);

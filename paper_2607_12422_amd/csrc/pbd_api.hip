@@ -289,7 +289,10 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     }
     if (pre) kps = std::max(kps, PREFILL_KPS);
     const int s_launch = pre ? y.S_pre : std::min(y.S_max, cdiv(y.max_seq, kps) + 1);   // split-KV grid columns
-    const bool qsplit = pre || c->qsplit > 0 || (c->qsplit < 0 && B * y.NKV * s_launch < 256);
+    // one work-group per 16 query rows: always for prefill chunks; by default
+    // when the split grid leaves CUs idle or a work item has at most three
+    // query tiles (the one-tile work-group runs two waves per SIMD)
+    const bool qsplit = pre || c->qsplit > 0 || (c->qsplit < 0 && (QT <= 3 || B * y.NKV * s_launch < 256));
     const int QTw = qsplit ? 1 : QT;                // ... per attention work-group
     const float scale = y.r > 0 ? c->cfg.lora_alpha / (float)y.r : 0.f;
     const bool lora = q.adapter && y.r > 0;
