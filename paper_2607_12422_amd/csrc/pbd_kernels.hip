@@ -1287,14 +1287,38 @@ __global__ void k_combine(CombineArgs a) {
             add(wgt, ov[s]);
         }
     } else {
-        float mx = -1e30f;
-        for (int s = 0; s < a.s_launch; ++s) mx = fmaxf(mx, a.part_ml[(pr0 + s) * 2]);
-        for (int s = 0; s < a.s_launch; ++s) {
-            const float ms = a.part_ml[(pr0 + s) * 2];
-            if (!(ms > -INFINITY)) continue;
-            const float wgt = exp2f(ms - mx);
-            L += wgt * a.part_ml[(pr0 + s) * 2 + 1];
-            add(wgt, (const float4*)(a.part_o + (pr0 + s) * a.head_dim + d0));
+        // many splits: groups of eight loaded at once, merged online (the
+        // running maximum raised between groups, the sums rescaled)
+        float mx = -INFINITY;
+        for (int s0 = 0; s0 < a.s_launch; s0 += 8) {
+            float ms[8], ls[8];
+            float4 ov[8][EPL / 4];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const int sc = min(s0 + c, a.s_launch - 1);     // valid index; masked below
+                ms[c] = s0 + c < a.s_launch ? a.part_ml[(pr0 + sc) * 2] : -INFINITY;
+                ls[c] = a.part_ml[(pr0 + sc) * 2 + 1];
+#pragma unroll
+                for (int q = 0; q < EPL / 4; ++q) ov[c][q] = ((const float4*)(a.part_o + (pr0 + sc) * a.head_dim + d0))[q];
+            }
+            float mg = mx;
+#pragma unroll
+            for (int c = 0; c < 8; ++c) mg = fmaxf(mg, ms[c]);
+            if (!(mg > -INFINITY)) continue;
+            if (mx > -INFINITY && mg > mx) {
+                const float f = exp2f(mx - mg);
+                L *= f;
+#pragma unroll
+                for (int i = 0; i < EPL; ++i) o[i] *= f;
+            }
+            mx = mg;
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                if (!(ms[c] > -INFINITY)) continue;
+                const float wgt = exp2f(ms[c] - mx);
+                L += wgt * ls[c];
+                add(wgt, ov[c]);
+            }
         }
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
