@@ -289,7 +289,8 @@ int pbd_sync_status(pbd_ctx* ctx, pbd_stream_t stream, int32_t* status);
  * Attention split tuning: prefix keys per split-KV work item of the step
  * passes (a positive multiple of 16), or 0 (default) for automatic: 256,
  * doubled while batch * n_kv_heads * ceil(max_seq / keys) exceeds 2560 work
- * items.  Prefill chunks use at least 1024.  Other values: PBD_ERR_INVALID_ARG.
+ * items or ceil(max_seq / keys) exceeds 16 splits.  Prefill chunks use at
+ * least 1024.  Other values: PBD_ERR_INVALID_ARG.
  */
 int pbd_set_attn_keys_per_split(pbd_ctx* ctx, int32_t keys);
 

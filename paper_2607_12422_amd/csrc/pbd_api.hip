@@ -22,8 +22,9 @@ thread_local std::string g_init_error;
 constexpr int MAX_DIM = 16384;   // bound on hidden, ffn and n_q_heads*head_dim
 constexpr int LMHEAD_GRID = 512;  // work-groups of the persistent LM head (two per CU)
 constexpr int PREFILL_KPS = 1024; // keys per attention split in prefill chunks (many query groups)
-constexpr int ATTN_KPS = 256;     // keys per attention split of a step pass, unless the grid is too large
-constexpr int ATTN_GRID_CAP = 2560; // ... then doubled while batch x KV heads x splits exceeds this (10 per CU)
+constexpr int ATTN_KPS = 256;     // keys per attention split of a step pass, doubled while the grid is too
+constexpr int ATTN_GRID_CAP = 2560; // large (batch x KV heads x splits above this, 10 per CU) or there are
+constexpr int ATTN_SPLIT_CAP = 16;  // more splits than this (their partials cost the merge a load each)
 constexpr int BIG_MIN_MT = 8;    // passes of >= 128 rows (prefill chunks, batches of 8+) use the large-M projection
 constexpr size_t MAX_LDS = 160 * 1024;   // LDS one gfx950 work-group may allocate
 
@@ -285,7 +286,9 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     int kps = c->kps;
     if (kps == 0) {       // automatic: long prefixes at large batch take fewer, longer splits
         kps = ATTN_KPS;
-        while (kps < y.max_seq && (size_t)B * y.NKV * cdiv(y.max_seq, kps) > (size_t)ATTN_GRID_CAP) kps *= 2;
+        while (kps < y.max_seq && ((size_t)B * y.NKV * cdiv(y.max_seq, kps) > (size_t)ATTN_GRID_CAP ||
+                                   cdiv(y.max_seq, kps) > ATTN_SPLIT_CAP))
+            kps *= 2;
     }
     if (pre) kps = std::max(kps, PREFILL_KPS);
     const int s_launch = pre ? y.S_pre : std::min(y.S_max, cdiv(y.max_seq, kps) + 1);   // split-KV grid columns
