@@ -288,7 +288,7 @@ int pbd_sync_status(pbd_ctx* ctx, pbd_stream_t stream, int32_t* status);
 /*
  * Attention split tuning: prefix keys per split-KV work item of the step
  * passes (a positive multiple of 16), or 0 (default) for automatic: 256,
- * doubled while batch * n_kv_heads * ceil(max_seq / keys) exceeds 2560 work
+ * doubled while batch * n_kv_heads * ceil(max_seq / keys) exceeds 1280 work
  * items or ceil(max_seq / keys) exceeds 16 splits.  Prefill chunks use at
  * least 1024.  Other values: PBD_ERR_INVALID_ARG.
  */

@@ -23,7 +23,7 @@ constexpr int MAX_DIM = 16384;   // bound on hidden, ffn and n_q_heads*head_dim
 constexpr int LMHEAD_GRID = 512;  // work-groups of the persistent LM head (two per CU)
 constexpr int PREFILL_KPS = 1024; // keys per attention split in prefill chunks (many query groups)
 constexpr int ATTN_KPS = 256;     // keys per attention split of a step pass, doubled while the grid is too
-constexpr int ATTN_GRID_CAP = 2560; // large (batch x KV heads x splits above this, 10 per CU) or there are
+constexpr int ATTN_GRID_CAP = 1280; // large (batch x KV heads x splits above this, 5 per CU) or there are
 constexpr int ATTN_SPLIT_CAP = 16;  // more splits than this (their partials cost the merge a load each)
 constexpr int BIG_MIN_MT = 8;    // passes of >= 128 rows (prefill chunks, batches of 8+) use the large-M projection
 constexpr size_t MAX_LDS = 160 * 1024;   // LDS one gfx950 work-group may allocate
