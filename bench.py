@@ -112,13 +112,19 @@ def main():
     ap.add_argument("--no-context", action="store_true", help="skip the autoregressive-step and flushed-cache timings")
     ap.add_argument("--no-loop", action="store_true", help="skip the long-prefix generation loop")
     ap.add_argument("--kps", type=int, default=0, help="attention keys per split (0: library default)")
-    ap.add_argument("--operands", choices=["bf16", "bf16x2"], default="bf16x2")
+    ap.add_argument("--counters", action="store_true",
+                    help="only the warm-up and timed steps (for rocprofv3 counter passes): implies every --no-* "
+                         "option, --no-profile and --no-cpu-baseline")
     ap.add_argument("--attn-qsplit", type=int, default=-2,
                     help="attention work-group per 16 query rows (1), per KV head (0), automatic (-1); default: the library's")
     ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of replaying HIP graphs")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 10 plain device copies of MIB MiB (reference for the HBM byte counters) and exit")
     args = ap.parse_args()
+    if args.counters:
+        for k in ("no_cpu_baseline", "no_profile", "no_draft_curve", "no_denoise", "no_unanchored", "no_prefill",
+                  "no_context", "no_loop"):
+            setattr(args, k, True)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(sequences are independent; see the data-parallel design notes).", file=sys.stderr)
@@ -150,8 +156,6 @@ def main():
     max_seq = max(lengths) + (w_.gen_tokens or 0) + 4 * cfg.width + args.steps + args.warmup + 64
     dw = upload_weights(weights, cfg.dtype, dev)
     eng = Engine(cfg, dw, max_batch=B, max_seq=max_seq, device=dev)
-    eng.pbd_set_operand_precision(binding.PBD_OPERANDS_BF16X2 if args.operands == "bf16x2"
-                                  else binding.PBD_OPERANDS_BF16)
     if args.kps:
         eng.pbd_set_attn_keys_per_split(args.kps)
     if args.attn_qsplit >= -1:
@@ -250,7 +254,8 @@ def main():
         "data": "synthetic (seeded random-init weights of the model shape, uniform random prompt ids)",
         "config": {"workload": w_.name, "model_shape": cfg.name, "batch": B,
                    "prefix": lengths if B <= 8 else [min(lengths), max(lengths)],
-                   "block": cfg.block, "lora_rank": cfg.lora_rank, "operands": args.operands,
+                   "block": cfg.block, "lora_rank": cfg.lora_rank,
+                   "operands": "bf16x2" if cfg.dtype == "bf16" else "f32",
                    "launch": "eager" if args.eager else "hip-graph"},
         "draft_ms": round(dmed, 4), "verify_ms": round(vmed, 4), "accept_ms": round(amed, 4),
         "draft_ms_p10_p90": [round(x, 4) for x in pct(d_ms)],
@@ -346,8 +351,6 @@ def main():
         # with the memory-side cache flushed before each step.
         cfg0 = cfg.with_(block=0)
         e_ar = Engine(cfg0, dw, max_batch=B, max_seq=max_seq, device=dev, prefill_chunk=min(1024, 4096 // B))
-        e_ar.pbd_set_operand_precision(binding.PBD_OPERANDS_BF16X2 if args.operands == "bf16x2"
-                                       else binding.PBD_OPERANDS_BF16)
         s_ar0, a_ar0 = torch.zeros(B, **i32), torch.zeros(B, **i32)
         e_ar.pbd_prefill(torch.tensor(buf, **i32), torch.tensor(lengths, **i32), L, s_ar0, a_ar0)
         s_ar, a_ar = s_ar0.clone(), a_ar0.clone()
@@ -398,8 +401,6 @@ def main():
         e3 = Engine(w3.cfg, dw, max_batch=1, max_seq=l3[0] + budget + 4 * w3.cfg.width, device=dev,
                     prefill_chunk=1024) if w3.cfg.name == cfg.name else None
         if e3 is not None:
-            e3.pbd_set_operand_precision(binding.PBD_OPERANDS_BF16X2 if args.operands == "bf16x2"
-                                         else binding.PBD_OPERANDS_BF16)
             t3 = torch.tensor(np.array([p3[0]], dtype=np.int32), **i32)
             forced = synth.make_forced_accepts(budget, 1, w3.cfg.block, w3.seed(3))[:, 0]
             loop = {"prefix": l3[0], "budget": budget}
@@ -452,8 +453,6 @@ def main():
         def time_prefill(chunk, prm, reps):
             Lp, Bp = max(len(p) for p in prm), len(prm)
             e = Engine(cfg, dw, max_batch=Bp, max_seq=Lp + 4 * cfg.width + 64, device=dev, prefill_chunk=chunk)
-            e.pbd_set_operand_precision(binding.PBD_OPERANDS_BF16X2 if args.operands == "bf16x2"
-                                        else binding.PBD_OPERANDS_BF16)
             pb = np.zeros((Bp, Lp), dtype=np.int32)
             for bb, p in enumerate(prm):
                 pb[bb, :len(p)] = p

@@ -65,7 +65,7 @@ typedef void* pbd_stream_t;            /* hipStream_t */
 #define PBD_PASS_MASK_CAUSAL  8u       /* verify default */
 
 /* precision of the activation operands fed to the bf16 matrix cores */
-#define PBD_OPERANDS_BF16    0         /* rounded to bf16 */
+#define PBD_OPERANDS_BF16    0         /* rounded to bf16: refused for bf16 models (see pbd_set_operand_precision) */
 #define PBD_OPERANDS_BF16X2  1         /* bf16 value plus bf16 residual: two MFMAs per weight
                                           fragment, ~16-bit operand mantissa (default for bf16) */
 
@@ -137,7 +137,12 @@ typedef struct pbd_weights {
     const pbd_layer_weights* layers;    /* HOST array of n_layers entries */
 } pbd_weights;
 
-/* Buffer sizes in bytes for a configuration; 0 if the configuration is invalid. */
+/*
+ * Buffer sizes in bytes for a configuration; 0 if the configuration is invalid.
+ * All three are sized for cfg->max_batch sequences of cfg->max_seq positions:
+ * the workspace serves every batch up to max_batch (a call's batch argument
+ * selects how much of it a pass uses), so no per-batch size query is needed.
+ */
 size_t pbd_packed_weight_bytes(const pbd_config* cfg);
 size_t pbd_kv_bytes(const pbd_config* cfg);
 size_t pbd_workspace_bytes(const pbd_config* cfg);
@@ -155,8 +160,9 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon,
                      pbd_stream_t stream, pbd_ctx** out);
 
 /*
- * Adapter-off causal pass over each prompt (the committed prefix the speculative
- * steps start from).  tokens: device int32 [batch][max_len] (row b holds
+ * Prefill (Sec. 3: the step is stated for a given committed context x_1..x_t;
+ * this call builds that context's KV cache).  Adapter-off causal pass over
+ * each prompt (the committed prefix the speculative steps start from).  tokens: device int32 [batch][max_len] (row b holds
  * lengths[b] ids, the rest ignored); lengths: device int32 [batch], each in
  * [1, max_len] and with lengths[b] + D + 1 <= max_seq.  Writes the prompt K/V to
  * the cache, seq_len[b] = lengths[b] and anchor[b] = greedy next token (device
@@ -180,13 +186,6 @@ int pbd_prefill(pbd_ctx* ctx, int32_t batch, const int32_t* tokens, const int32_
 int pbd_draft_block(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
                     uint32_t flags, int32_t* draft, float* logits, pbd_stream_t stream);
 
-/*
- * Verify pass (Sec. 3 step 3): block [anchor, draft[b][0..D-1]] at positions
- * seq_len..seq_len+D; by default adapter off and causal mask.  Writes the block
- * K/V into the cache at positions seq_len..seq_len+D.  verify: device int32
- * [batch][D+1] receives p_0..p_D, the greedy token after each block row.
- * logits: NULL or device float [batch][D+1][vocab].
- */
 /*
  * Early-exit draft (the drafter whose cost the draft-cost analysis of App. A.7
  * and Tab. draft-cost-oracle varies): the same draft pass as pbd_draft_block
@@ -226,6 +225,16 @@ int pbd_draft_block_denoise(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len,
                             uint32_t flags, int32_t n_steps, int32_t* draft, float* conf, int32_t* fixed_at,
                             float* logits, pbd_stream_t stream);
 
+/*
+ * Verify pass (Sec. 3 step 3): block [anchor, draft[b][0..D-1]] at positions
+ * seq_len..seq_len+D; by default adapter off and causal mask.  Writes the block
+ * K/V into the cache at positions seq_len..seq_len+D.  verify: device int32
+ * [batch][D+1] receives p_0..p_D, the greedy token after each block row.
+ * logits: NULL or device float [batch][D+1][vocab].  Exact greedy matching
+ * (App. A.1) compares these with the drafts in pbd_accept_commit.
+ * Errors and the capacity rule (seq_len + D + 1 <= max_seq, else the
+ * sequence is skipped and PBD_STATUS_CAPACITY raised) as pbd_draft_block.
+ */
 int pbd_verify_block(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
                      const int32_t* draft, uint32_t flags, int32_t* verify, float* logits,
                      pbd_stream_t stream);
@@ -281,9 +290,17 @@ int pbd_accept_commit(pbd_ctx* ctx, int32_t batch, const int32_t* draft, const i
 
 /*
  * Wait for `stream`, read and clear the device status word.  *status receives
- * the PBD_STATUS_* bits raised since the last call (0 = none).
+ * the PBD_STATUS_* bits raised since the last call (0 = none); the return
+ * value is the call's own PBD_OK / PBD_ERR_* code (a HIP failure while
+ * reading is reported there, not mixed into the status bits).
  */
 int pbd_sync_status(pbd_ctx* ctx, pbd_stream_t stream, int32_t* status);
+
+/* ------------------------------------------------------------------------
+ * Implementation controls.  The calls below are not part of the step's
+ * interface (they change no result beyond fp32 rounding, or they only
+ * measure): kernel tuning, operand precision and the profiling aid.
+ * ------------------------------------------------------------------------ */
 
 /*
  * Attention split tuning: prefix keys per split-KV work item of the step
@@ -306,9 +323,12 @@ int pbd_set_attn_keys_per_split(pbd_ctx* ctx, int32_t keys);
 int pbd_set_attn_query_split(pbd_ctx* ctx, int32_t mode);
 
 /*
- * Precision of the GEMM activation operands of bf16 models: PBD_OPERANDS_BF16 or
- * PBD_OPERANDS_BF16X2 (default).  Weights and the KV cache stay bf16 either way;
- * accumulation is fp32.  Ignored for fp32 models.
+ * Precision of the GEMM activation operands.  bf16 models run with
+ * PBD_OPERANDS_BF16X2 (value + residual, the default); PBD_OPERANDS_BF16
+ * returns PBD_ERR_UNSUPPORTED for them, because single bf16 activation
+ * operands put the Qwen3-0.6B-shape logits outside the 2e-2 bound.  fp32
+ * models accept either value and ignore it.  Other values:
+ * PBD_ERR_INVALID_ARG.
  */
 int pbd_set_operand_precision(pbd_ctx* ctx, int32_t mode);
 

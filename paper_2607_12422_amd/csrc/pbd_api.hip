@@ -205,7 +205,7 @@ struct pbd_ctx {
     int kps;
     int qsplit;          // attention: one work-group per 16 query rows (1), per KV head (0), or
                          // automatic (-1: split when the split-KV grid leaves most CUs idle)
-    bool split;          // GEMM activation operands as bf16 hi + bf16 residual
+    bool split;          // GEMM activation operands as bf16 hi + bf16 residual (always, for bf16 models)
     Profiler prof;
     std::string err;
 };
@@ -331,7 +331,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     // residual GEMMs (n = hidden) have few output tiles: split K so that the
     // whole chip streams their weights (one m-group only)
     auto split_k = [&](FGemmArgs& g) {
-        if (g.n_tiles <= 128 && MT <= fgemm_mgroup(EPI_RESID, MT)) {
+        if (g.n_tiles <= 128 && MT <= fgemm_mgroup(EPI_RESID, MT, g.lora ? g.rt : 0)) {
             g.ksplit = y.ksplit;
             g.part = (float*)(ws + y.w_kpart);
             g.cnt = (unsigned*)(ws + y.w_kcnt);
@@ -349,9 +349,19 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         b.out = g.out; b.ldo = g.ldo;                // STORE (q/k/v); the other projections use epilogues
         return b;
     };
-    // with the adapter: the shrink of the projection's nsrc LoRA A matrices,
-    // stacked in the packed layout as one [nsrc RT][kb] tile matrix, then the
-    // projection with the expand
+    // with the adapter, the large-M projection is two launches (timed
+    // separately): the shrink of the projection's nsrc LoRA A matrices,
+    // stacked in the packed layout as one [nsrc RT][kb] tile matrix, into u;
+    // then the projection with the expand
+    auto launch_shrink = [&](const FGemmArgs& g, int nsrc) -> hipError_t {
+        const size_t src_frags = (size_t)y.RT * g.kb * 64;              // uint4 per source matrix
+        for (int i = 1; i < nsrc; ++i)
+            if (g.la[i] != g.la[0] + i * src_frags) return hipErrorInvalidValue;
+        BigGemmArgs sh{};
+        sh.w = g.la[0]; sh.n_tiles = nsrc * y.RT; sh.kb = g.kb; sh.xhi = g.xhi; sh.xlo = g.xlo;
+        sh.M = g.M; sh.MT = g.MT; sh.n_sq = 0; sh.out = ubig; sh.ldo = nsrc * y.RT * 16;
+        return launch_gemm_big(dt, sh, st);
+    };
     auto launch_big = [&](const FGemmArgs& g, int nsrc, int epi = EPI_STORE) -> hipError_t {
         BigGemmArgs b = big_args(g);
         if (epi == EPI_SWIGLU) { b.sw_hi = g.nx_hi; b.sw_lo = g.nx_lo; b.sw_MT = g.n_MT; }
@@ -360,20 +370,17 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
             b.rn_MT = g.n_MT; b.rsq = g.sq_out; b.rsq_stride = g.sq_stride;
         }
         if (lora) {
-            const size_t src_frags = (size_t)y.RT * g.kb * 64;          // uint4 per source matrix
-            for (int i = 1; i < nsrc; ++i)
-                if (g.la[i] != g.la[0] + i * src_frags) return hipErrorInvalidValue;
-            BigGemmArgs sh{};
-            sh.w = g.la[0]; sh.n_tiles = nsrc * y.RT; sh.kb = g.kb; sh.xhi = g.xhi; sh.xlo = g.xlo;
-            sh.M = g.M; sh.MT = g.MT; sh.n_sq = 0; sh.out = ubig; sh.ldo = nsrc * y.RT * 16;
-            const hipError_t e = launch_gemm_big(dt, sh, st);
-            if (e != hipSuccess) return e;
-            b.u = ubig; b.ldu = sh.ldo; b.lrt = y.RT; b.lora_mode = g.lora_mode;
+            b.u = ubig; b.ldu = nsrc * y.RT * 16; b.lrt = y.RT; b.lora_mode = g.lora_mode;
             b.tile_split0 = g.tile_split0; b.tile_split1 = g.tile_split1;
             b.W = g.W; b.adapter_from = g.adapter_from; b.scale = g.scale; b.lb = g.lb;
         }
         return launch_gemm_big(dt, b, st);
     };
+#define PBD_BIG(G, NSRC, EPI, WHAT)                                                                      \
+    do {                                                                                                \
+        if (lora) PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_shrink(G, NSRC), WHAT " (LoRA shrink)");     \
+        PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(G, NSRC, EPI), WHAT);                              \
+    } while (0)
     const int L = q.n_layers > 0 ? q.n_layers : y.L;
     for (int l = 0; l < L; ++l) {
         const Layout::LayerOff& lo_ = y.lay[l];
@@ -385,7 +392,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         for (int i = 0; i < 3; ++i) g.la[i] = (const uint4*)(pk + lo_.la[i]);
         g.lb = pk + lo_.lb_qkv;
         g.out = (float*)(ws + y.w_qkv); g.ldo = y.nqkv;
-        if (big) PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 3), "qkv gemm");
+        if (big) PBD_BIG(g, 3, EPI_STORE, "qkv gemm");
         else PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_STORE, st), "qkv gemm");
 
         AttnArgs at{};
@@ -445,7 +452,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.sq_out = sq_m;
         split_k(g);
         if (big) {
-            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 1, EPI_RESID), "o gemm");
+            PBD_BIG(g, 1, EPI_RESID, "o gemm");
         } else {
             PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "o gemm");
         }
@@ -458,7 +465,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.nx_hi = hi(y.w_xd); g.nx_lo = lo(y.w_xd); g.n_MT = MT;
         if (big) {
             // SwiGLU in the GEMM epilogue: the down projection's operand directly
-            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 2, EPI_SWIGLU), "gate/up gemm");
+            PBD_BIG(g, 2, EPI_SWIGLU, "gate/up gemm");
         } else {
             PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_SWIGLU, st), "gate/up gemm");
         }
@@ -471,7 +478,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.nx_hi = hi(y.w_xa); g.nx_lo = lo(y.w_xa); g.n_MT = MT; g.sq_out = sq_a;
         split_k(g);
         if (big) {
-            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(g, 1, EPI_RESID), "down gemm");
+            PBD_BIG(g, 1, EPI_RESID, "down gemm");
         } else {
             PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_fgemm(dt, g, EPI_RESID, st), "down gemm");
         }
@@ -528,6 +535,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_argmax(am, st), "argmax");
     return PBD_OK;
 }
+#undef PBD_BIG
 
 int check_ctx(const pbd_ctx* c) {
     if (!c) { g_init_error = "context is NULL"; return PBD_ERR_INVALID_ARG; }
@@ -903,7 +911,11 @@ int pbd_set_operand_precision(pbd_ctx* c, int32_t mode) {
     if (rc) return rc;
     if (mode != PBD_OPERANDS_BF16 && mode != PBD_OPERANDS_BF16X2)
         return fail(c, PBD_ERR_INVALID_ARG, "unknown operand precision mode");
-    c->split = mode == PBD_OPERANDS_BF16X2;
+    // single bf16 operands put the Qwen3-0.6B-shape draft logits up to 0.0226
+    // from the float64 reference, outside the 2e-2 bound the passes are held to
+    if (c->cfg.dtype == PBD_DTYPE_BF16 && mode == PBD_OPERANDS_BF16)
+        return fail(c, PBD_ERR_UNSUPPORTED, "single bf16 activation operands miss the 2e-2 logit bound; "
+                                            "bf16 models run with value + residual operands only");
     return PBD_OK;
 }
 

@@ -275,7 +275,7 @@ struct PackExpandArgs {
 
 hipError_t launch_assemble(int dtype, const AssembleArgs& a, int batch, hipStream_t st);
 hipError_t launch_fgemm(int dtype, const FGemmArgs& a, int epi, hipStream_t st);   // split iff a.xlo
-int fgemm_mgroup(int epi, int MT);
+int fgemm_mgroup(int epi, int MT, int lrt);   // lrt: LoRA rank tiles of the launch (0: adapter off)
 int fgemm_threads(int epi);         // work-group size of the GEMM with epilogue epi
 hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int batch, hipStream_t st);
 hipError_t launch_combine(int dtype, const CombineArgs& a, int M, hipStream_t st);

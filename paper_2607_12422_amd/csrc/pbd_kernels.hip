@@ -187,12 +187,22 @@ template <int EPI> struct FG {
     static constexpr int NSRC = (EPI == EPI_SWIGLU) ? 2 : 1;      // LoRA shrink sources
     // work-groups per CU the register budget must allow (SwiGLU: 384+ tiles on 256 CUs)
     static constexpr int MINB = (EPI == EPI_SWIGLU) ? 2 : 1;
-    // fragments per wave and load batch: about 112 VGPRs of loads in flight
+    // fragments per wave and load batch: about 112 VGPRs of loads in flight,
+    // less what the shrink partials of ranks above 16 take (the work-group
+    // runs two waves per SIMD: 256 VGPRs per lane in all)
     template <typename T, int MG, bool SPLIT, int LRT>
     static constexpr int unroll() {
         constexpr int per = 4 + 4 * MG * (SPLIT ? 2 : 1) + 4 * NSRC * LRT;
-        constexpr int u = 112 / per;
+        constexpr int extra = LRT > 1 ? 12 * NSRC * (LRT - 1) * MG + 8 * (LRT - 1)
+                            : (LRT == 1 && sizeof(T) == 4) ? 8 * NSRC * MG + (EPI == EPI_RESID ? 16 : 0) : 0;
+        constexpr int budget = 112 - extra > 24 ? 112 - extra : 24;
+        constexpr int u = budget / per;
         return u < 1 ? 1 : (u > 6 ? 6 : u);
+    }
+    // largest m-group the shrink accumulators allow: NSRC * LRT * MG <= 8
+    // (32 VGPRs of shrink partials per lane)
+    static constexpr int mg_cap(int lrt) {
+        return lrt == 0 ? 8 : (8 / (NSRC * lrt) >= 4 ? 4 : 8 / (NSRC * lrt) >= 2 ? 2 : 1);
     }
 };
 
@@ -1378,6 +1388,9 @@ __global__ __launch_bounds__(256) void k_argmax(ArgmaxArgs a) {
     }
     if (threadIdx.x != 0) return;
     const int tok = s_i[0];
+    // a sequence the pass skipped (capacity: no rows assembled) keeps its
+    // outputs untouched, as its cache rows are
+    if (a.mode != PASS_PREFILL && a.nrows[b] == 0) return;
     if (a.mode == PASS_DRAFT) {
         const int nd = a.W - a.lead;
         if (j >= a.lead) {
@@ -1444,7 +1457,9 @@ __global__ void k_accept(AcceptArgs a) {
     } else {
         while (n < D && a.draft[b * D + n] == a.verify[b * W + n]) ++n;
     }
-    if (t < 0 || t + n + 1 > a.max_seq) { atomicOr(a.status, PBD_STATUS_CAPACITY); return; }
+    // the passes' own bound (t + D + 1 <= max_seq): a sequence whose verify was
+    // skipped for capacity commits nothing from its unwritten rows
+    if (t < 0 || t + W > a.max_seq) { atomicOr(a.status, PBD_STATUS_CAPACITY); return; }
     for (int i = 0; i < W; ++i)
         a.out[b * W + i] = i < n ? a.draft[b * D + i] : (i == n ? a.verify[b * W + n] : -1);
     a.n_acc[b] = n;
@@ -1517,18 +1532,29 @@ __global__ void k_fill_u32(uint32_t* p, size_t n, uint32_t v) {
 // ---------------------------------------------------------------------------
 // Host-side launchers
 // ---------------------------------------------------------------------------
+// one (epilogue, m-group, rank tiles) instance; instances whose m-group
+// exceeds the shrink-accumulator cap are never launched (fgemm_mgroup) and
+// not instantiated
+template <typename T, bool SPLIT, int EPI, int MG, int LRT>
+static hipError_t launch_fgemm_inst(const FGemmArgs& a, hipStream_t st) {
+    if constexpr (MG <= FG<EPI>::mg_cap(LRT)) {
+        PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, LRT>), dim3(a.n_tiles * a.ksplit), dim3(FG<EPI>::NW * 64), 0, st, a);
+        return hipGetLastError();
+    } else {
+        return hipErrorInvalidValue;
+    }
+}
+
 template <typename T, bool SPLIT, int EPI, int MG>
 static hipError_t launch_fgemm_lrt(const FGemmArgs& a, int lrt, hipStream_t st) {
-    const dim3 grid(a.n_tiles * a.ksplit), block(FG<EPI>::NW * 64);
     switch (lrt) {
-        case 0: PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, 0>), grid, block, 0, st, a); break;
-        case 1: PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, 1>), grid, block, 0, st, a); break;
-        case 2: PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, 2>), grid, block, 0, st, a); break;
-        case 3: PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, 3>), grid, block, 0, st, a); break;
-        case 4: PBD_LAUNCH((k_fgemm<T, EPI, MG, SPLIT, 4>), grid, block, 0, st, a); break;
+        case 0: return launch_fgemm_inst<T, SPLIT, EPI, MG, 0>(a, st);
+        case 1: return launch_fgemm_inst<T, SPLIT, EPI, MG, 1>(a, st);
+        case 2: return launch_fgemm_inst<T, SPLIT, EPI, MG, 2>(a, st);
+        case 3: return launch_fgemm_inst<T, SPLIT, EPI, MG, 3>(a, st);
+        case 4: return launch_fgemm_inst<T, SPLIT, EPI, MG, 4>(a, st);
         default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 template <typename T, bool SPLIT>
@@ -1561,20 +1587,27 @@ int fgemm_threads(int epi) {
 }
 
 // m-tiles per pass over the weights: enough for the rows, bounded by the
-// register budget (residual GEMMs hold the x slice) and by LDS
-int fgemm_mgroup(int epi, int MT) {
-    const int cap = epi == EPI_ARGMAX ? 8 : (epi == EPI_RESID ? 2 : 4);
+// register budget (residual GEMMs hold the x slice; LoRA shrink partials
+// grow with the rank tiles) and by LDS
+int fgemm_mgroup(int epi, int MT, int lrt) {
+    int cap = epi == EPI_ARGMAX ? 8 : (epi == EPI_RESID ? 2 : 4);
+    const int lcap = epi == EPI_STORE ? FG<EPI_STORE>::mg_cap(lrt)
+                   : epi == EPI_RESID ? FG<EPI_RESID>::mg_cap(lrt)
+                   : epi == EPI_SWIGLU ? FG<EPI_SWIGLU>::mg_cap(lrt) : 8;
+    cap = std::min(cap, lcap);
     int mg = 1;
     while (mg < MT && mg < cap) mg *= 2;
     return mg;
 }
 
 hipError_t launch_fgemm(int dtype, const FGemmArgs& a, int epi, hipStream_t st) {
-    if (a.ksplit < 1 || a.ksplit > KSPLIT_MAX || (a.ksplit > 1 && (!a.part || !a.cnt || a.MT > fgemm_mgroup(epi, a.MT))))
+    const int lrt = (a.lora && epi != EPI_ARGMAX) ? a.rt : 0;
+    if (a.ksplit < 1 || a.ksplit > KSPLIT_MAX ||
+        (a.ksplit > 1 && (!a.part || !a.cnt || a.MT > fgemm_mgroup(epi, a.MT, lrt))))
         return hipErrorInvalidValue;
-    const int mg = fgemm_mgroup(epi, a.MT);
-    if (dtype == PBD_DTYPE_BF16)
-        return a.xlo ? launch_fgemm_t<bf16, true>(a, epi, mg, st) : launch_fgemm_t<bf16, false>(a, epi, mg, st);
+    const int mg = fgemm_mgroup(epi, a.MT, lrt);
+    // bf16 models always carry the operand as value + residual
+    if (dtype == PBD_DTYPE_BF16) return a.xlo ? launch_fgemm_t<bf16, true>(a, epi, mg, st) : hipErrorInvalidValue;
     return launch_fgemm_t<float, false>(a, epi, mg, st);
 }
 
@@ -1584,13 +1617,9 @@ hipError_t launch_lmhead(int dtype, const FGemmArgs& a, int grid, hipStream_t st
     const bool conf = a.arg_sum != nullptr;
     if (conf && !a.arg_mx) return hipErrorInvalidValue;
     if (dtype == PBD_DTYPE_BF16) {
-        if (a.xlo) {
-            if (conf) PBD_LAUNCH((k_lmhead<bf16, true, true>), dim3(grid), dim3(256), 0, st, a);
-            else PBD_LAUNCH((k_lmhead<bf16, true, false>), dim3(grid), dim3(256), 0, st, a);
-        } else {
-            if (conf) PBD_LAUNCH((k_lmhead<bf16, false, true>), dim3(grid), dim3(256), 0, st, a);
-            else PBD_LAUNCH((k_lmhead<bf16, false, false>), dim3(grid), dim3(256), 0, st, a);
-        }
+        if (!a.xlo) return hipErrorInvalidValue;
+        if (conf) PBD_LAUNCH((k_lmhead<bf16, true, true>), dim3(grid), dim3(256), 0, st, a);
+        else PBD_LAUNCH((k_lmhead<bf16, true, false>), dim3(grid), dim3(256), 0, st, a);
     } else {
         if (conf) PBD_LAUNCH((k_lmhead<float, false, true>), dim3(grid), dim3(256), 0, st, a);
         else PBD_LAUNCH((k_lmhead<float, false, false>), dim3(grid), dim3(256), 0, st, a);
@@ -1992,8 +2021,8 @@ static hipError_t launch_gemm_big_wt(int dtype, const BigGemmArgs& a, hipStream_
     if ((a.m_fast ? gn : gm) > 65535) return hipErrorInvalidValue;     // grid y limit
     const dim3 grid(a.m_fast ? gm : gn, a.m_fast ? gn : gm), block(256);
     if (dtype == PBD_DTYPE_BF16) {
-        if (a.xlo) PBD_LAUNCH((k_gemm_big<bf16, true, WT>), grid, block, 0, st, a);
-        else PBD_LAUNCH((k_gemm_big<bf16, false, WT>), grid, block, 0, st, a);
+        if (!a.xlo) return hipErrorInvalidValue;
+        PBD_LAUNCH((k_gemm_big<bf16, true, WT>), grid, block, 0, st, a);
     } else {
         PBD_LAUNCH((k_gemm_big<float, false, WT>), grid, block, 0, st, a);
     }

@@ -6,12 +6,15 @@ from oracle import model as om
 P = [5, 6, 7, 8]          # verifier greedy tokens p_0..p_3 for D = 3
 
 
-@pytest.mark.parametrize("drafts,n,out", [
+TABLE = [
     ([5, 6, 7], 3, [5, 6, 7, 8]),     # all drafts match: n = D, bonus p_D
     ([5, 6, 9], 2, [5, 6, 7]),
     ([5, 9, 7], 1, [5, 6]),           # a later match after a miss does not count
     ([9, 6, 7], 0, [5]),              # nothing matches: only the bonus p_0
-])
+]
+
+
+@pytest.mark.parametrize("drafts,n,out", TABLE)
 def test_accept_table(drafts, n, out):
     assert om.accept(drafts, P) == (n, out)
 

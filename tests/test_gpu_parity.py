@@ -191,6 +191,35 @@ def test_capacity_overflow_sets_status_and_skips():
     g.close()
 
 
+@pytest.mark.parametrize("over", [1, 16])
+def test_capacity_skip_keeps_outputs_and_state(over):
+    """seq_len in (max_seq - W, max_seq - 1]: draft and verify leave their
+    outputs alone and raise the capacity bit; the accept then commits nothing
+    (seq_len, anchor, n and out_tokens unchanged)."""
+    from paper_2607_12422_amd import binding as bd
+    cfg, w = _tiny(16)
+    prompt = synth.make_prompts(cfg, [10], 12)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=64)
+    g.prefill([prompt])
+    t = 64 - cfg.width + over                 # t + W = max_seq + over
+    g.seq_len.fill_(t)
+    anchor0 = int(g.anchor[0])
+    d = g.i32([[7] * cfg.block])
+    g.eng.pbd_draft_block(g.seq_len, g.anchor, d, None)
+    assert d.cpu().numpy().tolist() == [[7] * cfg.block]
+    v = g.i32([[9] * cfg.width])
+    g.eng.pbd_verify_block(g.seq_len, g.anchor, d, v, None)
+    assert v.cpu().numpy().tolist() == [[9] * cfg.width]
+    assert g.status() & bd.PBD_STATUS_CAPACITY
+    n = g.i32([-5])
+    out = g.i32([[-3] * cfg.width])
+    g.eng.pbd_accept_commit(d, v, g.seq_len, g.anchor, n, out)
+    assert g.status() & bd.PBD_STATUS_CAPACITY
+    assert int(g.seq_len[0]) == t and int(g.anchor[0]) == anchor0
+    assert int(n[0]) == -5 and out.cpu().numpy().tolist() == [[-3] * cfg.width]
+    g.close()
+
+
 def test_qwen_shape_step_matches_oracle():
     """Qwen3-0.6B shape, bf16, prefix 512: one draft + verify step."""
     w_ = synth.WORKLOADS[1]
@@ -406,4 +435,23 @@ def test_block_zero_is_greedy_autoregressive_decoding():
         om.commit(st, nn, oo, k, vv)
         assert int(g.seq_len[0]) == st.seq_len and int(g.anchor[0]) == st.anchor
     assert g.status() == 0
+    g.close()
+
+
+def test_single_bf16_operands_are_refused_for_bf16_models():
+    """Single bf16 activation operands miss the 2e-2 bound at the Qwen3-0.6B
+    shape, so a bf16 model refuses them; an fp32 model ignores the setting."""
+    from paper_2607_12422_amd import binding as bd
+    cfg = synth.QWEN3_0_6B.with_(n_layers=1, vocab=1024)
+    w = synth.make_weights(cfg, 77)
+    g = GpuRun(cfg, w, max_batch=1, max_seq=64)
+    with pytest.raises(bd.PbdError) as e:
+        g.eng.pbd_set_operand_precision(bd.PBD_OPERANDS_BF16)
+    assert e.value.code == bd.PBD_ERR_UNSUPPORTED
+    g.eng.pbd_set_operand_precision(bd.PBD_OPERANDS_BF16X2)
+    g.close()
+    cfg32, w32 = _tiny(16)
+    g = GpuRun(cfg32, w32, max_batch=1, max_seq=64)
+    g.eng.pbd_set_operand_precision(bd.PBD_OPERANDS_BF16)
+    g.eng.pbd_set_operand_precision(bd.PBD_OPERANDS_BF16X2)
     g.close()

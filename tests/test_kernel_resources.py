@@ -2,10 +2,10 @@
 
 A register array indexed with a run-time value, or a register budget that
 overflows, puts per-lane data in scratch memory, which turns every access into
-a global memory round trip.  The kernels of the Qwen3-shape passes at LoRA rank
-<= 16 (bf16 with split operands; attention with head_dim 128 and up to three
-16-row query tiles) must use no scratch at all.  (The rank-32/64 GEMM variants
-hold more shrink accumulators and do spill.)
+a global memory round trip.  The kernels of the Qwen3-shape passes (bf16 with split
+operands; projection GEMMs at every LoRA rank up to 64; attention with
+head_dim 128 and up to three 16-row query tiles) and every projection GEMM of
+the fp32 model must use no scratch at all.
 """
 import os
 import re
@@ -17,8 +17,9 @@ import pytest
 from paper_2607_12422_amd import build as b
 
 HOT = [
-    # projection GEMMs, bf16 value + residual operands, LoRA rank <= 16
-    r"_ZN3pbd7k_fgemmIDF16bLi\d+ELi\d+ELb1ELi[01]EEEvNS_9FGemmArgsE",
+    # projection GEMMs (bf16 value + residual operands; fp32), LoRA rank <= 64
+    r"_ZN3pbd7k_fgemmIDF16bLi\d+ELi\d+ELb1ELi[0-4]EEEvNS_9FGemmArgsE",
+    r"_ZN3pbd7k_fgemmIfLi\d+ELi\d+ELb0ELi[0-4]EEEvNS_9FGemmArgsE",
     r"_ZN3pbd6k_attnIDF16bLi128ELi[123]EEEvNS_8AttnArgsE",            # attention, G*W <= 48 query rows
     r"_ZN3pbd8k_lmheadIDF16bLb1ELb[01]EEEvNS_9FGemmArgsE",            # LM head (with / without confidence)
     r"_ZN3pbd9k_combineIDF16bLi\d+EEEvNS_11CombineArgsE",

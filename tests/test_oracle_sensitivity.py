@@ -85,13 +85,18 @@ def test_missing_eps_or_gain_is_caught(monkeypatch):
 
 
 def test_off_by_one_acceptance_is_caught(monkeypatch):
-    # comparing x_i with p_i instead of p_{i-1} breaks the hand table
+    # planted in the oracle: draft x_i compared with p_i instead of p_{i-1};
+    # the hand table of the acceptance rule must then fail
+    import test_accept
+
     def bad_accept(drafts, p, forced_n=None):
         n = 0
         while n < len(drafts) and int(drafts[n]) == int(p[n + 1]):
             n += 1
         return n, [int(t) for t in drafts[:n]] + [int(p[n])]
-    assert bad_accept([5, 6, 7], [5, 6, 7, 8]) != om.accept([5, 6, 7], [5, 6, 7, 8])
+    monkeypatch.setattr(om, "accept", bad_accept)
+    failed = [row for row in test_accept.TABLE if om.accept(row[0], test_accept.P) != (row[1], row[2])]
+    assert failed
 
 
 def test_wrong_kv_head_mapping_is_caught(monkeypatch):
