@@ -76,12 +76,15 @@ typedef void* pbd_stream_t;            /* hipStream_t */
 #define PBD_KCLASS_COMBINE  3          /* split merge + O-projection operand */
 #define PBD_KCLASS_NORM     4          /* unused: RMSNorm and the LoRA shrink are fused into the GEMMs */
 #define PBD_KCLASS_OTHER    5          /* block assembly, final argmax */
-#define PBD_KCLASS_COUNT    6
+#define PBD_KCLASS_FUSED    6          /* persistent batch-1 layer stack (all layers of a pass in one launch) */
+#define PBD_KCLASS_COUNT    7
 
 /* bits of the device status word */
 #define PBD_STATUS_CAPACITY  1         /* seq_len + W > max_seq, or prompt length out of range */
 #define PBD_STATUS_TOKEN     2         /* a token id outside [0, vocab) */
 #define PBD_STATUS_FORCED_N  4         /* forced accepted count outside [0, D] */
+#define PBD_STATUS_TIMEOUT   8         /* a bounded wait of the persistent batch-1 pass gave up:
+                                          that pass's outputs are invalid */
 
 /*
  * Model and capacity description.  The backbone is a Qwen3-style decoder
@@ -333,6 +336,29 @@ int pbd_set_attn_query_split(pbd_ctx* ctx, int32_t mode);
 int pbd_set_operand_precision(pbd_ctx* ctx, int32_t mode);
 
 /*
+ * Pass execution mode.  0: batch-1 draft and verify passes of the
+ * Qwen3-0.6B layer shape (bf16, hidden 1024, 16 query / 8 KV heads of 128,
+ * FFN 3072, LoRA rank <= 16, D + 1 <= 32 rows, max_seq <= 4960, on a
+ * 256-CU device) run their layer stack as one persistent kernel; other
+ * passes use one kernel per operator.  1 (default): one kernel per operator
+ * always.
+ * Both give the same results up to fp32 rounding.  Other values:
+ * PBD_ERR_INVALID_ARG.
+ */
+int pbd_set_pass_mode(pbd_ctx* ctx, int32_t mode);
+
+/*
+ * Bound of each wait inside the persistent pass, in polls (0: the default,
+ * about a quarter of a second).  A wait that runs out sets
+ * PBD_STATUS_TIMEOUT, releases every other wait and lets the kernel finish;
+ * the pass's outputs are then invalid.  polls = 1 also makes every
+ * work-group of the persistent pass first wait on a word that nothing ever
+ * sets, so that the bounded-wait path is always taken (for tests of it).
+ * Negative: PBD_ERR_INVALID_ARG.
+ */
+int pbd_set_wait_limit(pbd_ctx* ctx, int32_t polls);
+
+/*
  * Profiling aid: while enabled, every kernel of a pass is launched with a pair
  * of HIP events attached to its dispatch (hipExtLaunchKernel), which record the
  * kernel's own start and end on the call's stream.  Use it with direct calls,
@@ -343,6 +369,20 @@ int pbd_set_operand_precision(pbd_ctx* ctx, int32_t mode);
  */
 int pbd_profile_enable(pbd_ctx* ctx, int32_t on);
 int pbd_profile_read(pbd_ctx* ctx, int32_t kclass, double* total_ms, int64_t* launches);
+
+/*
+ * Profiling aid of the persistent batch-1 pass: copies the stage timestamps
+ * of the last such pass on ctx to the host (synchronises the device).  out:
+ * host uint64 array of max_entries; entry (((g * 32 + r) * 64 + l) * 8 + s)
+ * * 4 + k is, for rank r of XCD group g in layer l < 64 and stage s (R, Q,
+ * A, M, O, R2, GU, D), the device clock (100 MHz) when the stage's wait
+ * began (k = 0), when its inputs were ready (k = 1), when its compute waves
+ * finished (k = 2; GEMM stages) and when its output was published (k = 3;
+ * Q, A, GU).  l = n_layers holds the final norm's start and end (stage 0,
+ * k = 0 and 1).  Entries not recorded hold stale values.  *n_written
+ * receives min(max_entries, 524288).
+ */
+int pbd_profile_stage_times(pbd_ctx* ctx, uint64_t* out, int32_t max_entries, int32_t* n_written);
 
 /* Message of the last failed call on ctx (or of the last failed init if ctx is NULL). */
 const char* pbd_last_error(const pbd_ctx* ctx);

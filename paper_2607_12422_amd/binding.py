@@ -34,18 +34,19 @@ PBD_PASS_MASK_CAUSAL = 8
 PBD_OPERANDS_BF16 = 0
 PBD_OPERANDS_BF16X2 = 1
 
-KCLASSES = ("gemm", "lmhead", "attn", "combine", "norm", "other")
+KCLASSES = ("gemm", "lmhead", "attn", "combine", "norm", "other", "fused")
 
 PBD_STATUS_CAPACITY = 1
 PBD_STATUS_TOKEN = 2
 PBD_STATUS_FORCED_N = 4
+PBD_STATUS_TIMEOUT = 8
 
 EXPORTED = (
     "pbd_packed_weight_bytes", "pbd_kv_bytes", "pbd_workspace_bytes", "pbd_init_weights",
     "pbd_prefill", "pbd_draft_block", "pbd_draft_block_layers", "pbd_draft_block_denoise",
     "pbd_verify_block", "pbd_draft_block_unanchored", "pbd_verify_block_unanchored", "pbd_accept_commit",
     "pbd_sync_status", "pbd_set_attn_keys_per_split", "pbd_set_attn_query_split", "pbd_set_operand_precision",
-    "pbd_profile_enable", "pbd_profile_read", "pbd_last_error", "pbd_destroy",
+    "pbd_set_pass_mode", "pbd_set_wait_limit", "pbd_profile_enable", "pbd_profile_read", "pbd_profile_stage_times", "pbd_last_error", "pbd_destroy",
 )
 
 
@@ -104,9 +105,13 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         "pbd_set_attn_keys_per_split": (ctypes.c_int, [vp, i32]),
         "pbd_set_attn_query_split": (ctypes.c_int, [vp, i32]),
         "pbd_set_operand_precision": (ctypes.c_int, [vp, i32]),
+        "pbd_set_pass_mode": (ctypes.c_int, [vp, i32]),
+        "pbd_set_wait_limit": (ctypes.c_int, [vp, i32]),
         "pbd_profile_enable": (ctypes.c_int, [vp, i32]),
         "pbd_profile_read": (ctypes.c_int, [vp, i32, ctypes.POINTER(ctypes.c_double),
                                             ctypes.POINTER(ctypes.c_int64)]),
+        "pbd_profile_stage_times": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_uint64), i32,
+                                                    ctypes.POINTER(i32)]),
         "pbd_last_error": (ctypes.c_char_p, [vp]),
         "pbd_destroy": (None, [vp]),
     }
@@ -288,6 +293,12 @@ class Engine:
     def pbd_set_operand_precision(self, mode: int):
         _check(self.lib.pbd_set_operand_precision(self.ctx, int(mode)), self.ctx)
 
+    def pbd_set_pass_mode(self, mode: int):
+        _check(self.lib.pbd_set_pass_mode(self.ctx, int(mode)), self.ctx)
+
+    def pbd_set_wait_limit(self, polls: int):
+        _check(self.lib.pbd_set_wait_limit(self.ctx, int(polls)), self.ctx)
+
     def pbd_profile_enable(self, on: bool = True):
         _check(self.lib.pbd_profile_enable(self.ctx, 1 if on else 0), self.ctx)
 
@@ -296,6 +307,15 @@ class Engine:
         n = ctypes.c_int64(0)
         _check(self.lib.pbd_profile_read(self.ctx, int(kclass), ctypes.byref(ms), ctypes.byref(n)), self.ctx)
         return ms.value, n.value
+
+    def pbd_profile_stage_times(self):
+        """Stage timestamps of the last persistent pass: uint64 array [8][32][64][8][4]."""
+        import numpy as np
+        n = 8 * 32 * 64 * 8 * 4
+        buf = (ctypes.c_uint64 * n)()
+        got = ctypes.c_int32(0)
+        _check(self.lib.pbd_profile_stage_times(self.ctx, buf, n, ctypes.byref(got)), self.ctx)
+        return np.frombuffer(buf, dtype=np.uint64, count=got.value).reshape(8, 32, 64, 8, 4).copy()
 
     def close(self):
         if getattr(self, "ctx", None):

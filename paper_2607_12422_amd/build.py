@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 LIB_DIR = os.path.join(HERE, "lib")
 LIB_PATH = os.path.join(LIB_DIR, "libpbd.so")
 
-SOURCES = ["pbd_kernels.hip", "pbd_api.hip"]
+SOURCES = ["pbd_kernels.hip", "pbd_fused.hip", "pbd_api.hip"]
 ARCH = "gfx950"
 # Packed FP32 ops are disabled for all device code (the compiler would otherwise
 # form v_pk_* FP32 instructions from ordinary float code).

@@ -8,6 +8,7 @@
 #include <string>
 #include <vector>
 
+#include "pbd_fused.h"
 #include "pbd_kernels.h"
 
 using namespace pbd;
@@ -27,6 +28,7 @@ constexpr int ATTN_GRID_CAP = 1280; // large (batch x KV heads x splits above th
 constexpr int ATTN_SPLIT_CAP = 16;  // more splits than this (their partials cost the merge a load each)
 constexpr int BIG_MIN_MT = 8;    // passes of >= 128 rows (prefill chunks, batches of 8+) use the large-M projection
 constexpr size_t MAX_LDS = 160 * 1024;   // LDS one gfx950 work-group may allocate
+constexpr unsigned PBD_DEFAULT_WAIT = 1u << 18;   // polls per wait of the persistent pass (~0.25 s)
 
 // Every size and offset the library uses, derived from a validated config.
 struct Layout {
@@ -58,6 +60,9 @@ struct Layout {
     size_t w_u;                                      // its LoRA shrink u = A x, [M][sources * RT * 16] fp32
     size_t w_dn_tok, w_dn_conf;                      // one denoising pass's candidates and confidences
     int ksplit;                                      // K slices of the residual GEMMs
+    bool fused_shape;                                // the persistent batch-1 pass supports this model
+    size_t w_fused;                                  // its workspace region
+    size_t lay_stride;                               // bytes between consecutive layers' packed blocks
 };
 
 int validate(const pbd_config* c, std::string& err) {
@@ -183,6 +188,14 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.big = y.Mmax >= BIG_MIN_MT * 16;
     y.w_u = y.big && y.r > 0 ? take((size_t)y.Mmax * 3 * y.RT * 16 * 4) : 0;   // LoRA shrink, large-M path
     y.w_dn_conf = take((size_t)y.Bmax * y.D * 4);
+    // persistent batch-1 pass: the Qwen3-0.6B layer shape, bf16, LoRA rank
+    // <= 16, at most FUSED_MAX_ROWS block rows, and every attention split's
+    // K/V blocks within its LDS ring (<= 10 key blocks per split of 31)
+    y.fused_shape = y.dtype == PBD_DTYPE_BF16 && y.H == 1024 && y.F == 3072 && y.NQ == 16 && y.NKV == 8 &&
+                    y.HD == 128 && y.RT <= 1 && y.W <= FUSED_MAX_ROWS && y.L <= 255 && y.nblk <= 310 &&
+                    c->qk_norm && y.packed_bytes < ((size_t)1 << 32);
+    y.w_fused = y.fused_shape ? take(fused_ws_bytes()) : 0;
+    y.lay_stride = y.L > 1 ? y.lay[1].qkv - y.lay[0].qkv : 0;
     y.ws_bytes = off;
 }
 
@@ -206,6 +219,10 @@ struct pbd_ctx {
     int qsplit;          // attention: one work-group per 16 query rows (1), per KV head (0), or
                          // automatic (-1: split when the split-KV grid leaves most CUs idle)
     bool split;          // GEMM activation operands as bf16 hi + bf16 residual (always, for bf16 models)
+    int pass_mode;       // 0: persistent batch-1 pass where supported; 1: one kernel per operator
+    unsigned wait_limit; // polls per wait of the persistent pass
+    bool force_timeout;  // tests: the persistent pass first waits on a word no one sets
+    bool fused_dev;      // the device runs the persistent pass (256 CUs, one work-group each)
     Profiler prof;
     std::string err;
 };
@@ -317,6 +334,9 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     as.tokens = (int*)(ws + y.w_tokens); as.pos0 = pos0; as.nrows = nrows; as.status = status;
     as.embed = pk + y.p_embed; as.gain = pk + y.lay[0].attn_norm; as.x = x;
     as.op_hi = hi(y.w_xa); as.op_lo = lo(y.w_xa); as.sq = sq_a;
+    const bool fused = y.fused_shape && c->fused_dev && c->pass_mode == 0 && !pre && B == 1 &&
+                       !q.anchor_cached && !q.no_anchor && split;
+    if (fused) as.fused_ctl = (unsigned*)(ws + y.w_fused + fused_ctl_offset());
     PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_assemble(dt, as, B, st), "assemble");
 
     auto base_gemm = [&](FGemmArgs& g, size_t w_off, int tiles, int kb, const size_t* xop) {
@@ -328,6 +348,57 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         g.W = W; g.adapter_from = q.anchor_cached ? 1 : 0; g.excl_from = lead;
         g.ksplit = 1;
     };
+    if (fused) {
+        // the whole layer stack in one persistent launch, then the tied LM
+        // head on its final-norm operand and the argmax
+        const int L = q.n_layers > 0 ? q.n_layers : y.L;
+        const Layout::LayerOff& l0 = y.lay[0];
+        FusedArgs fa{};
+        fa.L = L; fa.M = M; fa.qk_norm = 1;
+        fa.full_from = q.causal ? W : 0;
+        fa.kv_rows = q.write_kv ? W : 0;
+        fa.Bmax = y.Bmax; fa.nblk = y.nblk; fa.lm_MT = MT; fa.lm_sq_stride = y.Mmax;
+        fa.spin_limit = c->wait_limit;
+        fa.force_timeout = c->force_timeout ? 1 : 0;
+        fa.nrows = nrows;
+        fa.eps = c->cfg.rms_eps; fa.scale = scale;
+        fa.scale_log2 = (float)(1.0 / sqrt((double)y.HD) * 1.4426950408889634);
+        fa.pos0 = pos0; fa.x0 = x; fa.pk = pk; fa.lay_stride = (uint32_t)y.lay_stride;
+        fa.off_qkv = (uint32_t)l0.qkv; fa.off_o = (uint32_t)l0.o; fa.off_gu = (uint32_t)l0.gu; fa.off_d = (uint32_t)l0.d;
+        fa.off_attn_norm = (uint32_t)l0.attn_norm; fa.off_mlp_norm = (uint32_t)l0.mlp_norm;
+        fa.off_q_norm = (uint32_t)l0.q_norm; fa.off_k_norm = (uint32_t)l0.k_norm;
+        for (int i = 0; i < 7; ++i) fa.off_la[i] = (uint32_t)l0.la[i];
+        fa.off_lb_qkv = (uint32_t)l0.lb_qkv; fa.off_lb_o = (uint32_t)l0.lb_o; fa.off_lb_gu = (uint32_t)l0.lb_gu;
+        fa.off_lb_d = (uint32_t)l0.lb_d;
+        fa.final_norm = pk + y.p_final_norm; fa.rope = (const float2*)(pk + y.p_rope);
+        fa.kcache = c->kv; fa.vcache = c->kv + y.kv_half;
+        fa.ws = ws + y.w_fused;
+        fa.lm_hi = hi(y.w_xa); fa.lm_lo = lo(y.w_xa); fa.lm_sq = sq_a;
+        fa.status = status;
+        PBD_TIMED(c, st, PBD_KCLASS_FUSED, launch_fused(fa, lora, st), "persistent layer stack");
+
+        FGemmArgs ge;
+        base_gemm(ge, y.p_embed, y.tiles_e, y.kb_e, y.w_xa);
+        ge.lora = 0; ge.sq = sq_a; ge.n_sq = 32;
+        ge.logits = q.logits; ge.ldo = y.V;
+        ge.arg_val = (float*)(ws + y.w_arg_val); ge.arg_idx = (int*)(ws + y.w_arg_idx);
+        ge.exclude = q.mode == PASS_DRAFT ? c->cfg.mask_id : -1;
+        if (q.conf) {
+            ge.arg_mx = (float*)(ws + y.w_arg_mx);
+            ge.arg_sum = (float*)(ws + y.w_arg_sum);
+        }
+        const int n_part = std::min(y.tiles_e, LMHEAD_GRID);
+        PBD_TIMED(c, st, PBD_KCLASS_LMHEAD, launch_lmhead(dt, ge, n_part, st), "lm head");
+        ArgmaxArgs am{};
+        am.M = M; am.W = W; am.n_tiles = n_part; am.mode = q.mode; am.chunk_pos = q.chunk_pos;
+        am.arg_val = ge.arg_val; am.arg_idx = ge.arg_idx; am.out = q.out_tokens;
+        am.lengths = q.lengths; am.nrows = nrows; am.seq_len_out = q.seq_len_out;
+        am.arg_mx = ge.arg_mx; am.arg_sum = ge.arg_sum; am.conf = q.conf;
+        am.lead = lead; am.out0 = q.out0; am.out0_stride = y.D + 1;
+        am.out_stride = W; am.out_off = 0;
+        PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_argmax(am, st), "argmax");
+        return PBD_OK;
+    }
     // residual GEMMs (n = hidden) have few output tiles: split K so that the
     // whole chip streams their weights (one m-group only)
     auto split_k = [&](FGemmArgs& g) {
@@ -625,6 +696,30 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
     c->kps = 0;
     c->qsplit = -1;
     c->split = cfg->dtype == PBD_DTYPE_BF16;
+    c->pass_mode = 1;
+    c->wait_limit = PBD_DEFAULT_WAIT;
+    c->force_timeout = false;
+    c->fused_dev = false;
+    if (y.fused_shape) {
+        // one work-group per CU on the 256 CUs of the eight XCDs, all resident at once
+        int dev = 0, ncu = 0, occ = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && ncu == 256 &&
+            fused_occupancy(&occ) == hipSuccess && occ >= 1)
+            c->fused_dev = true;
+        // the packed layers must be equally spaced for the kernel's per-layer offsets
+        for (int l = 1; l < y.L && c->fused_dev; ++l) {
+            const Layout::LayerOff &a0 = y.lay[0], &al = y.lay[l];
+            const size_t d = (size_t)l * y.lay_stride;
+            if (al.qkv != a0.qkv + d || al.o != a0.o + d || al.gu != a0.gu + d || al.d != a0.d + d ||
+                al.attn_norm != a0.attn_norm + d || al.mlp_norm != a0.mlp_norm + d || al.q_norm != a0.q_norm + d ||
+                al.k_norm != a0.k_norm + d || al.lb_qkv != a0.lb_qkv + d || al.lb_o != a0.lb_o + d ||
+                al.lb_gu != a0.lb_gu + d || al.lb_d != a0.lb_d + d)
+                c->fused_dev = false;
+            for (int i = 0; i < 7; ++i)
+                if (al.la[i] != a0.la[i] + d) c->fused_dev = false;
+        }
+    }
     hipStream_t st = (hipStream_t)stream;
     const int dt = y.dtype;
     {
@@ -919,6 +1014,23 @@ int pbd_set_operand_precision(pbd_ctx* c, int32_t mode) {
     return PBD_OK;
 }
 
+int pbd_set_pass_mode(pbd_ctx* c, int32_t mode) {
+    int rc = check_ctx(c);
+    if (rc) return rc;
+    if (mode != 0 && mode != 1) return fail(c, PBD_ERR_INVALID_ARG, "pass mode must be 0 or 1");
+    c->pass_mode = mode;
+    return PBD_OK;
+}
+
+int pbd_set_wait_limit(pbd_ctx* c, int32_t polls) {
+    int rc = check_ctx(c);
+    if (rc) return rc;
+    if (polls < 0) return fail(c, PBD_ERR_INVALID_ARG, "wait limit must be >= 0");
+    c->wait_limit = polls == 0 ? PBD_DEFAULT_WAIT : (unsigned)polls;
+    c->force_timeout = polls == 1;
+    return PBD_OK;
+}
+
 int pbd_profile_enable(pbd_ctx* c, int32_t on) {
     int rc = check_ctx(c);
     if (rc) return rc;
@@ -946,6 +1058,19 @@ int pbd_profile_read(pbd_ctx* c, int32_t kclass, double* total_ms, int64_t* laun
     }
     *total_ms = tot;
     *launches = n;
+    return PBD_OK;
+}
+
+int pbd_profile_stage_times(pbd_ctx* c, uint64_t* out, int32_t max_entries, int32_t* n_written) {
+    int rc = check_ctx(c);
+    if (rc) return rc;
+    if (!out || !n_written || max_entries < 0) return fail(c, PBD_ERR_INVALID_ARG, "bad stage-time query");
+    if (!c->ly.fused_shape) return fail(c, PBD_ERR_UNSUPPORTED, "the model does not use the persistent pass");
+    const int n = std::min(max_entries, fused_trace_entries());
+    PBD_HIP(c, hipDeviceSynchronize(), "sync");
+    PBD_HIP(c, hipMemcpy(out, c->ws + c->ly.w_fused + fused_trace_offset(), (size_t)n * 8, hipMemcpyDeviceToHost),
+            "read stage times");
+    *n_written = n;
     return PBD_OK;
 }
 

@@ -1,0 +1,1183 @@
+// Persistent single-launch layer stack of one batch-1 pass (draft or verify,
+// Sec. 3 steps 1-3) for the Qwen3-0.6B layer shape on gfx950.
+//
+// Why one launch: at batch 1 a pass streams 0.9 GB of layer weights through
+// 28 x 5 dependent stages.  As separate kernels each stage is a cold burst
+// of 4-12 MB behind a launch, and the chain runs at about an eighth of the
+// HBM rate.  Weights do not depend on activations, so a resident kernel can
+// stream them continuously while the activations hop from stage to stage.
+//
+// Layout of the work (256 work-groups, one per CU, eight XCDs of 32):
+//   * XCD g is "group" g and owns KV head g (the shape has exactly eight):
+//     the q rows of heads 2g, 2g+1 and the k/v rows of head g, the attention
+//     of that head, the O-projection K-slice of those two heads, and the
+//     FFN columns [384 g, 384 g + 384) of gate/up and the matching K-slice of
+//     down.  Every group keeps its own copy of the residual stream.
+//   * Inside a group, rank r (0..31) owns the columns [32 r, 32 r + 32) of
+//     the residual copy.
+//   * Per layer: R (residual update from the eight groups' down-projection
+//     partials, attention RMSNorm operand), Q (q/k/v tile), A (split-KV
+//     attention partial), M (merge of the partials, one query row per rank),
+//     O (O-projection partial over the group's heads), R2 (residual update
+//     from the O partials, MLP RMSNorm operand), GU (gate/up tiles + SwiGLU),
+//     D (down-projection partial over the group's FFN slice).
+//   * Handoffs inside a group go through the XCD's L2: plain stores, then a
+//     per-rank flag; consumers poll the flags and read with L1-bypassing
+//     (sc1) loads.  The two handoffs between groups per layer (O and D
+//     partials) carry a tag word in every 8-byte pair written through to
+//     memory, so consumers poll the data itself; no fence is ever needed.
+//     Buffers alternate by layer parity and every flag / tag holds
+//     (epoch, layer), so nothing from an earlier layer or pass is mistaken
+//     for current data.
+//   * Each work-group has 8 compute waves and 2 loader waves.  The loader
+//     waves stream the work-group's weight fragments and its attention
+//     split's K/V blocks, in stage order, straight into an LDS ring with
+//     global_load_lds (non-temporal), keeping up to the ring's 80 KiB in
+//     flight.  Compute waves never issue a global load that a later wait
+//     would have to drain behind the prefetch.  Loader waves take part in
+//     every work-group barrier and wait for a stage's fragments before the
+//     barrier that opens that stage.
+//   * Every wait is bounded: on expiry the wait sets PBD_STATUS_TIMEOUT and
+//     an abort word that releases every other waiter, and the kernel runs
+//     to its end.
+// RMSNorm is folded as in the skinny GEMM: operands carry x * g, per-rank
+// row sums of squares give r_m, applied to the accumulators.  LoRA (App.
+// A.2) runs unmerged in every tile (shrink on the same operand fragments,
+// expand per wave before the cross-wave reduction; for the K-split O and
+// down projections each group's partial carries its own expand, summed
+// with the partials by linearity).
+#include "pbd_device.h"
+#include "pbd_fused.h"
+#include "pbd_kernels.h"
+
+#include <hip/hip_ext.h>
+
+namespace pbd {
+namespace fz {
+
+constexpr int H = 1024, F = 3072, NQ = 16, NKV = 8, HD = 128, G = NQ / NKV;
+constexpr int NGRP = 8, NRANK = 32;
+constexpr int NWC = 6, NWL = 2, NTHR = (NWC + NWL) * WAVE;   // 8 waves: 256 VGPRs each
+constexpr int MW = FUSED_MAX_ROWS;     // rows per pass
+constexpr int QRMAX = G * MW;          // query rows per KV head
+constexpr int KBH = H / 32;            // fragments over the hidden size
+constexpr int FPW = (KBH + NWC - 1) / NWC;  // hidden-size fragments per compute wave (6)
+constexpr int NEL = (MW * 32 + NWC * WAVE - 1) / (NWC * WAVE);   // residual-slice elements per thread
+constexpr int KB_O = NQ * HD / 32;     // 64
+constexpr int KB_D = F / 32;           // 96
+constexpr int GQKV = (G + 2) * HD;     // a group's q/k/v columns (512)
+constexpr int GO = G * HD;             // a group's O-projection K-slice (256)
+constexpr int GF = F / NGRP;           // a group's FFN columns (384)
+constexpr int NSLOT = 80;              // LDS ring slots of 1 KiB (even: the two loaders take alternate items)
+static_assert(NSLOT % 2 == 0, "ring slots come in pairs");
+constexpr int LDQ = HD + 8;            // bf16 row pitch of the attention LDS rows
+constexpr int PB = HD + 4;             // fp32 pitch of a merged attention row
+constexpr int APW = HD + 4;            // fp32 words per stored attention partial row (m, l, o[128], pad)
+
+enum { ST_R = 0, ST_Q, ST_A, ST_M, ST_O, ST_R2, ST_GU, ST_D, NSTAGE };
+enum { FL_R = 0, FL_Q, FL_A, FL_M, FL_R2, FL_GU, NFLAG };
+constexpr int TRACE_LAYERS = 64;       // layers covered by the stage timestamps
+__host__ __device__ constexpr int n_barriers(int st) { return st == ST_A ? 4 : 2; }
+
+// LDS map (bytes)
+constexpr size_t RING_BYTES = (size_t)NSLOT * 1024;
+constexpr size_t SRED_BYTES = (size_t)2 * NWC * 2 * WAVE * 16;                     // GEMM reduction
+constexpr size_t QL_BYTES = (size_t)QRMAX * LDQ * 2, KL_BYTES = (size_t)32 * LDQ * 2, VL_BYTES = (size_t)32 * HD * 2;
+constexpr size_t PBUF_BYTES = (size_t)4 * 16 * PB * 4;
+constexpr size_t ATT_BYTES = QL_BYTES + KL_BYTES + VL_BYTES + PBUF_BYTES;
+constexpr size_t SCR_BYTES = (SRED_BYTES > ATT_BYTES ? SRED_BYTES : ATT_BYTES);
+constexpr size_t XS_BYTES = (size_t)MW * 32 * 4;
+constexpr size_t MISC_BYTES = 512;
+constexpr size_t LDS_BYTES = RING_BYTES + SCR_BYTES + XS_BYTES + MISC_BYTES;
+static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+
+// Workspace of the persistent pass (bytes), parity-doubled per-group buffers.
+struct WsMap {
+    size_t flags, xn, xm, sq, sqm, qkv, apart, oop, hop, parto, partd, ctl, trace, total;
+};
+__host__ __device__ inline WsMap ws_map() {
+    WsMap w{};
+    size_t off = 0;
+    auto take = [&](size_t b) { size_t o = off; off += (b + 255) / 256 * 256; return o; };
+    w.flags = take((size_t)NFLAG * 2 * NGRP * NRANK * 4);
+    w.xn = take((size_t)2 * NGRP * MW * H * 4);
+    w.xm = take((size_t)2 * NGRP * MW * H * 4);
+    w.sq = take((size_t)2 * NGRP * NRANK * MW * 4);
+    w.sqm = take((size_t)2 * NGRP * NRANK * MW * 4);
+    w.qkv = take((size_t)2 * NGRP * MW * GQKV * 4);
+    w.apart = take((size_t)2 * NGRP * NRANK * QRMAX * APW * 4);
+    w.oop = take((size_t)2 * NGRP * MW * GO * 4);
+    w.hop = take((size_t)2 * NGRP * MW * GF * 4);
+    w.parto = take((size_t)2 * NGRP * MW * H * 8);
+    w.partd = take((size_t)2 * NGRP * MW * H * 8);
+    w.ctl = take(256);
+    w.trace = take((size_t)NGRP * NRANK * TRACE_LAYERS * NSTAGE * 4 * 8);
+    w.total = off;
+    return w;
+}
+
+typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
+typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
+
+// Cache-policy bits of buffer instructions: sc0 = 1, nt = 2, sc1 = 16.
+constexpr int SC1 = 16, SC01 = 17, NT = 2;
+
+__device__ __forceinline__ unsigned xcc_id() {
+    unsigned v;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 16)" : "=s"(v));
+    return v & 0xf;
+}
+
+__device__ __forceinline__ unsigned ld_sc1_u32(const unsigned* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wait until vmcnt <= n for a run-time n in [0, 40] (loader waves).
+__device__ __forceinline__ void wait_vm(int n) {
+#define PBD_VMW(k) case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
+    switch (n) {
+        PBD_VMW(0) PBD_VMW(1) PBD_VMW(2) PBD_VMW(3) PBD_VMW(4) PBD_VMW(5) PBD_VMW(6) PBD_VMW(7)
+        PBD_VMW(8) PBD_VMW(9) PBD_VMW(10) PBD_VMW(11) PBD_VMW(12) PBD_VMW(13) PBD_VMW(14) PBD_VMW(15)
+        PBD_VMW(16) PBD_VMW(17) PBD_VMW(18) PBD_VMW(19) PBD_VMW(20) PBD_VMW(21) PBD_VMW(22) PBD_VMW(23)
+        PBD_VMW(24) PBD_VMW(25) PBD_VMW(26) PBD_VMW(27) PBD_VMW(28) PBD_VMW(29) PBD_VMW(30) PBD_VMW(31)
+        PBD_VMW(32) PBD_VMW(33) PBD_VMW(34) PBD_VMW(35) PBD_VMW(36) PBD_VMW(37) PBD_VMW(38) PBD_VMW(39)
+        default: asm volatile("s_waitcnt vmcnt(40)" ::: "memory"); break;
+    }
+#undef PBD_VMW
+}
+
+__device__ __forceinline__ void bar() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// value -> bf16 value + bf16 residual, 8 consecutive k of one operand row
+__device__ __forceinline__ void split8(const float* v, uint4& hi, uint4& lo) {
+    bf16 h[8], l[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        h[i] = (bf16)v[i];
+        l[i] = (bf16)(v[i] - (float)h[i]);
+    }
+    __builtin_memcpy(&hi, h, 16);
+    __builtin_memcpy(&lo, l, 16);
+}
+
+__device__ __forceinline__ void mma_k4s(f32x4& acc, const uint2& a, const f32x4& p) {
+    f32x4 hh, ll;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        hh[e] = (float)(bf16)p[e];
+        ll[e] = p[e] - hh[e];
+    }
+    mma_k4(acc, a, hh);
+    mma_k4(acc, a, ll);
+}
+
+// Static per-work-group schedule: which weight tiles, K/V blocks and
+// fragments a rank loads in each stage.
+struct Sched {
+    int g, r, t, nkb, s_pre;
+    // Q tile (global tile index in the packed q/k/v weights) of this rank
+    __device__ int q_tile() const { return r < 16 ? 16 * g + r : (r < 24 ? 128 + 8 * g + (r - 16) : 192 + 8 * g + (r - 24)); }
+    // LoRA source of the Q tile: 0 q, 1 k, 2 v
+    __device__ int q_src() const { return r < 16 ? 0 : (r < 24 ? 1 : 2); }
+    __device__ int gu_t1() const { return 48 * g + r; }
+    __device__ int gu_t2() const { return 48 * g + 32 + r / 2; }
+    // prefix key blocks of this rank's attention split (rank 31: the block keys)
+    __device__ int kb_begin() const { return r < s_pre ? (r * nkb) / s_pre : 0; }
+    __device__ int kb_count() const { return r < s_pre ? ((r + 1) * nkb) / s_pre - (r * nkb) / s_pre : 0; }
+    __device__ int items(int st) const {
+        switch (st) {
+            case ST_Q: return KBH;
+            case ST_A: return 8 * kb_count();
+            case ST_O: return 16;
+            case ST_GU: return 2 * KBH;
+            case ST_D: return 24;
+            default: return 0;
+        }
+    }
+};
+
+template <bool LORA>
+__global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char* ring = smem;
+    unsigned char* scr = smem + RING_BYTES;
+    float* xs = (float*)(smem + RING_BYTES + SCR_BYTES);               // [MW][32] residual slice
+    float* s_rm = (float*)(smem + RING_BYTES + SCR_BYTES + XS_BYTES);  // [MW]
+    int* s_id = (int*)(s_rm + MW);                                       // group, rank, t
+
+    int tid = threadIdx.x;
+    const int wid = __builtin_amdgcn_readfirstlane(tid / WAVE);   // wave-uniform (scalar)
+    int lane = tid % WAVE;
+    int lrow = lane % 16, lgrp = lane / 16;
+    const WsMap wm = ws_map();
+    char* ws = (char*)a.ws;
+    unsigned* ctl = (unsigned*)(ws + wm.ctl);
+    unsigned* abort_w = ctl + 9;
+
+    if (tid == 0) {
+        const unsigned x = xcc_id();
+        const unsigned rk = __hip_atomic_fetch_add(ctl + x, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_id[0] = (int)x;
+        s_id[1] = (int)rk;
+        s_id[2] = a.pos0[0];
+        s_id[3] = (int)ctl[8];
+        s_id[4] = a.nrows[0];
+    }
+    __syncthreads();
+    // a sequence skipped for capacity: no cache write, no outputs (every
+    // work-group reads the same word, so all leave together)
+    if (__builtin_amdgcn_readfirstlane(s_id[4]) == 0) return;
+    // wave-uniform from here on (scalar registers, and so every address derived from them)
+    Sched sc;
+    sc.g = __builtin_amdgcn_readfirstlane(s_id[0]);
+    sc.r = __builtin_amdgcn_readfirstlane(s_id[1]);
+    sc.t = __builtin_amdgcn_readfirstlane(s_id[2]);
+    const unsigned epoch = (unsigned)__builtin_amdgcn_readfirstlane(s_id[3]);
+    if (sc.g >= NGRP || sc.r >= NRANK) {
+        // placement is not 8 x 32 (never seen): report; the work-groups that
+        // wait for the missing ranks time out and the pass ends with an error
+        if (tid == 0) {
+            atomicOr(a.status, PBD_STATUS_TIMEOUT);
+            __hip_atomic_store(abort_w, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        return;
+    }
+    sc.nkb = (sc.t + 15) / 16;
+    sc.s_pre = sc.nkb < NRANK - 1 ? sc.nkb : NRANK - 1;
+    const int g = sc.g, r = sc.r, t = sc.t, M = a.M;
+    const int QR = G * M, QT = (QR + 15) / 16;
+    const int L = a.L;
+
+    __amdgpu_buffer_rsrc_t rws = __builtin_amdgcn_make_buffer_rsrc(ws, 0, 0x7fffffff, 0x00020000);
+
+    // ------------------------------------------------------------------
+    // Loader waves: ring fill in stage order, in step with the barriers.
+    // ------------------------------------------------------------------
+    if (wid >= NWC) {
+        const int lid = wid - NWC;
+        const char* pk = (const char*)a.pk;
+        // Every stage's items are runs of consecutive 1 KiB fragments in
+        // memory; item i is fragment i % per of run i / per, and run j starts
+        // at base + (j & 1) * odd + (j >> 1) * pair (+ the layer's offset).
+        // Stage sizes and run lengths are even, so with items dealt out by
+        // the parity of their global index this loader takes offsets
+        // lid, lid + 2, ... of every run.
+        const int q_tile = sc.q_tile(), t1 = sc.gu_t1(), t2 = sc.gu_t2(), kb0 = sc.kb_begin();
+        const bool half_mine = ((lrow / 4) & 1) == (r & 1);   // rows of the half gate/up tile
+        const size_t kv_layer = (size_t)a.Bmax * NKV * a.nblk * 16 * HD * 2;
+        const char* kv_k = a.kcache + (size_t)g * a.nblk * 16 * HD * 2 + (size_t)kb0 * (16 * HD * 2);
+        const char* kv_v = a.vcache + (size_t)g * a.nblk * 16 * HD * 2 + (size_t)kb0 * (16 * HD * 2);
+        // issue cursor: layer, stage, item (even), global item index, ring slot,
+        // run, offset in the run, and the stage's run parameters
+        int cl = 0, cs = -1, ci = 0, cn = 0, cg = 0, slot = 0, rj = 0, rk = 0;
+        int per = 1;
+        bool half = false;
+        const char* sbase = pk;      // run 0 of the stage at layer cl
+        const char* rbase = pk;      // current run
+        long odd = 0, pair = 0;
+        auto run_base = [&]() { rbase = sbase + (rj & 1) * odd + (rj >> 1) * pair; };
+        auto enter_stage = [&]() {
+            // stage cs of layer cl
+            ci = 0; rj = 0; rk = 0;
+            cn = sc.items(cs);
+            half = false; odd = 0; pair = 0; per = 2;
+            const char* lb = pk + (size_t)cl * a.lay_stride;
+            switch (cs) {
+                case ST_Q: per = KBH; sbase = lb + a.off_qkv + (size_t)q_tile * KBH * 1024; break;
+                case ST_A:
+                    per = 4; sbase = kv_k + (size_t)cl * kv_layer;
+                    odd = (long)(kv_v - kv_k); pair = 16 * HD * 2; break;
+                case ST_O: per = 8; sbase = lb + a.off_o + ((size_t)2 * r * KB_O + 8 * g) * 1024; odd = (long)KB_O * 1024; break;
+                case ST_GU:
+                    per = KBH; sbase = lb + a.off_gu + (size_t)t1 * KBH * 1024;
+                    odd = (long)(t2 - t1) * KBH * 1024; half = true; break;
+                case ST_D: per = 12; sbase = lb + a.off_d + ((size_t)2 * r * KB_D + 12 * g) * 1024; odd = (long)KB_D * 1024; break;
+                default: break;
+            }
+            run_base();
+        };
+        auto issue_to = [&](int limit) {
+            while (cg < limit) {
+                if (ci >= cn) {
+                    if (++cs == NSTAGE) { cs = 0; ++cl; }
+                    if (cl >= L) break;
+                    enter_stage();
+                    continue;
+                }
+                // the rest of the current run, up to the limit (both even)
+                const int n = min(per - rk, limit - cg);
+                const bool act = !(half && (rj & 1)) || half_mine;
+                const char* src = rbase + (rk + lid) * 1024 + lane * 16;
+                for (int i = 0; i < n; i += 2) {
+                    if (act)
+                        __builtin_amdgcn_global_load_lds((const void*)src,
+                                                         (__attribute__((address_space(3))) void*)(ring + (slot + lid) * 1024),
+                                                         16, 0, NT);
+                    src += 2048;
+                    slot = slot + 2 == NSLOT ? 0 : slot + 2;
+                }
+                ci += n; cg += n; rk += n;
+                if (rk >= per) { rk = 0; ++rj; run_base(); }
+            }
+        };
+        int stage_begin = 0;       // global index of the first item of the barrier-phase stage
+        issue_to(NSLOT);
+        for (int l = 0; l < L; ++l) {
+            for (int st = 0; st < NSTAGE; ++st) {
+                const int n = sc.items(st), end = stage_begin + n;
+                const int nb = n_barriers(st);
+                for (int b = 0; b < nb; ++b) {
+                    if (b == 0 && n > 0) {
+                        // everything before this stage is released, so its remaining
+                        // items fit; issue them, then wait for this loader's share
+                        issue_to(end);
+                        const int later = cg - end;
+                        const int mine_later = (later + ((end & 1) == lid ? 1 : 0)) / 2;
+                        wait_vm(mine_later < 40 ? mine_later : 40);
+                    }
+                    asm volatile("s_barrier" ::: "memory");
+                    if (b == nb - 1) stage_begin = end;          // the stage's slots are released
+                    // look ahead while the compute waves work
+                    issue_to(stage_begin + NSLOT);
+                }
+            }
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        return;
+    }
+
+    // ------------------------------------------------------------------
+    // Compute waves
+    // ------------------------------------------------------------------
+    int ring_base = 0;                   // global ring index of the current stage's first item
+    const unsigned spin_limit = a.spin_limit;
+    bool aborted = false;
+    auto give_up = [&]() {
+        atomicOr(a.status, PBD_STATUS_TIMEOUT);
+        __hip_atomic_store(abort_w, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        aborted = true;
+    };
+    // wave 0, lanes 0..31: wait until all 32 ranks' flags of (flag kind, parity) hold tag
+    auto wait_flags = [&](int fk, int p, unsigned tag) {
+        if (wid != 0) return;
+        const unsigned* f = (const unsigned*)(ws + wm.flags) + (((size_t)fk * 2 + p) * NGRP + g) * NRANK;
+        unsigned spins = 0;
+        bool ok = lane >= NRANK;
+        while (!__all(ok)) {
+            if (!ok) ok = ld_sc1_u32(f + lane) == tag;
+            if (++spins > spin_limit || ((spins & 63) == 0 && ld_sc1_u32(abort_w))) {
+                if (lane == 0 && spins > spin_limit) give_up();
+                break;
+            }
+        }
+    };
+    auto set_flag = [&](int fk, int p, unsigned tag) {
+        // after this wave's (and, by the preceding barrier, every wave's) stores
+        unsigned* f = (unsigned*)(ws + wm.flags) + (((size_t)fk * 2 + p) * NGRP + g) * NRANK + r;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __builtin_amdgcn_raw_buffer_store_b32(tag, rws, (unsigned)((char*)f - ws), 0, 0);
+    };
+    auto ring_frag = [&](int i) -> uint4 {
+        return *(const uint4*)(ring + (size_t)((ring_base + i) % NSLOT) * 1024 + lane * 16);
+    };
+    // B operand of fragment f (k in [32 f, 32 f + 32)) for m-tile mt, in two
+    // phases so that a stage issues all its loads before the first wait: the
+    // load (row clamped into [0, M): always a valid address) and the split
+    // into bf16 value + residual (rows past M zeroed)
+    auto opnd_load = [&](size_t base_off, int ld, int f, int mt, f32x4& v0, f32x4& v1) {
+        const int m = min(mt * 16 + lrow, M - 1);
+        const unsigned off = (unsigned)(base_off + ((size_t)m * ld + f * 32 + lgrp * 8) * 4);
+        v0 = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rws, off, 0, SC1));
+        v1 = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rws, off + 16, 0, SC1));
+    };
+    auto opnd_make = [&](const f32x4& v0, const f32x4& v1, int mt, uint4& hi, uint4& lo) {
+        const bool live = mt * 16 + lrow < M;
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[i] = live ? v0[i] : 0.f;
+            v[4 + i] = live ? v1[i] : 0.f;
+        }
+        split8(v, hi, lo);
+    };
+    f32x4* s_red = (f32x4*)scr;          // [tile][wave][mt][lane]
+    // wave 0 after barrier B: sum over waves w0..w0+nw-1 of tile tt -> value for (row n, m)
+    auto red_val = [&](int tt, int w0, int nw, int n, int m) -> float {
+        const int mt = m / 16, ln = (n / 4) * 16 + m % 16, e = n % 4;
+        float v = 0.f;
+        for (int w = w0; w < w0 + nw; ++w) v += s_red[((tt * NWC + w) * 2 + mt) * WAVE + ln][e];
+        return v;
+    };
+    const float* rope = (const float*)a.rope;
+    const char* pk = (const char*)a.pk;
+    const int MT = (M + 15) / 16;
+
+    if (a.force_timeout && wid == 0) {
+        // tests of the bounded wait: ctl[10] is never written
+        unsigned spins = 0;
+        while (ld_sc1_u32(ctl + 10) == 0u) {
+            if (++spins > spin_limit) {
+                if (lane == 0) give_up();
+                break;
+            }
+        }
+    }
+    // residual slice from the assembled block (x [M][H], written by the previous kernel)
+    for (int i = tid; i < MW * 32; i += NWC * WAVE) {
+        const int m = i / 32, c = i % 32;
+        xs[i] = m < M ? a.x0[(size_t)m * H + 32 * r + c] : 0.f;
+    }
+
+    // stage timestamps of rank 0 of every group (profiling aid, 100 MHz clock)
+    unsigned long long* trace = (unsigned long long*)(ws + wm.trace);
+    auto stamp = [&](int l, int st, int k) {
+        if (wid == 0 && lane == 0 && l < TRACE_LAYERS)
+            trace[((((size_t)g * NRANK + r) * TRACE_LAYERS + l) * NSTAGE + st) * 4 + k] = __builtin_amdgcn_s_memrealtime();
+    };
+    // wave 0, lanes 0..7: wait until the last pair producer group `lane` writes
+    // into this rank's columns of layer pl's partial carries pl's tag (its
+    // other pairs are checked one by one when read)
+    auto wait_partials = [&](bool from_o, int pl) {
+        if (wid != 0) return;
+        const unsigned ptag = (epoch << 8) | (unsigned)pl;
+        const size_t base = (from_o ? wm.parto : wm.partd) + ((size_t)(pl & 1) * NGRP) * MW * H * 8;
+        const unsigned off = (unsigned)(base + (((size_t)(lane % NGRP) * MW + (M - 1)) * H + 32 * r + 31) * 8);
+        unsigned spins = 0;
+        bool ok = lane >= NGRP;
+        while (!__all(ok)) {
+            if (!ok) ok = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws, off, 0, SC01)).y == ptag;
+            if (++spins > spin_limit || ((spins & 63) == 0 && ld_sc1_u32(abort_w))) {
+                if (lane == 0 && spins > spin_limit) give_up();
+                break;
+            }
+        }
+    };
+    // R / R2 / final: residual update from the eight groups' partials (none at
+    // layer 0's R), operand x * gain of the next RMSNorm and per-row sums of squares
+    auto stage_reduce = [&](int l, bool from_o, const void* gain, size_t out_x, size_t out_sq, bool final_out) {
+        const int p = l & 1;
+        const bool poll = from_o || l > 0;
+        // partials of layer l (O) or l - 1 (down) from every group: all 16
+        // pairs of this thread's two elements are requested before any wait
+        const int pl = from_o ? l : l - 1;
+        const unsigned ptag = (epoch << 8) | (unsigned)(pl & 0xff);
+        const size_t base = (from_o ? wm.parto : wm.partd) + ((size_t)(pl & 1) * NGRP) * MW * H * 8;
+        uint2 pr[NEL][NGRP];
+        if (poll) {
+#pragma unroll
+            for (int e0 = 0; e0 < NEL; ++e0) {
+                const int idx = tid + e0 * NWC * WAVE;
+                const int m = min(idx / 32, M - 1), c = idx % 32;
+#pragma unroll
+                for (int x = 0; x < NGRP; ++x)
+                    pr[e0][x] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws,
+                        (unsigned)(base + (((size_t)x * MW + m) * H + 32 * r + c) * 8), 0, SC01));
+            }
+        }
+#pragma unroll
+        for (int e0 = 0; e0 < NEL; ++e0) {
+            const int idx = tid + e0 * NWC * WAVE;
+            const int m = idx / 32, c = idx % 32;
+            const bool live = m < M;
+            float xv = live ? xs[idx] : 0.f;            // live implies idx < M * 32
+            if (poll && live) {
+                float sum = 0.f;
+#pragma unroll
+                for (int x = 0; x < NGRP; ++x) {
+                    uint2 q = pr[e0][x];
+                    // a pair not yet written through: poll it alone (rare)
+                    unsigned spins = 0;
+                    while (q.y != ptag) {
+                        if (++spins > spin_limit || ((spins & 63) == 0 && ld_sc1_u32(abort_w))) {
+                            if (spins > spin_limit) give_up();
+                            q.x = 0u;
+                            break;
+                        }
+                        q = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws,
+                            (unsigned)(base + (((size_t)x * MW + m) * H + 32 * r + c) * 8), 0, SC01));
+                    }
+                    sum += __uint_as_float(q.x);          // group order
+                }
+                xv += sum;
+                xs[idx] = xv;
+            }
+            // operand and the row's sum of squares over the rank's 32 columns
+            const float ov = live ? xv * (float)((const bf16*)gain)[32 * r + c] : 0.f;
+            float ss = xv * xv;
+#pragma unroll
+            for (int o = 16; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 32);
+            if (final_out) {
+                if (live) {
+                    const bf16 h = (bf16)ov;
+                    const bf16 lo = (bf16)(ov - (float)h);
+                    const size_t e = xfrag_elem<bf16>(m, 32 * r + c, a.lm_MT);
+                    ((bf16*)a.lm_hi)[e] = h;
+                    ((bf16*)a.lm_lo)[e] = lo;
+                    if (c == 0) a.lm_sq[(size_t)r * a.lm_sq_stride + m] = ss;
+                }
+            } else if (live) {
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(ov), rws,
+                    (unsigned)(out_x + ((((size_t)p * NGRP + g) * MW + m) * H + 32 * r + c) * 4), 0, 0);
+                if (c == 0)
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(ss), rws,
+                        (unsigned)(out_sq + ((((size_t)p * NGRP + g) * NRANK + r) * MW + m) * 4), 0, 0);
+            }
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    };
+
+    // r_m of every row from the 32 ranks' partial sums of squares (wave 0, lanes < M)
+    auto load_rm = [&](size_t sq_off, int p) {
+        if (wid == 0 && lane < MW) {
+            const int m = min(lane, M - 1);
+            float v[NRANK];
+#pragma unroll
+            for (int q = 0; q < NRANK; ++q)
+                v[q] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rws,
+                    (unsigned)(sq_off + ((((size_t)p * NGRP + g) * NRANK + q) * MW + m) * 4), 0, SC1));
+            float sm = 0.f;
+#pragma unroll
+            for (int q = 0; q < NRANK; ++q) sm += v[q];
+            s_rm[lane] = rsqrtf(sm / (float)H + a.eps);
+        }
+    };
+
+    for (int l = 0; l < L; ++l) {
+        // lane-derived offsets are recomputed in every layer instead of being
+        // kept live (and spilled) across the whole loop
+        asm volatile("" : "+v"(tid), "+v"(lane), "+v"(lrow), "+v"(lgrp));
+        const int p = l & 1;
+        const unsigned tag = (epoch << 8) | (unsigned)l;
+        const size_t lay = (size_t)l * a.lay_stride;
+
+        // ---------------- R: residual from the down partials, attention-norm operand
+        stamp(l, ST_R, 0);
+        if (l > 0) wait_partials(false, l - 1);
+        bar();
+        stamp(l, ST_R, 1);
+        stage_reduce(l, false, pk + a.off_attn_norm + lay, wm.xn, wm.sq, false);
+        bar();                                           // all waves' stores done
+        if (wid == 0 && lane == 0) set_flag(FL_R, p, tag);
+
+        // ---------------- Q: q/k/v tile
+        stamp(l, ST_Q, 0);
+        wait_flags(FL_R, p, tag);
+        bar();                                           // inputs ready, ring holds the tile
+        stamp(l, ST_Q, 1);
+        load_rm(wm.sq, p);
+        {
+            const size_t xb = wm.xn + ((size_t)p * NGRP + g) * MW * H * 4;
+            f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
+            f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
+            const int src = sc.q_src();
+            const uint4* la = (const uint4*)(pk + a.off_la[src] + lay);
+            // fragments f = wid + NWC j of the hidden size
+            f32x4 xv[FPW][2][2];
+            uint4 av[FPW];
+#pragma unroll
+            for (int j = 0; j < FPW; ++j) {
+                const int f = min(wid + NWC * j, KBH - 1);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) opnd_load(xb, H, f, mt, xv[j][mt][0], xv[j][mt][1]);
+                if (LORA) av[j] = la[(size_t)f * WAVE + lane];
+            }
+#pragma unroll
+            for (int j = 0; j < FPW; ++j) {
+                if (wid + NWC * j >= KBH) continue;
+                const uint4 w = ring_frag(wid + NWC * j);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) {
+                    if (mt >= MT) continue;
+                    uint4 xh, xl;
+                    opnd_make(xv[j][mt][0], xv[j][mt][1], mt, xh, xl);
+                    mma_frag<bf16>(acc[mt], w, xh);
+                    mma_frag<bf16>(acc[mt], w, xl);
+                    if (LORA) {
+                        mma_frag<bf16>(uacc[mt], av[j], xh);
+                        mma_frag<bf16>(uacc[mt], av[j], xl);
+                    }
+                }
+            }
+            if (LORA) {
+                uint2 bv;
+                __builtin_memcpy(&bv, (const bf16*)(pk + a.off_lb_qkv + lay) + ((size_t)sc.q_tile() * WAVE + lane) * 4, 8);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bv, uacc[mt] * a.scale);
+            }
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt) s_red[((0 * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
+        }
+        stamp(l, ST_Q, 2);
+        bar();
+        if (wid == 0) {
+            // tile [16][M] -> qkv columns 16 r .. of the group's [M][512]
+            const size_t qb = wm.qkv + ((size_t)p * NGRP + g) * MW * GQKV * 4;
+            for (int i = lane; i < 16 * M; i += WAVE) {
+                const int n = i % 16, m = i / 16;
+                const float v = red_val(0, 0, NWC, n, m) * s_rm[m];
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rws,
+                    (unsigned)(qb + ((size_t)m * GQKV + 16 * r + n) * 4), 0, 0);
+            }
+            set_flag(FL_Q, p, tag);
+        }
+        stamp(l, ST_Q, 3);
+        ring_base += sc.items(ST_Q);
+
+        // ---------------- A: attention split
+        stamp(l, ST_A, 0);
+        wait_flags(FL_Q, p, tag);
+        bar();
+        stamp(l, ST_A, 1);
+        {
+            bf16* q_l = (bf16*)scr;                                   // [QRMAX][LDQ]
+            bf16* kb_l = (bf16*)(scr + QL_BYTES);                      // [32][LDQ]
+            bf16* vb_l = (bf16*)(scr + QL_BYTES + KL_BYTES);           // [32][HD]
+            float* pbuf = (float*)(scr + QL_BYTES + KL_BYTES + VL_BYTES);   // [4][16][PB]
+            const bool blk = r == NRANK - 1;
+            const size_t qb = wm.qkv + ((size_t)p * NGRP + g) * MW * GQKV * 4;
+            typedef RowPrep<bf16, HD> RP;
+            static_assert(RP::NP == 4, "row segments are 4 floats");
+            auto ld4 = [&](size_t off) -> typename RP::fv {
+                return __builtin_bit_cast(typename RP::fv, __builtin_amdgcn_raw_buffer_load_b128(rws, (unsigned)off, 0, SC1));
+            };
+            // prep rows: query rows q < QR (head q / M, block row q % M), then
+            // (block split) the key / value rows j < M, padded to the key block
+            const int nkrow = blk ? ((M + 15) / 16) * 16 : 0;
+            const int nrow = QR + nkrow;
+            Gains<bf16, HD> gq, gk;
+            if (a.qk_norm) {
+                gq.load(pk + a.off_q_norm + lay, lrow);
+                gk.load(pk + a.off_k_norm + lay, lrow);
+            }
+            float gql[RP::NP], gqh[RP::NP], gkl[RP::NP], gkh[RP::NP];
+            gq.get(a.qk_norm, gql, gqh);
+            gk.get(a.qk_norm, gkl, gkh);
+            // 16 lanes per row; lane group tg (of NG16) takes query rows tg +
+            // NG16 k and (block split) key/value rows tg + NG16 k; every load
+            // is issued first
+            constexpr int NG16 = NWC * WAVE / 16;
+            constexpr int NQR = (QRMAX + NG16 - 1) / NG16, NKR = (32 + NG16 - 1) / NG16;
+            const int tg = tid / 16;
+            typename RP::fv ql[NQR], qh[NQR];
+            typename RP::fv2 qc[NQR];
+#pragma unroll
+            for (int k = 0; k < NQR; ++k) {
+                const int rc = min(tg + NG16 * k, QR - 1);
+                const int hl = rc / M, j = rc % M;
+                ql[k] = ld4(qb + ((size_t)j * GQKV + hl * HD + RP::NP * lrow) * 4);
+                qh[k] = ld4(qb + ((size_t)j * GQKV + hl * HD + RP::HALF + RP::NP * lrow) * 4);
+                qc[k] = *(const typename RP::fv2*)((const float2*)rope + (size_t)(t + j) * RP::HALF + RP::NP * lrow);
+            }
+            typename RP::fv kl[NKR], kh[NKR], vl[NKR], vh[NKR];
+            typename RP::fv2 kc[NKR];
+            if (blk) {
+#pragma unroll
+                for (int k = 0; k < NKR; ++k) {
+                    const int jk = min(tg + NG16 * k, M - 1);
+                    const size_t rb = qb + (size_t)jk * GQKV * 4;
+                    kl[k] = ld4(rb + (2 * HD + RP::NP * lrow) * 4);
+                    kh[k] = ld4(rb + (2 * HD + RP::HALF + RP::NP * lrow) * 4);
+                    vl[k] = ld4(rb + (3 * HD + RP::NP * lrow) * 4);
+                    vh[k] = ld4(rb + (3 * HD + RP::HALF + RP::NP * lrow) * 4);
+                    kc[k] = *(const typename RP::fv2*)((const float2*)rope + (size_t)(t + jk) * RP::HALF + RP::NP * lrow);
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < NQR; ++k) {
+                const int row = tg + NG16 * k;
+                if (row < QR) {
+                    RP rp;
+                    bf16 lo[RP::NP], hi[RP::NP];
+                    rp.lo = ql[k];
+                    rp.hi = qh[k];
+                    rp.cs = qc[k];
+                    rp.finish(q_l + row * LDQ, true, gql, gqh, a.qk_norm, a.eps, lrow, lo, hi);
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < NKR; ++k) {
+                const int j = tg + NG16 * k;
+                if (!blk || j >= nkrow) continue;
+                const bool live = j < M;
+                RP rp;
+                bf16 lo[RP::NP], hi[RP::NP];
+                rp.lo = kl[k];
+                rp.hi = kh[k];
+                rp.cs = kc[k];
+                rp.finish(kb_l + j * LDQ, live, gkl, gkh, a.qk_norm, a.eps, lrow, lo, hi);
+                bf16 v0[RP::NP], v1[RP::NP];
+#pragma unroll
+                for (int pp = 0; pp < RP::NP; ++pp) {
+                    v0[pp] = (bf16)(live ? vl[k][pp] : 0.f);
+                    v1[pp] = (bf16)(live ? vh[k][pp] : 0.f);
+                    vb_l[j * HD + RP::NP * lrow + pp] = v0[pp];
+                    vb_l[j * HD + RP::HALF + RP::NP * lrow + pp] = v1[pp];
+                }
+                if (live && j < a.kv_rows) {
+                    // verify: append the block K/V to the cache at t + j
+                    const int pos = t + j;
+                    const size_t head = (((size_t)l * a.Bmax) * NKV + g) * (size_t)a.nblk * 16 * HD;
+                    bf16* kblk = (bf16*)a.kcache + head + (size_t)(pos / 16) * 16 * HD;
+                    bf16* vblk = (bf16*)a.vcache + head + (size_t)(pos / 16) * 16 * HD;
+#pragma unroll
+                    for (int pp = 0; pp < RP::NP; ++pp) {
+                        const int i0 = RP::NP * lrow + pp;
+                        kblk[kblock_elem<bf16>(pos % 16, i0)] = lo[pp];
+                        kblk[kblock_elem<bf16>(pos % 16, i0 + RP::HALF)] = hi[pp];
+                        vblk[vblock_elem(pos % 16, i0)] = v0[pp];
+                        vblk[vblock_elem(pos % 16, i0 + RP::HALF)] = v1[pp];
+                    }
+                }
+            }
+            bar();
+            // key loop: wave w < 2 QT takes query tile w % QT and half w / QT of the blocks
+            const int nb = blk ? (M + 15) / 16 : sc.kb_count();
+            const int kb0 = sc.kb_begin();
+            const int nparts = 2 * QT <= NWC ? 2 : 1;      // waves per query tile (key halves)
+            const bool act = wid < nparts * QT;
+            const int qt = wid % QT, half = wid / QT;
+            const int hb = nparts == 2 ? (nb + 1) / 2 : nb;
+            const int b_lo = half == 0 ? 0 : hb, b_hi = half == 0 ? hb : nb;
+            f32x4 o_acc[HD / 16];
+#pragma unroll
+            for (int dt = 0; dt < HD / 16; ++dt) o_acc[dt] = f32x4{0, 0, 0, 0};
+            float m_run = -1e30f, l_run = 0.f;
+            const int qcol = qt * 16 + lrow;                  // query row of this lane's column
+            const int jq = qcol < QR ? qcol % M : 0;
+            if (act) {
+                uint4 qf[HD / 32];
+#pragma unroll
+                for (int ds = 0; ds < HD / 32; ++ds) qf[ds] = *(const uint4*)(q_l + (qt * 16 + lrow) * LDQ + ds * 32 + lgrp * 8);
+                bool first = true;
+                for (int bi = b_lo; bi < b_hi; ++bi) {
+                    uint4 kf[HD / 32];
+                    uint2 vf[HD / 16];
+                    if (blk) {
+#pragma unroll
+                        for (int ds = 0; ds < HD / 32; ++ds)
+                            kf[ds] = *(const uint4*)(kb_l + (bi * 16 + lrow) * LDQ + ds * 32 + lgrp * 8);
+#pragma unroll
+                        for (int dt = 0; dt < HD / 16; ++dt) {
+                            bf16 tmp[4];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) tmp[e] = vb_l[(bi * 16 + lgrp * 4 + e) * HD + dt * 16 + lrow];
+                            __builtin_memcpy(&vf[dt], tmp, 8);
+                        }
+                    } else {
+#pragma unroll
+                        for (int ds = 0; ds < HD / 32; ++ds) kf[ds] = ring_frag(bi * 8 + ds);
+#pragma unroll
+                        for (int dt = 0; dt < HD / 16; ++dt)
+                            vf[dt] = *(const uint2*)(ring + (size_t)((ring_base + bi * 8 + 4 + dt / 2) % NSLOT) * 1024 +
+                                                     (dt % 2) * 512 + lane * 8);
+                    }
+                    f32x4 s = f32x4{0, 0, 0, 0};
+#pragma unroll
+                    for (int ds = 0; ds < HD / 32; ++ds) mma_frag<bf16>(s, kf[ds], qf[ds]);
+                    float sv[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int kk = bi * 16 + lgrp * 4 + e;
+                        bool ok;
+                        if (blk) ok = kk < M && (kk <= jq || jq >= a.full_from);
+                        else ok = (kb0 * 16 + kk) < t;
+                        ok = ok && qcol < QR;
+                        sv[e] = ok ? s[e] * a.scale_log2 : -INFINITY;
+                    }
+                    float mloc = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+                    mloc = xrow_max(mloc);
+                    const float m_new = fmaxf(m_run, mloc);
+                    if (!first) {
+                        const float corr = exp2f(m_run - m_new);
+                        l_run *= corr;
+#pragma unroll
+                        for (int dt = 0; dt < HD / 16; ++dt) o_acc[dt] *= corr;
+                    }
+                    first = false;
+                    m_run = m_new;
+                    f32x4 pr;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        pr[e] = exp2f(sv[e] - m_run);
+                        l_run += pr[e];
+                    }
+#pragma unroll
+                    for (int dt = 0; dt < HD / 16; ++dt) mma_k4(o_acc[dt], vf[dt], pr);
+                }
+                l_run = xrow_sum(l_run);
+                if (half == 1) {
+                    float* pb = pbuf + (size_t)(qt * 16 + lrow) * PB;
+                    if (lgrp == 0) { pb[HD] = m_run; pb[HD + 1] = l_run; }
+#pragma unroll
+                    for (int dt = 0; dt < HD / 16; ++dt) *(f32x4*)(pb + dt * 16 + lgrp * 4) = o_acc[dt];
+                }
+            }
+            bar();
+            if (act && half == 0) {
+                // merge with the other half (if it had blocks) in place of the pair buffer
+                float* pb = pbuf + (size_t)(qt * 16 + lrow) * PB;
+                float m1 = -1e30f, l1 = 0.f;
+                const bool other = b_hi < nb;
+                if (other) { m1 = pb[HD]; l1 = pb[HD + 1]; }
+                const float mx = fmaxf(m_run, m1);
+                const float f0 = exp2f(m_run - mx), f1 = other ? exp2f(m1 - mx) : 0.f;
+#pragma unroll
+                for (int dt = 0; dt < HD / 16; ++dt) {
+                    f32x4 o1 = other ? *(const f32x4*)(pb + dt * 16 + lgrp * 4) : f32x4{0, 0, 0, 0};
+                    o_acc[dt] = o_acc[dt] * f0 + o1 * f1;
+                }
+                const float ltot = l_run * f0 + l1 * f1;
+                // a column with no visible key keeps max -inf and sum 0
+                const bool any = ltot > 0.f;
+#pragma unroll
+                for (int dt = 0; dt < HD / 16; ++dt) *(f32x4*)(pb + dt * 16 + lgrp * 4) = o_acc[dt];
+                if (lgrp == 0) { pb[HD] = any ? mx : -INFINITY; pb[HD + 1] = any ? ltot : 0.f; }
+            }
+            bar();
+            if (wid == 0) {
+                // partial of split r for every query row: (m, l, o[128])
+                const size_t ab0 = wm.apart + ((((size_t)p * NGRP + g) * NRANK + r) * QRMAX) * APW * 4;
+                const bool has = nb > 0;
+                for (int i = lane; i < QR * (HD / 4 + 1); i += WAVE) {
+                    const int q = i / (HD / 4 + 1), c4 = i % (HD / 4 + 1);
+                    const float* pb = pbuf + (size_t)q * PB;
+                    f32x4 v;
+                    if (c4 < HD / 4) v = has ? *(const f32x4*)(pb + c4 * 4) : f32x4{0, 0, 0, 0};
+                    else v = f32x4{has ? pb[HD] : -INFINITY, has ? pb[HD + 1] : 0.f, 0.f, 0.f};
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rws,
+                        (unsigned)(ab0 + ((size_t)q * APW + (c4 < HD / 4 ? 4 + c4 * 4 : 0)) * 4), 0, 0);
+                }
+                set_flag(FL_A, p, tag);
+            }
+        }
+        stamp(l, ST_A, 3);
+        ring_base += sc.items(ST_A);
+
+        // ---------------- M: merge the 32 split partials of query rows r, r + 32
+        stamp(l, ST_M, 0);
+        wait_flags(FL_A, p, tag);
+        bar();
+        stamp(l, ST_M, 1);
+        if (wid < 2) {
+            const int q = r + 32 * wid;
+            if (q < QR) {
+                const size_t ab = wm.apart + (((size_t)p * NGRP + g) * NRANK) * QRMAX * APW * 4;
+                // lane s < 32 holds split s's (m, l); weights formed there and
+                // broadcast one split at a time (fixed split order)
+                float mls = -INFINITY, lls = 0.f;
+                if (lane < NRANK) {
+                    const unsigned off = (unsigned)(ab + (((size_t)lane * QRMAX + q) * APW) * 4);
+                    mls = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rws, off, 0, SC1));
+                    lls = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rws, off + 4, 0, SC1));
+                }
+                const float mx = wave_max(mls);
+                const float wl = (mls > -INFINITY) ? exp2f(mls - mx) : 0.f;
+                float o0 = 0.f, o1 = 0.f, Ls = 0.f;
+                for (int s0 = 0; s0 < NRANK; s0 += 16) {
+                    uint2 ov[16];
+                    float w8[16];
+#pragma unroll
+                    for (int k = 0; k < 16; ++k) {
+                        w8[k] = __shfl(wl, s0 + k, 64);
+                        const unsigned off = (unsigned)(ab + (((size_t)(s0 + k) * QRMAX + q) * APW + 4 + 2 * lane) * 4);
+                        ov[k] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws, off, 0, SC1));
+                    }
+#pragma unroll
+                    for (int k = 0; k < 16; ++k) {
+                        o0 += w8[k] * __uint_as_float(ov[k].x);
+                        o1 += w8[k] * __uint_as_float(ov[k].y);
+                        Ls += w8[k] * __shfl(lls, s0 + k, 64);
+                    }
+                }
+                const float inv = Ls > 0.f ? 1.f / Ls : 0.f;
+                const int hl = q / M, j = q % M;
+                const size_t ob = wm.oop + ((size_t)p * NGRP + g) * MW * GO * 4;
+                const uint2 st2 = make_uint2(__float_as_uint(o0 * inv), __float_as_uint(o1 * inv));
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{st2.x, st2.y}, rws,
+                    (unsigned)(ob + ((size_t)j * GO + hl * HD + 2 * lane) * 4), 0, 0);
+            }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+        bar();
+        if (wid == 0 && lane == 0) set_flag(FL_M, p, tag);
+
+        // ---------------- O: O-projection partial over the group's heads
+        stamp(l, ST_O, 0);
+        wait_flags(FL_M, p, tag);
+        bar();
+        stamp(l, ST_O, 1);
+        {
+            const size_t ob = wm.oop + ((size_t)p * NGRP + g) * MW * GO * 4;
+            // tile tt = wid / 3; fragments f = wid % 3 + 3 j of the group's 8
+            const int tt = wid / 3, f0 = wid % 3;
+            f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
+            f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
+            const uint4* la = (const uint4*)(pk + a.off_la[3] + lay);
+            f32x4 xv[3][2][2];
+            uint4 av[3];
+#pragma unroll
+            for (int j = 0; j < 3; ++j) {
+                const int f = min(f0 + 3 * j, 7);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) opnd_load(ob, GO, f, mt, xv[j][mt][0], xv[j][mt][1]);
+                if (LORA) av[j] = la[(size_t)(8 * g + f) * WAVE + lane];
+            }
+#pragma unroll
+            for (int j = 0; j < 3; ++j) {
+                if (f0 + 3 * j >= 8) continue;
+                const uint4 w = ring_frag(tt * 8 + f0 + 3 * j);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) {
+                    if (mt >= MT) continue;
+                    uint4 xh, xl;
+                    opnd_make(xv[j][mt][0], xv[j][mt][1], mt, xh, xl);
+                    mma_frag<bf16>(acc[mt], w, xh);
+                    mma_frag<bf16>(acc[mt], w, xl);
+                    if (LORA) {
+                        mma_frag<bf16>(uacc[mt], av[j], xh);
+                        mma_frag<bf16>(uacc[mt], av[j], xl);
+                    }
+                }
+            }
+            if (LORA) {
+                uint2 bv;
+                __builtin_memcpy(&bv, (const bf16*)(pk + a.off_lb_o + lay) + ((size_t)(2 * r + tt) * WAVE + lane) * 4, 8);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bv, uacc[mt] * a.scale);
+            }
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt) s_red[((tt * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
+        }
+        stamp(l, ST_O, 2);
+        bar();
+        if (wid == 0) {
+            // partial [M][32 columns] with tags, written through to memory
+            const size_t pb = wm.parto + (((size_t)p * NGRP + g) * MW) * H * 8;
+            for (int i = lane; i < 16 * M; i += WAVE) {
+                const int m = i / 16, c2 = (i % 16) * 2;            // columns c2, c2 + 1 of the rank's 32
+                const int tt = c2 / 16, n = c2 % 16;
+                const float v0 = red_val(tt, tt * 3, 3, n, m);
+                const float v1 = red_val(tt, tt * 3, 3, n + 1, m);
+                const u32x4 pr = {__float_as_uint(v0), tag, __float_as_uint(v1), tag};
+                __builtin_amdgcn_raw_buffer_store_b128(pr, rws,
+                    (unsigned)(pb + ((size_t)m * H + 32 * r + c2) * 8), 0, SC1);
+            }
+        }
+        ring_base += sc.items(ST_O);
+
+        // ---------------- R2: residual from the O partials, MLP-norm operand
+        stamp(l, ST_R2, 0);
+        wait_partials(true, l);
+        bar();
+        stamp(l, ST_R2, 1);
+        stage_reduce(l, true, pk + a.off_mlp_norm + lay, wm.xm, wm.sqm, false);
+        bar();
+        if (wid == 0 && lane == 0) set_flag(FL_R2, p, tag);
+
+        // ---------------- GU: gate/up tiles + SwiGLU
+        stamp(l, ST_GU, 0);
+        wait_flags(FL_R2, p, tag);
+        bar();
+        stamp(l, ST_GU, 1);
+        load_rm(wm.sqm, p);
+        {
+            const size_t xb = wm.xm + ((size_t)p * NGRP + g) * MW * H * 4;
+            f32x4 acc[2][2] = {{f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}, {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}};
+            f32x4 ug[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}, uu[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
+            const uint4* lag = (const uint4*)(pk + a.off_la[4] + lay);
+            const uint4* lau = (const uint4*)(pk + a.off_la[5] + lay);
+            const bool mine2 = ((lrow / 4) & 1) == (r & 1);
+            f32x4 xv[FPW][2][2];
+            uint4 ag[FPW], au[FPW];
+#pragma unroll
+            for (int j = 0; j < FPW; ++j) {
+                const int f = min(wid + NWC * j, KBH - 1);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) opnd_load(xb, H, f, mt, xv[j][mt][0], xv[j][mt][1]);
+                if (LORA) {
+                    ag[j] = lag[(size_t)f * WAVE + lane];
+                    au[j] = lau[(size_t)f * WAVE + lane];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < FPW; ++j) {
+                const int f = wid + NWC * j;
+                if (f >= KBH) continue;
+                const uint4 w1 = ring_frag(f);
+                uint4 w2 = ring_frag(KBH + f);
+                if (!mine2) w2 = uint4{0, 0, 0, 0};
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) {
+                    if (mt >= MT) continue;
+                    uint4 xh, xl;
+                    opnd_make(xv[j][mt][0], xv[j][mt][1], mt, xh, xl);
+                    mma_frag<bf16>(acc[0][mt], w1, xh);
+                    mma_frag<bf16>(acc[0][mt], w1, xl);
+                    mma_frag<bf16>(acc[1][mt], w2, xh);
+                    mma_frag<bf16>(acc[1][mt], w2, xl);
+                    if (LORA) {
+                        mma_frag<bf16>(ug[mt], ag[j], xh);
+                        mma_frag<bf16>(ug[mt], ag[j], xl);
+                        mma_frag<bf16>(uu[mt], au[j], xh);
+                        mma_frag<bf16>(uu[mt], au[j], xl);
+                    }
+                }
+            }
+            if (LORA) {
+#pragma unroll
+                for (int tt = 0; tt < 2; ++tt) {
+                    const int tile = tt == 0 ? sc.gu_t1() : sc.gu_t2();
+                    uint2 bv;
+                    __builtin_memcpy(&bv, (const bf16*)(pk + a.off_lb_gu + lay) + ((size_t)tile * WAVE + lane) * 4, 8);
+                    // rows 0-7 take the gate shrink, rows 8-15 the up shrink
+                    const uint2 bg = lrow < 8 ? bv : uint2{0, 0};
+                    const uint2 bu = lrow < 8 ? uint2{0, 0} : bv;
+#pragma unroll
+                    for (int mt = 0; mt < 2; ++mt) {
+                        if (mt >= MT) continue;
+                        mma_k4s(acc[tt][mt], bg, ug[mt] * a.scale);
+                        mma_k4s(acc[tt][mt], bu, uu[mt] * a.scale);
+                    }
+                }
+            }
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) s_red[((tt * NWC + wid) * 2 + mt) * WAVE + lane] = acc[tt][mt];
+        }
+        stamp(l, ST_GU, 2);
+        bar();
+        if (wid == 0) {
+            // h for the rank's 12 FFN columns: 8 from the full tile, 4 from the half tile
+            const size_t hb = wm.hop + ((size_t)p * NGRP + g) * MW * GF * 4;
+            for (int i = lane; i < 12 * M; i += WAVE) {
+                const int m = i / 12, c = i % 12;
+                int tt, gr, col;
+                if (c < 8) { tt = 0; gr = c; col = 8 * r + c; }
+                else { tt = 1; gr = 4 * (r & 1) + (c - 8); col = 256 + 4 * r + (c - 8); }
+                const float rm = s_rm[m];
+                const float gt = red_val(tt, 0, NWC, gr, m) * rm;
+                const float up = red_val(tt, 0, NWC, gr + 8, m) * rm;
+                const float hv = gt / (1.f + __expf(-gt)) * up;
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(hv), rws,
+                    (unsigned)(hb + ((size_t)m * GF + col) * 4), 0, 0);
+            }
+            set_flag(FL_GU, p, tag);
+        }
+        stamp(l, ST_GU, 3);
+        ring_base += sc.items(ST_GU);
+
+        // ---------------- D: down-projection partial over the group's FFN slice
+        stamp(l, ST_D, 0);
+        wait_flags(FL_GU, p, tag);
+        bar();
+        stamp(l, ST_D, 1);
+        {
+            const size_t hb = wm.hop + ((size_t)p * NGRP + g) * MW * GF * 4;
+            // tile tt = wid / 3; fragments f = wid % 3 + 3 j of the group's 12
+            const int tt = wid / 3, f0 = wid % 3;
+            f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
+            f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
+            const uint4* la = (const uint4*)(pk + a.off_la[6] + lay);
+            f32x4 xv[4][2][2];
+            uint4 av[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int f = f0 + 3 * j;
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) opnd_load(hb, GF, f, mt, xv[j][mt][0], xv[j][mt][1]);
+                if (LORA) av[j] = la[(size_t)(12 * g + f) * WAVE + lane];
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint4 w = ring_frag(tt * 12 + f0 + 3 * j);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) {
+                    if (mt >= MT) continue;
+                    uint4 xh, xl;
+                    opnd_make(xv[j][mt][0], xv[j][mt][1], mt, xh, xl);
+                    mma_frag<bf16>(acc[mt], w, xh);
+                    mma_frag<bf16>(acc[mt], w, xl);
+                    if (LORA) {
+                        mma_frag<bf16>(uacc[mt], av[j], xh);
+                        mma_frag<bf16>(uacc[mt], av[j], xl);
+                    }
+                }
+            }
+            if (LORA) {
+                uint2 bv;
+                __builtin_memcpy(&bv, (const bf16*)(pk + a.off_lb_d + lay) + ((size_t)(2 * r + tt) * WAVE + lane) * 4, 8);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bv, uacc[mt] * a.scale);
+            }
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt) s_red[((tt * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
+        }
+        bar();
+        if (wid == 0) {
+            const size_t pb = wm.partd + (((size_t)p * NGRP + g) * MW) * H * 8;
+            for (int i = lane; i < 16 * M; i += WAVE) {
+                const int m = i / 16, c2 = (i % 16) * 2;
+                const int tt = c2 / 16, n = c2 % 16;
+                const float v0 = red_val(tt, tt * 3, 3, n, m);
+                const float v1 = red_val(tt, tt * 3, 3, n + 1, m);
+                const u32x4 pr = {__float_as_uint(v0), tag, __float_as_uint(v1), tag};
+                __builtin_amdgcn_raw_buffer_store_b128(pr, rws,
+                    (unsigned)(pb + ((size_t)m * H + 32 * r + c2) * 8), 0, SC1);
+            }
+        }
+        ring_base += sc.items(ST_D);
+    }
+    // final RMSNorm operand of the LM head (group 0 writes it)
+    stamp(L, 0, 0);
+    if (g == 0) stage_reduce(L, false, a.final_norm, 0, 0, true);
+    stamp(L, 0, 1);
+}
+
+}  // namespace fz
+
+size_t fused_ws_bytes() { return fz::ws_map().total; }
+size_t fused_ctl_offset() { return fz::ws_map().ctl; }
+size_t fused_trace_offset() { return fz::ws_map().trace; }
+int fused_trace_entries() { return fz::NGRP * fz::NRANK * fz::TRACE_LAYERS * fz::NSTAGE * 4; }
+size_t fused_lds_bytes() { return fz::LDS_BYTES; }
+int fused_threads() { return fz::NTHR; }
+
+hipError_t fused_occupancy(int* blocks_per_cu) {
+    hipError_t e = hipFuncSetAttribute((const void*)fz::k_fused<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)fz::LDS_BYTES);
+    if (e != hipSuccess) return e;
+    e = hipFuncSetAttribute((const void*)fz::k_fused<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)fz::LDS_BYTES);
+    if (e != hipSuccess) return e;
+    int a = 0, b = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&a, fz::k_fused<false>, fz::NTHR, fz::LDS_BYTES);
+    if (e != hipSuccess) return e;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, fz::k_fused<true>, fz::NTHR, fz::LDS_BYTES);
+    if (e != hipSuccess) return e;
+    *blocks_per_cu = a < b ? a : b;
+    return hipSuccess;
+}
+
+hipError_t launch_fused(const FusedArgs& a, bool lora, hipStream_t st) {
+    if (a.M < 1 || a.M > FUSED_MAX_ROWS || a.L < 1 || a.L > 255) return hipErrorInvalidValue;
+    static bool attr_set[2] = {false, false};
+    auto kern = lora ? (const void*)fz::k_fused<true> : (const void*)fz::k_fused<false>;
+    if (!attr_set[lora ? 1 : 0]) {
+        hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fz::LDS_BYTES);
+        if (e != hipSuccess) return e;
+        attr_set[lora ? 1 : 0] = true;
+    }
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    get_launch_events(&e0, &e1);
+    if (e0) {
+        if (lora) hipExtLaunchKernelGGL((fz::k_fused<true>), dim3(256), dim3(fz::NTHR), fz::LDS_BYTES, st, e0, e1, 0, a);
+        else hipExtLaunchKernelGGL((fz::k_fused<false>), dim3(256), dim3(fz::NTHR), fz::LDS_BYTES, st, e0, e1, 0, a);
+    } else {
+        if (lora) hipLaunchKernelGGL((fz::k_fused<true>), dim3(256), dim3(fz::NTHR), fz::LDS_BYTES, st, a);
+        else hipLaunchKernelGGL((fz::k_fused<false>), dim3(256), dim3(fz::NTHR), fz::LDS_BYTES, st, a);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace pbd

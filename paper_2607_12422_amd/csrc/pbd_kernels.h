@@ -41,6 +41,7 @@ struct AssembleArgs {
     void* op_hi;           // first QKV operand x*g (fragments) and its bf16 residual
     void* op_lo;
     float* sq;             // [1][m_stride] per-row sum of squares
+    unsigned* fused_ctl;   // persistent pass next: its rank tickets and abort word are cleared and its epoch advanced (null: none)
 };
 
 struct FGemmArgs {
@@ -294,6 +295,7 @@ hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st
 hipError_t launch_fill_u32(void* p, size_t n_words, uint32_t v, hipStream_t st);
 // profiling: events that the next launch records its start and end into (null: none)
 void set_launch_events(hipEvent_t start, hipEvent_t stop);
+void get_launch_events(hipEvent_t* start, hipEvent_t* stop);
 size_t attn_smem_main(int dtype, int head_dim, int qt);
 size_t attn_smem_bytes(int dtype, int head_dim, int qt);
 

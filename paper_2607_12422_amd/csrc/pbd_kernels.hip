@@ -35,6 +35,10 @@ void set_launch_events(hipEvent_t start, hipEvent_t stop) {
     g_ev_start = start;
     g_ev_stop = stop;
 }
+void get_launch_events(hipEvent_t* start, hipEvent_t* stop) {
+    *start = g_ev_start;
+    *stop = g_ev_stop;
+}
 #define PBD_LAUNCH(KERNEL, GRID, BLOCK, SHMEM, ST, ...)                                              \
     do {                                                                                            \
         if (g_ev_start)                                                                             \
@@ -110,6 +114,12 @@ __global__ __launch_bounds__(256) void k_assemble(AssembleArgs a) {
     else tok = a.drafts[b * nd + j - a.lead];
     const bool bad_tok = tok < 0 || tok >= a.vocab;
     if (bad_tok) tok = 0;
+    if (threadIdx.x == 0 && a.fused_ctl && j == 0 && b == 0) {
+        // the persistent pass that follows reads these when it starts
+        for (int i = 0; i < 8; ++i) a.fused_ctl[i] = 0u;
+        a.fused_ctl[8] += 1u;
+        a.fused_ctl[9] = 0u;
+    }
     if (threadIdx.x == 0) {
         if (j == 0) {
             a.pos0[b] = pos0;
@@ -531,66 +541,6 @@ __global__ __launch_bounds__(FG<EPI>::NW * 64, FG<EPI>::MINB) void k_fgemm(FGemm
 // O^T += V^T P^T takes P^T directly from the score accumulators.  The four
 // waves take key blocks round-robin and merge in LDS at the end.
 // ---------------------------------------------------------------------------
-
-// Per-head RMSNorm and rotate-half RoPE of one row held by 16 lanes: lane l16
-// owns the NP pairs (i, i + HD/2) for i in [NP*l16, NP*l16 + NP), so the
-// rotation stays in the lane and the norm is a 16-lane DPP reduction.
-template <typename T, int HD>
-struct RowPrep {
-    static constexpr int HALF = HD / 2;
-    static constexpr int NP = HALF / 16;       // pairs per lane (4 or 2)
-    typedef float __attribute__((ext_vector_type(NP))) fv;
-    typedef float __attribute__((ext_vector_type(2 * NP))) fv2;
-    fv lo, hi;
-    fv2 cs;                                    // (cos, sin) of the NP pairs
-    // vector loads from always-valid addresses; dead rows are zeroed in finish
-    __device__ void load(const float* src, const float2* rope_row, int l16) {
-        lo = *(const fv*)(src + NP * l16);
-        hi = *(const fv*)(src + HALF + NP * l16);
-        cs = *(const fv2*)(rope_row + NP * l16);
-    }
-    // normalise with this lane's gains and rotate; writes the row into dst[HD]
-    // as T and returns the lane's values
-    __device__ void finish(T* dst, bool live, const float* g_lo, const float* g_hi, bool qk_norm, float eps, int l16,
-                           T* out_lo, T* out_hi) {
-        float inv = live ? 1.f : 0.f;
-        if (qk_norm) {
-            float ss = 0.f;
-#pragma unroll
-            for (int p = 0; p < NP; ++p) ss += lo[p] * lo[p] + hi[p] * hi[p];
-            inv = live ? rsqrtf(row16_sum(ss) / (float)HD + eps) : 0.f;
-        }
-#pragma unroll
-        for (int p = 0; p < NP; ++p) {
-            const int i = NP * l16 + p;
-            const float y0 = lo[p] * inv * g_lo[p], y1 = hi[p] * inv * g_hi[p];
-            const float c = cs[2 * p], sn = cs[2 * p + 1];
-            out_lo[p] = from_f32<T>(y0 * c - y1 * sn);
-            out_hi[p] = from_f32<T>(y1 * c + y0 * sn);
-            dst[i] = out_lo[p];
-            dst[i + HALF] = out_hi[p];
-        }
-    }
-};
-
-// this lane's RMSNorm gains: raw loads now, conversion at first use
-template <typename T, int HD>
-struct Gains {
-    static constexpr int NP = RowPrep<T, HD>::NP, HALF = HD / 2;
-    typedef T __attribute__((ext_vector_type(NP))) tv;
-    tv rlo, rhi;
-    __device__ void load(const void* gain, int l16) {
-        rlo = *(const tv*)((const T*)gain + NP * l16);
-        rhi = *(const tv*)((const T*)gain + HALF + NP * l16);
-    }
-    __device__ void get(bool qk_norm, float* g_lo, float* g_hi) const {
-#pragma unroll
-        for (int p = 0; p < NP; ++p) {
-            g_lo[p] = qk_norm ? to_f32(rlo[p]) : 1.f;
-            g_hi[p] = qk_norm ? to_f32(rhi[p]) : 1.f;
-        }
-    }
-};
 
 // Prefill chunk: per-head RMSNorm and RoPE of the chunk's keys, appended to
 // the cache with the values before the chunk's attention reads them.  One

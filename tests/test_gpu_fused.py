@@ -1,0 +1,197 @@
+"""GPU parity of the persistent batch-1 pass (one launch for the layer stack).
+
+Batch-1 draft and verify passes of the Qwen3-0.6B layer shape run their 28
+(here: 2 or 3) layers as one persistent kernel.  These tests run it through
+the C ABI on a model of that layer shape with few layers and a 4096-token
+vocabulary, so that the float64 oracle finishes in seconds, and check:
+  * that the persistent kernel is the one that ran in pass mode 0 (its
+    kernel class is timed) and that pass mode 1 (one kernel per operator,
+    the default) does not use it;
+  * draft and verify logits against the oracle within 2e-2, token ids equal
+    at decisive rows, for several block widths (the query rows of a KV head
+    span one to four 16-row tiles) and prefix lengths (attention splits of
+    zero to several key blocks);
+  * the verify's cache rows, through a loop of forced-acceptance rounds in
+    which every draft reads the rows earlier verifies appended;
+  * the early-exit draft (first k layers);
+  * with the adapter off and the causal mask, draft = verify bitwise;
+  * the bounded wait: a forced expiry raises PBD_STATUS_TIMEOUT, the kernel
+    finishes, and the next pass is correct again.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import model as om
+
+from gpu_harness import GpuRun, decisive
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+def _cfg(D=16, layers=2, **kw):
+    return synth.QWEN3_0_6B.with_(n_layers=layers, vocab=4096, block=D, **kw)
+
+
+def _oracle_prefill(m, prompt, gpu_anchor):
+    cfg = m.cfg
+    empty = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim)) for _ in range(cfg.n_layers)]
+    lg, k, v = m.forward_block(prompt, 0, empty, empty, causal=True, adapter_on=False,
+                               logit_rows=[len(prompt) - 1])
+    if decisive(lg, TOL)[0]:
+        assert int(np.argmax(lg[0])) == int(gpu_anchor)
+    return om.SeqState(k, v, int(gpu_anchor), tokens=list(prompt) + [int(gpu_anchor)],
+                       generated=[int(gpu_anchor)])
+
+
+def _check(gpu_logits, gpu_tokens, ref_logits, rows, exclude=None, what=""):
+    err = float(np.abs(gpu_logits - ref_logits).max())
+    print(f"{what}: max-abs {err:.4f}")
+    assert err <= TOL, (what, err)
+    lg = ref_logits[rows].copy()
+    dec = decisive(lg, TOL, exclude)
+    if exclude is not None:
+        lg[:, exclude] = -np.inf
+    ref = np.argmax(lg, axis=-1)
+    assert np.all(gpu_tokens[dec] == ref[dec]), (what, gpu_tokens, ref, dec)
+
+
+def _fused_launches(g, fn):
+    from paper_2607_12422_amd import binding as bd
+    g.eng.pbd_profile_enable(True)
+    out = fn()
+    g.torch.cuda.synchronize()
+    _, n = g.eng.pbd_profile_read(bd.KCLASSES.index("fused"))
+    g.eng.pbd_profile_enable(False)
+    return out, n
+
+
+@pytest.mark.parametrize("D,t", [(16, 100), (16, 1000), (8, 37), (31, 260), (0, 50)])
+def test_fused_step_matches_oracle(D, t):
+    cfg = _cfg(D)
+    w = synth.make_weights(cfg, 6000 + D + t)
+    prompt = synth.make_prompts(cfg, [t], 6100 + t)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=t + 3 * cfg.width)
+    g.eng.pbd_set_pass_mode(0)
+    anchor = g.prefill([prompt])
+    if D > 0:
+        (d, dlg), nd = _fused_launches(g, g.draft)
+    else:
+        d, nd = g.zeros(1, 1), 1            # D = 0: the verify of [anchor] alone (a greedy decode step)
+    (v, vlg), nv = _fused_launches(g, lambda: g.verify(d))
+    assert nd == 1 and nv == 1, (nd, nv)
+    assert g.status() == 0
+    m = om.OracleModel(w)
+    st = _oracle_prefill(m, prompt, anchor[0])
+    if D > 0:
+        _, dl_ref = om.draft(m, st)
+        _check(dlg.cpu().numpy()[0], d.cpu().numpy()[0], dl_ref, slice(1, None), exclude=cfg.mask_id,
+               what=f"D={D} t={t} draft")
+    _, vl_ref, _, _ = om.verify(m, st, d.cpu().numpy()[0][:D])
+    _check(vlg.cpu().numpy()[0], v.cpu().numpy()[0], vl_ref, slice(None), what=f"D={D} t={t} verify")
+    g.close()
+
+
+def test_per_operator_mode_does_not_use_the_persistent_kernel():
+    cfg = _cfg()
+    w = synth.make_weights(cfg, 6200)
+    prompt = synth.make_prompts(cfg, [90], 6201)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=200)
+    g.eng.pbd_set_pass_mode(0)
+    g.prefill([prompt])
+    (d0, dlg0), n0 = _fused_launches(g, g.draft)
+    g.eng.pbd_set_pass_mode(1)
+    (d1, dlg1), n1 = _fused_launches(g, g.draft)
+    assert n0 == 1 and n1 == 0
+    err = float((dlg0 - dlg1).abs().max())
+    print(f"persistent vs per-operator draft logits: max-abs {err:.2e}")
+    assert err <= TOL
+    g.close()
+
+
+def test_fused_forced_loop_follows_oracle():
+    """Three layers, prefix 70, eight rounds with forced acceptance counts:
+    every draft and verify after the first reads cache rows that earlier
+    persistent verifies appended."""
+    cfg = _cfg(layers=3)
+    w = synth.make_weights(cfg, 6300)
+    prompt = synth.make_prompts(cfg, [70], 6301)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=70 + 12 * cfg.width)
+    g.eng.pbd_set_pass_mode(0)
+    anchor = g.prefill([prompt])
+    m = om.OracleModel(w)
+    st = _oracle_prefill(m, prompt, anchor[0])
+    for rnd, fn in enumerate([3, 0, 16, 5, 1, 7, 2, 4]):
+        d, dlg = g.draft()
+        d_np = d.cpu().numpy()[0]
+        _, dl_ref = om.draft(m, st)
+        _check(dlg.cpu().numpy()[0], d_np, dl_ref, slice(1, None), exclude=cfg.mask_id, what=f"round {rnd} draft")
+        v, vlg = g.verify(d)
+        v_np = v.cpu().numpy()[0]
+        _, vl_ref, k, vv = om.verify(m, st, d_np)
+        _check(vlg.cpu().numpy()[0], v_np, vl_ref, slice(None), what=f"round {rnd} verify")
+        n, out = g.accept(d, v, forced=[fn])
+        nn, oo = om.accept(d_np, v_np, forced_n=fn)
+        om.commit(st, nn, oo, k, vv)
+        assert int(n[0]) == nn and list(out.cpu().numpy()[0][:nn + 1]) == oo
+        assert int(g.seq_len[0]) == st.seq_len and int(g.anchor[0]) == st.anchor
+    assert g.status() == 0
+    g.close()
+
+
+def test_fused_early_exit_draft_matches_oracle():
+    cfg = _cfg(layers=3)
+    w = synth.make_weights(cfg, 6400)
+    prompt = synth.make_prompts(cfg, [120], 6401)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=200)
+    g.eng.pbd_set_pass_mode(0)
+    anchor = g.prefill([prompt])
+    m = om.OracleModel(w)
+    st = _oracle_prefill(m, prompt, anchor[0])
+    for k in (1, 2):
+        d = g.zeros(1, cfg.block)
+        lg = g.zeros(1, cfg.width, cfg.vocab, dtype=g.torch.float32)
+        g.eng.pbd_draft_block_layers(g.seq_len, g.anchor, d, k, lg)
+        _, ref = om.draft(m, st, n_layers=k)
+        _check(lg.cpu().numpy()[0], d.cpu().numpy()[0], ref, slice(1, None), exclude=cfg.mask_id,
+               what=f"early exit k={k}")
+    g.close()
+
+
+def test_fused_causal_override_draft_equals_verify():
+    from paper_2607_12422_amd import binding as bd
+    cfg = _cfg()
+    w = synth.make_weights(cfg, 6500)
+    prompt = synth.make_prompts(cfg, [64], 6501)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=200)
+    g.eng.pbd_set_pass_mode(0)
+    g.prefill([prompt])
+    _, olg = g.draft(flags=bd.PBD_PASS_ADAPTER_OFF | bd.PBD_PASS_MASK_CAUSAL)
+    masks = g.i32(np.full((1, cfg.block), cfg.mask_id, dtype=np.int32))
+    _, mlg = g.verify(masks)
+    assert g.torch.equal(olg, mlg)
+    g.close()
+
+
+def test_fused_bounded_wait_gives_up_and_recovers():
+    from paper_2607_12422_amd import binding as bd
+    cfg = _cfg()
+    w = synth.make_weights(cfg, 6600)
+    prompt = synth.make_prompts(cfg, [80], 6601)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=200)
+    g.eng.pbd_set_pass_mode(0)
+    anchor = g.prefill([prompt])
+    g.eng.pbd_set_wait_limit(1)
+    g.draft()
+    assert g.status() & bd.PBD_STATUS_TIMEOUT
+    g.eng.pbd_set_wait_limit(0)
+    d, dlg = g.draft()
+    assert g.status() == 0
+    m = om.OracleModel(w)
+    st = _oracle_prefill(m, prompt, anchor[0])
+    _, dl_ref = om.draft(m, st)
+    _check(dlg.cpu().numpy()[0], d.cpu().numpy()[0], dl_ref, slice(1, None), exclude=cfg.mask_id,
+           what="draft after a forced expiry")
+    g.close()
