@@ -278,6 +278,26 @@ int pbd_verify_block_unanchored(pbd_ctx* ctx, int32_t batch, const int32_t* seq_
                                 uint32_t flags, int32_t* verify, float* logits, pbd_stream_t stream);
 
 /*
+ * pbd_verify_block for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same verify pass, arguments, outputs, flags and errors, with the pass's
+ * workspace regions in a static device array of PBD_NOALLOC_SCRATCH_BYTES
+ * that the library holds on every device it runs on until the process ends,
+ * instead of in the workspace given to pbd_init_weights (the device status
+ * word stays there).  It runs one kernel per operator whatever
+ * pbd_set_pass_mode chose, and allocates nothing.  The context's device must
+ * be current (else PBD_ERR_STATE).  A context whose pass needs more scratch
+ * than the array holds (about 12 MiB per sequence of max_batch at the
+ * Qwen3-0.6B shape) gets PBD_ERR_CAPACITY.  All calls on one device share
+ * the array: calls that overlap on a device (other streams, other threads,
+ * other contexts) race and must be serialised by the caller.
+ */
+#define PBD_NOALLOC_SCRATCH_BYTES (32u << 20)
+int pbd_verify_block_noalloc(pbd_ctx* ctx, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
+                             const int32_t* draft, uint32_t flags, int32_t* verify, float* logits,
+                             pbd_stream_t stream);
+
+/*
  * Acceptance and commit (Sec. 3 steps 4-5; App. A.1).  For each sequence:
  * n = largest k <= D with draft[i-1] == verify[i-1] for all i <= k (or
  * forced_n[b] if forced_n != NULL, device int32 [batch], each in [0, D]);

@@ -44,7 +44,7 @@ PBD_STATUS_TIMEOUT = 8
 EXPORTED = (
     "pbd_packed_weight_bytes", "pbd_kv_bytes", "pbd_workspace_bytes", "pbd_init_weights",
     "pbd_prefill", "pbd_draft_block", "pbd_draft_block_layers", "pbd_draft_block_denoise",
-    "pbd_verify_block", "pbd_draft_block_unanchored", "pbd_verify_block_unanchored", "pbd_accept_commit",
+    "pbd_verify_block", "pbd_verify_block_noalloc", "pbd_draft_block_unanchored", "pbd_verify_block_unanchored", "pbd_accept_commit",
     "pbd_sync_status", "pbd_set_attn_keys_per_split", "pbd_set_attn_query_split", "pbd_set_operand_precision",
     "pbd_set_pass_mode", "pbd_set_wait_limit", "pbd_profile_enable", "pbd_profile_read", "pbd_profile_stage_times", "pbd_last_error", "pbd_destroy",
 )
@@ -100,6 +100,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         "pbd_draft_block_unanchored": (ctypes.c_int, [vp, i32, vp, vp, u32, vp, vp, vp, vp]),
         "pbd_verify_block_unanchored": (ctypes.c_int, [vp, i32, vp, vp, u32, vp, vp, vp]),
         "pbd_verify_block": (ctypes.c_int, [vp, i32, vp, vp, vp, u32, vp, vp, vp]),
+        "pbd_verify_block_noalloc": (ctypes.c_int, [vp, i32, vp, vp, vp, u32, vp, vp, vp]),
         "pbd_accept_commit": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
         "pbd_sync_status": (ctypes.c_int, [vp, vp, ctypes.POINTER(i32)]),
         "pbd_set_attn_keys_per_split": (ctypes.c_int, [vp, i32]),
@@ -255,6 +256,13 @@ class Engine:
         B = int(seq_len.shape[0]) if batch is None else batch
         rc = self.lib.pbd_verify_block(self.ctx, B, _ptr(seq_len), _ptr(anchor), _ptr(draft), flags,
                                        _ptr(verify), _ptr(logits), _stream(stream))
+        _check(rc, self.ctx)
+
+    def pbd_verify_block_noalloc(self, seq_len, anchor, draft, verify, logits=None,
+                                 flags: int = PBD_PASS_DEFAULT, batch: Optional[int] = None, stream=None):
+        B = int(seq_len.shape[0]) if batch is None else batch
+        rc = self.lib.pbd_verify_block_noalloc(self.ctx, B, _ptr(seq_len), _ptr(anchor), _ptr(draft), flags,
+                                               _ptr(verify), _ptr(logits), _stream(stream))
         _check(rc, self.ctx)
 
     def pbd_draft_block_unanchored(self, seq_len, anchor, draft, verify, logits=None,

@@ -4,6 +4,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -13,12 +14,41 @@
 
 using namespace pbd;
 
+// Workspace of pbd_verify_block_noalloc, for callers that cannot allocate:
+// every device the library runs on holds one copy until the process ends.
+// Host code never uses this name as an address; it uses the per-device
+// address hipGetSymbolAddress returns (scratch_address below).
+static __device__ __align__(256) unsigned char scratch[PBD_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 thread_local std::string g_init_error;
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_addr[MAX_DEVICES];     // device address of `scratch` per device (null: not yet taken)
+
+// Address of `scratch` on device `dev`, which must be current; taken once per
+// device, when the array is also cleared on `st` (operand padding read by the
+// matrix cores must hold finite values, as in the caller's workspace).
+hipError_t scratch_address(int dev, hipStream_t st, char** out) {
+    *out = nullptr;
+    if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void* p = nullptr;
+        hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        e = launch_fill_u32(p, PBD_NOALLOC_SCRATCH_BYTES / 4, 0u, st);
+        if (e != hipSuccess) return e;
+        g_scratch_addr[dev] = (char*)p;
+    }
+    *out = g_scratch_addr[dev];
+    return hipSuccess;
+}
 
 constexpr int MAX_DIM = 16384;   // bound on hidden, ffn and n_q_heads*head_dim
 constexpr int LMHEAD_GRID = 512;  // work-groups of the persistent LM head (two per CU)
@@ -223,6 +253,8 @@ struct pbd_ctx {
     unsigned wait_limit; // polls per wait of the persistent pass
     bool force_timeout;  // tests: the persistent pass first waits on a word no one sets
     bool fused_dev;      // the device runs the persistent pass (256 CUs, one work-group each)
+    int dev;             // device the context was created on
+    char* noalloc;       // that device's address of the static scratch (pbd_verify_block_noalloc)
     Profiler prof;
     std::string err;
 };
@@ -289,11 +321,14 @@ struct PassReq {
     bool no_anchor;        // verify of the D drafts alone at seq_len + 1 (anchor already cached);
                            // predictions to out_tokens[b * (D + 1) + 1 + j]
     int* out0;
+    // non-null: the pass's workspace regions live here instead of in the
+    // context's workspace (the status word stays there); one kernel per operator
+    char* scratch;
 };
 
 int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     const Layout& y = c->ly;
-    char* ws = c->ws;
+    char* ws = q.scratch ? q.scratch : c->ws;
     char* pk = c->packed;
     const int dt = y.dtype;
     const bool pre = q.mode == PASS_PREFILL;         // prefill chunk: K/V appended first, chunk-mode attention
@@ -322,7 +357,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     float* sq_m = (float*)(ws + y.w_sq_m);
     int* pos0 = (int*)(ws + y.w_pos0);
     int* nrows = (int*)(ws + y.w_nrows);
-    int* status = (int*)(ws + y.w_status);
+    int* status = (int*)(c->ws + y.w_status);
     auto hi = [&](const size_t* o) { return (void*)(ws + o[0]); };
     auto lo = [&](const size_t* o) { return split ? (void*)(ws + o[1]) : (void*)nullptr; };
 
@@ -335,7 +370,14 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     as.embed = pk + y.p_embed; as.gain = pk + y.lay[0].attn_norm; as.x = x;
     as.op_hi = hi(y.w_xa); as.op_lo = lo(y.w_xa); as.sq = sq_a;
     const bool fused = y.fused_shape && c->fused_dev && c->pass_mode == 0 && !pre && B == 1 &&
-                       !q.anchor_cached && !q.no_anchor && split;
+                       !q.anchor_cached && !q.no_anchor && split && !q.scratch;
+    if (q.scratch) {
+        // the split-K arrival counters must start at zero; the scratch keeps
+        // whatever the last call on this device left (a fill kernel, not a
+        // memset, so that the call can be captured in a graph)
+        hipError_t e = launch_fill_u32(ws + y.w_kcnt, (size_t)y.tiles_o, 0u, st);
+        if (e != hipSuccess) return hip_fail(c, e, "clear split-K counters");
+    }
     if (fused) as.fused_ctl = (unsigned*)(ws + y.w_fused + fused_ctl_offset());
     PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_assemble(dt, as, B, st), "assemble");
 
@@ -700,6 +742,17 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
     c->wait_limit = PBD_DEFAULT_WAIT;
     c->force_timeout = false;
     c->fused_dev = false;
+    c->dev = -1;
+    c->noalloc = nullptr;
+    {
+        hipError_t e = hipGetDevice(&c->dev);
+        if (e == hipSuccess) e = scratch_address(c->dev, (hipStream_t)stream, &c->noalloc);
+        if (e != hipSuccess) {
+            std::string m = std::string("static scratch address: ") + hipGetErrorString(e);
+            delete c;
+            return fail(nullptr, PBD_ERR_HIP, m);
+        }
+    }
     if (y.fused_shape) {
         // one work-group per CU on the 256 CUs of the eight XCDs, all resident at once
         int dev = 0, ncu = 0, occ = 0;
@@ -920,6 +973,33 @@ int pbd_verify_block(pbd_ctx* c, int32_t batch, const int32_t* seq_len, const in
     PassReq q{};
     q.mode = PASS_VERIFY; q.B = batch; q.seq_len = seq_len; q.anchor = anchor; q.drafts = draft;
     q.adapter = adapter; q.causal = causal; q.write_kv = true; q.out_tokens = verify; q.logits = logits;
+    return run_pass(c, q, (hipStream_t)stream);
+}
+
+int pbd_verify_block_noalloc(pbd_ctx* c, int32_t batch, const int32_t* seq_len, const int32_t* anchor,
+                             const int32_t* draft, uint32_t flags, int32_t* verify, float* logits,
+                             pbd_stream_t stream) {
+    int rc = check_ctx(c);
+    if (rc) return rc;
+    if ((rc = check_batch(c, batch))) return rc;
+    if (!seq_len || !anchor || !draft || !verify) return fail(c, PBD_ERR_INVALID_ARG, "NULL pointer argument");
+    bool adapter, causal;
+    if ((rc = resolve_flags(c, flags, false, true, adapter, causal))) return rc;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev != c->dev || !c->noalloc)
+        return fail(c, PBD_ERR_STATE, "the context's device must be current");
+    // the pass uses the workspace regions below the persistent pass's own
+    const size_t need = c->ly.fused_shape ? c->ly.w_fused : c->ly.ws_bytes;
+    if (need > (size_t)PBD_NOALLOC_SCRATCH_BYTES) {
+        char buf[160];
+        snprintf(buf, sizeof buf, "the pass needs %zu bytes of scratch, more than the static %zu (lower max_batch)",
+                 need, (size_t)PBD_NOALLOC_SCRATCH_BYTES);
+        return fail(c, PBD_ERR_CAPACITY, buf);
+    }
+    PassReq q{};
+    q.mode = PASS_VERIFY; q.B = batch; q.seq_len = seq_len; q.anchor = anchor; q.drafts = draft;
+    q.adapter = adapter; q.causal = causal; q.write_kv = true; q.out_tokens = verify; q.logits = logits;
+    q.scratch = c->noalloc;
     return run_pass(c, q, (hipStream_t)stream);
 }
 
