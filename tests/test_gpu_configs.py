@@ -98,6 +98,7 @@ def test_config4_ragged_batch_sampled_sequences():
     g.close()
 
 
+@pytest.mark.timeout(900)        # the float64 oracle runs every round on the CPU
 def test_config3_long_prefix_generation_loop():
     """Prefix 4096, generation loop to 256 tokens with forced geometric
     acceptance (mean 3 committed per round), then 8 rounds of real greedy
@@ -144,6 +145,7 @@ def test_config3_long_prefix_generation_loop():
     g.close()
 
 
+@pytest.mark.timeout(900)        # the float64 oracle runs every round on the CPU
 def test_config5_full_batch_properties_and_sampled_sequence():
     """Batch 32, prefix 8192, D = 32 (W = 33, M = 1056), r = 64, one batched
     step.  Whole batch: sequence independence and the causal-override
