@@ -397,9 +397,10 @@ int pbd_profile_read(pbd_ctx* ctx, int32_t kclass, double* total_ms, int64_t* la
  * * 4 + k is, for rank r of XCD group g in layer l < 64 and stage s (R, Q,
  * A, M, O, R2, GU, D), the device clock (100 MHz) when the stage's wait
  * began (k = 0), when its inputs were ready (k = 1), when its compute waves
- * finished (k = 2; GEMM stages) and when its output was published (k = 3;
- * Q, A, GU).  l = n_layers holds the final norm's start and end (stage 0,
- * k = 0 and 1).  Entries not recorded hold stale values.  *n_written
+ * finished (k = 2; Q, O, GU), when its weight fragments were in LDS (k = 2;
+ * D) and when its flag was published (k = 3; R, Q, A, M, R2, GU).
+ * l = n_layers holds the final norm's start and end (stage 0, k = 0 and 1).
+ * Entries not recorded hold stale values.  *n_written
  * receives min(max_entries, 524288).
  */
 int pbd_profile_stage_times(pbd_ctx* ctx, uint64_t* out, int32_t max_entries, int32_t* n_written);

@@ -68,7 +68,7 @@ constexpr int KB_D = F / 32;           // 96
 constexpr int GQKV = (G + 2) * HD;     // a group's q/k/v columns (512)
 constexpr int GO = G * HD;             // a group's O-projection K-slice (256)
 constexpr int GF = F / NGRP;           // a group's FFN columns (384)
-constexpr int NSLOT = 80;              // LDS ring slots of 1 KiB (even: the two loaders take alternate items)
+constexpr int NSLOT = 88;              // LDS ring slots of 1 KiB (even: the two loaders take alternate items)
 static_assert(NSLOT % 2 == 0, "ring slots come in pairs");
 constexpr int LDQ = HD + 8;            // bf16 row pitch of the attention LDS rows
 constexpr int PB = HD + 4;             // fp32 pitch of a merged attention row
@@ -77,7 +77,10 @@ constexpr int APW = HD + 4;            // fp32 words per stored attention partia
 enum { ST_R = 0, ST_Q, ST_A, ST_M, ST_O, ST_R2, ST_GU, ST_D, NSTAGE };
 enum { FL_R = 0, FL_Q, FL_A, FL_M, FL_R2, FL_GU, NFLAG };
 constexpr int TRACE_LAYERS = 64;       // layers covered by the stage timestamps
-__host__ __device__ constexpr int n_barriers(int st) { return st == ST_A ? 4 : 2; }
+// work-group barriers per stage (the loader waves take part in every one)
+__host__ __device__ constexpr int n_barriers(int st) {
+    return st == ST_A ? 4 : (st == ST_R || st == ST_M || st == ST_R2) ? 1 : 2;
+}
 
 // LDS map (bytes)
 constexpr size_t RING_BYTES = (size_t)NSLOT * 1024;
@@ -121,6 +124,8 @@ typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
 
 // Cache-policy bits of buffer instructions: sc0 = 1, nt = 2, sc1 = 16.
 constexpr int SC1 = 16, SC01 = 17, NT = 2;
+// Range of the workspace's buffer resource (bytes) and an offset past it.
+constexpr unsigned WS_RANGE = 0x7fffffffu, OOB_OFF = 0x80000000u;
 
 __device__ __forceinline__ unsigned xcc_id() {
     unsigned v;
@@ -147,18 +152,6 @@ __device__ __forceinline__ void wait_vm(int n) {
 }
 
 __device__ __forceinline__ void bar() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
-// value -> bf16 value + bf16 residual, 8 consecutive k of one operand row
-__device__ __forceinline__ void split8(const float* v, uint4& hi, uint4& lo) {
-    bf16 h[8], l[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        h[i] = (bf16)v[i];
-        l[i] = (bf16)(v[i] - (float)h[i]);
-    }
-    __builtin_memcpy(&hi, h, 16);
-    __builtin_memcpy(&lo, l, 16);
-}
 
 __device__ __forceinline__ void mma_k4s(f32x4& acc, const uint2& a, const f32x4& p) {
     f32x4 hh, ll;
@@ -204,6 +197,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     float* xs = (float*)(smem + RING_BYTES + SCR_BYTES);               // [MW][32] residual slice
     float* s_rm = (float*)(smem + RING_BYTES + SCR_BYTES + XS_BYTES);  // [MW]
     int* s_id = (int*)(s_rm + MW);                                       // group, rank, t
+    unsigned* s_pub = (unsigned*)(s_id + 8);                             // waves past their stores
 
     int tid = threadIdx.x;
     const int wid = __builtin_amdgcn_readfirstlane(tid / WAVE);   // wave-uniform (scalar)
@@ -222,6 +216,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         s_id[2] = a.pos0[0];
         s_id[3] = (int)ctl[8];
         s_id[4] = a.nrows[0];
+        *s_pub = 0u;
     }
     __syncthreads();
     // a sequence skipped for capacity: no cache write, no outputs (every
@@ -248,7 +243,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     const int QR = G * M, QT = (QR + 15) / 16;
     const int L = a.L;
 
-    __amdgpu_buffer_rsrc_t rws = __builtin_amdgcn_make_buffer_rsrc(ws, 0, 0x7fffffff, 0x00020000);
+    __amdgpu_buffer_rsrc_t rws = __builtin_amdgcn_make_buffer_rsrc(ws, 0, WS_RANGE, 0x00020000);
 
     // ------------------------------------------------------------------
     // Loader waves: ring fill in stage order, in step with the barriers.
@@ -334,6 +329,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                         const int later = cg - end;
                         const int mine_later = (later + ((end & 1) == lid ? 1 : 0)) / 2;
                         wait_vm(mine_later < 40 ? mine_later : 40);
+                        if (st == ST_D && lid == 0 && lane == 0 && l < TRACE_LAYERS)
+                            ((unsigned long long*)(ws + wm.trace))[((((size_t)g * NRANK + r) * TRACE_LAYERS + l) * NSTAGE + ST_D) * 4 + 2] =
+                                __builtin_amdgcn_s_memrealtime();
                     }
                     asm volatile("s_barrier" ::: "memory");
                     if (b == nb - 1) stage_begin = end;          // the stage's slots are released
@@ -380,25 +378,42 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     auto ring_frag = [&](int i) -> uint4 {
         return *(const uint4*)(ring + (size_t)((ring_base + i) % NSLOT) * 1024 + lane * 16);
     };
-    // B operand of fragment f (k in [32 f, 32 f + 32)) for m-tile mt, in two
-    // phases so that a stage issues all its loads before the first wait: the
-    // load (row clamped into [0, M): always a valid address) and the split
-    // into bf16 value + residual (rows past M zeroed)
-    auto opnd_load = [&](size_t base_off, int ld, int f, int mt, f32x4& v0, f32x4& v1) {
-        const int m = min(mt * 16 + lrow, M - 1);
-        const unsigned off = (unsigned)(base_off + ((size_t)m * ld + f * 32 + lgrp * 8) * 4);
-        v0 = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rws, off, 0, SC1));
-        v1 = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rws, off + 16, 0, SC1));
+    // B operand of fragment f (k in [32 f, 32 f + 32)) for m-tile mt: the
+    // producer stored the operand as bf16 value [MW][ld] followed by its bf16
+    // residual [MW][ld].  Rows past M are given an offset beyond the buffer's
+    // range, where a buffer load reads zeros without touching memory.
+    auto opnd_load = [&](size_t base_off, int ld, int f, int mt, uint4& hi, uint4& lo) {
+        const int m = mt * 16 + lrow;
+        const unsigned off = m < M ? (unsigned)(base_off + ((size_t)m * ld + f * 32 + lgrp * 8) * 2) : OOB_OFF;
+        hi = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, off, 0, SC1));
+        lo = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, off + (unsigned)(MW * ld * 2), 0, SC1));
     };
-    auto opnd_make = [&](const f32x4& v0, const f32x4& v1, int mt, uint4& hi, uint4& lo) {
-        const bool live = mt * 16 + lrow < M;
-        float v[8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            v[i] = live ? v0[i] : 0.f;
-            v[4 + i] = live ? v1[i] : 0.f;
+    // element (m, k) of such an operand: value and residual
+    auto opnd_store = [&](size_t base_off, int ld, int m, int k, float v) {
+        const bf16 h = (bf16)v;
+        const bf16 lo = (bf16)(v - (float)h);
+        const unsigned off = (unsigned)(base_off + ((size_t)m * ld + k) * 2);
+        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, h), rws, off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, lo), rws, off + (unsigned)(MW * ld * 2), 0, 0);
+    };
+    // stage timestamps of every rank (profiling aid, 100 MHz clock): slot k
+    // of stage st in layer l, written by lane 0 of the calling wave
+    unsigned long long* trace = (unsigned long long*)(ws + wm.trace);
+    auto stamp_at = [&](int l, int st, int k) {
+        if (lane == 0 && l < TRACE_LAYERS)
+            trace[((((size_t)g * NRANK + r) * TRACE_LAYERS + l) * NSTAGE + st) * 4 + k] = __builtin_amdgcn_s_memrealtime();
+    };
+    // after a stage's stores: every compute wave waits for its own, and the
+    // last of them to arrive publishes the flag (and stamps slot 3 of stage st)
+    auto publish = [&](int fk, int p, unsigned tag, int l, int st) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        unsigned old = 0;
+        if (lane == 0) old = __hip_atomic_fetch_add(s_pub, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        old = __builtin_amdgcn_readfirstlane(old);
+        if (old % NWC == NWC - 1) {
+            if (lane == 0) set_flag(fk, p, tag);
+            stamp_at(l, st, 3);
         }
-        split8(v, hi, lo);
     };
     f32x4* s_red = (f32x4*)scr;          // [tile][wave][mt][lane]
     // wave 0 after barrier B: sum over waves w0..w0+nw-1 of tile tt -> value for (row n, m)
@@ -428,11 +443,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         xs[i] = m < M ? a.x0[(size_t)m * H + 32 * r + c] : 0.f;
     }
 
-    // stage timestamps of rank 0 of every group (profiling aid, 100 MHz clock)
-    unsigned long long* trace = (unsigned long long*)(ws + wm.trace);
     auto stamp = [&](int l, int st, int k) {
-        if (wid == 0 && lane == 0 && l < TRACE_LAYERS)
-            trace[((((size_t)g * NRANK + r) * TRACE_LAYERS + l) * NSTAGE + st) * 4 + k] = __builtin_amdgcn_s_memrealtime();
+        if (wid == 0) stamp_at(l, st, k);
     };
     // wave 0, lanes 0..7: wait until the last pair producer group `lane` writes
     // into this rank's columns of layer pl's partial carries pl's tag (its
@@ -516,8 +528,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     if (c == 0) a.lm_sq[(size_t)r * a.lm_sq_stride + m] = ss;
                 }
             } else if (live) {
-                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(ov), rws,
-                    (unsigned)(out_x + ((((size_t)p * NGRP + g) * MW + m) * H + 32 * r + c) * 4), 0, 0);
+                opnd_store(out_x + ((size_t)p * NGRP + g) * MW * H * 4, H, m, 32 * r + c, ov);
                 if (c == 0)
                     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(ss), rws,
                         (unsigned)(out_sq + ((((size_t)p * NGRP + g) * NRANK + r) * MW + m) * 4), 0, 0);
@@ -527,18 +538,24 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     };
 
     // r_m of every row from the 32 ranks' partial sums of squares (wave 0, lanes < M)
-    auto load_rm = [&](size_t sq_off, int p) {
-        if (wid == 0 && lane < MW) {
-            const int m = min(lane, M - 1);
-            float v[NRANK];
+    // in two phases, so that the operand loads issued in between overlap
+    // them: lane (row m, half h) of wave 0 sums ranks 16 h .. 16 h + 15
+    auto rm_issue = [&](size_t sq_off, int p, float (&v)[NRANK / 2]) {
+        if (wid == 0) {
+            const int m = min(lane % MW, M - 1), h = lane / MW;
 #pragma unroll
-            for (int q = 0; q < NRANK; ++q)
+            for (int q = 0; q < NRANK / 2; ++q)
                 v[q] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rws,
-                    (unsigned)(sq_off + ((((size_t)p * NGRP + g) * NRANK + q) * MW + m) * 4), 0, SC1));
+                    (unsigned)(sq_off + ((((size_t)p * NGRP + g) * NRANK + NRANK / 2 * h + q) * MW + m) * 4), 0, SC1));
+        }
+    };
+    auto rm_finish = [&](const float (&v)[NRANK / 2]) {
+        if (wid == 0) {
             float sm = 0.f;
 #pragma unroll
-            for (int q = 0; q < NRANK; ++q) sm += v[q];
-            s_rm[lane] = rsqrtf(sm / (float)H + a.eps);
+            for (int q = 0; q < NRANK / 2; ++q) sm += v[q];
+            sm += __shfl_xor(sm, MW, WAVE);
+            if (lane < MW) s_rm[lane] = rsqrtf(sm / (float)H + a.eps);
         }
     };
 
@@ -556,31 +573,32 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         bar();
         stamp(l, ST_R, 1);
         stage_reduce(l, false, pk + a.off_attn_norm + lay, wm.xn, wm.sq, false);
-        bar();                                           // all waves' stores done
-        if (wid == 0 && lane == 0) set_flag(FL_R, p, tag);
+        publish(FL_R, p, tag, l, ST_R);
 
         // ---------------- Q: q/k/v tile
         stamp(l, ST_Q, 0);
         wait_flags(FL_R, p, tag);
         bar();                                           // inputs ready, ring holds the tile
         stamp(l, ST_Q, 1);
-        load_rm(wm.sq, p);
         {
+            float rmv[NRANK / 2];
+            rm_issue(wm.sq, p, rmv);
             const size_t xb = wm.xn + ((size_t)p * NGRP + g) * MW * H * 4;
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             const int src = sc.q_src();
             const uint4* la = (const uint4*)(pk + a.off_la[src] + lay);
             // fragments f = wid + NWC j of the hidden size
-            f32x4 xv[FPW][2][2];
+            uint4 xh[FPW][2], xl[FPW][2];
             uint4 av[FPW];
 #pragma unroll
             for (int j = 0; j < FPW; ++j) {
                 const int f = min(wid + NWC * j, KBH - 1);
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) opnd_load(xb, H, f, mt, xv[j][mt][0], xv[j][mt][1]);
+                for (int mt = 0; mt < 2; ++mt) opnd_load(xb, H, f, mt, xh[j][mt], xl[j][mt]);
                 if (LORA) av[j] = la[(size_t)f * WAVE + lane];
             }
+            rm_finish(rmv);
 #pragma unroll
             for (int j = 0; j < FPW; ++j) {
                 if (wid + NWC * j >= KBH) continue;
@@ -588,13 +606,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
-                    uint4 xh, xl;
-                    opnd_make(xv[j][mt][0], xv[j][mt][1], mt, xh, xl);
-                    mma_frag<bf16>(acc[mt], w, xh);
-                    mma_frag<bf16>(acc[mt], w, xl);
+                    mma_frag<bf16>(acc[mt], w, xh[j][mt]);
+                    mma_frag<bf16>(acc[mt], w, xl[j][mt]);
                     if (LORA) {
-                        mma_frag<bf16>(uacc[mt], av[j], xh);
-                        mma_frag<bf16>(uacc[mt], av[j], xl);
+                        mma_frag<bf16>(uacc[mt], av[j], xh[j][mt]);
+                        mma_frag<bf16>(uacc[mt], av[j], xl[j][mt]);
                     }
                 }
             }
@@ -609,18 +625,17 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
         stamp(l, ST_Q, 2);
         bar();
-        if (wid == 0) {
+        {
             // tile [16][M] -> qkv columns 16 r .. of the group's [M][512]
             const size_t qb = wm.qkv + ((size_t)p * NGRP + g) * MW * GQKV * 4;
-            for (int i = lane; i < 16 * M; i += WAVE) {
+            for (int i = tid; i < 16 * M; i += NWC * WAVE) {
                 const int n = i % 16, m = i / 16;
                 const float v = red_val(0, 0, NWC, n, m) * s_rm[m];
                 __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rws,
                     (unsigned)(qb + ((size_t)m * GQKV + 16 * r + n) * 4), 0, 0);
             }
-            set_flag(FL_Q, p, tag);
+            publish(FL_Q, p, tag, l, ST_Q);
         }
-        stamp(l, ST_Q, 3);
         ring_base += sc.items(ST_Q);
 
         // ---------------- A: attention split
@@ -834,11 +849,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 if (lgrp == 0) { pb[HD] = any ? mx : -INFINITY; pb[HD + 1] = any ? ltot : 0.f; }
             }
             bar();
-            if (wid == 0) {
+            {
                 // partial of split r for every query row: (m, l, o[128])
                 const size_t ab0 = wm.apart + ((((size_t)p * NGRP + g) * NRANK + r) * QRMAX) * APW * 4;
                 const bool has = nb > 0;
-                for (int i = lane; i < QR * (HD / 4 + 1); i += WAVE) {
+                for (int i = tid; i < QR * (HD / 4 + 1); i += NWC * WAVE) {
                     const int q = i / (HD / 4 + 1), c4 = i % (HD / 4 + 1);
                     const float* pb = pbuf + (size_t)q * PB;
                     f32x4 v;
@@ -847,10 +862,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rws,
                         (unsigned)(ab0 + ((size_t)q * APW + (c4 < HD / 4 ? 4 + c4 * 4 : 0)) * 4), 0, 0);
                 }
-                set_flag(FL_A, p, tag);
+                publish(FL_A, p, tag, l, ST_A);
             }
         }
-        stamp(l, ST_A, 3);
         ring_base += sc.items(ST_A);
 
         // ---------------- M: merge the 32 split partials of query rows r, r + 32
@@ -892,14 +906,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 const float inv = Ls > 0.f ? 1.f / Ls : 0.f;
                 const int hl = q / M, j = q % M;
                 const size_t ob = wm.oop + ((size_t)p * NGRP + g) * MW * GO * 4;
-                const uint2 st2 = make_uint2(__float_as_uint(o0 * inv), __float_as_uint(o1 * inv));
-                __builtin_amdgcn_raw_buffer_store_b64(u32x2{st2.x, st2.y}, rws,
-                    (unsigned)(ob + ((size_t)j * GO + hl * HD + 2 * lane) * 4), 0, 0);
+                opnd_store(ob, GO, j, hl * HD + 2 * lane, o0 * inv);
+                opnd_store(ob, GO, j, hl * HD + 2 * lane + 1, o1 * inv);
             }
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         }
-        bar();
-        if (wid == 0 && lane == 0) set_flag(FL_M, p, tag);
+        publish(FL_M, p, tag, l, ST_M);
 
         // ---------------- O: O-projection partial over the group's heads
         stamp(l, ST_O, 0);
@@ -913,13 +924,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             const uint4* la = (const uint4*)(pk + a.off_la[3] + lay);
-            f32x4 xv[3][2][2];
+            uint4 xh[3][2], xl[3][2];
             uint4 av[3];
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
                 const int f = min(f0 + 3 * j, 7);
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) opnd_load(ob, GO, f, mt, xv[j][mt][0], xv[j][mt][1]);
+                for (int mt = 0; mt < 2; ++mt) opnd_load(ob, GO, f, mt, xh[j][mt], xl[j][mt]);
                 if (LORA) av[j] = la[(size_t)(8 * g + f) * WAVE + lane];
             }
 #pragma unroll
@@ -929,13 +940,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
-                    uint4 xh, xl;
-                    opnd_make(xv[j][mt][0], xv[j][mt][1], mt, xh, xl);
-                    mma_frag<bf16>(acc[mt], w, xh);
-                    mma_frag<bf16>(acc[mt], w, xl);
+                    mma_frag<bf16>(acc[mt], w, xh[j][mt]);
+                    mma_frag<bf16>(acc[mt], w, xl[j][mt]);
                     if (LORA) {
-                        mma_frag<bf16>(uacc[mt], av[j], xh);
-                        mma_frag<bf16>(uacc[mt], av[j], xl);
+                        mma_frag<bf16>(uacc[mt], av[j], xh[j][mt]);
+                        mma_frag<bf16>(uacc[mt], av[j], xl[j][mt]);
                     }
                 }
             }
@@ -950,10 +959,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
         stamp(l, ST_O, 2);
         bar();
-        if (wid == 0) {
+        {
             // partial [M][32 columns] with tags, written through to memory
             const size_t pb = wm.parto + (((size_t)p * NGRP + g) * MW) * H * 8;
-            for (int i = lane; i < 16 * M; i += WAVE) {
+            for (int i = tid; i < 16 * M; i += NWC * WAVE) {
                 const int m = i / 16, c2 = (i % 16) * 2;            // columns c2, c2 + 1 of the rank's 32
                 const int tt = c2 / 16, n = c2 % 16;
                 const float v0 = red_val(tt, tt * 3, 3, n, m);
@@ -971,34 +980,35 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         bar();
         stamp(l, ST_R2, 1);
         stage_reduce(l, true, pk + a.off_mlp_norm + lay, wm.xm, wm.sqm, false);
-        bar();
-        if (wid == 0 && lane == 0) set_flag(FL_R2, p, tag);
+        publish(FL_R2, p, tag, l, ST_R2);
 
         // ---------------- GU: gate/up tiles + SwiGLU
         stamp(l, ST_GU, 0);
         wait_flags(FL_R2, p, tag);
         bar();
         stamp(l, ST_GU, 1);
-        load_rm(wm.sqm, p);
         {
+            float rmv[NRANK / 2];
+            rm_issue(wm.sqm, p, rmv);
             const size_t xb = wm.xm + ((size_t)p * NGRP + g) * MW * H * 4;
             f32x4 acc[2][2] = {{f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}, {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}};
             f32x4 ug[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}, uu[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             const uint4* lag = (const uint4*)(pk + a.off_la[4] + lay);
             const uint4* lau = (const uint4*)(pk + a.off_la[5] + lay);
             const bool mine2 = ((lrow / 4) & 1) == (r & 1);
-            f32x4 xv[FPW][2][2];
+            uint4 xh[FPW][2], xl[FPW][2];
             uint4 ag[FPW], au[FPW];
 #pragma unroll
             for (int j = 0; j < FPW; ++j) {
                 const int f = min(wid + NWC * j, KBH - 1);
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) opnd_load(xb, H, f, mt, xv[j][mt][0], xv[j][mt][1]);
+                for (int mt = 0; mt < 2; ++mt) opnd_load(xb, H, f, mt, xh[j][mt], xl[j][mt]);
                 if (LORA) {
                     ag[j] = lag[(size_t)f * WAVE + lane];
                     au[j] = lau[(size_t)f * WAVE + lane];
                 }
             }
+            rm_finish(rmv);
 #pragma unroll
             for (int j = 0; j < FPW; ++j) {
                 const int f = wid + NWC * j;
@@ -1009,17 +1019,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
-                    uint4 xh, xl;
-                    opnd_make(xv[j][mt][0], xv[j][mt][1], mt, xh, xl);
-                    mma_frag<bf16>(acc[0][mt], w1, xh);
-                    mma_frag<bf16>(acc[0][mt], w1, xl);
-                    mma_frag<bf16>(acc[1][mt], w2, xh);
-                    mma_frag<bf16>(acc[1][mt], w2, xl);
+                    mma_frag<bf16>(acc[0][mt], w1, xh[j][mt]);
+                    mma_frag<bf16>(acc[0][mt], w1, xl[j][mt]);
+                    mma_frag<bf16>(acc[1][mt], w2, xh[j][mt]);
+                    mma_frag<bf16>(acc[1][mt], w2, xl[j][mt]);
                     if (LORA) {
-                        mma_frag<bf16>(ug[mt], ag[j], xh);
-                        mma_frag<bf16>(ug[mt], ag[j], xl);
-                        mma_frag<bf16>(uu[mt], au[j], xh);
-                        mma_frag<bf16>(uu[mt], au[j], xl);
+                        mma_frag<bf16>(ug[mt], ag[j], xh[j][mt]);
+                        mma_frag<bf16>(ug[mt], ag[j], xl[j][mt]);
+                        mma_frag<bf16>(uu[mt], au[j], xh[j][mt]);
+                        mma_frag<bf16>(uu[mt], au[j], xl[j][mt]);
                     }
                 }
             }
@@ -1047,10 +1055,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
         stamp(l, ST_GU, 2);
         bar();
-        if (wid == 0) {
+        {
             // h for the rank's 12 FFN columns: 8 from the full tile, 4 from the half tile
             const size_t hb = wm.hop + ((size_t)p * NGRP + g) * MW * GF * 4;
-            for (int i = lane; i < 12 * M; i += WAVE) {
+            for (int i = tid; i < 12 * M; i += NWC * WAVE) {
                 const int m = i / 12, c = i % 12;
                 int tt, gr, col;
                 if (c < 8) { tt = 0; gr = c; col = 8 * r + c; }
@@ -1059,12 +1067,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 const float gt = red_val(tt, 0, NWC, gr, m) * rm;
                 const float up = red_val(tt, 0, NWC, gr + 8, m) * rm;
                 const float hv = gt / (1.f + __expf(-gt)) * up;
-                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(hv), rws,
-                    (unsigned)(hb + ((size_t)m * GF + col) * 4), 0, 0);
+                opnd_store(hb, GF, m, col, hv);
             }
-            set_flag(FL_GU, p, tag);
+            publish(FL_GU, p, tag, l, ST_GU);
         }
-        stamp(l, ST_GU, 3);
         ring_base += sc.items(ST_GU);
 
         // ---------------- D: down-projection partial over the group's FFN slice
@@ -1079,13 +1085,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             const uint4* la = (const uint4*)(pk + a.off_la[6] + lay);
-            f32x4 xv[4][2][2];
+            uint4 xh[4][2], xl[4][2];
             uint4 av[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int f = f0 + 3 * j;
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) opnd_load(hb, GF, f, mt, xv[j][mt][0], xv[j][mt][1]);
+                for (int mt = 0; mt < 2; ++mt) opnd_load(hb, GF, f, mt, xh[j][mt], xl[j][mt]);
                 if (LORA) av[j] = la[(size_t)(12 * g + f) * WAVE + lane];
             }
 #pragma unroll
@@ -1094,13 +1100,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
-                    uint4 xh, xl;
-                    opnd_make(xv[j][mt][0], xv[j][mt][1], mt, xh, xl);
-                    mma_frag<bf16>(acc[mt], w, xh);
-                    mma_frag<bf16>(acc[mt], w, xl);
+                    mma_frag<bf16>(acc[mt], w, xh[j][mt]);
+                    mma_frag<bf16>(acc[mt], w, xl[j][mt]);
                     if (LORA) {
-                        mma_frag<bf16>(uacc[mt], av[j], xh);
-                        mma_frag<bf16>(uacc[mt], av[j], xl);
+                        mma_frag<bf16>(uacc[mt], av[j], xh[j][mt]);
+                        mma_frag<bf16>(uacc[mt], av[j], xl[j][mt]);
                     }
                 }
             }
@@ -1114,9 +1118,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             for (int mt = 0; mt < 2; ++mt) s_red[((tt * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
         }
         bar();
-        if (wid == 0) {
+        {
             const size_t pb = wm.partd + (((size_t)p * NGRP + g) * MW) * H * 8;
-            for (int i = lane; i < 16 * M; i += WAVE) {
+            for (int i = tid; i < 16 * M; i += NWC * WAVE) {
                 const int m = i / 16, c2 = (i % 16) * 2;
                 const int tt = c2 / 16, n = c2 % 16;
                 const float v0 = red_val(tt, tt * 3, 3, n, m);
