@@ -356,12 +356,11 @@ int pbd_set_attn_query_split(pbd_ctx* ctx, int32_t mode);
 int pbd_set_operand_precision(pbd_ctx* ctx, int32_t mode);
 
 /*
- * Pass execution mode.  0: batch-1 draft and verify passes of the
+ * Pass execution mode.  0 (default): batch-1 draft and verify passes of the
  * Qwen3-0.6B layer shape (bf16, hidden 1024, 16 query / 8 KV heads of 128,
  * FFN 3072, LoRA rank <= 16, D + 1 <= 32 rows, max_seq <= 4960, on a
  * 256-CU device) run their layer stack as one persistent kernel; other
- * passes use one kernel per operator.  1 (default): one kernel per operator
- * always.
+ * passes use one kernel per operator.  1: one kernel per operator always.
  * Both give the same results up to fp32 rounding.  Other values:
  * PBD_ERR_INVALID_ARG.
  */

@@ -738,7 +738,7 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
     c->kps = 0;
     c->qsplit = -1;
     c->split = cfg->dtype == PBD_DTYPE_BF16;
-    c->pass_mode = 1;
+    c->pass_mode = 0;
     c->wait_limit = PBD_DEFAULT_WAIT;
     c->force_timeout = false;
     c->fused_dev = false;

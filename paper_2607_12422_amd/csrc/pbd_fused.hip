@@ -70,6 +70,7 @@ constexpr int GO = G * HD;             // a group's O-projection K-slice (256)
 constexpr int GF = F / NGRP;           // a group's FFN columns (384)
 constexpr int NSLOT = 88;              // LDS ring slots of 1 KiB (even: the two loaders take alternate items)
 static_assert(NSLOT % 2 == 0, "ring slots come in pairs");
+constexpr int LOOKAHEAD = 12;          // ring items issued ahead per barrier interval (even)
 constexpr int LDQ = HD + 8;            // bf16 row pitch of the attention LDS rows
 constexpr int PB = HD + 4;             // fp32 pitch of a merged attention row
 constexpr int APW = HD + 4;            // fp32 words per stored attention partial row (m, l, o[128], pad)
@@ -335,8 +336,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     }
                     asm volatile("s_barrier" ::: "memory");
                     if (b == nb - 1) stage_begin = end;          // the stage's slots are released
-                    // look ahead while the compute waves work
-                    issue_to(stage_begin + NSLOT);
+                    // look ahead while the compute waves work, a bounded number
+                    // of items per barrier interval: a long burst would keep
+                    // this wave from the next barrier
+                    issue_to(min(stage_begin + NSLOT, cg + LOOKAHEAD));
                 }
             }
         }
@@ -728,21 +731,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     vb_l[j * HD + RP::NP * lrow + pp] = v0[pp];
                     vb_l[j * HD + RP::HALF + RP::NP * lrow + pp] = v1[pp];
                 }
-                if (live && j < a.kv_rows) {
-                    // verify: append the block K/V to the cache at t + j
-                    const int pos = t + j;
-                    const size_t head = (((size_t)l * a.Bmax) * NKV + g) * (size_t)a.nblk * 16 * HD;
-                    bf16* kblk = (bf16*)a.kcache + head + (size_t)(pos / 16) * 16 * HD;
-                    bf16* vblk = (bf16*)a.vcache + head + (size_t)(pos / 16) * 16 * HD;
-#pragma unroll
-                    for (int pp = 0; pp < RP::NP; ++pp) {
-                        const int i0 = RP::NP * lrow + pp;
-                        kblk[kblock_elem<bf16>(pos % 16, i0)] = lo[pp];
-                        kblk[kblock_elem<bf16>(pos % 16, i0 + RP::HALF)] = hi[pp];
-                        vblk[vblock_elem(pos % 16, i0)] = v0[pp];
-                        vblk[vblock_elem(pos % 16, i0 + RP::HALF)] = v1[pp];
-                    }
-                }
             }
             bar();
             // key loop: wave w < 2 QT takes query tile w % QT and half w / QT of the blocks
@@ -911,6 +899,22 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
         }
         publish(FL_M, p, tag, l, ST_M);
+        if (r == NRANK - 1 && a.kv_rows > 0) {
+            // verify: append the block K/V (still in LDS from the attention
+            // stage) to the cache at t .. t + kv_rows - 1, after the flag, so
+            // that the stores stay off the stage chain
+            const bf16* kb_l = (const bf16*)(scr + QL_BYTES);
+            const bf16* vb_l = (const bf16*)(scr + QL_BYTES + KL_BYTES);
+            const int nr = min(M, a.kv_rows);
+            const size_t head = (((size_t)l * a.Bmax) * NKV + g) * (size_t)a.nblk * 16 * HD;
+            for (int i = tid; i < nr * HD; i += NWC * WAVE) {
+                const int j = i / HD, dd = i % HD, pos = t + j;
+                bf16* kblk = (bf16*)a.kcache + head + (size_t)(pos / 16) * 16 * HD;
+                bf16* vblk = (bf16*)a.vcache + head + (size_t)(pos / 16) * 16 * HD;
+                kblk[kblock_elem<bf16>(pos % 16, dd)] = kb_l[j * LDQ + dd];
+                vblk[vblock_elem(pos % 16, dd)] = vb_l[j * HD + dd];
+            }
+        }
 
         // ---------------- O: O-projection partial over the group's heads
         stamp(l, ST_O, 0);

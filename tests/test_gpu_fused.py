@@ -4,9 +4,9 @@ Batch-1 draft and verify passes of the Qwen3-0.6B layer shape run their 28
 (here: 2 or 3) layers as one persistent kernel.  These tests run it through
 the C ABI on a model of that layer shape with few layers and a 4096-token
 vocabulary, so that the float64 oracle finishes in seconds, and check:
-  * that the persistent kernel is the one that ran in pass mode 0 (its
-    kernel class is timed) and that pass mode 1 (one kernel per operator,
-    the default) does not use it;
+  * that the persistent kernel is the one that ran in pass mode 0 (the
+    default; its kernel class is timed) and that pass mode 1 (one kernel
+    per operator) does not use it;
   * draft and verify logits against the oracle within 2e-2, token ids equal
     at decisive rows, for several block widths (the query rows of a KV head
     span one to four 16-row tiles) and prefix lengths (attention splits of
