@@ -5,12 +5,19 @@ draft pass (D = 16), the adapter-off causal verify pass, and longest-prefix
 acceptance with KV commit.  Default workload: the Qwen3-0.6B shape in bf16 with
 LoRA r = 16, batch 1, prefix 512 (synthetic random-init weights and prompts).
 
-Prints one JSON line (rank 0): ms per step, draft and verify pass times, their
-ratio, the HBM roofline fraction of the dominant kernel (the weight-streaming
-GEMMs, timed with HIP events by the library's profiling aid), and the CPU
-oracle timed on the host on a bounded sample of the same workload.
+Prints one JSON line: ms per step, draft and verify pass times, their ratio,
+the HBM roofline fraction of the dominant kernel (timed with HIP events by the
+library's profiling aid on the stream the kernels run on), the step times of
+the two large-batch workloads, and the CPU oracle timed on the host on a
+bounded sample of the same workload.
 
-    python bench.py [--steps K] [--warmup W] [--workload I] [--no-cpu-baseline]
+The top-level process never touches the GPU.  It runs the measurement in
+fresh child processes (the first one with every extra section, the others the
+timed steps and the per-pass repetitions only), reports the mean and standard
+deviation over them, then times the oracle itself.  ``--child`` runs one
+measuring process directly (rocprofv3 runs use it, with ``--counters``).
+
+    python bench.py [--steps K] [--warmup W] [--workload I] [--processes P] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -47,14 +54,14 @@ def algorithmic_bytes(cfg, batch, prefixes):
     )
 
 
-def counter_traffic(name="k_fgemm_traffic.txt"):
-    """HBM bytes per launch of the projection GEMM from the committed rocprofv3
-    counter summary (FETCH_SIZE and WRITE_SIZE passes, scaled by a plain copy's
+def counter_traffic(name, source):
+    """HBM bytes per launch of a kernel from a committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE passes, scaled by a plain copy's
     readings).  None when the summary is missing or was taken on another
-    version of the kernel source."""
+    version of the kernel's source file."""
     import hashlib
     path = os.path.join(ROOT, "profiles", name)
-    src = os.path.join(ROOT, "paper_2607_12422_amd", "csrc", "pbd_kernels.hip")
+    src = os.path.join(ROOT, "paper_2607_12422_amd", "csrc", source)
     try:
         kv = {}
         for line in open(path):
@@ -69,38 +76,126 @@ def counter_traffic(name="k_fgemm_traffic.txt"):
         return None
 
 
-def cpu_baseline(w_, weights, prompts, reps=3):
-    """The oracle (float64 NumPy) on the host: one draft + verify + accept at
-    the workload's shape for the first sequence, median of `reps`; prefill
-    excluded.  Returns the JSON object."""
+def cpu_baseline(w_, min_reps=5, min_seconds=10.0):
+    """The oracle on the host, run with float32 weights and activations (its
+    default is float64): one draft + verify + accept at the workload's shape
+    for the first sequence, repeated until at least `min_reps` repetitions and
+    `min_seconds` of work, median; prefill excluded.  Returns the JSON object."""
     import numpy as np
+    import synth
     from oracle import model as om
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = len(os.sched_getaffinity(0))
-    m = om.OracleModel(weights)
+    weights = synth.make_weights(w_.cfg, w_.seed(0))
+    _, prompts = synth.workload_inputs(w_)
+    m = om.OracleModel(weights, dtype=np.float32)
     st = om.prefill(m, prompts[0])
     times = []
-    for _ in range(reps):
+    t_all = time.perf_counter()
+    while len(times) < min_reps or time.perf_counter() - t_all < min_seconds:
         t0 = time.perf_counter_ns()
         d, _ = om.draft(m, st)
         p, _, k, v = om.verify(m, st, d)
         om.accept(d, p)
         times.append((time.perf_counter_ns() - t0) / 1e6)
     ms = statistics.median(times)
-    per_seq = ms
-    return {"value": round(per_seq * w_.batch, 3), "unit": "ms", "cores": int(threads), "kind": "oracle",
-            "sample": f"1 of {w_.batch} sequence(s), prefix {len(prompts[0])}: draft+verify+accept, "
-                      f"median of {reps} (float64 NumPy); value scaled to the batch",
-            "measured_ms_per_sequence": round(per_seq, 3)}
+    return {"value": round(ms * w_.batch, 3), "unit": "ms", "cores": int(threads), "kind": "oracle",
+            "sample": f"1 of {w_.batch} sequence(s), prefix {len(prompts[0])}: draft+verify+accept with float32 "
+                      f"weights and activations, median of {len(times)} repetitions; value scaled to the batch",
+            "measured_ms_per_sequence": round(ms, 3), "host_cores": len(os.sched_getaffinity(0))}
+
+
+def _mean_sd(xs):
+    xs = [float(x) for x in xs]
+    return {"mean": round(statistics.fmean(xs), 4), "sd": round(statistics.stdev(xs), 4) if len(xs) > 1 else 0.0,
+            "n": len(xs)}
+
+
+def run_child(extra, timeout_s):
+    """One measuring process (bench.py --child ...); returns its JSON line."""
+    import subprocess
+    cmd = [sys.executable, "-u", os.path.abspath(__file__), "--child"] + extra
+    print("bench: " + " ".join(cmd[2:]), file=sys.stderr, flush=True)
+    t0 = time.time()
+    p = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=None, timeout=timeout_s, text=True)
+    if p.returncode != 0:
+        raise SystemExit(f"bench: child {' '.join(extra)} exited with status {p.returncode}")
+    lines = [ln for ln in p.stdout.splitlines() if ln.startswith("{")]
+    if not lines:
+        raise SystemExit(f"bench: child {' '.join(extra)} printed no result")
+    print(f"bench: child done in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    return json.loads(lines[-1])
+
+
+def parent_main(args):
+    """Fresh measuring processes, then the oracle on the host; never touches the GPU."""
+    import synth
+    base = ["--steps", str(args.steps), "--warmup", str(args.warmup), "--workload", str(args.workload)]
+    for k in ("no_profile", "no_draft_curve", "no_denoise", "no_unanchored", "no_prefill", "no_context", "no_loop",
+              "eager"):
+        if getattr(args, k):
+            base.append("--" + k.replace("_", "-"))
+    if args.kps:
+        base += ["--kps", str(args.kps)]
+    if args.attn_qsplit >= -1:
+        base += ["--attn-qsplit", str(args.attn_qsplit)]
+    if args.pass_mode >= 0:
+        base += ["--pass-mode", str(args.pass_mode)]
+    minimal = ["--no-profile", "--no-draft-curve", "--no-denoise", "--no-unanchored", "--no-prefill", "--no-context",
+               "--no-loop"]
+    runs = [run_child(base, 1500)]
+    for _ in range(1, args.processes):
+        runs.append(run_child(base + minimal, 600))
+    result = dict(runs[0])
+    steps = [r["ms_per_step"] for r in runs]
+    result["value"] = result["ms_per_step"] = round(statistics.fmean(steps), 4)
+    result["draft_ms"] = round(statistics.fmean(r["draft_ms"] for r in runs), 4)
+    result["verify_ms"] = round(statistics.fmean(r["verify_ms"] for r in runs), 4)
+    result["accept_ms"] = round(statistics.fmean(r["accept_ms"] for r in runs), 4)
+    result["draft_verify_ratio"] = round(result["draft_ms"] / result["verify_ms"], 4)
+    result["tokens_per_s"] = round(statistics.fmean(r["tokens_per_s"] for r in runs), 2)
+    hb = result["hbm"]
+    for part in ("draft", "verify"):
+        gbps = hb[part + "_bytes"] / result[part + "_ms"] / 1e6
+        hb[part + "_gbps"] = round(gbps, 1)
+        hb[part + "_pct_peak"] = round(100 * gbps / HBM_PEAK_GBPS, 2)
+    result["repeat"] = {
+        "processes": len(runs),
+        "note": "mean and sample sd over fresh processes of each process's value (step: K timed steps; "
+                "passes: median of the timed steps); pass_replays pools every process's per-pass replays",
+        "ms_per_step": _mean_sd(steps),
+        "draft_ms": _mean_sd([r["draft_ms"] for r in runs]),
+        "verify_ms": _mean_sd([r["verify_ms"] for r in runs]),
+        "pass_replays": {
+            part: _mean_sd([x for r in runs for x in r["pass_replays"][part]])
+            for part in ("draft", "verify")},
+    }
+    for r in runs:
+        r.pop("pass_replays", None)
+    result.pop("pass_replays", None)
+    if not args.no_large_batch:
+        large = []
+        for wi in (3, 4):
+            w_ = synth.WORKLOADS[wi]
+            rr = run_child(["--steps", str(max(5, min(args.steps, 20))), "--warmup", "3", "--workload", str(wi),
+                            "--prefill-chunk", str(max(16, 4096 // w_.batch))] + minimal, 900)
+            large.append({k: rr[k] for k in ("config", "ms_per_step", "draft_ms", "verify_ms", "accept_ms",
+                                             "draft_verify_ratio", "tokens_per_s", "hbm", "device_status",
+                                             "steps", "warmup")})
+        result["large_batch"] = large
+    if not args.no_cpu_baseline:
+        print("bench: CPU oracle baseline", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(synth.WORKLOADS[args.workload])
+    print(json.dumps(result), flush=True)
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -120,15 +215,28 @@ def main():
     ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of replaying HIP graphs")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 10 plain device copies of MIB MiB (reference for the HBM byte counters) and exit")
+    ap.add_argument("--child", action="store_true", help="measure in this process (no child processes, no CPU baseline)")
+    ap.add_argument("--processes", type=int, default=3, help="fresh measuring processes (top-level run)")
+    ap.add_argument("--no-large-batch", action="store_true", help="skip the batch-8 and batch-32 step timings")
+    ap.add_argument("--pass-mode", type=int, default=-1,
+                    help="0: persistent batch-1 pass where supported, 1: one kernel per operator; default: the library's")
+    ap.add_argument("--prefill-chunk", type=int, default=0, help="prompt rows per sequence per prefill pass (0: D + 1)")
+    ap.add_argument("--replays", type=int, default=100, help="per-pass graph replays timed one by one")
     args = ap.parse_args()
+    if args.counters or args.copy_calibration:
+        args.child = True
     if args.counters:
         for k in ("no_cpu_baseline", "no_profile", "no_draft_curve", "no_denoise", "no_unanchored", "no_prefill",
                   "no_context", "no_loop"):
             setattr(args, k, True)
+        args.replays = 0
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(sequences are independent; see the data-parallel design notes).", file=sys.stderr)
         sys.exit(2)
+    if not args.child:
+        parent_main(args)
+        return
 
     import numpy as np
     import torch
@@ -155,7 +263,9 @@ def main():
     B = w_.batch
     max_seq = max(lengths) + (w_.gen_tokens or 0) + 4 * cfg.width + args.steps + args.warmup + 64
     dw = upload_weights(weights, cfg.dtype, dev)
-    eng = Engine(cfg, dw, max_batch=B, max_seq=max_seq, device=dev)
+    eng = Engine(cfg, dw, max_batch=B, max_seq=max_seq, device=dev, prefill_chunk=args.prefill_chunk)
+    if args.pass_mode >= 0:
+        eng.pbd_set_pass_mode(args.pass_mode)
     if args.kps:
         eng.pbd_set_attn_keys_per_split(args.kps)
     if args.attn_qsplit >= -1:
@@ -240,6 +350,20 @@ def main():
     v_ms = [ev[k][1].elapsed_time(ev[k][2]) for k in range(args.warmup, n_iter)]
     a_ms = [ev[k][2].elapsed_time(ev[k][3]) for k in range(args.warmup, n_iter)]
     committed = int(committed_acc.sum())
+    # per-pass repetitions: draft and verify replayed alternately, each timed
+    # on its own (the state stays at the prefill's: no accept in between)
+    rep_d, rep_v = [], []
+    if args.replays > 0:
+        re = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.replays)]
+        for e in re:
+            e[0].record(stream)
+            parts[0]()
+            e[1].record(stream)
+            parts[1]()
+            e[2].record(stream)
+        torch.cuda.synchronize()
+        rep_d = [round(e[0].elapsed_time(e[1]), 5) for e in re]
+        rep_v = [round(e[1].elapsed_time(e[2]), 5) for e in re]
     status = eng.pbd_sync_status()
     dmed, vmed, amed = statistics.median(d_ms), statistics.median(v_ms), statistics.median(a_ms)
     byt = algorithmic_bytes(cfg, B, lengths)
@@ -270,6 +394,7 @@ def main():
         "paper_context": {"draft_ms": 50.285, "verify_ms": 50.621, "hardware": "not stated",
                           "note": "Tab. profile; serving-runtime bound, context only"},
         "device_status": status, "setup_s": round(setup_s, 1), "timed_wall_s": round(wall, 3),
+        "pass_replays": {"draft": rep_d, "verify": rep_v},
     }
 
     def time_graph(fn, reps):
@@ -504,24 +629,55 @@ def main():
         eng.pbd_profile_enable(False)
         prof = {name: {"total_ms": round(ms, 4), "launches": n, "avg_us": round(1e3 * ms / max(n, 1), 3)}
                 for name, (ms, n) in tot.items()}
-        g = prof["gemm"]
-        gemm_bytes = args.steps * (byt["gemm_draft"] + byt["gemm_verify"])
-        gemm_launch_bytes = gemm_bytes / max(g["launches"], 1)
-        ach = gemm_launch_bytes / (g["avg_us"] * 1e-6) / 1e9
-        result["roofline"] = {"bound": "hbm", "kernel": "k_fgemm (q/k/v, o, gate/up, down projections; both passes)",
-                              "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                              "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": counter_traffic(),
-                              "bytes_per_launch": round(gemm_launch_bytes), "avg_launch_us": g["avg_us"]}
         lm = prof["lmhead"]
         lm_ach = byt["lmhead"] / (lm["avg_us"] * 1e-6) / 1e9 if lm["launches"] else 0.0
         result["lmhead_roofline"] = {"kernel": "k_lmhead", "achieved": round(lm_ach, 1),
                                      "frac": round(lm_ach / HBM_PEAK_GBPS, 4), "avg_launch_us": lm["avg_us"]}
+        fz = prof["fused"]
+        if fz["launches"] == 2 * args.steps:
+            # persistent pass: one launch per pass streams every layer's weights
+            # (+ LoRA in the draft) and the K/V (read; verify: + the block's write)
+            kv_r = byt["draft"] - byt["gemm_draft"] - byt["lmhead"]
+            kv_w = byt["verify"] - byt["gemm_verify"] - byt["lmhead"] - kv_r
+            launch_bytes = (byt["gemm_draft"] + byt["gemm_verify"] + 2 * kv_r + kv_w) / 2
+            ach = launch_bytes / (fz["avg_us"] * 1e-6) / 1e9
+            result["roofline"] = {
+                "bound": "hbm", "kernel": "k_fused (persistent layer stack of the draft and the verify pass)",
+                "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
+                "traffic": counter_traffic("k_fused_traffic.txt", "pbd_fused.hip"),
+                "bytes_per_launch": round(launch_bytes), "avg_launch_us": fz["avg_us"]}
+        else:
+            g = prof["gemm"]
+            gemm_bytes = args.steps * (byt["gemm_draft"] + byt["gemm_verify"])
+            gemm_launch_bytes = gemm_bytes / max(g["launches"], 1)
+            ach = gemm_launch_bytes / (g["avg_us"] * 1e-6) / 1e9 if g["launches"] else 0.0
+            result["roofline"] = {"bound": "hbm", "kernel": "k_fgemm (q/k/v, o, gate/up, down projections; both passes)",
+                                  "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                  "frac": round(ach / HBM_PEAK_GBPS, 4),
+                                  "traffic": counter_traffic("k_fgemm_traffic.txt", "pbd_kernels.hip"),
+                                  "bytes_per_launch": round(gemm_launch_bytes), "avg_launch_us": g["avg_us"]}
         result["kernel_classes"] = prof
         kernel_sum = sum(v["total_ms"] for v in prof.values()) / args.steps
         result["kernel_time_ms_per_step"] = round(kernel_sum, 4)
+        if fz["launches"] and not args.eager:
+            # context: the same passes with one kernel per operator (graphs)
+            eng.pbd_set_pass_mode(1)
+            reps = max(10, args.steps // 2)
+            po = {"draft_ms": round(time_graph(do_draft, reps), 4), "verify_ms": round(time_graph(do_verify, reps), 4)}
+            eng.pbd_profile_enable(True)
+            for k in range(10):
+                do_draft()
+                do_verify()
+            torch.cuda.synchronize()
+            ms, n = eng.pbd_profile_read(binding.KCLASSES.index("gemm"))
+            eng.pbd_profile_enable(False)
+            if n:
+                gb = 10 * (byt["gemm_draft"] + byt["gemm_verify"]) / n
+                po["k_fgemm_avg_launch_us"] = round(1e3 * ms / n, 3)
+                po["k_fgemm_frac"] = round(gb / (ms / n * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)
+            eng.pbd_set_pass_mode(0 if args.pass_mode < 0 else args.pass_mode)
+            result["per_operator_mode"] = po
 
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w_, weights, prompts)
     eng.close()
     print(json.dumps(result), flush=True)
 

@@ -62,7 +62,7 @@ def rope(v: np.ndarray, positions: np.ndarray, theta: float) -> np.ndarray:
     sin = np.sin(ang)[:, None, :]
     a = v[..., :half]
     b = v[..., half:]
-    return np.concatenate([a * cos - b * sin, b * cos + a * sin], axis=-1)
+    return np.concatenate([a * cos - b * sin, b * cos + a * sin], axis=-1).astype(v.dtype, copy=False)
 
 
 def silu(x: np.ndarray) -> np.ndarray:
@@ -88,10 +88,11 @@ def greedy_argmax(logits: np.ndarray, exclude: Optional[int] = None) -> int:
 # ---------------------------------------------------------------------------
 
 class OracleModel:
-    """The backbone plus its LoRA adapter, held in float64."""
+    """The backbone plus its LoRA adapter, held in float64 (the benchmark's
+    host baseline also runs it with float32 arrays; parity uses float64)."""
 
-    def __init__(self, w: Weights):
-        f = lambda a: np.asarray(a, dtype=np.float64)
+    def __init__(self, w: Weights, dtype=np.float64):
+        f = lambda a: np.asarray(a, dtype=dtype)
         self.cfg: ModelConfig = w.cfg
         self.embed = f(w.embed)
         self.final_norm = f(w.final_norm)
@@ -154,7 +155,7 @@ class OracleModel:
             K = np.concatenate([cache_k[li], k], axis=0)          # [pos0+n, hkv, d]
             V = np.concatenate([cache_v[li], v], axis=0)
             vis = np.concatenate([np.ones((n, pos0), dtype=bool), block_vis], axis=1)
-            o = np.empty((n, hq, d))
+            o = np.empty((n, hq, d), dtype=x.dtype)
             for h in range(hq):
                 g = h // group
                 s = (q[:, h, :] @ K[:, g, :].T) / np.sqrt(d)       # [n, pos0+n]
@@ -191,7 +192,7 @@ def prefill(model: OracleModel, prompt: Sequence[int]) -> SeqState:
     """Adapter-off causal pass over the prompt; its greedy next token is the
     first generated token and the first anchor."""
     cfg = model.cfg
-    empty = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim)) for _ in range(cfg.n_layers)]
+    empty = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim), dtype=model.embed.dtype) for _ in range(cfg.n_layers)]
     lg, k, v = model.forward_block(prompt, 0, empty, empty, causal=True,
                                    adapter_on=False, logit_rows=[len(prompt) - 1])
     anchor = greedy_argmax(lg[0])
