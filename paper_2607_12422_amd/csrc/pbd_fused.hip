@@ -170,15 +170,15 @@ __device__ __forceinline__ void mma_k4s(f32x4& acc, const uint2& a, const f32x4&
 struct Sched {
     int g, r, t, nkb, s_pre;
     // Q tile (global tile index in the packed q/k/v weights) of this rank
-    __device__ int q_tile() const { return r < 16 ? 16 * g + r : (r < 24 ? 128 + 8 * g + (r - 16) : 192 + 8 * g + (r - 24)); }
+    __device__ __forceinline__ int q_tile() const { return r < 16 ? 16 * g + r : (r < 24 ? 128 + 8 * g + (r - 16) : 192 + 8 * g + (r - 24)); }
     // LoRA source of the Q tile: 0 q, 1 k, 2 v
-    __device__ int q_src() const { return r < 16 ? 0 : (r < 24 ? 1 : 2); }
-    __device__ int gu_t1() const { return 48 * g + r; }
-    __device__ int gu_t2() const { return 48 * g + 32 + r / 2; }
+    __device__ __forceinline__ int q_src() const { return r < 16 ? 0 : (r < 24 ? 1 : 2); }
+    __device__ __forceinline__ int gu_t1() const { return 48 * g + r; }
+    __device__ __forceinline__ int gu_t2() const { return 48 * g + 32 + r / 2; }
     // prefix key blocks of this rank's attention split (rank 31: the block keys)
-    __device__ int kb_begin() const { return r < s_pre ? (r * nkb) / s_pre : 0; }
-    __device__ int kb_count() const { return r < s_pre ? ((r + 1) * nkb) / s_pre - (r * nkb) / s_pre : 0; }
-    __device__ int items(int st) const {
+    __device__ __forceinline__ int kb_begin() const { return r < s_pre ? (r * nkb) / s_pre : 0; }
+    __device__ __forceinline__ int kb_count() const { return r < s_pre ? ((r + 1) * nkb) / s_pre - (r * nkb) / s_pre : 0; }
+    __device__ __forceinline__ int items(int st) const {
         switch (st) {
             case ST_Q: return KBH;
             case ST_A: return 8 * kb_count();
@@ -580,26 +580,34 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---------------- Q: q/k/v tile
         stamp(l, ST_Q, 0);
-        wait_flags(FL_R, p, tag);
-        bar();                                           // inputs ready, ring holds the tile
-        stamp(l, ST_Q, 1);
         {
+            // the adapter's fragments do not depend on the activations: they
+            // are requested before the wait
+            uint4 av[FPW];
+            uint2 bvq;
+            if (LORA) {
+                const int src = sc.q_src();
+                const uint32_t la_off = src == 0 ? a.off_la[0] : (src == 1 ? a.off_la[1] : a.off_la[2]);
+                const uint4* la = (const uint4*)(pk + la_off + lay);
+#pragma unroll
+                for (int j = 0; j < FPW; ++j) av[j] = la[(size_t)min(wid + NWC * j, KBH - 1) * WAVE + lane];
+                __builtin_memcpy(&bvq, (const bf16*)(pk + a.off_lb_qkv + lay) + ((size_t)sc.q_tile() * WAVE + lane) * 4, 8);
+            }
+            wait_flags(FL_R, p, tag);
+            bar();                                           // inputs ready, ring holds the tile
+            stamp(l, ST_Q, 1);
             float rmv[NRANK / 2];
             rm_issue(wm.sq, p, rmv);
             const size_t xb = wm.xn + ((size_t)p * NGRP + g) * MW * H * 4;
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
-            const int src = sc.q_src();
-            const uint4* la = (const uint4*)(pk + a.off_la[src] + lay);
             // fragments f = wid + NWC j of the hidden size
             uint4 xh[FPW][2], xl[FPW][2];
-            uint4 av[FPW];
 #pragma unroll
             for (int j = 0; j < FPW; ++j) {
                 const int f = min(wid + NWC * j, KBH - 1);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) opnd_load(xb, H, f, mt, xh[j][mt], xl[j][mt]);
-                if (LORA) av[j] = la[(size_t)f * WAVE + lane];
             }
             rm_finish(rmv);
 #pragma unroll
@@ -618,10 +626,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 }
             }
             if (LORA) {
-                uint2 bv;
-                __builtin_memcpy(&bv, (const bf16*)(pk + a.off_lb_qkv + lay) + ((size_t)sc.q_tile() * WAVE + lane) * 4, 8);
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bv, uacc[mt] * a.scale);
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bvq, uacc[mt] * a.scale);
             }
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) s_red[((0 * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
@@ -643,9 +649,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---------------- A: attention split
         stamp(l, ST_A, 0);
-        wait_flags(FL_Q, p, tag);
-        bar();
-        stamp(l, ST_A, 1);
         {
             bf16* q_l = (bf16*)scr;                                   // [QRMAX][LDQ]
             bf16* kb_l = (bf16*)(scr + QL_BYTES);                      // [32][LDQ]
@@ -658,79 +661,84 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             auto ld4 = [&](size_t off) -> typename RP::fv {
                 return __builtin_bit_cast(typename RP::fv, __builtin_amdgcn_raw_buffer_load_b128(rws, (unsigned)off, 0, SC1));
             };
-            // prep rows: query rows q < QR (head q / M, block row q % M), then
-            // (block split) the key / value rows j < M, padded to the key block
-            const int nkrow = blk ? ((M + 15) / 16) * 16 : 0;
-            const int nrow = QR + nkrow;
+            // Row jobs of 16 lanes each: the query rows q < QR (head q / M,
+            // block row q % M), then (block split) the key rows and the value
+            // rows of the block.  Lane group tg (of NG16) takes jobs tg + NG16 k,
+            // NJ at a time; the position table and the norm gains are requested
+            // before the wait, the q/k/v values after it.
+            constexpr int NG16 = NWC * WAVE / 16, NJ = 3;
+            const int tg = tid / 16;
+            const int nkrow = blk ? ((M + 15) / 16) * 16 : 0;    // key rows incl. padding to the key block
+            const int njob = QR + (blk ? 2 * M : 0);
             Gains<bf16, HD> gq, gk;
             if (a.qk_norm) {
                 gq.load(pk + a.off_q_norm + lay, lrow);
                 gk.load(pk + a.off_k_norm + lay, lrow);
             }
+            // job j: kind (0 query, 1 key, 2 value), block row and source column
+            auto job = [&](int j, int& kind, int& row, int& col) {
+                if (j < QR) { kind = 0; row = j % M; col = (j / M) * HD; }
+                else if (j < QR + M) { kind = 1; row = j - QR; col = 2 * HD; }
+                else { kind = 2; row = j - QR - M; col = 3 * HD; }
+            };
+            typename RP::fv2 cs[NJ];
+#pragma unroll
+            for (int k = 0; k < NJ; ++k) {
+                int kind, row, col;
+                job(min(tg + NG16 * k, njob - 1), kind, row, col);
+                cs[k] = *(const typename RP::fv2*)((const float2*)rope + (size_t)(t + row) * RP::HALF + RP::NP * lrow);
+            }
+            wait_flags(FL_Q, p, tag);
+            bar();
+            stamp(l, ST_A, 1);
             float gql[RP::NP], gqh[RP::NP], gkl[RP::NP], gkh[RP::NP];
             gq.get(a.qk_norm, gql, gqh);
             gk.get(a.qk_norm, gkl, gkh);
-            // 16 lanes per row; lane group tg (of NG16) takes query rows tg +
-            // NG16 k and (block split) key/value rows tg + NG16 k; every load
-            // is issued first
-            constexpr int NG16 = NWC * WAVE / 16;
-            constexpr int NQR = (QRMAX + NG16 - 1) / NG16, NKR = (32 + NG16 - 1) / NG16;
-            const int tg = tid / 16;
-            typename RP::fv ql[NQR], qh[NQR];
-            typename RP::fv2 qc[NQR];
+            for (int j0 = 0; j0 < njob; j0 += NG16 * NJ) {
+                typename RP::fv vlo[NJ], vhi[NJ];
 #pragma unroll
-            for (int k = 0; k < NQR; ++k) {
-                const int rc = min(tg + NG16 * k, QR - 1);
-                const int hl = rc / M, j = rc % M;
-                ql[k] = ld4(qb + ((size_t)j * GQKV + hl * HD + RP::NP * lrow) * 4);
-                qh[k] = ld4(qb + ((size_t)j * GQKV + hl * HD + RP::HALF + RP::NP * lrow) * 4);
-                qc[k] = *(const typename RP::fv2*)((const float2*)rope + (size_t)(t + j) * RP::HALF + RP::NP * lrow);
-            }
-            typename RP::fv kl[NKR], kh[NKR], vl[NKR], vh[NKR];
-            typename RP::fv2 kc[NKR];
-            if (blk) {
+                for (int k = 0; k < NJ; ++k) {
+                    int kind, row, col;
+                    job(min(j0 + tg + NG16 * k, njob - 1), kind, row, col);
+                    const size_t rb = qb + ((size_t)row * GQKV + col + RP::NP * lrow) * 4;
+                    vlo[k] = ld4(rb);
+                    vhi[k] = ld4(rb + RP::HALF * 4);
+                    if (j0 > 0)
+                        cs[k] = *(const typename RP::fv2*)((const float2*)rope + (size_t)(t + row) * RP::HALF + RP::NP * lrow);
+                }
 #pragma unroll
-                for (int k = 0; k < NKR; ++k) {
-                    const int jk = min(tg + NG16 * k, M - 1);
-                    const size_t rb = qb + (size_t)jk * GQKV * 4;
-                    kl[k] = ld4(rb + (2 * HD + RP::NP * lrow) * 4);
-                    kh[k] = ld4(rb + (2 * HD + RP::HALF + RP::NP * lrow) * 4);
-                    vl[k] = ld4(rb + (3 * HD + RP::NP * lrow) * 4);
-                    vh[k] = ld4(rb + (3 * HD + RP::HALF + RP::NP * lrow) * 4);
-                    kc[k] = *(const typename RP::fv2*)((const float2*)rope + (size_t)(t + jk) * RP::HALF + RP::NP * lrow);
+                for (int k = 0; k < NJ; ++k) {
+                    const int j = j0 + tg + NG16 * k;
+                    if (j >= njob) continue;
+                    int kind, row, col;
+                    job(j, kind, row, col);
+                    if (kind == 2) {
+#pragma unroll
+                        for (int pp = 0; pp < RP::NP; ++pp) {
+                            vb_l[row * HD + RP::NP * lrow + pp] = (bf16)vlo[k][pp];
+                            vb_l[row * HD + RP::HALF + RP::NP * lrow + pp] = (bf16)vhi[k][pp];
+                        }
+                    } else {
+                        RP rp;
+                        bf16 lo[RP::NP], hi[RP::NP];
+                        rp.lo = vlo[k];
+                        rp.hi = vhi[k];
+                        rp.cs = cs[k];
+                        float gl[RP::NP], gh[RP::NP];
+#pragma unroll
+                        for (int pp = 0; pp < RP::NP; ++pp) {
+                            gl[pp] = kind == 0 ? gql[pp] : gkl[pp];
+                            gh[pp] = kind == 0 ? gqh[pp] : gkh[pp];
+                        }
+                        rp.finish(kind == 0 ? q_l + j * LDQ : kb_l + row * LDQ, true, gl, gh, a.qk_norm, a.eps, lrow, lo, hi);
+                    }
                 }
             }
-#pragma unroll
-            for (int k = 0; k < NQR; ++k) {
-                const int row = tg + NG16 * k;
-                if (row < QR) {
-                    RP rp;
-                    bf16 lo[RP::NP], hi[RP::NP];
-                    rp.lo = ql[k];
-                    rp.hi = qh[k];
-                    rp.cs = qc[k];
-                    rp.finish(q_l + row * LDQ, true, gql, gqh, a.qk_norm, a.eps, lrow, lo, hi);
-                }
-            }
-#pragma unroll
-            for (int k = 0; k < NKR; ++k) {
-                const int j = tg + NG16 * k;
-                if (!blk || j >= nkrow) continue;
-                const bool live = j < M;
-                RP rp;
-                bf16 lo[RP::NP], hi[RP::NP];
-                rp.lo = kl[k];
-                rp.hi = kh[k];
-                rp.cs = kc[k];
-                rp.finish(kb_l + j * LDQ, live, gkl, gkh, a.qk_norm, a.eps, lrow, lo, hi);
-                bf16 v0[RP::NP], v1[RP::NP];
-#pragma unroll
-                for (int pp = 0; pp < RP::NP; ++pp) {
-                    v0[pp] = (bf16)(live ? vl[k][pp] : 0.f);
-                    v1[pp] = (bf16)(live ? vh[k][pp] : 0.f);
-                    vb_l[j * HD + RP::NP * lrow + pp] = v0[pp];
-                    vb_l[j * HD + RP::HALF + RP::NP * lrow + pp] = v1[pp];
-                }
+            // key and value rows past the block, up to the key block: zeros
+            for (int i = tid; i < (nkrow - M) * HD; i += NWC * WAVE) {
+                const int j = M + i / HD, d = i % HD;
+                kb_l[j * LDQ + d] = (bf16)0.f;
+                vb_l[j * HD + d] = (bf16)0.f;
             }
             bar();
             // key loop: wave w < 2 QT takes query tile w % QT and half w / QT of the blocks
@@ -918,24 +926,29 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---------------- O: O-projection partial over the group's heads
         stamp(l, ST_O, 0);
-        wait_flags(FL_M, p, tag);
-        bar();
-        stamp(l, ST_O, 1);
         {
-            const size_t ob = wm.oop + ((size_t)p * NGRP + g) * MW * GO * 4;
             // tile tt = wid / 3; fragments f = wid % 3 + 3 j of the group's 8
             const int tt = wid / 3, f0 = wid % 3;
+            uint4 av[3];
+            uint2 bvo;
+            if (LORA) {
+                const uint4* la = (const uint4*)(pk + a.off_la[3] + lay);
+#pragma unroll
+                for (int j = 0; j < 3; ++j) av[j] = la[(size_t)(8 * g + min(f0 + 3 * j, 7)) * WAVE + lane];
+                __builtin_memcpy(&bvo, (const bf16*)(pk + a.off_lb_o + lay) + ((size_t)(2 * r + tt) * WAVE + lane) * 4, 8);
+            }
+            wait_flags(FL_M, p, tag);
+            bar();
+            stamp(l, ST_O, 1);
+            const size_t ob = wm.oop + ((size_t)p * NGRP + g) * MW * GO * 4;
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
-            const uint4* la = (const uint4*)(pk + a.off_la[3] + lay);
             uint4 xh[3][2], xl[3][2];
-            uint4 av[3];
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
                 const int f = min(f0 + 3 * j, 7);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) opnd_load(ob, GO, f, mt, xh[j][mt], xl[j][mt]);
-                if (LORA) av[j] = la[(size_t)(8 * g + f) * WAVE + lane];
             }
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
@@ -953,10 +966,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 }
             }
             if (LORA) {
-                uint2 bv;
-                __builtin_memcpy(&bv, (const bf16*)(pk + a.off_lb_o + lay) + ((size_t)(2 * r + tt) * WAVE + lane) * 4, 8);
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bv, uacc[mt] * a.scale);
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bvo, uacc[mt] * a.scale);
             }
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) s_red[((tt * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
@@ -988,29 +999,38 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---------------- GU: gate/up tiles + SwiGLU
         stamp(l, ST_GU, 0);
-        wait_flags(FL_R2, p, tag);
-        bar();
-        stamp(l, ST_GU, 1);
         {
+            uint4 ag[FPW], au[FPW];
+            uint2 bvg[2];
+            if (LORA) {
+                const uint4* lag = (const uint4*)(pk + a.off_la[4] + lay);
+                const uint4* lau = (const uint4*)(pk + a.off_la[5] + lay);
+#pragma unroll
+                for (int j = 0; j < FPW; ++j) {
+                    const int f = min(wid + NWC * j, KBH - 1);
+                    ag[j] = lag[(size_t)f * WAVE + lane];
+                    au[j] = lau[(size_t)f * WAVE + lane];
+                }
+#pragma unroll
+                for (int tt = 0; tt < 2; ++tt)
+                    __builtin_memcpy(&bvg[tt], (const bf16*)(pk + a.off_lb_gu + lay) +
+                                                   ((size_t)(tt == 0 ? sc.gu_t1() : sc.gu_t2()) * WAVE + lane) * 4, 8);
+            }
+            wait_flags(FL_R2, p, tag);
+            bar();
+            stamp(l, ST_GU, 1);
             float rmv[NRANK / 2];
             rm_issue(wm.sqm, p, rmv);
             const size_t xb = wm.xm + ((size_t)p * NGRP + g) * MW * H * 4;
             f32x4 acc[2][2] = {{f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}, {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}};
             f32x4 ug[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}, uu[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
-            const uint4* lag = (const uint4*)(pk + a.off_la[4] + lay);
-            const uint4* lau = (const uint4*)(pk + a.off_la[5] + lay);
             const bool mine2 = ((lrow / 4) & 1) == (r & 1);
             uint4 xh[FPW][2], xl[FPW][2];
-            uint4 ag[FPW], au[FPW];
 #pragma unroll
             for (int j = 0; j < FPW; ++j) {
                 const int f = min(wid + NWC * j, KBH - 1);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) opnd_load(xb, H, f, mt, xh[j][mt], xl[j][mt]);
-                if (LORA) {
-                    ag[j] = lag[(size_t)f * WAVE + lane];
-                    au[j] = lau[(size_t)f * WAVE + lane];
-                }
             }
             rm_finish(rmv);
 #pragma unroll
@@ -1038,9 +1058,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             if (LORA) {
 #pragma unroll
                 for (int tt = 0; tt < 2; ++tt) {
-                    const int tile = tt == 0 ? sc.gu_t1() : sc.gu_t2();
-                    uint2 bv;
-                    __builtin_memcpy(&bv, (const bf16*)(pk + a.off_lb_gu + lay) + ((size_t)tile * WAVE + lane) * 4, 8);
+                    const uint2 bv = bvg[tt];
                     // rows 0-7 take the gate shrink, rows 8-15 the up shrink
                     const uint2 bg = lrow < 8 ? bv : uint2{0, 0};
                     const uint2 bu = lrow < 8 ? uint2{0, 0} : bv;
@@ -1079,24 +1097,29 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---------------- D: down-projection partial over the group's FFN slice
         stamp(l, ST_D, 0);
-        wait_flags(FL_GU, p, tag);
-        bar();
-        stamp(l, ST_D, 1);
         {
-            const size_t hb = wm.hop + ((size_t)p * NGRP + g) * MW * GF * 4;
             // tile tt = wid / 3; fragments f = wid % 3 + 3 j of the group's 12
             const int tt = wid / 3, f0 = wid % 3;
+            uint4 av[4];
+            uint2 bvd;
+            if (LORA) {
+                const uint4* la = (const uint4*)(pk + a.off_la[6] + lay);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) av[j] = la[(size_t)(12 * g + f0 + 3 * j) * WAVE + lane];
+                __builtin_memcpy(&bvd, (const bf16*)(pk + a.off_lb_d + lay) + ((size_t)(2 * r + tt) * WAVE + lane) * 4, 8);
+            }
+            wait_flags(FL_GU, p, tag);
+            bar();
+            stamp(l, ST_D, 1);
+            const size_t hb = wm.hop + ((size_t)p * NGRP + g) * MW * GF * 4;
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
-            const uint4* la = (const uint4*)(pk + a.off_la[6] + lay);
             uint4 xh[4][2], xl[4][2];
-            uint4 av[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int f = f0 + 3 * j;
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) opnd_load(hb, GF, f, mt, xh[j][mt], xl[j][mt]);
-                if (LORA) av[j] = la[(size_t)(12 * g + f) * WAVE + lane];
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -1113,10 +1136,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 }
             }
             if (LORA) {
-                uint2 bv;
-                __builtin_memcpy(&bv, (const bf16*)(pk + a.off_lb_d + lay) + ((size_t)(2 * r + tt) * WAVE + lane) * 4, 8);
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bv, uacc[mt] * a.scale);
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bvd, uacc[mt] * a.scale);
             }
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) s_red[((tt * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];

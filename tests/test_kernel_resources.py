@@ -2,8 +2,8 @@
 
 A register array indexed with a run-time value, or a register budget that
 overflows, puts per-lane data in scratch memory, which turns every access into
-a global memory round trip.  The kernels of the Qwen3-shape passes (bf16 with split
-operands; projection GEMMs at every LoRA rank up to 64; attention with
+a global memory round trip.  The kernels of the Qwen3-shape passes (the persistent
+layer stack; bf16 with split operands; projection GEMMs at every LoRA rank up to 64; attention with
 head_dim 128 and up to three 16-row query tiles) and every projection GEMM of
 the fp32 model must use no scratch at all.
 """
@@ -31,6 +31,8 @@ HOT = [
     r"_ZN3pbd10k_gemm_bigIDF16bLb[01]ELi[24]EEEvNS_11BigGemmArgsE",
     r"_ZN3pbd9k_kvwriteIDF16bLi128EEEvNS_11KVWriteArgsE",
     r"_ZN3pbd13k_gather_lastIDF16bEEvNS_10GatherArgsE",
+    # the persistent batch-1 layer stack (adapter on / off)
+    r"_ZN3pbd2fz7k_fusedILb[01]EEEvNS_9FusedArgsE",
 ]
 
 
@@ -39,9 +41,11 @@ def test_hot_kernels_use_no_scratch(tmp_path):
     cc = b.hipcc()
     if not shutil.which(cc) and not os.path.exists(cc):
         pytest.skip("hipcc not available")
-    cmd = [cc, *b.FLAGS, "-c", os.path.join(b.CSRC, "pbd_kernels.hip"), "-o", str(tmp_path / "k.o"),
-           "-Rpass-analysis=kernel-resource-usage"]
-    out = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True).stdout
+    out = ""
+    for src in ("pbd_kernels.hip", "pbd_fused.hip"):
+        cmd = [cc, *b.FLAGS, "-c", os.path.join(b.CSRC, src), "-o", str(tmp_path / (src + ".o")),
+               "-Rpass-analysis=kernel-resource-usage"]
+        out += subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True).stdout
     usage = {}
     name = None
     for line in out.splitlines():
