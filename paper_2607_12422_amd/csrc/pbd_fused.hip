@@ -62,7 +62,8 @@ constexpr int MW = FUSED_MAX_ROWS;     // rows per pass
 constexpr int QRMAX = G * MW;          // query rows per KV head
 constexpr int KBH = H / 32;            // fragments over the hidden size
 constexpr int FPW = (KBH + NWC - 1) / NWC;  // hidden-size fragments per compute wave (6)
-constexpr int NEL = (MW * 32 + NWC * WAVE - 1) / (NWC * WAVE);   // residual-slice elements per thread
+constexpr int RR = NWC * WAVE / 16;   // rows per round of the residual stage (16 column pairs per row)
+constexpr int NRR = (MW + RR - 1) / RR; // rounds
 constexpr int KB_O = NQ * HD / 32;     // 64
 constexpr int KB_D = F / 32;           // 96
 constexpr int GQKV = (G + 2) * HD;     // a group's q/k/v columns (512)
@@ -381,24 +382,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     auto ring_frag = [&](int i) -> uint4 {
         return *(const uint4*)(ring + (size_t)((ring_base + i) % NSLOT) * 1024 + lane * 16);
     };
-    // B operand of fragment f (k in [32 f, 32 f + 32)) for m-tile mt: the
-    // producer stored the operand as bf16 value [MW][ld] followed by its bf16
-    // residual [MW][ld].  Rows past M are given an offset beyond the buffer's
-    // range, where a buffer load reads zeros without touching memory.
-    auto opnd_load = [&](size_t base_off, int ld, int f, int mt, uint4& hi, uint4& lo) {
-        const int m = mt * 16 + lrow;
-        const unsigned off = m < M ? (unsigned)(base_off + ((size_t)m * ld + f * 32 + lgrp * 8) * 2) : OOB_OFF;
-        hi = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, off, 0, SC1));
-        lo = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, off + (unsigned)(MW * ld * 2), 0, SC1));
-    };
-    // element (m, k) of such an operand: value and residual
-    auto opnd_store = [&](size_t base_off, int ld, int m, int k, float v) {
-        const bf16 h = (bf16)v;
-        const bf16 lo = (bf16)(v - (float)h);
-        const unsigned off = (unsigned)(base_off + ((size_t)m * ld + k) * 2);
-        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, h), rws, off, 0, 0);
-        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, lo), rws, off + (unsigned)(MW * ld * 2), 0, 0);
-    };
     // stage timestamps of every rank (profiling aid, 100 MHz clock): slot k
     // of stage st in layer l, written by lane 0 of the calling wave
     unsigned long long* trace = (unsigned long long*)(ws + wm.trace);
@@ -468,97 +451,141 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
     };
     // R / R2 / final: residual update from the eight groups' partials (none at
-    // layer 0's R), operand x * gain of the next RMSNorm and per-row sums of squares
-    auto stage_reduce = [&](int l, bool from_o, const void* gain, size_t out_x, size_t out_sq, bool final_out) {
+    // layer 0's R), operand x * gain of the next RMSNorm and per-row sums of
+    // squares.  Thread tid owns row tid / 16 (+ RR per round) and the column
+    // pair 2 (tid % 16) of the rank's 32, so that every partial read is one
+    // 16-byte load per group and a row's 16 column pairs sit in one DPP row.
+    // `gv` is this thread's pair of gains (requested before the stage's wait).
+    auto stage_reduce = [&](int l, bool from_o, float2 gv, size_t out_x, size_t out_sq, bool final_out) {
         const int p = l & 1;
         const bool poll = from_o || l > 0;
-        // partials of layer l (O) or l - 1 (down) from every group: all 16
-        // pairs of this thread's two elements are requested before any wait
+        // partials of layer l (O) or l - 1 (down) from every group
         const int pl = from_o ? l : l - 1;
         const unsigned ptag = (epoch << 8) | (unsigned)(pl & 0xff);
-        const size_t base = (from_o ? wm.parto : wm.partd) + ((size_t)(pl & 1) * NGRP) * MW * H * 8;
-        uint2 pr[NEL][NGRP];
-        if (poll) {
+        const unsigned base = (unsigned)((from_o ? wm.parto : wm.partd) + ((size_t)(pl & 1) * NGRP) * MW * H * 8);
+        const int cp = tid % 16, c2 = 2 * cp;
+        float2* xs2 = (float2*)xs;
 #pragma unroll
-            for (int e0 = 0; e0 < NEL; ++e0) {
-                const int idx = tid + e0 * NWC * WAVE;
-                const int m = min(idx / 32, M - 1), c = idx % 32;
+        for (int e = 0; e < NRR; ++e) {
+            if (e * RR >= M) break;
+            const int m = tid / 16 + RR * e;
+            const bool live = m < M;
+            // all eight groups' pairs requested before any is used
+            const unsigned voff = base + (unsigned)(((min(m, M - 1) * H) + 32 * r + c2) * 8);
+            u32x4 q[NGRP];
+            if (poll) {
 #pragma unroll
                 for (int x = 0; x < NGRP; ++x)
-                    pr[e0][x] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws,
-                        (unsigned)(base + (((size_t)x * MW + m) * H + 32 * r + c) * 8), 0, SC01));
+                    q[x] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff, x * MW * H * 8, SC01));
             }
-        }
-#pragma unroll
-        for (int e0 = 0; e0 < NEL; ++e0) {
-            const int idx = tid + e0 * NWC * WAVE;
-            const int m = idx / 32, c = idx % 32;
-            const bool live = m < M;
-            float xv = live ? xs[idx] : 0.f;            // live implies idx < M * 32
+            float2 xv = live ? xs2[m * 16 + cp] : float2{0.f, 0.f};
             if (poll && live) {
-                float sum = 0.f;
+                float s0 = 0.f, s1 = 0.f;
 #pragma unroll
                 for (int x = 0; x < NGRP; ++x) {
-                    uint2 q = pr[e0][x];
+                    u32x4 v = q[x];
                     // a pair not yet written through: poll it alone (rare)
                     unsigned spins = 0;
-                    while (q.y != ptag) {
+                    while (v.y != ptag || v.w != ptag) {
                         if (++spins > spin_limit || ((spins & 63) == 0 && ld_sc1_u32(abort_w))) {
                             if (spins > spin_limit) give_up();
-                            q.x = 0u;
+                            v.x = 0u;
+                            v.z = 0u;
                             break;
                         }
-                        q = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws,
-                            (unsigned)(base + (((size_t)x * MW + m) * H + 32 * r + c) * 8), 0, SC01));
+                        v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff, x * MW * H * 8, SC01));
                     }
-                    sum += __uint_as_float(q.x);          // group order
+                    s0 += __uint_as_float(v.x);           // group order
+                    s1 += __uint_as_float(v.z);
                 }
-                xv += sum;
-                xs[idx] = xv;
+                xv.x += s0;
+                xv.y += s1;
+                xs2[m * 16 + cp] = xv;
             }
             // operand and the row's sum of squares over the rank's 32 columns
-            const float ov = live ? xv * (float)((const bf16*)gain)[32 * r + c] : 0.f;
-            float ss = xv * xv;
-#pragma unroll
-            for (int o = 16; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 32);
+            const float o0 = live ? xv.x * gv.x : 0.f, o1 = live ? xv.y * gv.y : 0.f;
+            const float ss = row16_sum(xv.x * xv.x + xv.y * xv.y);
             if (final_out) {
                 if (live) {
-                    const bf16 h = (bf16)ov;
-                    const bf16 lo = (bf16)(ov - (float)h);
-                    const size_t e = xfrag_elem<bf16>(m, 32 * r + c, a.lm_MT);
-                    ((bf16*)a.lm_hi)[e] = h;
-                    ((bf16*)a.lm_lo)[e] = lo;
-                    if (c == 0) a.lm_sq[(size_t)r * a.lm_sq_stride + m] = ss;
+#pragma unroll
+                    for (int k = 0; k < 2; ++k) {
+                        const float ov = k == 0 ? o0 : o1;
+                        const bf16 h = (bf16)ov;
+                        const bf16 lo = (bf16)(ov - (float)h);
+                        const size_t el = xfrag_elem<bf16>(m, 32 * r + c2 + k, a.lm_MT);
+                        ((bf16*)a.lm_hi)[el] = h;
+                        ((bf16*)a.lm_lo)[el] = lo;
+                    }
+                    if (cp == 0) a.lm_sq[(size_t)r * a.lm_sq_stride + m] = ss;
                 }
             } else if (live) {
-                opnd_store(out_x + ((size_t)p * NGRP + g) * MW * H * 4, H, m, 32 * r + c, ov);
-                if (c == 0)
+                const bf16 h0 = (bf16)o0, h1 = (bf16)o1;
+                const bf16 l0 = (bf16)(o0 - (float)h0), l1 = (bf16)(o1 - (float)h1);
+                const unsigned hp = (unsigned)__builtin_bit_cast(unsigned short, h0) | ((unsigned)__builtin_bit_cast(unsigned short, h1) << 16);
+                const unsigned lp = (unsigned)__builtin_bit_cast(unsigned short, l0) | ((unsigned)__builtin_bit_cast(unsigned short, l1) << 16);
+                const unsigned ooff = (unsigned)(out_x + ((size_t)p * NGRP + g) * MW * H * 4 + ((size_t)m * H + 32 * r + c2) * 2);
+                __builtin_amdgcn_raw_buffer_store_b32(hp, rws, ooff, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(lp, rws, ooff, MW * H * 2, 0);
+                if (cp == 0)
                     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(ss), rws,
-                        (unsigned)(out_sq + ((((size_t)p * NGRP + g) * NRANK + r) * MW + m) * 4), 0, 0);
+                        (unsigned)(out_sq + ((((size_t)p * NGRP + g) * MW + m) * NRANK + r) * 4), 0, 0);
             }
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     };
+    // this thread's pair of RMSNorm gains for stage_reduce
+    auto gain_pair = [&](const void* gain) -> float2 {
+        unsigned w;
+        __builtin_memcpy(&w, (const bf16*)gain + 32 * r + 2 * (tid % 16), 4);
+        return float2{(float)__builtin_bit_cast(bf16, (unsigned short)(w & 0xffff)),
+                      (float)__builtin_bit_cast(bf16, (unsigned short)(w >> 16))};
+    };
 
     // r_m of every row from the 32 ranks' partial sums of squares (wave 0, lanes < M)
     // in two phases, so that the operand loads issued in between overlap
-    // them: lane (row m, half h) of wave 0 sums ranks 16 h .. 16 h + 15
-    auto rm_issue = [&](size_t sq_off, int p, float (&v)[NRANK / 2]) {
+    // them: lane (row m, half h) of wave 0 sums ranks 16 h .. 16 h + 15, which
+    // lie next to each other ([parity][group][row][rank])
+    auto rm_issue = [&](size_t sq_off, int p, u32x4 (&v)[NRANK / 8]) {
         if (wid == 0) {
             const int m = min(lane % MW, M - 1), h = lane / MW;
+            const unsigned off = (unsigned)(sq_off + ((((size_t)p * NGRP + g) * MW + m) * NRANK + NRANK / 2 * h) * 4);
 #pragma unroll
-            for (int q = 0; q < NRANK / 2; ++q)
-                v[q] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rws,
-                    (unsigned)(sq_off + ((((size_t)p * NGRP + g) * NRANK + NRANK / 2 * h + q) * MW + m) * 4), 0, SC1));
+            for (int q = 0; q < NRANK / 8; ++q)
+                v[q] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rws, off + 16 * q, 0, SC1));
         }
     };
-    auto rm_finish = [&](const float (&v)[NRANK / 2]) {
+    auto rm_finish = [&](const u32x4 (&v)[NRANK / 8]) {
         if (wid == 0) {
             float sm = 0.f;
 #pragma unroll
-            for (int q = 0; q < NRANK / 2; ++q) sm += v[q];
+            for (int q = 0; q < NRANK / 8; ++q)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) sm += __uint_as_float(v[q][e]);
             sm += __shfl_xor(sm, MW, WAVE);
             if (lane < MW) s_rm[lane] = rsqrtf(sm / (float)H + a.eps);
+        }
+    };
+    // lane offset of the operand row mt * 16 + lrow at this lane's k-group;
+    // rows past the block get an offset beyond the buffer's range, where a
+    // buffer load reads zeros without touching memory
+    auto opnd_lane = [&](size_t base_off, int ld, int mt) -> unsigned {
+        const int m = mt * 16 + lrow;
+        return m < M ? (unsigned)(base_off + ((size_t)m * ld + lgrp * 8) * 2) : OOB_OFF;
+    };
+    // fragment at byte offset fo past the lane offset: value, and its
+    // residual MW * ld bf16 further
+    auto ld_frag = [&](unsigned voff, unsigned fo, int ld, uint4& hi, uint4& lo) {
+        hi = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, 0, SC1));
+        lo = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, MW * ld * 2, SC1));
+    };
+    // the same for the second m-tile, where only the lanes of live rows issue
+    // the loads (for a 17-row block, one row in sixteen)
+    auto ld_frag1 = [&](bool live, unsigned voff, unsigned fo, int ld, uint4& hi, uint4& lo) {
+        hi = uint4{0, 0, 0, 0};
+        lo = uint4{0, 0, 0, 0};
+        if (live) {
+            hi = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, 0, SC1));
+            lo = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, MW * ld * 2, SC1));
         }
     };
 
@@ -572,10 +599,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---------------- R: residual from the down partials, attention-norm operand
         stamp(l, ST_R, 0);
-        if (l > 0) wait_partials(false, l - 1);
-        bar();
-        stamp(l, ST_R, 1);
-        stage_reduce(l, false, pk + a.off_attn_norm + lay, wm.xn, wm.sq, false);
+        {
+            const float2 gv = gain_pair(pk + a.off_attn_norm + lay);
+            if (l > 0) wait_partials(false, l - 1);
+            bar();
+            stamp(l, ST_R, 1);
+            stage_reduce(l, false, gv, wm.xn, wm.sq, false);
+        }
         publish(FL_R, p, tag, l, ST_R);
 
         // ---------------- Q: q/k/v tile
@@ -596,18 +626,23 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             wait_flags(FL_R, p, tag);
             bar();                                           // inputs ready, ring holds the tile
             stamp(l, ST_Q, 1);
-            float rmv[NRANK / 2];
+            u32x4 rmv[NRANK / 8];
             rm_issue(wm.sq, p, rmv);
             const size_t xb = wm.xn + ((size_t)p * NGRP + g) * MW * H * 4;
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             // fragments f = wid + NWC j of the hidden size
+            // fragments f = wid + NWC j (the last ones past the hidden size are
+            // read from the next row and not used)
             uint4 xh[FPW][2], xl[FPW][2];
+            {
+                const unsigned v0 = opnd_lane(xb, H, 0) + wid * 64, v1 = opnd_lane(xb, H, 1) + wid * 64;
+                const bool live1 = 16 + lrow < M;
 #pragma unroll
-            for (int j = 0; j < FPW; ++j) {
-                const int f = min(wid + NWC * j, KBH - 1);
-#pragma unroll
-                for (int mt = 0; mt < 2; ++mt) opnd_load(xb, H, f, mt, xh[j][mt], xl[j][mt]);
+                for (int j = 0; j < FPW; ++j) {
+                    ld_frag(v0, j * NWC * 64, H, xh[j][0], xl[j][0]);
+                    ld_frag1(live1, v1, j * NWC * 64, H, xh[j][1], xl[j][1]);
+                }
             }
             rm_finish(rmv);
 #pragma unroll
@@ -871,39 +906,42 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         if (wid < 2) {
             const int q = r + 32 * wid;
             if (q < QR) {
-                const size_t ab = wm.apart + (((size_t)p * NGRP + g) * NRANK) * QRMAX * APW * 4;
-                // lane s < 32 holds split s's (m, l); weights formed there and
-                // broadcast one split at a time (fixed split order)
-                float mls = -INFINITY, lls = 0.f;
-                if (lane < NRANK) {
-                    const unsigned off = (unsigned)(ab + (((size_t)lane * QRMAX + q) * APW) * 4);
-                    mls = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rws, off, 0, SC1));
-                    lls = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rws, off + 4, 0, SC1));
-                }
+                const unsigned ab = (unsigned)(wm.apart + (((size_t)p * NGRP + g) * NRANK) * QRMAX * APW * 4);
+                // every split's (m, l) (lane s < 32 holds split s's) and this
+                // lane's two dims of every split's o, all requested at once
+                uint2 ml = uint2{__float_as_uint(-INFINITY), 0u};
+                if (lane < NRANK)
+                    ml = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws,
+                        ab + (unsigned)(((size_t)lane * QRMAX + q) * APW * 4), 0, SC1));
+                uint2 ov[NRANK];
+                const unsigned ob0 = ab + (unsigned)(((size_t)q * APW + 4 + 2 * lane) * 4);
+#pragma unroll
+                for (int k = 0; k < NRANK; ++k)
+                    ov[k] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws, ob0, k * QRMAX * APW * 4, SC1));
+                const float mls = __uint_as_float(ml.x);
                 const float mx = wave_max(mls);
                 const float wl = (mls > -INFINITY) ? exp2f(mls - mx) : 0.f;
+                const float wll = wl * __uint_as_float(ml.y);
+                // merged in fixed split order, the weights read from their lanes
                 float o0 = 0.f, o1 = 0.f, Ls = 0.f;
-                for (int s0 = 0; s0 < NRANK; s0 += 16) {
-                    uint2 ov[16];
-                    float w8[16];
 #pragma unroll
-                    for (int k = 0; k < 16; ++k) {
-                        w8[k] = __shfl(wl, s0 + k, 64);
-                        const unsigned off = (unsigned)(ab + (((size_t)(s0 + k) * QRMAX + q) * APW + 4 + 2 * lane) * 4);
-                        ov[k] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws, off, 0, SC1));
-                    }
-#pragma unroll
-                    for (int k = 0; k < 16; ++k) {
-                        o0 += w8[k] * __uint_as_float(ov[k].x);
-                        o1 += w8[k] * __uint_as_float(ov[k].y);
-                        Ls += w8[k] * __shfl(lls, s0 + k, 64);
-                    }
+                for (int k = 0; k < NRANK; ++k) {
+                    const float w = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__float_as_uint(wl), k));
+                    o0 += w * __uint_as_float(ov[k].x);
+                    o1 += w * __uint_as_float(ov[k].y);
+                    Ls += __builtin_bit_cast(float, __builtin_amdgcn_readlane(__float_as_uint(wll), k));
                 }
                 const float inv = Ls > 0.f ? 1.f / Ls : 0.f;
                 const int hl = q / M, j = q % M;
                 const size_t ob = wm.oop + ((size_t)p * NGRP + g) * MW * GO * 4;
-                opnd_store(ob, GO, j, hl * HD + 2 * lane, o0 * inv);
-                opnd_store(ob, GO, j, hl * HD + 2 * lane + 1, o1 * inv);
+                const float y0 = o0 * inv, y1 = o1 * inv;
+                const bf16 h0 = (bf16)y0, h1 = (bf16)y1;
+                const bf16 l0 = (bf16)(y0 - (float)h0), l1 = (bf16)(y1 - (float)h1);
+                const unsigned hp = (unsigned)__builtin_bit_cast(unsigned short, h0) | ((unsigned)__builtin_bit_cast(unsigned short, h1) << 16);
+                const unsigned lp = (unsigned)__builtin_bit_cast(unsigned short, l0) | ((unsigned)__builtin_bit_cast(unsigned short, l1) << 16);
+                const unsigned ooff = (unsigned)(ob + ((size_t)j * GO + hl * HD + 2 * lane) * 2);
+                __builtin_amdgcn_raw_buffer_store_b32(hp, rws, ooff, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(lp, rws, ooff, MW * GO * 2, 0);
             }
         }
         publish(FL_M, p, tag, l, ST_M);
@@ -943,12 +981,16 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             const size_t ob = wm.oop + ((size_t)p * NGRP + g) * MW * GO * 4;
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
+            // fragments f0 + 3 j of the group's 8 (f = 8 is read from the next row, unused)
             uint4 xh[3][2], xl[3][2];
+            {
+                const unsigned v0 = opnd_lane(ob, GO, 0) + f0 * 64, v1 = opnd_lane(ob, GO, 1) + f0 * 64;
+                const bool live1 = 16 + lrow < M;
 #pragma unroll
-            for (int j = 0; j < 3; ++j) {
-                const int f = min(f0 + 3 * j, 7);
-#pragma unroll
-                for (int mt = 0; mt < 2; ++mt) opnd_load(ob, GO, f, mt, xh[j][mt], xl[j][mt]);
+                for (int j = 0; j < 3; ++j) {
+                    ld_frag(v0, j * 3 * 64, GO, xh[j][0], xl[j][0]);
+                    ld_frag1(live1, v1, j * 3 * 64, GO, xh[j][1], xl[j][1]);
+                }
             }
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
@@ -991,10 +1033,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---------------- R2: residual from the O partials, MLP-norm operand
         stamp(l, ST_R2, 0);
-        wait_partials(true, l);
-        bar();
-        stamp(l, ST_R2, 1);
-        stage_reduce(l, true, pk + a.off_mlp_norm + lay, wm.xm, wm.sqm, false);
+        {
+            const float2 gv = gain_pair(pk + a.off_mlp_norm + lay);
+            wait_partials(true, l);
+            bar();
+            stamp(l, ST_R2, 1);
+            stage_reduce(l, true, gv, wm.xm, wm.sqm, false);
+        }
         publish(FL_R2, p, tag, l, ST_R2);
 
         // ---------------- GU: gate/up tiles + SwiGLU
@@ -1019,18 +1064,23 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             wait_flags(FL_R2, p, tag);
             bar();
             stamp(l, ST_GU, 1);
-            float rmv[NRANK / 2];
+            u32x4 rmv[NRANK / 8];
             rm_issue(wm.sqm, p, rmv);
             const size_t xb = wm.xm + ((size_t)p * NGRP + g) * MW * H * 4;
             f32x4 acc[2][2] = {{f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}, {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}};
             f32x4 ug[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}}, uu[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             const bool mine2 = ((lrow / 4) & 1) == (r & 1);
+            // fragments f = wid + NWC j (the last ones past the hidden size are
+            // read from the next row and not used)
             uint4 xh[FPW][2], xl[FPW][2];
+            {
+                const unsigned v0 = opnd_lane(xb, H, 0) + wid * 64, v1 = opnd_lane(xb, H, 1) + wid * 64;
+                const bool live1 = 16 + lrow < M;
 #pragma unroll
-            for (int j = 0; j < FPW; ++j) {
-                const int f = min(wid + NWC * j, KBH - 1);
-#pragma unroll
-                for (int mt = 0; mt < 2; ++mt) opnd_load(xb, H, f, mt, xh[j][mt], xl[j][mt]);
+                for (int j = 0; j < FPW; ++j) {
+                    ld_frag(v0, j * NWC * 64, H, xh[j][0], xl[j][0]);
+                    ld_frag1(live1, v1, j * NWC * 64, H, xh[j][1], xl[j][1]);
+                }
             }
             rm_finish(rmv);
 #pragma unroll
@@ -1080,16 +1130,26 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         {
             // h for the rank's 12 FFN columns: 8 from the full tile, 4 from the half tile
             const size_t hb = wm.hop + ((size_t)p * NGRP + g) * MW * GF * 4;
-            for (int i = tid; i < 12 * M; i += NWC * WAVE) {
-                const int m = i / 12, c = i % 12;
+            // (pairs of adjacent columns per thread)
+            for (int i = tid; i < 6 * M; i += NWC * WAVE) {
+                const int m = i / 6, c = 2 * (i % 6);
                 int tt, gr, col;
                 if (c < 8) { tt = 0; gr = c; col = 8 * r + c; }
                 else { tt = 1; gr = 4 * (r & 1) + (c - 8); col = 256 + 4 * r + (c - 8); }
                 const float rm = s_rm[m];
-                const float gt = red_val(tt, 0, NWC, gr, m) * rm;
-                const float up = red_val(tt, 0, NWC, gr + 8, m) * rm;
-                const float hv = gt / (1.f + __expf(-gt)) * up;
-                opnd_store(hb, GF, m, col, hv);
+                unsigned short hs[2], ls[2];
+#pragma unroll
+                for (int k = 0; k < 2; ++k) {
+                    const float gt = red_val(tt, 0, NWC, gr + k, m) * rm;
+                    const float up = red_val(tt, 0, NWC, gr + k + 8, m) * rm;
+                    const float hv = gt / (1.f + __expf(-gt)) * up;
+                    const bf16 h = (bf16)hv;
+                    hs[k] = __builtin_bit_cast(unsigned short, h);
+                    ls[k] = __builtin_bit_cast(unsigned short, (bf16)(hv - (float)h));
+                }
+                const unsigned ooff = (unsigned)(hb + ((size_t)m * GF + col) * 2);
+                __builtin_amdgcn_raw_buffer_store_b32((unsigned)hs[0] | ((unsigned)hs[1] << 16), rws, ooff, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b32((unsigned)ls[0] | ((unsigned)ls[1] << 16), rws, ooff, MW * GF * 2, 0);
             }
             publish(FL_GU, p, tag, l, ST_GU);
         }
@@ -1115,11 +1175,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             uint4 xh[4][2], xl[4][2];
+            {
+                const unsigned v0 = opnd_lane(hb, GF, 0) + f0 * 64, v1 = opnd_lane(hb, GF, 1) + f0 * 64;
+                const bool live1 = 16 + lrow < M;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int f = f0 + 3 * j;
-#pragma unroll
-                for (int mt = 0; mt < 2; ++mt) opnd_load(hb, GF, f, mt, xh[j][mt], xl[j][mt]);
+                for (int j = 0; j < 4; ++j) {
+                    ld_frag(v0, j * 3 * 64, GF, xh[j][0], xl[j][0]);
+                    ld_frag1(live1, v1, j * 3 * 64, GF, xh[j][1], xl[j][1]);
+                }
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -1159,7 +1222,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     }
     // final RMSNorm operand of the LM head (group 0 writes it)
     stamp(L, 0, 0);
-    if (g == 0) stage_reduce(L, false, a.final_norm, 0, 0, true);
+    if (g == 0) stage_reduce(L, false, gain_pair(a.final_norm), 0, 0, true);
     stamp(L, 0, 1);
 }
 
