@@ -166,6 +166,31 @@ __device__ __forceinline__ void mma_k4s(f32x4& acc, const uint2& a, const f32x4&
     mma_k4(acc, a, ll);
 }
 
+// The layer GEMMs feed the matrix cores fp16 operands: the activations are
+// stored as fp16 (11 significant bits) and each lane's eight bf16 weights
+// of a fragment are converted in registers.  A bf16 value of magnitude in
+// [2^-14, 65504] is exactly an fp16 value; smaller weights round to the fp16
+// subnormal grid (absolute error below 2^-25).
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
+__device__ __forceinline__ f16x8 w_f16(const uint4& w) {
+    const unsigned u[4] = {w.x, w.y, w.z, w.w};
+    f16x8 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        r[2 * i] = (_Float16)__uint_as_float(u[i] << 16);
+        r[2 * i + 1] = (_Float16)__uint_as_float(u[i] & 0xffff0000u);
+    }
+    return r;
+}
+// acc += W_frag * X_frag (the activation fragment holds fp16 values)
+__device__ __forceinline__ void mma_h(f32x4& acc, const f16x8& w, const uint4& x) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(w, __builtin_bit_cast(f16x8, x), acc, 0, 0, 0);
+}
+__device__ __forceinline__ unsigned f16_pair(float a, float b) {
+    return (unsigned)__builtin_bit_cast(unsigned short, (_Float16)a) |
+           ((unsigned)__builtin_bit_cast(unsigned short, (_Float16)b) << 16);
+}
+
 // Static per-work-group schedule: which weight tiles, K/V blocks and
 // fragments a rank loads in each stage.
 struct Sched {
@@ -519,13 +544,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     if (cp == 0) a.lm_sq[(size_t)r * a.lm_sq_stride + m] = ss;
                 }
             } else if (live) {
-                const bf16 h0 = (bf16)o0, h1 = (bf16)o1;
-                const bf16 l0 = (bf16)(o0 - (float)h0), l1 = (bf16)(o1 - (float)h1);
-                const unsigned hp = (unsigned)__builtin_bit_cast(unsigned short, h0) | ((unsigned)__builtin_bit_cast(unsigned short, h1) << 16);
-                const unsigned lp = (unsigned)__builtin_bit_cast(unsigned short, l0) | ((unsigned)__builtin_bit_cast(unsigned short, l1) << 16);
                 const unsigned ooff = (unsigned)(out_x + ((size_t)p * NGRP + g) * MW * H * 4 + ((size_t)m * H + 32 * r + c2) * 2);
-                __builtin_amdgcn_raw_buffer_store_b32(hp, rws, ooff, 0, 0);
-                __builtin_amdgcn_raw_buffer_store_b32(lp, rws, ooff, MW * H * 2, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(f16_pair(o0, o1), rws, ooff, 0, 0);
                 if (cp == 0)
                     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(ss), rws,
                         (unsigned)(out_sq + ((((size_t)p * NGRP + g) * MW + m) * NRANK + r) * 4), 0, 0);
@@ -565,28 +585,23 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             if (lane < MW) s_rm[lane] = rsqrtf(sm / (float)H + a.eps);
         }
     };
-    // lane offset of the operand row mt * 16 + lrow at this lane's k-group;
+    // lane offset of the fp16 operand row mt * 16 + lrow at this lane's k-group;
     // rows past the block get an offset beyond the buffer's range, where a
     // buffer load reads zeros without touching memory
     auto opnd_lane = [&](size_t base_off, int ld, int mt) -> unsigned {
         const int m = mt * 16 + lrow;
         return m < M ? (unsigned)(base_off + ((size_t)m * ld + lgrp * 8) * 2) : OOB_OFF;
     };
-    // fragment at byte offset fo past the lane offset: value, and its
-    // residual MW * ld bf16 further
-    auto ld_frag = [&](unsigned voff, unsigned fo, int ld, uint4& hi, uint4& lo) {
-        hi = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, 0, SC1));
-        lo = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, MW * ld * 2, SC1));
+    // fp16 operand fragment at byte offset fo past the lane offset
+    auto ld_frag = [&](unsigned voff, unsigned fo) -> uint4 {
+        return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, 0, SC1));
     };
     // the same for the second m-tile, where only the lanes of live rows issue
-    // the loads (for a 17-row block, one row in sixteen)
-    auto ld_frag1 = [&](bool live, unsigned voff, unsigned fo, int ld, uint4& hi, uint4& lo) {
-        hi = uint4{0, 0, 0, 0};
-        lo = uint4{0, 0, 0, 0};
-        if (live) {
-            hi = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, 0, SC1));
-            lo = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, MW * ld * 2, SC1));
-        }
+    // the load (for a 17-row block, one row in sixteen)
+    auto ld_frag1 = [&](bool live, unsigned voff, unsigned fo) -> uint4 {
+        uint4 x = uint4{0, 0, 0, 0};
+        if (live) x = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, 0, SC1));
+        return x;
     };
 
     for (int l = 0; l < L; ++l) {
@@ -634,30 +649,28 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             // fragments f = wid + NWC j of the hidden size
             // fragments f = wid + NWC j (the last ones past the hidden size are
             // read from the next row and not used)
-            uint4 xh[FPW][2], xl[FPW][2];
+            uint4 xh[FPW][2];
             {
                 const unsigned v0 = opnd_lane(xb, H, 0) + wid * 64, v1 = opnd_lane(xb, H, 1) + wid * 64;
                 const bool live1 = 16 + lrow < M;
 #pragma unroll
                 for (int j = 0; j < FPW; ++j) {
-                    ld_frag(v0, j * NWC * 64, H, xh[j][0], xl[j][0]);
-                    ld_frag1(live1, v1, j * NWC * 64, H, xh[j][1], xl[j][1]);
+                    xh[j][0] = ld_frag(v0, j * NWC * 64);
+                    xh[j][1] = ld_frag1(live1, v1, j * NWC * 64);
                 }
             }
             rm_finish(rmv);
 #pragma unroll
             for (int j = 0; j < FPW; ++j) {
                 if (wid + NWC * j >= KBH) continue;
-                const uint4 w = ring_frag(wid + NWC * j);
+                const f16x8 w = w_f16(ring_frag(wid + NWC * j));
+                f16x8 ah;
+                if (LORA) ah = w_f16(av[j]);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
-                    mma_frag<bf16>(acc[mt], w, xh[j][mt]);
-                    mma_frag<bf16>(acc[mt], w, xl[j][mt]);
-                    if (LORA) {
-                        mma_frag<bf16>(uacc[mt], av[j], xh[j][mt]);
-                        mma_frag<bf16>(uacc[mt], av[j], xl[j][mt]);
-                    }
+                    mma_h(acc[mt], w, xh[j][mt]);
+                    if (LORA) mma_h(uacc[mt], ah, xh[j][mt]);
                 }
             }
             if (LORA) {
@@ -934,14 +947,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 const float inv = Ls > 0.f ? 1.f / Ls : 0.f;
                 const int hl = q / M, j = q % M;
                 const size_t ob = wm.oop + ((size_t)p * NGRP + g) * MW * GO * 4;
-                const float y0 = o0 * inv, y1 = o1 * inv;
-                const bf16 h0 = (bf16)y0, h1 = (bf16)y1;
-                const bf16 l0 = (bf16)(y0 - (float)h0), l1 = (bf16)(y1 - (float)h1);
-                const unsigned hp = (unsigned)__builtin_bit_cast(unsigned short, h0) | ((unsigned)__builtin_bit_cast(unsigned short, h1) << 16);
-                const unsigned lp = (unsigned)__builtin_bit_cast(unsigned short, l0) | ((unsigned)__builtin_bit_cast(unsigned short, l1) << 16);
                 const unsigned ooff = (unsigned)(ob + ((size_t)j * GO + hl * HD + 2 * lane) * 2);
-                __builtin_amdgcn_raw_buffer_store_b32(hp, rws, ooff, 0, 0);
-                __builtin_amdgcn_raw_buffer_store_b32(lp, rws, ooff, MW * GO * 2, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(f16_pair(o0 * inv, o1 * inv), rws, ooff, 0, 0);
             }
         }
         publish(FL_M, p, tag, l, ST_M);
@@ -982,29 +989,27 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             // fragments f0 + 3 j of the group's 8 (f = 8 is read from the next row, unused)
-            uint4 xh[3][2], xl[3][2];
+            uint4 xh[3][2];
             {
                 const unsigned v0 = opnd_lane(ob, GO, 0) + f0 * 64, v1 = opnd_lane(ob, GO, 1) + f0 * 64;
                 const bool live1 = 16 + lrow < M;
 #pragma unroll
                 for (int j = 0; j < 3; ++j) {
-                    ld_frag(v0, j * 3 * 64, GO, xh[j][0], xl[j][0]);
-                    ld_frag1(live1, v1, j * 3 * 64, GO, xh[j][1], xl[j][1]);
+                    xh[j][0] = ld_frag(v0, j * 3 * 64);
+                    xh[j][1] = ld_frag1(live1, v1, j * 3 * 64);
                 }
             }
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
                 if (f0 + 3 * j >= 8) continue;
-                const uint4 w = ring_frag(tt * 8 + f0 + 3 * j);
+                const f16x8 w = w_f16(ring_frag(tt * 8 + f0 + 3 * j));
+                f16x8 ah;
+                if (LORA) ah = w_f16(av[j]);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
-                    mma_frag<bf16>(acc[mt], w, xh[j][mt]);
-                    mma_frag<bf16>(acc[mt], w, xl[j][mt]);
-                    if (LORA) {
-                        mma_frag<bf16>(uacc[mt], av[j], xh[j][mt]);
-                        mma_frag<bf16>(uacc[mt], av[j], xl[j][mt]);
-                    }
+                    mma_h(acc[mt], w, xh[j][mt]);
+                    if (LORA) mma_h(uacc[mt], ah, xh[j][mt]);
                 }
             }
             if (LORA) {
@@ -1072,14 +1077,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             const bool mine2 = ((lrow / 4) & 1) == (r & 1);
             // fragments f = wid + NWC j (the last ones past the hidden size are
             // read from the next row and not used)
-            uint4 xh[FPW][2], xl[FPW][2];
+            uint4 xh[FPW][2];
             {
                 const unsigned v0 = opnd_lane(xb, H, 0) + wid * 64, v1 = opnd_lane(xb, H, 1) + wid * 64;
                 const bool live1 = 16 + lrow < M;
 #pragma unroll
                 for (int j = 0; j < FPW; ++j) {
-                    ld_frag(v0, j * NWC * 64, H, xh[j][0], xl[j][0]);
-                    ld_frag1(live1, v1, j * NWC * 64, H, xh[j][1], xl[j][1]);
+                    xh[j][0] = ld_frag(v0, j * NWC * 64);
+                    xh[j][1] = ld_frag1(live1, v1, j * NWC * 64);
                 }
             }
             rm_finish(rmv);
@@ -1087,21 +1092,21 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             for (int j = 0; j < FPW; ++j) {
                 const int f = wid + NWC * j;
                 if (f >= KBH) continue;
-                const uint4 w1 = ring_frag(f);
-                uint4 w2 = ring_frag(KBH + f);
-                if (!mine2) w2 = uint4{0, 0, 0, 0};
+                const f16x8 w1 = w_f16(ring_frag(f));
+                const f16x8 w2 = w_f16(mine2 ? ring_frag(KBH + f) : uint4{0, 0, 0, 0});
+                f16x8 gh, uh;
+                if (LORA) {
+                    gh = w_f16(ag[j]);
+                    uh = w_f16(au[j]);
+                }
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
-                    mma_frag<bf16>(acc[0][mt], w1, xh[j][mt]);
-                    mma_frag<bf16>(acc[0][mt], w1, xl[j][mt]);
-                    mma_frag<bf16>(acc[1][mt], w2, xh[j][mt]);
-                    mma_frag<bf16>(acc[1][mt], w2, xl[j][mt]);
+                    mma_h(acc[0][mt], w1, xh[j][mt]);
+                    mma_h(acc[1][mt], w2, xh[j][mt]);
                     if (LORA) {
-                        mma_frag<bf16>(ug[mt], ag[j], xh[j][mt]);
-                        mma_frag<bf16>(ug[mt], ag[j], xl[j][mt]);
-                        mma_frag<bf16>(uu[mt], au[j], xh[j][mt]);
-                        mma_frag<bf16>(uu[mt], au[j], xl[j][mt]);
+                        mma_h(ug[mt], gh, xh[j][mt]);
+                        mma_h(uu[mt], uh, xh[j][mt]);
                     }
                 }
             }
@@ -1137,19 +1142,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 if (c < 8) { tt = 0; gr = c; col = 8 * r + c; }
                 else { tt = 1; gr = 4 * (r & 1) + (c - 8); col = 256 + 4 * r + (c - 8); }
                 const float rm = s_rm[m];
-                unsigned short hs[2], ls[2];
+                float hv[2];
 #pragma unroll
                 for (int k = 0; k < 2; ++k) {
                     const float gt = red_val(tt, 0, NWC, gr + k, m) * rm;
                     const float up = red_val(tt, 0, NWC, gr + k + 8, m) * rm;
-                    const float hv = gt / (1.f + __expf(-gt)) * up;
-                    const bf16 h = (bf16)hv;
-                    hs[k] = __builtin_bit_cast(unsigned short, h);
-                    ls[k] = __builtin_bit_cast(unsigned short, (bf16)(hv - (float)h));
+                    hv[k] = gt / (1.f + __expf(-gt)) * up;
                 }
                 const unsigned ooff = (unsigned)(hb + ((size_t)m * GF + col) * 2);
-                __builtin_amdgcn_raw_buffer_store_b32((unsigned)hs[0] | ((unsigned)hs[1] << 16), rws, ooff, 0, 0);
-                __builtin_amdgcn_raw_buffer_store_b32((unsigned)ls[0] | ((unsigned)ls[1] << 16), rws, ooff, MW * GF * 2, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(f16_pair(hv[0], hv[1]), rws, ooff, 0, 0);
             }
             publish(FL_GU, p, tag, l, ST_GU);
         }
@@ -1174,28 +1175,26 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             const size_t hb = wm.hop + ((size_t)p * NGRP + g) * MW * GF * 4;
             f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
-            uint4 xh[4][2], xl[4][2];
+            uint4 xh[4][2];
             {
                 const unsigned v0 = opnd_lane(hb, GF, 0) + f0 * 64, v1 = opnd_lane(hb, GF, 1) + f0 * 64;
                 const bool live1 = 16 + lrow < M;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    ld_frag(v0, j * 3 * 64, GF, xh[j][0], xl[j][0]);
-                    ld_frag1(live1, v1, j * 3 * 64, GF, xh[j][1], xl[j][1]);
+                    xh[j][0] = ld_frag(v0, j * 3 * 64);
+                    xh[j][1] = ld_frag1(live1, v1, j * 3 * 64);
                 }
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const uint4 w = ring_frag(tt * 12 + f0 + 3 * j);
+                const f16x8 w = w_f16(ring_frag(tt * 12 + f0 + 3 * j));
+                f16x8 ah;
+                if (LORA) ah = w_f16(av[j]);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
-                    mma_frag<bf16>(acc[mt], w, xh[j][mt]);
-                    mma_frag<bf16>(acc[mt], w, xl[j][mt]);
-                    if (LORA) {
-                        mma_frag<bf16>(uacc[mt], av[j], xh[j][mt]);
-                        mma_frag<bf16>(uacc[mt], av[j], xl[j][mt]);
-                    }
+                    mma_h(acc[mt], w, xh[j][mt]);
+                    if (LORA) mma_h(uacc[mt], ah, xh[j][mt]);
                 }
             }
             if (LORA) {
