@@ -74,6 +74,9 @@ struct Layout {
         size_t qkv, o, gu, d, attn_norm, mlp_norm, q_norm, k_norm;
         size_t la[7];                  // LoRA shrink tiles, order q k v o gate up down
         size_t lb_qkv, lb_o, lb_gu, lb_d;  // LoRA expand blocks
+        // fp16 copies of the projection and LoRA A fragments, read by the
+        // persistent batch-1 pass (its matrix cores take fp16 operands)
+        size_t qkv16, o16, gu16, d16, la16[7];
     };
     std::vector<LayerOff> lay;
     size_t p_embed, p_final_norm, p_rope, packed_bytes;
@@ -160,6 +163,12 @@ void make_layout(const pbd_config* c, Layout& y) {
     const size_t EB = (size_t)64 * 4 * y.esz;     // bytes per LoRA expand block
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
+    // persistent batch-1 pass: the Qwen3-0.6B layer shape, bf16, LoRA rank
+    // <= 16, at most FUSED_MAX_ROWS block rows, and every attention split's
+    // K/V blocks within its LDS ring (<= 10 key blocks per split of 31)
+    const bool fused_cand = y.dtype == PBD_DTYPE_BF16 && y.H == 1024 && y.F == 3072 && y.NQ == 16 && y.NKV == 8 &&
+                            y.HD == 128 && y.RT <= 1 && y.W <= FUSED_MAX_ROWS && y.L <= 255 && y.nblk <= 310 &&
+                            c->qk_norm;
     y.p_embed = take((size_t)y.tiles_e * y.kb_e * FR);
     y.lay.resize(y.L);
     const int kb_in[7] = {y.kb_qkv, y.kb_qkv, y.kb_qkv, y.kb_o, y.kb_gu, y.kb_gu, y.kb_d};
@@ -178,6 +187,15 @@ void make_layout(const pbd_config* c, Layout& y) {
         o.lb_o = take((size_t)y.tiles_o * y.RT * EB);
         o.lb_gu = take((size_t)y.tiles_gu * y.RT * EB);
         o.lb_d = take((size_t)y.tiles_d * y.RT * EB);
+        o.qkv16 = o.o16 = o.gu16 = o.d16 = 0;
+        for (int i = 0; i < 7; ++i) o.la16[i] = 0;
+        if (fused_cand) {
+            o.qkv16 = take((size_t)y.tiles_qkv * y.kb_qkv * FR);
+            o.o16 = take((size_t)y.tiles_o * y.kb_o * FR);
+            o.gu16 = take((size_t)y.tiles_gu * y.kb_gu * FR);
+            o.d16 = take((size_t)y.tiles_d * y.kb_d * FR);
+            for (int i = 0; i < 7; ++i) o.la16[i] = take((size_t)y.RT * kb_in[i] * FR);
+        }
     }
     y.p_final_norm = take(y.H * y.esz);
     y.p_rope = take((size_t)y.max_seq * (y.HD / 2) * 8);
@@ -218,12 +236,8 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.big = y.Mmax >= BIG_MIN_MT * 16;
     y.w_u = y.big && y.r > 0 ? take((size_t)y.Mmax * 3 * y.RT * 16 * 4) : 0;   // LoRA shrink, large-M path
     y.w_dn_conf = take((size_t)y.Bmax * y.D * 4);
-    // persistent batch-1 pass: the Qwen3-0.6B layer shape, bf16, LoRA rank
-    // <= 16, at most FUSED_MAX_ROWS block rows, and every attention split's
-    // K/V blocks within its LDS ring (<= 10 key blocks per split of 31)
-    y.fused_shape = y.dtype == PBD_DTYPE_BF16 && y.H == 1024 && y.F == 3072 && y.NQ == 16 && y.NKV == 8 &&
-                    y.HD == 128 && y.RT <= 1 && y.W <= FUSED_MAX_ROWS && y.L <= 255 && y.nblk <= 310 &&
-                    c->qk_norm && y.packed_bytes < ((size_t)1 << 32);
+    // (its byte offsets into the packed weights are 32-bit)
+    y.fused_shape = fused_cand && y.packed_bytes < ((size_t)1 << 32);
     y.w_fused = y.fused_shape ? take(fused_ws_bytes()) : 0;
     y.lay_stride = y.L > 1 ? y.lay[1].qkv - y.lay[0].qkv : 0;
     y.ws_bytes = off;
@@ -406,10 +420,10 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         fa.eps = c->cfg.rms_eps; fa.scale = scale;
         fa.scale_log2 = (float)(1.0 / sqrt((double)y.HD) * 1.4426950408889634);
         fa.pos0 = pos0; fa.x0 = x; fa.pk = pk; fa.lay_stride = (uint32_t)y.lay_stride;
-        fa.off_qkv = (uint32_t)l0.qkv; fa.off_o = (uint32_t)l0.o; fa.off_gu = (uint32_t)l0.gu; fa.off_d = (uint32_t)l0.d;
+        fa.off_qkv = (uint32_t)l0.qkv16; fa.off_o = (uint32_t)l0.o16; fa.off_gu = (uint32_t)l0.gu16; fa.off_d = (uint32_t)l0.d16;
         fa.off_attn_norm = (uint32_t)l0.attn_norm; fa.off_mlp_norm = (uint32_t)l0.mlp_norm;
         fa.off_q_norm = (uint32_t)l0.q_norm; fa.off_k_norm = (uint32_t)l0.k_norm;
-        for (int i = 0; i < 7; ++i) fa.off_la[i] = (uint32_t)l0.la[i];
+        for (int i = 0; i < 7; ++i) fa.off_la[i] = (uint32_t)l0.la16[i];
         fa.off_lb_qkv = (uint32_t)l0.lb_qkv; fa.off_lb_o = (uint32_t)l0.lb_o; fa.off_lb_gu = (uint32_t)l0.lb_gu;
         fa.off_lb_d = (uint32_t)l0.lb_d;
         fa.final_norm = pk + y.p_final_norm; fa.rope = (const float2*)(pk + y.p_rope);
@@ -767,10 +781,11 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
             if (al.qkv != a0.qkv + d || al.o != a0.o + d || al.gu != a0.gu + d || al.d != a0.d + d ||
                 al.attn_norm != a0.attn_norm + d || al.mlp_norm != a0.mlp_norm + d || al.q_norm != a0.q_norm + d ||
                 al.k_norm != a0.k_norm + d || al.lb_qkv != a0.lb_qkv + d || al.lb_o != a0.lb_o + d ||
-                al.lb_gu != a0.lb_gu + d || al.lb_d != a0.lb_d + d)
+                al.lb_gu != a0.lb_gu + d || al.lb_d != a0.lb_d + d || al.qkv16 != a0.qkv16 + d ||
+                al.o16 != a0.o16 + d || al.gu16 != a0.gu16 + d || al.d16 != a0.d16 + d)
                 c->fused_dev = false;
             for (int i = 0; i < 7; ++i)
-                if (al.la[i] != a0.la[i] + d) c->fused_dev = false;
+                if (al.la[i] != a0.la[i] + d || al.la16[i] != a0.la16[i] + d) c->fused_dev = false;
         }
     }
     hipStream_t st = (hipStream_t)stream;
@@ -852,6 +867,19 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
                 const int rows[1] = {y.r};
                 const void* w[1] = {lw.lora_a[i]};
                 PBD_INIT_HIP(pack(lo.la[i], y.RT, in_f[i] / y.FK, in_f[i], MAP_CONCAT, 1, rows, w), "pack lora A");
+            }
+        }
+        if (y.fused_shape) {
+            // the persistent pass's fp16 copies of this layer's fragments
+            auto cvt = [&](size_t src, size_t dst, size_t bytes) { return launch_bf16_to_f16(c->packed + src, c->packed + dst, bytes / 4, st); };
+            PBD_INIT_HIP(cvt(lo.qkv, lo.qkv16, (size_t)y.tiles_qkv * y.kb_qkv * 1024), "fp16 qkv");
+            PBD_INIT_HIP(cvt(lo.o, lo.o16, (size_t)y.tiles_o * y.kb_o * 1024), "fp16 o");
+            PBD_INIT_HIP(cvt(lo.gu, lo.gu16, (size_t)y.tiles_gu * y.kb_gu * 1024), "fp16 gate/up");
+            PBD_INIT_HIP(cvt(lo.d, lo.d16, (size_t)y.tiles_d * y.kb_d * 1024), "fp16 down");
+            if (y.r > 0) {
+                const int in_f[7] = {y.H, y.H, y.H, y.NQ * y.HD, y.H, y.H, y.F};
+                for (int i = 0; i < 7; ++i)
+                    PBD_INIT_HIP(cvt(lo.la[i], lo.la16[i], (size_t)y.RT * (in_f[i] / y.FK) * 1024), "fp16 lora A");
             }
         }
         PBD_INIT_HIP(hipMemcpyAsync(c->packed + lo.attn_norm, lw.attn_norm, y.H * y.esz, hipMemcpyDeviceToDevice, st), "copy norm");

@@ -167,21 +167,13 @@ __device__ __forceinline__ void mma_k4s(f32x4& acc, const uint2& a, const f32x4&
 }
 
 // The layer GEMMs feed the matrix cores fp16 operands: the activations are
-// stored as fp16 (11 significant bits) and each lane's eight bf16 weights
-// of a fragment are converted in registers.  A bf16 value of magnitude in
-// [2^-14, 65504] is exactly an fp16 value; smaller weights round to the fp16
-// subnormal grid (absolute error below 2^-25).
+// stored as fp16 (11 significant bits), and the projection and LoRA A
+// fragments are read from an fp16 copy of the packed bf16 weights made at
+// initialisation.  A bf16 value of magnitude in [2^-14, 65504] is exactly an
+// fp16 value; smaller weights round to the fp16 subnormal grid (absolute
+// error below 2^-25).
 typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
-__device__ __forceinline__ f16x8 w_f16(const uint4& w) {
-    const unsigned u[4] = {w.x, w.y, w.z, w.w};
-    f16x8 r;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        r[2 * i] = (_Float16)__uint_as_float(u[i] << 16);
-        r[2 * i + 1] = (_Float16)__uint_as_float(u[i] & 0xffff0000u);
-    }
-    return r;
-}
+__device__ __forceinline__ f16x8 w_f16(const uint4& w) { return __builtin_bit_cast(f16x8, w); }
 // acc += W_frag * X_frag (the activation fragment holds fp16 values)
 __device__ __forceinline__ void mma_h(f32x4& acc, const f16x8& w, const uint4& x) {
     acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(w, __builtin_bit_cast(f16x8, x), acc, 0, 0, 0);
@@ -611,9 +603,22 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         const int p = l & 1;
         const unsigned tag = (epoch << 8) | (unsigned)l;
         const size_t lay = (size_t)l * a.lay_stride;
+        // The adapter's fragments do not depend on the activations: each
+        // GEMM stage's LoRA A fragments and B block are requested one stage
+        // ahead, so that they arrive (from HBM) while earlier stages wait.
+        uint4 laQ[FPW], laO[3], laG[FPW], laU[FPW], laD[4];
+        uint2 lbQ, lbO, lbG[2], lbD;
 
         // ---------------- R: residual from the down partials, attention-norm operand
         stamp(l, ST_R, 0);
+        if (LORA) {
+            const int src = sc.q_src();
+            const uint32_t la_off = src == 0 ? a.off_la[0] : (src == 1 ? a.off_la[1] : a.off_la[2]);
+            const uint4* la = (const uint4*)(pk + la_off + lay);
+#pragma unroll
+            for (int j = 0; j < FPW; ++j) laQ[j] = la[(size_t)min(wid + NWC * j, KBH - 1) * WAVE + lane];
+            __builtin_memcpy(&lbQ, (const bf16*)(pk + a.off_lb_qkv + lay) + ((size_t)sc.q_tile() * WAVE + lane) * 4, 8);
+        }
         {
             const float2 gv = gain_pair(pk + a.off_attn_norm + lay);
             if (l > 0) wait_partials(false, l - 1);
@@ -626,18 +631,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         // ---------------- Q: q/k/v tile
         stamp(l, ST_Q, 0);
         {
-            // the adapter's fragments do not depend on the activations: they
-            // are requested before the wait
-            uint4 av[FPW];
-            uint2 bvq;
-            if (LORA) {
-                const int src = sc.q_src();
-                const uint32_t la_off = src == 0 ? a.off_la[0] : (src == 1 ? a.off_la[1] : a.off_la[2]);
-                const uint4* la = (const uint4*)(pk + la_off + lay);
-#pragma unroll
-                for (int j = 0; j < FPW; ++j) av[j] = la[(size_t)min(wid + NWC * j, KBH - 1) * WAVE + lane];
-                __builtin_memcpy(&bvq, (const bf16*)(pk + a.off_lb_qkv + lay) + ((size_t)sc.q_tile() * WAVE + lane) * 4, 8);
-            }
             wait_flags(FL_R, p, tag);
             bar();                                           // inputs ready, ring holds the tile
             stamp(l, ST_Q, 1);
@@ -665,7 +658,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 if (wid + NWC * j >= KBH) continue;
                 const f16x8 w = w_f16(ring_frag(wid + NWC * j));
                 f16x8 ah;
-                if (LORA) ah = w_f16(av[j]);
+                if (LORA) ah = w_f16(laQ[j]);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
@@ -675,7 +668,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
             if (LORA) {
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bvq, uacc[mt] * a.scale);
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], lbQ, uacc[mt] * a.scale);
             }
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) s_red[((0 * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
@@ -913,6 +906,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---------------- M: merge the 32 split partials of query rows r, r + 32
         stamp(l, ST_M, 0);
+        if (LORA) {
+            const int tt = wid / 3, f0 = wid % 3;
+            const uint4* la = (const uint4*)(pk + a.off_la[3] + lay);
+#pragma unroll
+            for (int j = 0; j < 3; ++j) laO[j] = la[(size_t)(8 * g + min(f0 + 3 * j, 7)) * WAVE + lane];
+            __builtin_memcpy(&lbO, (const bf16*)(pk + a.off_lb_o + lay) + ((size_t)(2 * r + tt) * WAVE + lane) * 4, 8);
+        }
         wait_flags(FL_A, p, tag);
         bar();
         stamp(l, ST_M, 1);
@@ -974,14 +974,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         {
             // tile tt = wid / 3; fragments f = wid % 3 + 3 j of the group's 8
             const int tt = wid / 3, f0 = wid % 3;
-            uint4 av[3];
-            uint2 bvo;
-            if (LORA) {
-                const uint4* la = (const uint4*)(pk + a.off_la[3] + lay);
-#pragma unroll
-                for (int j = 0; j < 3; ++j) av[j] = la[(size_t)(8 * g + min(f0 + 3 * j, 7)) * WAVE + lane];
-                __builtin_memcpy(&bvo, (const bf16*)(pk + a.off_lb_o + lay) + ((size_t)(2 * r + tt) * WAVE + lane) * 4, 8);
-            }
             wait_flags(FL_M, p, tag);
             bar();
             stamp(l, ST_O, 1);
@@ -1004,7 +996,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 if (f0 + 3 * j >= 8) continue;
                 const f16x8 w = w_f16(ring_frag(tt * 8 + f0 + 3 * j));
                 f16x8 ah;
-                if (LORA) ah = w_f16(av[j]);
+                if (LORA) ah = w_f16(laO[j]);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
@@ -1014,7 +1006,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
             if (LORA) {
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bvo, uacc[mt] * a.scale);
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], lbO, uacc[mt] * a.scale);
             }
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) s_red[((tt * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
@@ -1038,6 +1030,20 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---------------- R2: residual from the O partials, MLP-norm operand
         stamp(l, ST_R2, 0);
+        if (LORA) {
+            const uint4* lag = (const uint4*)(pk + a.off_la[4] + lay);
+            const uint4* lau = (const uint4*)(pk + a.off_la[5] + lay);
+#pragma unroll
+            for (int j = 0; j < FPW; ++j) {
+                const int f = min(wid + NWC * j, KBH - 1);
+                laG[j] = lag[(size_t)f * WAVE + lane];
+                laU[j] = lau[(size_t)f * WAVE + lane];
+            }
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt)
+                __builtin_memcpy(&lbG[tt], (const bf16*)(pk + a.off_lb_gu + lay) +
+                                               ((size_t)(tt == 0 ? sc.gu_t1() : sc.gu_t2()) * WAVE + lane) * 4, 8);
+        }
         {
             const float2 gv = gain_pair(pk + a.off_mlp_norm + lay);
             wait_partials(true, l);
@@ -1050,21 +1056,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         // ---------------- GU: gate/up tiles + SwiGLU
         stamp(l, ST_GU, 0);
         {
-            uint4 ag[FPW], au[FPW];
-            uint2 bvg[2];
+            // the down stage's adapter fragments, one stage ahead
             if (LORA) {
-                const uint4* lag = (const uint4*)(pk + a.off_la[4] + lay);
-                const uint4* lau = (const uint4*)(pk + a.off_la[5] + lay);
+                const int tt = wid / 3, f0 = wid % 3;
+                const uint4* la = (const uint4*)(pk + a.off_la[6] + lay);
 #pragma unroll
-                for (int j = 0; j < FPW; ++j) {
-                    const int f = min(wid + NWC * j, KBH - 1);
-                    ag[j] = lag[(size_t)f * WAVE + lane];
-                    au[j] = lau[(size_t)f * WAVE + lane];
-                }
-#pragma unroll
-                for (int tt = 0; tt < 2; ++tt)
-                    __builtin_memcpy(&bvg[tt], (const bf16*)(pk + a.off_lb_gu + lay) +
-                                                   ((size_t)(tt == 0 ? sc.gu_t1() : sc.gu_t2()) * WAVE + lane) * 4, 8);
+                for (int j = 0; j < 4; ++j) laD[j] = la[(size_t)(12 * g + f0 + 3 * j) * WAVE + lane];
+                __builtin_memcpy(&lbD, (const bf16*)(pk + a.off_lb_d + lay) + ((size_t)(2 * r + tt) * WAVE + lane) * 4, 8);
             }
             wait_flags(FL_R2, p, tag);
             bar();
@@ -1096,8 +1094,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 const f16x8 w2 = w_f16(mine2 ? ring_frag(KBH + f) : uint4{0, 0, 0, 0});
                 f16x8 gh, uh;
                 if (LORA) {
-                    gh = w_f16(ag[j]);
-                    uh = w_f16(au[j]);
+                    gh = w_f16(laG[j]);
+                    uh = w_f16(laU[j]);
                 }
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
@@ -1113,7 +1111,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             if (LORA) {
 #pragma unroll
                 for (int tt = 0; tt < 2; ++tt) {
-                    const uint2 bv = bvg[tt];
+                    const uint2 bv = lbG[tt];
                     // rows 0-7 take the gate shrink, rows 8-15 the up shrink
                     const uint2 bg = lrow < 8 ? bv : uint2{0, 0};
                     const uint2 bu = lrow < 8 ? uint2{0, 0} : bv;
@@ -1161,14 +1159,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         {
             // tile tt = wid / 3; fragments f = wid % 3 + 3 j of the group's 12
             const int tt = wid / 3, f0 = wid % 3;
-            uint4 av[4];
-            uint2 bvd;
-            if (LORA) {
-                const uint4* la = (const uint4*)(pk + a.off_la[6] + lay);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) av[j] = la[(size_t)(12 * g + f0 + 3 * j) * WAVE + lane];
-                __builtin_memcpy(&bvd, (const bf16*)(pk + a.off_lb_d + lay) + ((size_t)(2 * r + tt) * WAVE + lane) * 4, 8);
-            }
             wait_flags(FL_GU, p, tag);
             bar();
             stamp(l, ST_D, 1);
@@ -1189,7 +1179,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             for (int j = 0; j < 4; ++j) {
                 const f16x8 w = w_f16(ring_frag(tt * 12 + f0 + 3 * j));
                 f16x8 ah;
-                if (LORA) ah = w_f16(av[j]);
+                if (LORA) ah = w_f16(laD[j]);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     if (mt >= MT) continue;
@@ -1199,7 +1189,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
             if (LORA) {
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], bvd, uacc[mt] * a.scale);
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], lbD, uacc[mt] * a.scale);
             }
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) s_red[((tt * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];

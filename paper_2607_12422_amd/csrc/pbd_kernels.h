@@ -293,6 +293,8 @@ hipError_t launch_remask(const RemaskArgs& a, int batch, hipStream_t st);
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st);
 hipError_t launch_pack_expand(int dtype, const PackExpandArgs& a, hipStream_t st);
 hipError_t launch_fill_u32(void* p, size_t n_words, uint32_t v, hipStream_t st);
+// fp16 copy of n_words words of packed bf16 pairs
+hipError_t launch_bf16_to_f16(const void* src, void* dst, size_t n_words, hipStream_t st);
 // profiling: events that the next launch records its start and end into (null: none)
 void set_launch_events(hipEvent_t start, hipEvent_t stop);
 void get_launch_events(hipEvent_t* start, hipEvent_t* stop);

@@ -1479,6 +1479,16 @@ __global__ void k_fill_u32(uint32_t* p, size_t n, uint32_t v) {
     for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
 }
 
+// fp16 copy of packed bf16 data (two values per word, round to nearest even;
+// exact for magnitudes in [2^-14, 65504])
+__global__ void k_bf16_to_f16(const uint32_t* src, uint32_t* dst, size_t n) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+        const uint32_t u = src[i];
+        const _Float16 lo = (_Float16)__uint_as_float(u << 16), hi = (_Float16)__uint_as_float(u & 0xffff0000u);
+        dst[i] = (uint32_t)__builtin_bit_cast(unsigned short, lo) | ((uint32_t)__builtin_bit_cast(unsigned short, hi) << 16);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Host-side launchers
 // ---------------------------------------------------------------------------
@@ -1996,6 +2006,11 @@ hipError_t launch_accept(const AcceptArgs& a, hipStream_t st) {
     PBD_LAUNCH(k_accept, dim3((a.B + 63) / 64), dim3(64), 0, st, a);
     return hipGetLastError();
 }
+hipError_t launch_bf16_to_f16(const void* src, void* dst, size_t n_words, hipStream_t st) {
+    PBD_LAUNCH(k_bf16_to_f16, dim3(1024), dim3(256), 0, st, (const uint32_t*)src, (uint32_t*)dst, n_words);
+    return hipGetLastError();
+}
+
 hipError_t launch_fill_u32(void* p, size_t n_words, uint32_t v, hipStream_t st) {
     if (n_words == 0) return hipSuccess;
     PBD_LAUNCH(k_fill_u32, dim3(1024), dim3(256), 0, st, (uint32_t*)p, n_words, v);
