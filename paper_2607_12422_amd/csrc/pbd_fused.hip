@@ -419,11 +419,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
     };
     f32x4* s_red = (f32x4*)scr;          // [tile][wave][mt][lane]
-    // wave 0 after barrier B: sum over waves w0..w0+nw-1 of tile tt -> value for (row n, m)
-    auto red_val = [&](int tt, int w0, int nw, int n, int m) -> float {
-        const int mt = m / 16, ln = (n / 4) * 16 + m % 16, e = n % 4;
-        float v = 0.f;
-        for (int w = w0; w < w0 + nw; ++w) v += s_red[((tt * NWC + w) * 2 + mt) * WAVE + ln][e];
+    // after barrier B: sum over waves w0..w0+nw-1 (in wave order) of tile tt's
+    // accumulator quad holding rows n = 4 q .. 4 q + 3 of block row m
+    auto red_quad = [&](int tt, int w0, int nw, int q, int m) -> f32x4 {
+        const int mt = m / 16, ln = q * 16 + m % 16;
+        f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int w = w0; w < w0 + nw; ++w) v += s_red[((tt * NWC + w) * 2 + mt) * WAVE + ln];
         return v;
     };
     const float* rope = (const float*)a.rope;
@@ -676,13 +677,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         stamp(l, ST_Q, 2);
         bar();
         {
-            // tile [16][M] -> qkv columns 16 r .. of the group's [M][512]
+            // tile [16][M] -> qkv columns 16 r .. of the group's [M][512], four columns per thread
             const size_t qb = wm.qkv + ((size_t)p * NGRP + g) * MW * GQKV * 4;
-            for (int i = tid; i < 16 * M; i += NWC * WAVE) {
-                const int n = i % 16, m = i / 16;
-                const float v = red_val(0, 0, NWC, n, m) * s_rm[m];
-                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rws,
-                    (unsigned)(qb + ((size_t)m * GQKV + 16 * r + n) * 4), 0, 0);
+            for (int i = tid; i < 4 * M; i += NWC * WAVE) {
+                const int q = i % 4, m = i / 4;
+                const f32x4 v = red_quad(0, 0, NWC, q, m) * s_rm[m];
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rws,
+                    (unsigned)(qb + ((size_t)m * GQKV + 16 * r + 4 * q) * 4), 0, 0);
             }
             publish(FL_Q, p, tag, l, ST_Q);
         }
@@ -1016,14 +1017,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         {
             // partial [M][32 columns] with tags, written through to memory
             const size_t pb = wm.parto + (((size_t)p * NGRP + g) * MW) * H * 8;
-            for (int i = tid; i < 16 * M; i += NWC * WAVE) {
-                const int m = i / 16, c2 = (i % 16) * 2;            // columns c2, c2 + 1 of the rank's 32
-                const int tt = c2 / 16, n = c2 % 16;
-                const float v0 = red_val(tt, tt * 3, 3, n, m);
-                const float v1 = red_val(tt, tt * 3, 3, n + 1, m);
-                const u32x4 pr = {__float_as_uint(v0), tag, __float_as_uint(v1), tag};
-                __builtin_amdgcn_raw_buffer_store_b128(pr, rws,
-                    (unsigned)(pb + ((size_t)m * H + 32 * r + c2) * 8), 0, SC1);
+            for (int i = tid; i < 8 * M; i += NWC * WAVE) {
+                // columns 16 tt + 4 q .. + 3 of the rank's 32
+                const int m = i / 8, tt = (i % 8) / 4, q = i % 4;
+                const f32x4 v = red_quad(tt, tt * 3, 3, q, m);
+                const unsigned off = (unsigned)(pb + ((size_t)m * H + 32 * r + 16 * tt + 4 * q) * 8);
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v[0]), tag, __float_as_uint(v[1]), tag}, rws, off, 0, SC1);
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v[2]), tag, __float_as_uint(v[3]), tag}, rws, off + 16, 0, SC1);
             }
         }
         ring_base += sc.items(ST_O);
@@ -1133,22 +1133,23 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         {
             // h for the rank's 12 FFN columns: 8 from the full tile, 4 from the half tile
             const size_t hb = wm.hop + ((size_t)p * NGRP + g) * MW * GF * 4;
-            // (pairs of adjacent columns per thread)
-            for (int i = tid; i < 6 * M; i += NWC * WAVE) {
-                const int m = i / 6, c = 2 * (i % 6);
-                int tt, gr, col;
-                if (c < 8) { tt = 0; gr = c; col = 8 * r + c; }
-                else { tt = 1; gr = 4 * (r & 1) + (c - 8); col = 256 + 4 * r + (c - 8); }
+            // (four adjacent columns per thread: gate rows 4 q .. 4 q + 3 of the
+            // tile, up rows 8 + 4 q ..)
+            for (int i = tid; i < 3 * M; i += NWC * WAVE) {
+                const int m = i / 3, jq = i % 3;
+                const int tt = jq < 2 ? 0 : 1, q = jq < 2 ? jq : (r & 1);
+                const int col = jq < 2 ? 8 * r + 4 * jq : 256 + 4 * r;
                 const float rm = s_rm[m];
-                float hv[2];
+                const f32x4 gq = red_quad(tt, 0, NWC, q, m), uq = red_quad(tt, 0, NWC, q + 2, m);
+                float hv[4];
 #pragma unroll
-                for (int k = 0; k < 2; ++k) {
-                    const float gt = red_val(tt, 0, NWC, gr + k, m) * rm;
-                    const float up = red_val(tt, 0, NWC, gr + k + 8, m) * rm;
-                    hv[k] = gt / (1.f + __expf(-gt)) * up;
+                for (int e = 0; e < 4; ++e) {
+                    const float gt = gq[e] * rm;
+                    const float up = uq[e] * rm;
+                    hv[e] = gt / (1.f + __expf(-gt)) * up;
                 }
                 const unsigned ooff = (unsigned)(hb + ((size_t)m * GF + col) * 2);
-                __builtin_amdgcn_raw_buffer_store_b32(f16_pair(hv[0], hv[1]), rws, ooff, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{f16_pair(hv[0], hv[1]), f16_pair(hv[2], hv[3])}, rws, ooff, 0, 0);
             }
             publish(FL_GU, p, tag, l, ST_GU);
         }
@@ -1197,14 +1198,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         bar();
         {
             const size_t pb = wm.partd + (((size_t)p * NGRP + g) * MW) * H * 8;
-            for (int i = tid; i < 16 * M; i += NWC * WAVE) {
-                const int m = i / 16, c2 = (i % 16) * 2;
-                const int tt = c2 / 16, n = c2 % 16;
-                const float v0 = red_val(tt, tt * 3, 3, n, m);
-                const float v1 = red_val(tt, tt * 3, 3, n + 1, m);
-                const u32x4 pr = {__float_as_uint(v0), tag, __float_as_uint(v1), tag};
-                __builtin_amdgcn_raw_buffer_store_b128(pr, rws,
-                    (unsigned)(pb + ((size_t)m * H + 32 * r + c2) * 8), 0, SC1);
+            for (int i = tid; i < 8 * M; i += NWC * WAVE) {
+                // columns 16 tt + 4 q .. + 3 of the rank's 32
+                const int m = i / 8, tt = (i % 8) / 4, q = i % 4;
+                const f32x4 v = red_quad(tt, tt * 3, 3, q, m);
+                const unsigned off = (unsigned)(pb + ((size_t)m * H + 32 * r + 16 * tt + 4 * q) * 8);
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v[0]), tag, __float_as_uint(v[1]), tag}, rws, off, 0, SC1);
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v[2]), tag, __float_as_uint(v[3]), tag}, rws, off + 16, 0, SC1);
             }
         }
         ring_base += sc.items(ST_D);
