@@ -377,14 +377,27 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         aborted = true;
     };
     // wave 0, lanes 0..31: wait until all 32 ranks' flags of (flag kind, parity) hold tag
+    // Polls keep three loads in flight per lane, so that a word is seen about
+    // one round trip after it lands rather than up to two.
     auto wait_flags = [&](int fk, int p, unsigned tag) {
         if (wid != 0) return;
-        const unsigned* f = (const unsigned*)(ws + wm.flags) + (((size_t)fk * 2 + p) * NGRP + g) * NRANK;
-        unsigned spins = 0;
+        const unsigned* f = (const unsigned*)(ws + wm.flags) + (((size_t)fk * 2 + p) * NGRP + g) * NRANK + (lane & (NRANK - 1));
         bool ok = lane >= NRANK;
-        while (!__all(ok)) {
-            if (!ok) ok = ld_sc1_u32(f + lane) == tag;
-            if (++spins > spin_limit || ((spins & 63) == 0 && ld_sc1_u32(abort_w))) {
+        unsigned q[3];
+#pragma unroll
+        for (int k = 0; k < 3; ++k) q[k] = ld_sc1_u32(f);
+        unsigned spins = 0;
+        for (;;) {
+            bool done = false;
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                ok = ok || q[k] == tag;
+                if (__all(ok)) { done = true; break; }
+                q[k] = ld_sc1_u32(f);
+            }
+            if (done) break;
+            spins += 3;
+            if (spins > spin_limit || ((spins & 63) < 3 && ld_sc1_u32(abort_w))) {
                 if (lane == 0 && spins > spin_limit) give_up();
                 break;
             }
@@ -457,12 +470,26 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         if (wid != 0) return;
         const unsigned ptag = (epoch << 8) | (unsigned)pl;
         const size_t base = (from_o ? wm.parto : wm.partd) + ((size_t)(pl & 1) * NGRP) * MW * H * 8;
-        const unsigned off = (unsigned)(base + (((size_t)(lane % NGRP) * MW + (M - 1)) * H + 32 * r + 31) * 8);
-        unsigned spins = 0;
+        // system-scope loads: past this XCD's L2, which may hold the buffer's older contents
+        const unsigned long long* pp = (const unsigned long long*)(ws + base +
+            (((size_t)(lane % NGRP) * MW + (M - 1)) * H + 32 * r + 31) * 8);
+        auto ldp = [&]() { return (unsigned)(__hip_atomic_load(pp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) >> 32); };
         bool ok = lane >= NGRP;
-        while (!__all(ok)) {
-            if (!ok) ok = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws, off, 0, SC01)).y == ptag;
-            if (++spins > spin_limit || ((spins & 63) == 0 && ld_sc1_u32(abort_w))) {
+        unsigned q[3];
+#pragma unroll
+        for (int k = 0; k < 3; ++k) q[k] = ldp();
+        unsigned spins = 0;
+        for (;;) {
+            bool done = false;
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                ok = ok || q[k] == ptag;
+                if (__all(ok)) { done = true; break; }
+                q[k] = ldp();
+            }
+            if (done) break;
+            spins += 3;
+            if (spins > spin_limit || ((spins & 63) < 3 && ld_sc1_u32(abort_w))) {
                 if (lane == 0 && spins > spin_limit) give_up();
                 break;
             }
