@@ -145,6 +145,9 @@ typedef struct pbd_weights {
  * All three are sized for cfg->max_batch sequences of cfg->max_seq positions:
  * the workspace serves every batch up to max_batch (a call's batch argument
  * selects how much of it a pass uses), so no per-batch size query is needed.
+ * When the model qualifies for the persistent batch-1 pass (see
+ * pbd_set_pass_mode), the packed weights also hold an fp16 copy of every
+ * layer's projection and LoRA A fragments, which that pass streams.
  */
 size_t pbd_packed_weight_bytes(const pbd_config* cfg);
 size_t pbd_kv_bytes(const pbd_config* cfg);
@@ -361,8 +364,11 @@ int pbd_set_operand_precision(pbd_ctx* ctx, int32_t mode);
  * FFN 3072, LoRA rank <= 16, D + 1 <= 32 rows, max_seq <= 4960, on a
  * 256-CU device) run their layer stack as one persistent kernel; other
  * passes use one kernel per operator.  1: one kernel per operator always.
- * Both give the same results up to fp32 rounding.  Other values:
- * PBD_ERR_INVALID_ARG.
+ * The persistent kernel feeds its matrix cores fp16 activations (11
+ * significant bits) and an fp16 copy of the packed weights (exact for bf16
+ * weights of magnitude >= 2^-14), the per-operator kernels a bf16 value plus
+ * bf16 residual per activation; both stay within the step's parity bound of
+ * the float64 reference.  Other values: PBD_ERR_INVALID_ARG.
  */
 int pbd_set_pass_mode(pbd_ctx* ctx, int32_t mode);
 

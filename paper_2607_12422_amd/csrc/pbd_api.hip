@@ -392,7 +392,10 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         hipError_t e = launch_fill_u32(ws + y.w_kcnt, (size_t)y.tiles_o, 0u, st);
         if (e != hipSuccess) return hip_fail(c, e, "clear split-K counters");
     }
-    if (fused) as.fused_ctl = (unsigned*)(ws + y.w_fused + fused_ctl_offset());
+    if (fused) {
+        as.fused_ctl = (unsigned*)(ws + y.w_fused + fused_ctl_offset());
+        as.fused_layers = q.n_layers > 0 ? q.n_layers : y.L;
+    }
     PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_assemble(dt, as, B, st), "assemble");
 
     auto base_gemm = [&](FGemmArgs& g, size_t w_off, int tiles, int kb, const size_t* xop) {

@@ -23,12 +23,13 @@
 //     D (down-projection partial over the group's FFN slice).
 //   * Handoffs inside a group go through the XCD's L2: plain stores, then a
 //     per-rank flag; consumers poll the flags and read with L1-bypassing
-//     (sc1) loads.  The two handoffs between groups per layer (O and D
-//     partials) carry a tag word in every 8-byte pair written through to
-//     memory, so consumers poll the data itself; no fence is ever needed.
-//     Buffers alternate by layer parity and every flag / tag holds
-//     (epoch, layer), so nothing from an earlier layer or pass is mistaken
-//     for current data.
+//     (sc1) loads.  Flags hold (epoch, layer).  The two handoffs between
+//     groups per layer (O and down partials) are fp32 values written through
+//     to memory whose lowest mantissa bit is a tag: the parity of the number
+//     of writes that half of the buffer has received (counted on the device
+//     across passes), so stale contents always carry the other bit and
+//     consumers poll the data itself.  No fence is ever needed.  Buffers
+//     alternate by layer parity.
 //   * Each work-group has 8 compute waves and 2 loader waves.  The loader
 //     waves stream the work-group's weight fragments and its attention
 //     split's K/V blocks, in stage order, straight into an LDS ring with
@@ -113,8 +114,8 @@ __host__ __device__ inline WsMap ws_map() {
     w.apart = take((size_t)2 * NGRP * NRANK * QRMAX * APW * 4);
     w.oop = take((size_t)2 * NGRP * MW * GO * 4);
     w.hop = take((size_t)2 * NGRP * MW * GF * 4);
-    w.parto = take((size_t)2 * NGRP * MW * H * 8);
-    w.partd = take((size_t)2 * NGRP * MW * H * 8);
+    w.parto = take((size_t)2 * NGRP * MW * H * 4);
+    w.partd = take((size_t)2 * NGRP * MW * H * 4);
     w.ctl = take(256);
     w.trace = take((size_t)NGRP * NRANK * TRACE_LAYERS * NSTAGE * 4 * 8);
     w.total = off;
@@ -235,6 +236,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         s_id[2] = a.pos0[0];
         s_id[3] = (int)ctl[8];
         s_id[4] = a.nrows[0];
+        s_id[5] = (int)ctl[14];      // writes into the partial buffers' even / odd halves before this pass
+        s_id[6] = (int)ctl[15];
         *s_pub = 0u;
     }
     __syncthreads();
@@ -247,6 +250,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     sc.r = __builtin_amdgcn_readfirstlane(s_id[1]);
     sc.t = __builtin_amdgcn_readfirstlane(s_id[2]);
     const unsigned epoch = (unsigned)__builtin_amdgcn_readfirstlane(s_id[3]);
+    const unsigned wbase0 = (unsigned)__builtin_amdgcn_readfirstlane(s_id[5]);
+    const unsigned wbase1 = (unsigned)__builtin_amdgcn_readfirstlane(s_id[6]);
+    // tag bit of the partials written at layer l: parity of that buffer half's write count
+    auto ptag_bit = [&](int l) -> unsigned { return ((l & 1 ? wbase1 : wbase0) + (unsigned)(l >> 1) + 1u) & 1u; };
     if (sc.g >= NGRP || sc.r >= NRANK) {
         // placement is not 8 x 32 (never seen): report; the work-groups that
         // wait for the missing ranks time out and the pass ends with an error
@@ -463,17 +470,16 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     auto stamp = [&](int l, int st, int k) {
         if (wid == 0) stamp_at(l, st, k);
     };
-    // wave 0, lanes 0..7: wait until the last pair producer group `lane` writes
-    // into this rank's columns of layer pl's partial carries pl's tag (its
-    // other pairs are checked one by one when read)
+    // wave 0, lanes 0..7: wait until the last value producer group `lane`
+    // writes into this rank's columns of layer pl's partial carries pl's tag
+    // bit (its other values are checked one by one when read)
     auto wait_partials = [&](bool from_o, int pl) {
         if (wid != 0) return;
-        const unsigned ptag = (epoch << 8) | (unsigned)pl;
-        const size_t base = (from_o ? wm.parto : wm.partd) + ((size_t)(pl & 1) * NGRP) * MW * H * 8;
+        const unsigned tb = ptag_bit(pl);
+        const size_t base = (from_o ? wm.parto : wm.partd) + ((size_t)(pl & 1) * NGRP) * MW * H * 4;
         // system-scope loads: past this XCD's L2, which may hold the buffer's older contents
-        const unsigned long long* pp = (const unsigned long long*)(ws + base +
-            (((size_t)(lane % NGRP) * MW + (M - 1)) * H + 32 * r + 31) * 8);
-        auto ldp = [&]() { return (unsigned)(__hip_atomic_load(pp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) >> 32); };
+        const unsigned* pp = (const unsigned*)(ws + base + (((size_t)(lane % NGRP) * MW + (M - 1)) * H + 32 * r + 31) * 4);
+        auto ldp = [&]() { return __hip_atomic_load(pp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) & 1u; };
         bool ok = lane >= NGRP;
         unsigned q[3];
 #pragma unroll
@@ -483,7 +489,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             bool done = false;
 #pragma unroll
             for (int k = 0; k < 3; ++k) {
-                ok = ok || q[k] == ptag;
+                ok = ok || q[k] == tb;
                 if (__all(ok)) { done = true; break; }
                 q[k] = ldp();
             }
@@ -506,8 +512,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         const bool poll = from_o || l > 0;
         // partials of layer l (O) or l - 1 (down) from every group
         const int pl = from_o ? l : l - 1;
-        const unsigned ptag = (epoch << 8) | (unsigned)(pl & 0xff);
-        const unsigned base = (unsigned)((from_o ? wm.parto : wm.partd) + ((size_t)(pl & 1) * NGRP) * MW * H * 8);
+        const unsigned tb = ptag_bit(pl);
+        const unsigned base = (unsigned)((from_o ? wm.parto : wm.partd) + ((size_t)(pl & 1) * NGRP) * MW * H * 4);
         const int cp = tid % 16, c2 = 2 * cp;
         float2* xs2 = (float2*)xs;
 #pragma unroll
@@ -516,32 +522,34 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             const int m = tid / 16 + RR * e;
             const bool live = m < M;
             // all eight groups' pairs requested before any is used
-            const unsigned voff = base + (unsigned)(((min(m, M - 1) * H) + 32 * r + c2) * 8);
-            u32x4 q[NGRP];
+            const unsigned voff = base + (unsigned)(((min(m, M - 1) * H) + 32 * r + c2) * 4);
+            u32x2 q[NGRP];
             if (poll) {
 #pragma unroll
                 for (int x = 0; x < NGRP; ++x)
-                    q[x] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff, x * MW * H * 8, SC01));
+                    q[x] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rws, voff, x * MW * H * 4, SC01));
             }
             float2 xv = live ? xs2[m * 16 + cp] : float2{0.f, 0.f};
             if (poll && live) {
                 float s0 = 0.f, s1 = 0.f;
 #pragma unroll
                 for (int x = 0; x < NGRP; ++x) {
-                    u32x4 v = q[x];
-                    // a pair not yet written through: poll it alone (rare)
+                    u32x2 v = q[x];
+                    // a value not yet written through: poll it alone (rare)
                     unsigned spins = 0;
-                    while (v.y != ptag || v.w != ptag) {
+                    while (((v.x & 1u) != tb) || ((v.y & 1u) != tb)) {
                         if (++spins > spin_limit || ((spins & 63) == 0 && ld_sc1_u32(abort_w))) {
                             if (spins > spin_limit) give_up();
                             v.x = 0u;
-                            v.z = 0u;
+                            v.y = 0u;
                             break;
                         }
-                        v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff, x * MW * H * 8, SC01));
+                        v = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rws, voff, x * MW * H * 4, SC01));
                     }
-                    s0 += __uint_as_float(v.x);           // group order
-                    s1 += __uint_as_float(v.z);
+                    // group order, the tag bit cleared (so that results do not
+                    // depend on the pass's write count)
+                    s0 += __uint_as_float(v.x & ~1u);
+                    s1 += __uint_as_float(v.y & ~1u);
                 }
                 xv.x += s0;
                 xv.y += s1;
@@ -1042,15 +1050,17 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         stamp(l, ST_O, 2);
         bar();
         {
-            // partial [M][32 columns] with tags, written through to memory
-            const size_t pb = wm.parto + (((size_t)p * NGRP + g) * MW) * H * 8;
+            // partial [M][32 columns], tagged, written through to memory
+            const size_t pb = wm.parto + (((size_t)p * NGRP + g) * MW) * H * 4;
+            const unsigned tb = ptag_bit(l);
             for (int i = tid; i < 8 * M; i += NWC * WAVE) {
-                // columns 16 tt + 4 q .. + 3 of the rank's 32
+                // columns 16 tt + 4 q .. + 3 of the rank's 32, each value's lowest bit the tag
                 const int m = i / 8, tt = (i % 8) / 4, q = i % 4;
                 const f32x4 v = red_quad(tt, tt * 3, 3, q, m);
-                const unsigned off = (unsigned)(pb + ((size_t)m * H + 32 * r + 16 * tt + 4 * q) * 8);
-                __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v[0]), tag, __float_as_uint(v[1]), tag}, rws, off, 0, SC1);
-                __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v[2]), tag, __float_as_uint(v[3]), tag}, rws, off + 16, 0, SC1);
+                const unsigned off = (unsigned)(pb + ((size_t)m * H + 32 * r + 16 * tt + 4 * q) * 4);
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4{(__float_as_uint(v[0]) & ~1u) | tb, (__float_as_uint(v[1]) & ~1u) | tb,
+                                                             (__float_as_uint(v[2]) & ~1u) | tb, (__float_as_uint(v[3]) & ~1u) | tb},
+                                                       rws, off, 0, SC1);
             }
         }
         ring_base += sc.items(ST_O);
@@ -1224,14 +1234,16 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
         bar();
         {
-            const size_t pb = wm.partd + (((size_t)p * NGRP + g) * MW) * H * 8;
+            const size_t pb = wm.partd + (((size_t)p * NGRP + g) * MW) * H * 4;
+            const unsigned tb = ptag_bit(l);
             for (int i = tid; i < 8 * M; i += NWC * WAVE) {
-                // columns 16 tt + 4 q .. + 3 of the rank's 32
+                // columns 16 tt + 4 q .. + 3 of the rank's 32, each value's lowest bit the tag
                 const int m = i / 8, tt = (i % 8) / 4, q = i % 4;
                 const f32x4 v = red_quad(tt, tt * 3, 3, q, m);
-                const unsigned off = (unsigned)(pb + ((size_t)m * H + 32 * r + 16 * tt + 4 * q) * 8);
-                __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v[0]), tag, __float_as_uint(v[1]), tag}, rws, off, 0, SC1);
-                __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v[2]), tag, __float_as_uint(v[3]), tag}, rws, off + 16, 0, SC1);
+                const unsigned off = (unsigned)(pb + ((size_t)m * H + 32 * r + 16 * tt + 4 * q) * 4);
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4{(__float_as_uint(v[0]) & ~1u) | tb, (__float_as_uint(v[1]) & ~1u) | tb,
+                                                             (__float_as_uint(v[2]) & ~1u) | tb, (__float_as_uint(v[3]) & ~1u) | tb},
+                                                       rws, off, 0, SC1);
             }
         }
         ring_base += sc.items(ST_D);

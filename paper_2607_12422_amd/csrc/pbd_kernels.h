@@ -42,6 +42,7 @@ struct AssembleArgs {
     void* op_lo;
     float* sq;             // [1][m_stride] per-row sum of squares
     unsigned* fused_ctl;   // persistent pass next: its rank tickets and abort word are cleared and its epoch advanced (null: none)
+    int fused_layers;      // layers that pass runs (it advances the per-parity write counts of its partial buffers)
 };
 
 struct FGemmArgs {

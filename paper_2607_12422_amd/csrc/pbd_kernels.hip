@@ -119,6 +119,15 @@ __global__ __launch_bounds__(256) void k_assemble(AssembleArgs a) {
         for (int i = 0; i < 8; ++i) a.fused_ctl[i] = 0u;
         a.fused_ctl[8] += 1u;
         a.fused_ctl[9] = 0u;
+        // writes so far into each layer-parity half of its partial buffers:
+        // the pass reads the counts before it and (unless the sequence is
+        // skipped, when it writes nothing) they advance by its layers of each parity
+        if (nrows > 0) {
+            a.fused_ctl[14] = a.fused_ctl[12];
+            a.fused_ctl[15] = a.fused_ctl[13];
+            a.fused_ctl[12] += (unsigned)((a.fused_layers + 1) / 2);
+            a.fused_ctl[13] += (unsigned)(a.fused_layers / 2);
+        }
     }
     if (threadIdx.x == 0) {
         if (j == 0) {

@@ -176,7 +176,12 @@ def test_config5_full_batch_properties_and_sampled_sequence():
     assert g.torch.equal(olg, mlg)
     del olg, mlg
 
-    # sequence independence: sequence 0 alone gives the same logits
+    # sequence independence: sequence 0 alone gives the same logits up to the
+    # rounding differences of its kernels.  Alone (33 rows) it runs the skinny
+    # projection GEMM and the automatic keys per split of a batch of one; in
+    # the batch (1056 rows) the large-M GEMM and longer splits.  The two sum
+    # in different orders and round the attention weights to bf16 over
+    # different splits: 2.6e-3 (draft) / 2.2e-3 (verify) measured, bound 5e-3.
     g1 = GpuRun(cfg, w, max_batch=1, max_seq=max_seq, dev_weights=g.dw)
     a1 = g1.prefill([prompts[0]])
     assert int(a1[0]) == int(anchors[0])
@@ -185,7 +190,7 @@ def test_config5_full_batch_properties_and_sampled_sequence():
     for alone, batched, what in ((dlg1.cpu().numpy()[0], dlg_np[0], "draft"), (vlg1.cpu().numpy()[0], vlg_np[0], "verify")):
         err = float(np.abs(alone - batched).max())
         print(f"config 5 sequence 0 alone vs in the batch ({what}): max-abs {err:.2e}")
-        assert err <= 1e-2
+        assert err <= 5e-3
     dec = decisive(dlg_np[0][1:], 2e-2, cfg.mask_id)
     assert np.array_equal(d1.cpu().numpy()[0][dec], d_np[0][dec])
     g1.close()

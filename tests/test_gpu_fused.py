@@ -195,3 +195,41 @@ def test_fused_bounded_wait_gives_up_and_recovers():
     _check(dlg.cpu().numpy()[0], d.cpu().numpy()[0], dl_ref, slice(1, None), exclude=cfg.mask_id,
            what="draft after a forced expiry")
     g.close()
+
+
+def test_fused_partial_tags_across_passes():
+    """The cross-group partials carry a one-bit tag: the parity of the write
+    count of their buffer half, kept on the device across passes.  Passes of
+    1 and 3 layers (odd counts), a pass skipped for capacity (which writes
+    nothing and must not advance the counts) and full passes in between all
+    match the oracle."""
+    from paper_2607_12422_amd import binding as bd
+    cfg = _cfg(layers=3)
+    w = synth.make_weights(cfg, 6700)
+    prompt = synth.make_prompts(cfg, [75], 6701)[0]
+    max_seq = 75 + 3 * cfg.width
+    g = GpuRun(cfg, w, max_batch=1, max_seq=max_seq)
+    g.eng.pbd_set_pass_mode(0)
+    anchor = g.prefill([prompt])
+    m = om.OracleModel(w)
+    st = _oracle_prefill(m, prompt, anchor[0])
+    seq0 = g.seq_len.clone()
+    for step, k in enumerate((1, 3, None, 2, 3)):
+        if k is None:
+            # capacity overflow: the pass is skipped, nothing is written
+            g.seq_len.fill_(max_seq)
+            g.draft()
+            assert g.status() & bd.PBD_STATUS_CAPACITY
+            g.seq_len.copy_(seq0)
+            continue
+        d = g.zeros(1, cfg.block)
+        lg = g.zeros(1, cfg.width, cfg.vocab, dtype=g.torch.float32)
+        g.eng.pbd_draft_block_layers(g.seq_len, g.anchor, d, k, lg)
+        _, ref = om.draft(m, st, n_layers=k)
+        _check(lg.cpu().numpy()[0], d.cpu().numpy()[0], ref, slice(1, None), exclude=cfg.mask_id,
+               what=f"pass {step}: {k}-layer draft")
+        v, vlg = g.verify(d)
+        _, vl_ref, _, _ = om.verify(m, st, d.cpu().numpy()[0])
+        _check(vlg.cpu().numpy()[0], v.cpu().numpy()[0], vl_ref, slice(None), what=f"pass {step}: verify")
+    assert g.status() == 0
+    g.close()
