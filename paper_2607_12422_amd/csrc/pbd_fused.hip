@@ -127,8 +127,8 @@ typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
 
 // Cache-policy bits of buffer instructions: sc0 = 1, nt = 2, sc1 = 16.
 constexpr int SC1 = 16, SC01 = 17, NT = 2;
-// Range of the workspace's buffer resource (bytes) and an offset past it.
-constexpr unsigned WS_RANGE = 0x7fffffffu, OOB_OFF = 0x80000000u;
+// Range of the workspace's buffer resource (bytes).
+constexpr unsigned WS_RANGE = 0x7fffffffu;
 
 __device__ __forceinline__ unsigned xcc_id() {
     unsigned v;
@@ -182,6 +182,14 @@ __device__ __forceinline__ void mma_h(f32x4& acc, const f16x8& w, const uint4& x
 __device__ __forceinline__ unsigned f16_pair(float a, float b) {
     return (unsigned)__builtin_bit_cast(unsigned short, (_Float16)a) |
            ((unsigned)__builtin_bit_cast(unsigned short, (_Float16)b) << 16);
+}
+
+// Byte offset of element (row m, column k) of a fragment-major fp16
+// activation operand: fragment k / 32 of m-tile m / 16 is 1 KiB at
+// (2 (k / 32) + m / 16) * 1024, in MFMA operand order (lane = 16 k-group +
+// row, eight consecutive k per lane).
+__device__ __forceinline__ unsigned opnd_elem(int m, int k) {
+    return (unsigned)(((((k / 32) * 2 + m / 16) * 64 + ((k % 32) / 8) * 16 + m % 16) * 8 + k % 8) * 2);
 }
 
 // Static per-work-group schedule: which weight tiles, K/V blocks and
@@ -572,7 +580,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     if (cp == 0) a.lm_sq[(size_t)r * a.lm_sq_stride + m] = ss;
                 }
             } else if (live) {
-                const unsigned ooff = (unsigned)(out_x + ((size_t)p * NGRP + g) * MW * H * 4 + ((size_t)m * H + 32 * r + c2) * 2);
+                const unsigned ooff = (unsigned)(out_x + ((size_t)p * NGRP + g) * MW * H * 4) + opnd_elem(m, 32 * r + c2);
                 __builtin_amdgcn_raw_buffer_store_b32(f16_pair(o0, o1), rws, ooff, 0, 0);
                 if (cp == 0)
                     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(ss), rws,
@@ -613,22 +621,22 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             if (lane < MW) s_rm[lane] = rsqrtf(sm / (float)H + a.eps);
         }
     };
-    // lane offset of the fp16 operand row mt * 16 + lrow at this lane's k-group;
-    // rows past the block get an offset beyond the buffer's range, where a
-    // buffer load reads zeros without touching memory
-    auto opnd_lane = [&](size_t base_off, int ld, int mt) -> unsigned {
-        const int m = mt * 16 + lrow;
-        return m < M ? (unsigned)(base_off + ((size_t)m * ld + lgrp * 8) * 2) : OOB_OFF;
+    // The fp16 activation operands are stored fragment-major: fragment f of
+    // m-tile mt is 1 KiB at byte (2 f + mt) * 1024, lane l's 16 bytes (row
+    // l % 16, k-group l / 16) at l * 16, so one wavefront load reads 1 KiB of
+    // contiguous memory.  Rows past the block are never written and stay zero.
+    auto opnd_lane = [&](size_t base_off, int mt) -> unsigned {
+        return (unsigned)(base_off + (size_t)mt * 1024 + (size_t)lane * 16);
     };
-    // fp16 operand fragment at byte offset fo past the lane offset
+    // fp16 operand fragment fo bytes past the lane offset (fo: a wave-uniform constant)
     auto ld_frag = [&](unsigned voff, unsigned fo) -> uint4 {
-        return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, 0, SC1));
+        return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff, fo, SC1));
     };
     // the same for the second m-tile, where only the lanes of live rows issue
     // the load (for a 17-row block, one row in sixteen)
     auto ld_frag1 = [&](bool live, unsigned voff, unsigned fo) -> uint4 {
         uint4 x = uint4{0, 0, 0, 0};
-        if (live) x = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff + fo, 0, SC1));
+        if (live) x = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rws, voff, fo, SC1));
         return x;
     };
 
@@ -680,12 +688,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             // read from the next row and not used)
             uint4 xh[FPW][2];
             {
-                const unsigned v0 = opnd_lane(xb, H, 0) + wid * 64, v1 = opnd_lane(xb, H, 1) + wid * 64;
+                const unsigned v0 = opnd_lane(xb, 0) + wid * 2048, v1 = opnd_lane(xb, 1) + wid * 2048;
                 const bool live1 = 16 + lrow < M;
 #pragma unroll
                 for (int j = 0; j < FPW; ++j) {
-                    xh[j][0] = ld_frag(v0, j * NWC * 64);
-                    xh[j][1] = ld_frag1(live1, v1, j * NWC * 64);
+                    xh[j][0] = ld_frag(v0, j * NWC * 2048);
+                    xh[j][1] = ld_frag1(live1, v1, j * NWC * 2048);
                 }
             }
             rm_finish(rmv);
@@ -983,7 +991,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 const float inv = Ls > 0.f ? 1.f / Ls : 0.f;
                 const int hl = q / M, j = q % M;
                 const size_t ob = wm.oop + ((size_t)p * NGRP + g) * MW * GO * 4;
-                const unsigned ooff = (unsigned)(ob + ((size_t)j * GO + hl * HD + 2 * lane) * 2);
+                const unsigned ooff = (unsigned)ob + opnd_elem(j, hl * HD + 2 * lane);
                 __builtin_amdgcn_raw_buffer_store_b32(f16_pair(o0 * inv, o1 * inv), rws, ooff, 0, 0);
             }
         }
@@ -1019,12 +1027,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             // fragments f0 + 3 j of the group's 8 (f = 8 is read from the next row, unused)
             uint4 xh[3][2];
             {
-                const unsigned v0 = opnd_lane(ob, GO, 0) + f0 * 64, v1 = opnd_lane(ob, GO, 1) + f0 * 64;
+                const unsigned v0 = opnd_lane(ob, 0) + f0 * 2048, v1 = opnd_lane(ob, 1) + f0 * 2048;
                 const bool live1 = 16 + lrow < M;
 #pragma unroll
                 for (int j = 0; j < 3; ++j) {
-                    xh[j][0] = ld_frag(v0, j * 3 * 64);
-                    xh[j][1] = ld_frag1(live1, v1, j * 3 * 64);
+                    xh[j][0] = ld_frag(v0, j * 3 * 2048);
+                    xh[j][1] = ld_frag1(live1, v1, j * 3 * 2048);
                 }
             }
 #pragma unroll
@@ -1114,12 +1122,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             // read from the next row and not used)
             uint4 xh[FPW][2];
             {
-                const unsigned v0 = opnd_lane(xb, H, 0) + wid * 64, v1 = opnd_lane(xb, H, 1) + wid * 64;
+                const unsigned v0 = opnd_lane(xb, 0) + wid * 2048, v1 = opnd_lane(xb, 1) + wid * 2048;
                 const bool live1 = 16 + lrow < M;
 #pragma unroll
                 for (int j = 0; j < FPW; ++j) {
-                    xh[j][0] = ld_frag(v0, j * NWC * 64);
-                    xh[j][1] = ld_frag1(live1, v1, j * NWC * 64);
+                    xh[j][0] = ld_frag(v0, j * NWC * 2048);
+                    xh[j][1] = ld_frag1(live1, v1, j * NWC * 2048);
                 }
             }
             rm_finish(rmv);
@@ -1185,7 +1193,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     const float up = uq[e] * rm;
                     hv[e] = gt / (1.f + __expf(-gt)) * up;
                 }
-                const unsigned ooff = (unsigned)(hb + ((size_t)m * GF + col) * 2);
+                const unsigned ooff = (unsigned)hb + opnd_elem(m, col);
                 __builtin_amdgcn_raw_buffer_store_b64(u32x2{f16_pair(hv[0], hv[1]), f16_pair(hv[2], hv[3])}, rws, ooff, 0, 0);
             }
             publish(FL_GU, p, tag, l, ST_GU);
@@ -1205,12 +1213,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             f32x4 uacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
             uint4 xh[4][2];
             {
-                const unsigned v0 = opnd_lane(hb, GF, 0) + f0 * 64, v1 = opnd_lane(hb, GF, 1) + f0 * 64;
+                const unsigned v0 = opnd_lane(hb, 0) + f0 * 2048, v1 = opnd_lane(hb, 1) + f0 * 2048;
                 const bool live1 = 16 + lrow < M;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    xh[j][0] = ld_frag(v0, j * 3 * 64);
-                    xh[j][1] = ld_frag1(live1, v1, j * 3 * 64);
+                    xh[j][0] = ld_frag(v0, j * 3 * 2048);
+                    xh[j][1] = ld_frag1(live1, v1, j * 3 * 2048);
                 }
             }
 #pragma unroll
