@@ -748,21 +748,27 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             };
             // Row jobs of 16 lanes each: the query rows q < QR (head q / M,
             // block row q % M), then (block split) the key rows and the value
-            // rows of the block.  Lane group tg (of NG16) takes jobs tg + NG16 k,
-            // NJ at a time; the position table and the norm gains are requested
-            // before the wait, the q/k/v values after it.
+            // rows of the block, or (verify, prefix splits) the key and value
+            // rows r and r + 31 of the block that this rank appends to the
+            // cache.  Lane group tg (of NG16) takes jobs tg + NG16 k, NJ at a
+            // time; the position table and the norm gains are requested before
+            // the wait, the q/k/v values after it.
             constexpr int NG16 = NWC * WAVE / 16, NJ = 3;
             const int tg = tid / 16;
             const int nkrow = blk ? ((M + 15) / 16) * 16 : 0;    // key rows incl. padding to the key block
-            const int njob = QR + (blk ? 2 * M : 0);
+            const int nkv = min(M, a.kv_rows);
+            const int ncr = blk ? 0 : (r < nkv ? 1 : 0) + (r + NRANK - 1 < nkv ? 1 : 0);   // cache rows of this rank
+            const int njob = QR + (blk ? 2 * M : 2 * ncr);
             Gains<bf16, HD> gq, gk;
             if (a.qk_norm) {
                 gq.load(pk + a.off_q_norm + lay, lrow);
                 gk.load(pk + a.off_k_norm + lay, lrow);
             }
-            // job j: kind (0 query, 1 key, 2 value), block row and source column
+            // job j: kind (0 query, 1 key, 2 value into LDS; 3 key, 4 value
+            // into the cache), block row and source column
             auto job = [&](int j, int& kind, int& row, int& col) {
                 if (j < QR) { kind = 0; row = j % M; col = (j / M) * HD; }
+                else if (!blk) { const int c = j - QR; kind = 3 + (c & 1); row = r + (NRANK - 1) * (c >> 1); col = (2 + (c & 1)) * HD; }
                 else if (j < QR + M) { kind = 1; row = j - QR; col = 2 * HD; }
                 else { kind = 2; row = j - QR - M; col = 3 * HD; }
             };
@@ -803,6 +809,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                             vb_l[row * HD + RP::NP * lrow + pp] = (bf16)vlo[k][pp];
                             vb_l[row * HD + RP::HALF + RP::NP * lrow + pp] = (bf16)vhi[k][pp];
                         }
+                    } else if (kind == 4) {
+                        // value row for the cache: LDS row (row / 31) of the value
+                        // buffer, which prefix splits do not use otherwise
+                        const int cr = row / (NRANK - 1);
+#pragma unroll
+                        for (int pp = 0; pp < RP::NP; ++pp) {
+                            vb_l[cr * HD + RP::NP * lrow + pp] = (bf16)vlo[k][pp];
+                            vb_l[cr * HD + RP::HALF + RP::NP * lrow + pp] = (bf16)vhi[k][pp];
+                        }
                     } else {
                         RP rp;
                         bf16 lo[RP::NP], hi[RP::NP];
@@ -815,7 +830,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                             gl[pp] = kind == 0 ? gql[pp] : gkl[pp];
                             gh[pp] = kind == 0 ? gqh[pp] : gkh[pp];
                         }
-                        rp.finish(kind == 0 ? q_l + j * LDQ : kb_l + row * LDQ, true, gl, gh, a.qk_norm, a.eps, lrow, lo, hi);
+                        // (a key row for the cache goes to LDS row (row / 31) of the
+                        // key buffer, which prefix splits do not use otherwise)
+                        rp.finish(kind == 0 ? q_l + j * LDQ : kb_l + (kind == 1 ? row : row / (NRANK - 1)) * LDQ, true, gl, gh,
+                                  a.qk_norm, a.eps, lrow, lo, hi);
                     }
                 }
             }
@@ -996,20 +1014,21 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
         }
         publish(FL_M, p, tag, l, ST_M);
-        if (r == NRANK - 1 && a.kv_rows > 0) {
-            // verify: append the block K/V (still in LDS from the attention
-            // stage) to the cache at t .. t + kv_rows - 1, after the flag, so
-            // that the stores stay off the stage chain
+        {
+            // verify: this rank's rows r and r + 31 of the block K/V (kept in
+            // LDS since the attention stage) appended to the cache at t + row,
+            // after the flag, so that the stores stay off the stage chain
+            const int nkv = min(M, a.kv_rows);
+            const int ncr = r == NRANK - 1 ? 0 : (r < nkv ? 1 : 0) + (r + NRANK - 1 < nkv ? 1 : 0);
             const bf16* kb_l = (const bf16*)(scr + QL_BYTES);
             const bf16* vb_l = (const bf16*)(scr + QL_BYTES + KL_BYTES);
-            const int nr = min(M, a.kv_rows);
             const size_t head = (((size_t)l * a.Bmax) * NKV + g) * (size_t)a.nblk * 16 * HD;
-            for (int i = tid; i < nr * HD; i += NWC * WAVE) {
-                const int j = i / HD, dd = i % HD, pos = t + j;
+            for (int i = tid; i < ncr * HD; i += NWC * WAVE) {
+                const int cr = i / HD, dd = i % HD, pos = t + r + (NRANK - 1) * cr;
                 bf16* kblk = (bf16*)a.kcache + head + (size_t)(pos / 16) * 16 * HD;
                 bf16* vblk = (bf16*)a.vcache + head + (size_t)(pos / 16) * 16 * HD;
-                kblk[kblock_elem<bf16>(pos % 16, dd)] = kb_l[j * LDQ + dd];
-                vblk[vblock_elem(pos % 16, dd)] = vb_l[j * HD + dd];
+                kblk[kblock_elem<bf16>(pos % 16, dd)] = kb_l[cr * LDQ + dd];
+                vblk[vblock_elem(pos % 16, dd)] = vb_l[cr * HD + dd];
             }
         }
 
