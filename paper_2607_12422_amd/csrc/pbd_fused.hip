@@ -156,15 +156,21 @@ __device__ __forceinline__ void wait_vm(int n) {
 
 __device__ __forceinline__ void bar() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-__device__ __forceinline__ void mma_k4s(f32x4& acc, const uint2& a, const f32x4& p) {
-    f32x4 hh, ll;
+// LoRA expand acc += B u over the adapter's 16 rank entries: the bf16 B block
+// (lane: output row lane % 16, rank entries 4 (lane / 16) ..) and the scaled
+// shrink u (the shrink accumulator's layout) both as fp16 operands
+typedef __attribute__((ext_vector_type(4))) _Float16 f16x4;
+__device__ __forceinline__ void mma_k4h(f32x4& acc, const uint2& a, const f32x4& p) {
+    f16x4 av, pv;
+    const unsigned u[2] = {a.x, a.y};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        hh[e] = (float)(bf16)p[e];
-        ll[e] = p[e] - hh[e];
+    for (int i = 0; i < 2; ++i) {
+        av[2 * i] = (_Float16)__uint_as_float(u[i] << 16);
+        av[2 * i + 1] = (_Float16)__uint_as_float(u[i] & 0xffff0000u);
     }
-    mma_k4(acc, a, hh);
-    mma_k4(acc, a, ll);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) pv[e] = (_Float16)p[e];
+    acc = __builtin_amdgcn_mfma_f32_16x16x16f16(av, pv, acc, 0, 0, 0);
 }
 
 // The layer GEMMs feed the matrix cores fp16 operands: the activations are
@@ -712,7 +718,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
             if (LORA) {
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], lbQ, uacc[mt] * a.scale);
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4h(acc[mt], lbQ, uacc[mt] * a.scale);
             }
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) s_red[((0 * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
@@ -1069,7 +1075,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
             if (LORA) {
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], lbO, uacc[mt] * a.scale);
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4h(acc[mt], lbO, uacc[mt] * a.scale);
             }
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) s_red[((tt * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
@@ -1182,8 +1188,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
                     for (int mt = 0; mt < 2; ++mt) {
                         if (mt >= MT) continue;
-                        mma_k4s(acc[tt][mt], bg, ug[mt] * a.scale);
-                        mma_k4s(acc[tt][mt], bu, uu[mt] * a.scale);
+                        mma_k4h(acc[tt][mt], bg, ug[mt] * a.scale);
+                        mma_k4h(acc[tt][mt], bu, uu[mt] * a.scale);
                     }
                 }
             }
@@ -1254,7 +1260,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
             if (LORA) {
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4s(acc[mt], lbD, uacc[mt] * a.scale);
+                for (int mt = 0; mt < 2; ++mt) if (mt < MT) mma_k4h(acc[mt], lbD, uacc[mt] * a.scale);
             }
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) s_red[((tt * NWC + wid) * 2 + mt) * WAVE + lane] = acc[mt];
