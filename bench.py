@@ -379,7 +379,10 @@ def main():
         "config": {"workload": w_.name, "model_shape": cfg.name, "batch": B,
                    "prefix": lengths if B <= 8 else [min(lengths), max(lengths)],
                    "block": cfg.block, "lora_rank": cfg.lora_rank,
-                   "operands": "bf16x2" if cfg.dtype == "bf16" else "f32",
+                   # bf16 models: fp16 activation operands in the persistent batch-1
+                   # pass and in passes of >= 128 rows, bf16 value + residual otherwise
+                   "operands": ("f32" if cfg.dtype != "bf16" else
+                                "fp16" if B == 1 or B * (cfg.block + 1) >= 128 else "bf16x2"),
                    "launch": "eager" if args.eager else "hip-graph"},
         "draft_ms": round(dmed, 4), "verify_ms": round(vmed, 4), "accept_ms": round(amed, 4),
         "draft_ms_p10_p90": [round(x, 4) for x in pct(d_ms)],

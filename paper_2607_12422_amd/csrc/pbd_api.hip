@@ -75,11 +75,14 @@ struct Layout {
         size_t la[7];                  // LoRA shrink tiles, order q k v o gate up down
         size_t lb_qkv, lb_o, lb_gu, lb_d;  // LoRA expand blocks
         // fp16 copies of the projection and LoRA A fragments, read by the
-        // persistent batch-1 pass (its matrix cores take fp16 operands)
+        // persistent batch-1 pass and the large-M draft/verify passes (their
+        // matrix cores take fp16 operands)
         size_t qkv16, o16, gu16, d16, la16[7];
     };
     std::vector<LayerOff> lay;
     size_t p_embed, p_final_norm, p_rope, packed_bytes;
+    size_t p_embed16;                                // fp16 copy of the embedding fragments (f16big)
+    bool f16big;                                     // large-M draft/verify passes run on fp16 operands
     // KV cache
     size_t kv_half, kv_bytes;
     // workspace
@@ -91,6 +94,7 @@ struct Layout {
     size_t w_xc[2], w_sqc;                           // prefill: gathered last rows (LM-head operand, Σx² partials)
     bool big;                                        // passes of >= BIG_MIN_MT m-tiles can use the large-M GEMM
     size_t w_u;                                      // its LoRA shrink u = A x, [M][sources * RT * 16] fp32
+    size_t w_ukpart;                                 // the shrink's split-K slices [BIG_KSPLIT_MAX][w_u]
     size_t w_dn_tok, w_dn_conf;                      // one denoising pass's candidates and confidences
     int ksplit;                                      // K slices of the residual GEMMs
     bool fused_shape;                                // the persistent batch-1 pass supports this model
@@ -169,6 +173,9 @@ void make_layout(const pbd_config* c, Layout& y) {
     const bool fused_cand = y.dtype == PBD_DTYPE_BF16 && y.H == 1024 && y.F == 3072 && y.NQ == 16 && y.NKV == 8 &&
                             y.HD == 128 && y.RT <= 1 && y.W <= FUSED_MAX_ROWS && y.L <= 255 && y.nblk <= 310 &&
                             c->qk_norm;
+    // draft/verify passes of >= BIG_MIN_MT m-tiles of bf16 models take single
+    // fp16 activation operands against fp16 copies of the weight fragments
+    y.f16big = y.dtype == PBD_DTYPE_BF16 && (size_t)y.Bmax * y.W >= (size_t)BIG_MIN_MT * 16;
     y.p_embed = take((size_t)y.tiles_e * y.kb_e * FR);
     y.lay.resize(y.L);
     const int kb_in[7] = {y.kb_qkv, y.kb_qkv, y.kb_qkv, y.kb_o, y.kb_gu, y.kb_gu, y.kb_d};
@@ -189,7 +196,7 @@ void make_layout(const pbd_config* c, Layout& y) {
         o.lb_d = take((size_t)y.tiles_d * y.RT * EB);
         o.qkv16 = o.o16 = o.gu16 = o.d16 = 0;
         for (int i = 0; i < 7; ++i) o.la16[i] = 0;
-        if (fused_cand) {
+        if (fused_cand || y.f16big) {
             o.qkv16 = take((size_t)y.tiles_qkv * y.kb_qkv * FR);
             o.o16 = take((size_t)y.tiles_o * y.kb_o * FR);
             o.gu16 = take((size_t)y.tiles_gu * y.kb_gu * FR);
@@ -199,6 +206,7 @@ void make_layout(const pbd_config* c, Layout& y) {
     }
     y.p_final_norm = take(y.H * y.esz);
     y.p_rope = take((size_t)y.max_seq * (y.HD / 2) * 8);
+    y.p_embed16 = y.f16big ? take((size_t)y.tiles_e * y.kb_e * FR) : 0;
     y.packed_bytes = off;
 
     y.kv_half = (size_t)y.L * y.Bmax * y.NKV * y.nblk * 16 * y.HD * y.esz;
@@ -235,6 +243,7 @@ void make_layout(const pbd_config* c, Layout& y) {
     y.w_sqc = take((size_t)std::max(y.tiles_d, 1) * y.Bmax * 4);
     y.big = y.Mmax >= BIG_MIN_MT * 16;
     y.w_u = y.big && y.r > 0 ? take((size_t)y.Mmax * 3 * y.RT * 16 * 4) : 0;   // LoRA shrink, large-M path
+    y.w_ukpart = y.w_u ? take((size_t)BIG_KSPLIT_MAX * y.Mmax * 3 * y.RT * 16 * 4) : 0;
     y.w_dn_conf = take((size_t)y.Bmax * y.D * 4);
     // (its byte offsets into the packed weights are 32-bit)
     y.fused_shape = fused_cand && y.packed_bytes < ((size_t)1 << 32);
@@ -365,7 +374,13 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     const int QTw = qsplit ? 1 : QT;                // ... per attention work-group
     const float scale = y.r > 0 ? c->cfg.lora_alpha / (float)y.r : 0.f;
     const bool lora = q.adapter && y.r > 0;
-    const bool split = c->split && dt == PBD_DTYPE_BF16;
+    // passes of many rows (prefill chunks, large-batch steps): large-M
+    // projections, with the residual / SwiGLU epilogues in the GEMM
+    const bool big = MT >= BIG_MIN_MT && y.big && (!lora || y.w_u != 0);
+    // large-M draft/verify passes of bf16 models: single fp16 activation
+    // operands against the fp16 weight copies (one MFMA per fragment pair)
+    const bool h16 = big && !pre && y.f16big;
+    const bool split = c->split && dt == PBD_DTYPE_BF16 && !h16;
     float* x = (float*)(ws + y.w_x);
     float* sq_a = (float*)(ws + y.w_sq_a);
     float* sq_m = (float*)(ws + y.w_sq_m);
@@ -382,7 +397,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     as.seq_len = q.seq_len; as.anchor = q.anchor; as.drafts = q.drafts; as.prompt = q.prompt; as.lengths = q.lengths;
     as.tokens = (int*)(ws + y.w_tokens); as.pos0 = pos0; as.nrows = nrows; as.status = status;
     as.embed = pk + y.p_embed; as.gain = pk + y.lay[0].attn_norm; as.x = x;
-    as.op_hi = hi(y.w_xa); as.op_lo = lo(y.w_xa); as.sq = sq_a;
+    as.op_hi = hi(y.w_xa); as.op_lo = lo(y.w_xa); as.op_f16 = h16 ? 1 : 0; as.sq = sq_a;
     const bool fused = y.fused_shape && c->fused_dev && c->pass_mode == 0 && !pre && B == 1 &&
                        !q.anchor_cached && !q.no_anchor && split && !q.scratch;
     if (q.scratch) {
@@ -467,22 +482,28 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
             g.cnt = (unsigned*)(ws + y.w_kcnt);
         }
     };
-    // passes of many rows (prefill chunks, large-batch steps): large-M
-    // projections, with the residual / SwiGLU epilogues as row kernels on
-    // their fp32 output
-    const bool big = MT >= BIG_MIN_MT && y.big && (!lora || y.w_u != 0);
     float* ubig = (float*)(ws + y.w_u);
     auto big_args = [&](const FGemmArgs& g) {
         BigGemmArgs b{};
         b.w = g.w; b.n_tiles = g.n_tiles; b.kb = g.kb; b.xhi = g.xhi; b.xlo = g.xlo; b.M = g.M; b.MT = g.MT;
         b.sq = g.sq; b.n_sq = g.n_sq; b.sq_stride = g.sq_stride; b.norm_dim = g.norm_dim; b.eps = g.eps;
         b.out = g.out; b.ldo = g.ldo;                // STORE (q/k/v); the other projections use epilogues
+        b.op_f16 = h16 ? 1 : 0;
         return b;
     };
     // with the adapter, the large-M projection is two launches (timed
     // separately): the shrink of the projection's nsrc LoRA A matrices,
     // stacked in the packed layout as one [nsrc RT][kb] tile matrix, into u;
     // then the projection with the expand
+    // a few dozen 64 x 64 shrink blocks would walk the whole K: split K so
+    // that the launch has about 512 work-groups, then sum the slices in order
+    // (kper 0: one slice)
+    auto shrink_kper = [&](const FGemmArgs& g, int nsrc) -> int {
+        const int blocks = cdiv(nsrc * y.RT, 4) * cdiv(g.MT, 4);
+        const int want = std::min(BIG_KSPLIT_MAX, std::max(1, 512 / std::max(blocks, 1)));
+        return want > 1 && y.w_ukpart ? cdiv(g.kb, want) : 0;
+    };
+    const size_t u_kstride = (size_t)y.Mmax * 3 * y.RT * 16;
     auto launch_shrink = [&](const FGemmArgs& g, int nsrc) -> hipError_t {
         const size_t src_frags = (size_t)y.RT * g.kb * 64;              // uint4 per source matrix
         for (int i = 1; i < nsrc; ++i)
@@ -490,7 +511,20 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         BigGemmArgs sh{};
         sh.w = g.la[0]; sh.n_tiles = nsrc * y.RT; sh.kb = g.kb; sh.xhi = g.xhi; sh.xlo = g.xlo;
         sh.M = g.M; sh.MT = g.MT; sh.n_sq = 0; sh.out = ubig; sh.ldo = nsrc * y.RT * 16;
+        sh.op_f16 = h16 ? 1 : 0;
+        sh.kper = shrink_kper(g, nsrc);
+        if (sh.kper > 0) {
+            sh.out = (float*)(ws + y.w_ukpart);
+            sh.out_kstride = u_kstride;
+        }
         return launch_gemm_big(dt, sh, st);
+    };
+    auto launch_shrink_sum = [&](const FGemmArgs& g, int nsrc) -> hipError_t {
+        KSumArgs ka{};
+        ka.dst = ubig; ka.src = (const float*)(ws + y.w_ukpart);
+        ka.n = (size_t)g.M * nsrc * y.RT * 16; ka.stride = u_kstride;
+        ka.S = cdiv(g.kb, shrink_kper(g, nsrc));
+        return launch_ksum(ka, st);
     };
     auto launch_big = [&](const FGemmArgs& g, int nsrc, int epi = EPI_STORE) -> hipError_t {
         BigGemmArgs b = big_args(g);
@@ -508,7 +542,11 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     };
 #define PBD_BIG(G, NSRC, EPI, WHAT)                                                                      \
     do {                                                                                                \
-        if (lora) PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_shrink(G, NSRC), WHAT " (LoRA shrink)");     \
+        if (lora) {                                                                                     \
+            PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_shrink(G, NSRC), WHAT " (LoRA shrink)");           \
+            if (shrink_kper(G, NSRC) > 0)                                                               \
+                PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_shrink_sum(G, NSRC), WHAT " (LoRA shrink sum)"); \
+        }                                                                                               \
         PBD_TIMED(c, st, PBD_KCLASS_GEMM, launch_big(G, NSRC, EPI), WHAT);                              \
     } while (0)
     const int L = q.n_layers > 0 ? q.n_layers : y.L;
@@ -516,10 +554,10 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         const Layout::LayerOff& lo_ = y.lay[l];
         // q/k/v projection: attention RMSNorm folded in, LoRA per source matrix
         FGemmArgs g;
-        base_gemm(g, lo_.qkv, y.tiles_qkv, y.kb_qkv, y.w_xa);
+        base_gemm(g, h16 ? lo_.qkv16 : lo_.qkv, y.tiles_qkv, y.kb_qkv, y.w_xa);
         g.sq = sq_a; g.n_sq = l == 0 ? 1 : y.tiles_d;
         g.lora_mode = LORA_BY_TILE; g.tile_split0 = y.NQ * y.HD / 16; g.tile_split1 = (y.NQ + y.NKV) * y.HD / 16;
-        for (int i = 0; i < 3; ++i) g.la[i] = (const uint4*)(pk + lo_.la[i]);
+        for (int i = 0; i < 3; ++i) g.la[i] = (const uint4*)(pk + (h16 ? lo_.la16[i] : lo_.la[i]));
         g.lb = pk + lo_.lb_qkv;
         g.out = (float*)(ws + y.w_qkv); g.ldo = y.nqkv;
         if (big) PBD_BIG(g, 3, EPI_STORE, "qkv gemm");
@@ -572,12 +610,13 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         CombineArgs cb{};
         cb.W = W; cb.n_q = y.NQ; cb.head_dim = y.HD; cb.kps = kps; cb.s_launch = s_launch; cb.MT = MT;
         cb.pos0 = pos0; cb.part_o = at.part_o; cb.part_ml = at.part_ml;
-        cb.op_hi = hi(y.w_xo); cb.op_lo = lo(y.w_xo);
+        cb.op_hi = hi(y.w_xo); cb.op_lo = lo(y.w_xo); cb.op_f16 = h16 ? 1 : 0;
         PBD_TIMED(c, st, PBD_KCLASS_COMBINE, launch_combine(dt, cb, M, st), "attention combine");
 
         // O projection + residual; writes the MLP RMSNorm operand
-        base_gemm(g, lo_.o, y.tiles_o, y.kb_o, y.w_xo);
-        g.n_sq = 0; g.lora_mode = LORA_SINGLE; g.la[0] = (const uint4*)(pk + lo_.la[3]); g.lb = pk + lo_.lb_o;
+        base_gemm(g, h16 ? lo_.o16 : lo_.o, y.tiles_o, y.kb_o, y.w_xo);
+        g.n_sq = 0; g.lora_mode = LORA_SINGLE; g.la[0] = (const uint4*)(pk + (h16 ? lo_.la16[3] : lo_.la[3]));
+        g.lb = pk + lo_.lb_o;
         g.x = x; g.ldx = y.H; g.gnext = pk + lo_.mlp_norm; g.nx_hi = hi(y.w_xm); g.nx_lo = lo(y.w_xm); g.n_MT = MT;
         g.sq_out = sq_m;
         split_k(g);
@@ -588,9 +627,11 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         }
 
         // gate/up + SwiGLU: MLP RMSNorm folded in
-        base_gemm(g, lo_.gu, y.tiles_gu, y.kb_gu, y.w_xm);
+        base_gemm(g, h16 ? lo_.gu16 : lo_.gu, y.tiles_gu, y.kb_gu, y.w_xm);
         g.sq = sq_m; g.n_sq = y.tiles_o;
-        g.lora_mode = LORA_ROW_HALF; g.la[0] = (const uint4*)(pk + lo_.la[4]); g.la[1] = (const uint4*)(pk + lo_.la[5]);
+        g.lora_mode = LORA_ROW_HALF;
+        g.la[0] = (const uint4*)(pk + (h16 ? lo_.la16[4] : lo_.la[4]));
+        g.la[1] = (const uint4*)(pk + (h16 ? lo_.la16[5] : lo_.la[5]));
         g.lb = pk + lo_.lb_gu;
         g.nx_hi = hi(y.w_xd); g.nx_lo = lo(y.w_xd); g.n_MT = MT;
         if (big) {
@@ -601,8 +642,9 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
         }
 
         // down projection + residual; writes the next layer's (or the final) RMSNorm operand
-        base_gemm(g, lo_.d, y.tiles_d, y.kb_d, y.w_xd);
-        g.n_sq = 0; g.lora_mode = LORA_SINGLE; g.la[0] = (const uint4*)(pk + lo_.la[6]); g.lb = pk + lo_.lb_d;
+        base_gemm(g, h16 ? lo_.d16 : lo_.d, y.tiles_d, y.kb_d, y.w_xd);
+        g.n_sq = 0; g.lora_mode = LORA_SINGLE; g.la[0] = (const uint4*)(pk + (h16 ? lo_.la16[6] : lo_.la[6]));
+        g.lb = pk + lo_.lb_d;
         g.x = x; g.ldx = y.H;
         g.gnext = l + 1 < L ? pk + y.lay[l + 1].attn_norm : pk + y.p_final_norm;
         g.nx_hi = hi(y.w_xa); g.nx_lo = lo(y.w_xa); g.n_MT = MT; g.sq_out = sq_a;
@@ -617,7 +659,7 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
     // tied LM head with the final RMSNorm folded in, fused argmax (prefill:
     // on each sequence's last prompt row only, gathered into a compact operand)
     FGemmArgs ge;
-    base_gemm(ge, y.p_embed, y.tiles_e, y.kb_e, y.w_xa);
+    base_gemm(ge, h16 ? y.p_embed16 : y.p_embed, y.tiles_e, y.kb_e, y.w_xa);
     ge.lora = 0; ge.sq = sq_a; ge.n_sq = y.tiles_d;
     int lm_MT = MT;
     if (pre) {
@@ -836,6 +878,9 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
         const int rows[1] = {y.V};
         const void* w[1] = {canon->embed};
         PBD_INIT_HIP(pack(y.p_embed, y.tiles_e, y.kb_e, y.H, MAP_CONCAT, 1, rows, w), "pack embed");
+        if (y.p_embed16)
+            PBD_INIT_HIP(launch_bf16_to_f16(c->packed + y.p_embed, c->packed + y.p_embed16,
+                                            (size_t)y.tiles_e * y.kb_e * 1024 / 4, st), "fp16 embed");
     }
     for (int l = 0; l < y.L; ++l) {
         const pbd_layer_weights& lw = canon->layers[l];
@@ -872,8 +917,8 @@ int pbd_init_weights(const pbd_config* cfg, const pbd_weights* canon, void* pack
                 PBD_INIT_HIP(pack(lo.la[i], y.RT, in_f[i] / y.FK, in_f[i], MAP_CONCAT, 1, rows, w), "pack lora A");
             }
         }
-        if (y.fused_shape) {
-            // the persistent pass's fp16 copies of this layer's fragments
+        if (lo.qkv16) {
+            // fp16 copies of this layer's fragments (persistent pass, large-M passes)
             auto cvt = [&](size_t src, size_t dst, size_t bytes) { return launch_bf16_to_f16(c->packed + src, c->packed + dst, bytes / 4, st); };
             PBD_INIT_HIP(cvt(lo.qkv, lo.qkv16, (size_t)y.tiles_qkv * y.kb_qkv * 1024), "fp16 qkv");
             PBD_INIT_HIP(cvt(lo.o, lo.o16, (size_t)y.tiles_o * y.kb_o * 1024), "fp16 o");

@@ -40,6 +40,7 @@ struct AssembleArgs {
     float* x;              // [M][H] residual
     void* op_hi;           // first QKV operand x*g (fragments) and its bf16 residual
     void* op_lo;
+    int op_f16;            // bf16 model: the operand as fp16 in op_hi (op_lo unused)
     float* sq;             // [1][m_stride] per-row sum of squares
     unsigned* fused_ctl;   // persistent pass next: its rank tickets and abort word are cleared and its epoch advanced (null: none)
     int fused_layers;      // layers that pass runs (it advances the per-parity write counts of its partial buffers)
@@ -150,6 +151,8 @@ struct GatherArgs {
 
 // Large-M projection (prefill chunks): out[m][16 t + r] = r_m * (W x_m)[16 t + r]
 // for every row m and weight tile t, on the same packed operands as FGemmArgs.
+constexpr int BIG_KSPLIT_MAX = 8;     // K slices of a split-K large-M launch
+
 struct BigGemmArgs {
     const uint4* w;         // weight tiles [n_tiles][kb] fragments
     int n_tiles, kb;
@@ -184,6 +187,12 @@ struct BigGemmArgs {
     // grid order: m-blocks fastest (the blocks that share weight tiles run
     // together; for weights larger than the memory-side cache)
     int m_fast;
+    // split-K (plain STORE epilogue, no RMSNorm; the LoRA shrink): grid z =
+    // ceil(kb / kper) slices of kper K fragments (kper = 0: one slice); slice
+    // z stores its products at out + z * out_kstride, summed afterwards by
+    // launch_ksum
+    int kper;
+    size_t out_kstride;     // floats, >= M * ldo
     // SwiGLU epilogue (sw_hi set; gate/up tiles with rows 0-7 gate and 8-15
     // up of the same FFN columns): h = silu(gate) * up written as the down
     // projection's operand fragments (K = n_tiles * 8, sw_MT m-tiles); out is
@@ -203,6 +212,10 @@ struct BigGemmArgs {
     int rn_MT;
     float* rsq;
     int rsq_stride;
+    // bf16 model, single fp16 operands: xhi holds fp16 fragments (xlo null),
+    // w points to fp16 copies of the weight fragments, and the residual /
+    // SwiGLU epilogues write fp16 operands (rn_lo / sw_lo unused)
+    int op_f16;
 };
 
 struct CombineArgs {
@@ -212,6 +225,7 @@ struct CombineArgs {
     const float* part_ml;
     void* op_hi;            // O-projection operand fragments (K = n_q*head_dim)
     void* op_lo;
+    int op_f16;             // bf16 model: the operand as fp16 in op_hi (op_lo unused)
 };
 
 struct ArgmaxArgs {
@@ -289,6 +303,15 @@ hipError_t launch_lmhead(int dtype, const FGemmArgs& a, int grid, hipStream_t st
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t st);
 hipError_t launch_kvwrite(int dtype, int head_dim, const KVWriteArgs& a, int batch, hipStream_t st);
 hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStream_t st);
+// dst[i] = sum over s < S of src[s * stride + i] in slice order (the K
+// slices of a split-K large-M launch); n and stride multiples of 4
+struct KSumArgs {
+    float* dst;
+    const float* src;
+    size_t n, stride;
+    int S;
+};
+hipError_t launch_ksum(const KSumArgs& a, hipStream_t st);
 hipError_t launch_gemm_big(int dtype, const BigGemmArgs& a, hipStream_t st);   // split iff a.xlo
 hipError_t launch_remask(const RemaskArgs& a, int batch, hipStream_t st);
 hipError_t launch_pack(int dtype, const PackArgs& a, hipStream_t st);

@@ -58,10 +58,22 @@ static __device__ __forceinline__ void attn_splits(int t, int kps, int s_launch,
 }
 
 // Write EPL consecutive k values of one operand row (16-byte aligned run of
-// one lane's fragment slot) as value and residual, or plain T when lo is null.
+// one lane's fragment slot) as value and residual, or plain T when lo is null;
+// with h16 (bf16 models only) as fp16 values into hi.
 template <typename T>
-static __device__ __forceinline__ void put_operand_run(T* hi, T* lo, size_t e, const float* v) {
+static __device__ __forceinline__ void put_operand_run(T* hi, T* lo, size_t e, const float* v, bool h16 = false) {
     constexpr int EPL = Elt<T>::EPL;
+    if constexpr (EPL == 8) {
+        if (h16) {
+            _Float16 hh[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) hh[i] = (_Float16)v[i];
+            uint4 hv;
+            __builtin_memcpy(&hv, hh, 16);
+            *(uint4*)(hi + e) = hv;
+            return;
+        }
+    }
     T h[EPL], l[EPL];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
@@ -165,7 +177,7 @@ __global__ __launch_bounds__(256) void k_assemble(AssembleArgs a) {
             ss += xv[e] * xv[e];
             ov[e] = xv[e] * to_f32(gv[e]);
         }
-        put_operand_run<T>((T*)a.op_hi, (T*)a.op_lo, xfrag_elem<T>(m, k0, a.MT), ov);
+        put_operand_run<T>((T*)a.op_hi, (T*)a.op_lo, xfrag_elem<T>(m, k0, a.MT), ov, a.op_f16 != 0);
     }
     __shared__ float s_ss[8];
     ss = wave_sum(ss);
@@ -1293,7 +1305,7 @@ __global__ void k_combine(CombineArgs a) {
     const float inv = L > 0.f ? 1.f / L : 0.f;
 #pragma unroll
     for (int i = 0; i < EPL; ++i) o[i] *= inv;
-    put_operand_run<T>((T*)a.op_hi, (T*)a.op_lo, xfrag_elem<T>(m, h * a.head_dim + d0, a.MT), o);
+    put_operand_run<T>((T*)a.op_hi, (T*)a.op_lo, xfrag_elem<T>(m, h * a.head_dim + d0, a.MT), o, a.op_f16 != 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -1726,9 +1738,12 @@ hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStre
 // s * B u per tile before the r_m scaling (r_m (W x + s B A x), the same sum
 // the skinny GEMM forms in-tile).
 // ---------------------------------------------------------------------------
-// WT: tiles per wave in each direction (2: 64x64 blocks, 4: 128x128 blocks)
-template <typename T, bool SPLIT, int WT>
+// WT: tiles per wave in each direction (2: 64x64 blocks, 4: 128x128 blocks);
+// H16: fp16 operands and fp16 weight fragments (bf16 models), one MFMA per
+// fragment pair and fp16 operands written by the epilogues
+template <typename T, bool SPLIT, int WT, bool H16>
 __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
+    static_assert(!H16 || (!SPLIT && sizeof(T) == 2), "fp16 operands replace the bf16 pair");
     constexpr int BT = 2 * WT;                  // m- and n-tiles per block
     constexpr int FPW = BT / 4;                 // fragments of each kind a wave stages per step
     constexpr int NSL = 256 / (BT * 16);        // RMSNorm partial slices per row
@@ -1756,8 +1771,11 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
         mtw[k] = min(bm * BT + wid * FPW + k, a.MT - 1);
     }
     u32x4 gv[GS][3][FPW];                 // W, value, residual fragments of a step
+    // this work-group's K fragments [kf0, kf0 + nkf) (split-K: slice blockIdx.z)
+    const int kper = a.kper > 0 ? a.kper : a.kb;
+    const int kf0 = (int)blockIdx.z * kper, nkf = min(a.kb, kf0 + kper) - kf0;
     auto gload = [&](int f, int st) {
-        const int fc = min(f, a.kb - 1);
+        const int fc = kf0 + min(f, nkf - 1);
 #pragma unroll
         for (int k = 0; k < FPW; ++k) {
             gv[st][0][k] = *(const u32x4*)(a.w + ((size_t)ntw[k] * a.kb + fc) * WAVE + lane);
@@ -1796,7 +1814,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
     // Loads past K repeat the last step; their products are not formed.
     swrite(0, 0);
     lds_sync();
-    for (int f0 = 0; f0 < a.kb; f0 += GS) {
+    for (int f0 = 0; f0 < nkf; f0 += GS) {
 #pragma unroll
         for (int u = 0; u < GS; ++u) {
             const int buf = u & 1;
@@ -1810,13 +1828,18 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
             }
             swrite((u + 1) % GS, buf ^ 1);
             gload(f0 + u + GS, u);
-            if (f0 + u < a.kb) {
+            if (f0 + u < nkf) {
 #pragma unroll
                 for (int j = 0; j < WT; ++j)
 #pragma unroll
                     for (int i = 0; i < WT; ++i) {
-                        mma_frag<T>(acc[j][i], w2[i], h2[j]);
-                        if (SPLIT) mma_frag<T>(acc[j][i], w2[i], l2[j]);
+                        if (H16) {
+                            acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                                __builtin_bit_cast(f16x8, w2[i]), __builtin_bit_cast(f16x8, h2[j]), acc[j][i], 0, 0, 0);
+                        } else {
+                            mma_frag<T>(acc[j][i], w2[i], h2[j]);
+                            if (SPLIT) mma_frag<T>(acc[j][i], w2[i], l2[j]);
+                        }
                     }
             }
             lds_sync();
@@ -1938,7 +1961,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
                 for (int e = 0; e < 4; ++e) ov[4 + e] = __shfl_xor(ov[e], 16);   // next 4 columns (even lane groups)
                 const bool writer = EPL == 8 ? (lgrp % 2) == 0 : true;
                 if (live && writer)
-                    put_operand_run<T>((T*)a.rn_hi, (T*)a.rn_lo, xfrag_elem<T>(m, col0, a.rn_MT), ov);
+                    put_operand_run<T>((T*)a.rn_hi, (T*)a.rn_lo, xfrag_elem<T>(m, col0, a.rn_MT), ov, H16);
                 if (live && lgrp == 0) a.rsq[(size_t)nt * a.rsq_stride + m] = ss;
             }
         return;
@@ -1966,7 +1989,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
                 for (int e = 0; e < 4; ++e) h[4 + e] = __shfl_xor(h[e], 16);   // lane group 0 gets columns 4..7
                 const bool writer = EPL == 8 ? lgrp == 0 : lgrp < 2;
                 if (live && writer)
-                    put_operand_run<T>((T*)a.sw_hi, (T*)a.sw_lo, xfrag_elem<T>(m, nt * 8 + lgrp * 4, a.sw_MT), h);
+                    put_operand_run<T>((T*)a.sw_hi, (T*)a.sw_lo, xfrag_elem<T>(m, nt * 8 + lgrp * 4, a.sw_MT), h, H16);
             }
         return;
     }
@@ -1978,7 +2001,8 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
             if (mt >= a.MT || m >= a.M || nt >= a.n_tiles) continue;
             const float rm = s_rm[m - bm * BT * 16];
             const f32x4 v = acc[j][i] * rm;
-            *(float4*)(a.out + (size_t)m * a.ldo + nt * 16 + lgrp * 4) = float4{v[0], v[1], v[2], v[3]};
+            *(float4*)(a.out + (size_t)blockIdx.z * a.out_kstride + (size_t)m * a.ldo + nt * 16 + lgrp * 4) =
+                float4{v[0], v[1], v[2], v[3]};
         }
 }
 
@@ -1988,13 +2012,43 @@ template <int WT>
 static hipError_t launch_gemm_big_wt(int dtype, const BigGemmArgs& a, hipStream_t st) {
     const int gn = (a.n_tiles + 2 * WT - 1) / (2 * WT), gm = (a.MT + 2 * WT - 1) / (2 * WT);
     if ((a.m_fast ? gn : gm) > 65535) return hipErrorInvalidValue;     // grid y limit
-    const dim3 grid(a.m_fast ? gm : gn, a.m_fast ? gn : gm), block(256);
+    const int ks = a.kper > 0 ? (a.kb + a.kper - 1) / a.kper : 1;
+    if (ks > 1 && (ks > BIG_KSPLIT_MAX || a.out_kstride < (size_t)a.M * a.ldo || !a.out || a.arg_val || a.sw_hi ||
+                   a.rx || a.lrt > 0 || a.n_sq > 0))
+        return hipErrorInvalidValue;
+    const dim3 grid(a.m_fast ? gm : gn, a.m_fast ? gn : gm, ks), block(256);
     if (dtype == PBD_DTYPE_BF16) {
-        if (!a.xlo) return hipErrorInvalidValue;
-        PBD_LAUNCH((k_gemm_big<bf16, true, WT>), grid, block, 0, st, a);
+        if (a.op_f16) {
+            if (a.xlo) return hipErrorInvalidValue;
+            PBD_LAUNCH((k_gemm_big<bf16, false, WT, true>), grid, block, 0, st, a);
+        } else {
+            if (!a.xlo) return hipErrorInvalidValue;
+            PBD_LAUNCH((k_gemm_big<bf16, true, WT, false>), grid, block, 0, st, a);
+        }
     } else {
-        PBD_LAUNCH((k_gemm_big<float, false, WT>), grid, block, 0, st, a);
+        if (a.op_f16) return hipErrorInvalidValue;
+        PBD_LAUNCH((k_gemm_big<float, false, WT, false>), grid, block, 0, st, a);
     }
+    return hipGetLastError();
+}
+
+// Sum of the K slices of a split-K large-M launch, in slice order:
+// dst[i] = src[i] + src[stride + i] + ... (n a multiple of 4, 16-byte aligned)
+__global__ __launch_bounds__(256) void k_ksum(KSumArgs a) {
+    const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+    if (i >= a.n) return;
+    float4 v = *(const float4*)(a.src + i);
+    for (int s = 1; s < a.S; ++s) {
+        const float4 w = *(const float4*)(a.src + (size_t)s * a.stride + i);
+        v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+    }
+    *(float4*)(a.dst + i) = v;
+}
+
+hipError_t launch_ksum(const KSumArgs& a, hipStream_t st) {
+    if (a.n % 4 || a.stride % 4 || a.S < 1 || a.S > BIG_KSPLIT_MAX) return hipErrorInvalidValue;
+    if (a.n == 0) return hipSuccess;
+    PBD_LAUNCH(k_ksum, dim3((unsigned)((a.n / 4 + 255) / 256)), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 

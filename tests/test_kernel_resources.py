@@ -28,7 +28,7 @@ HOT = [
     r"_ZN3pbd8k_acceptENS_10AcceptArgsE",
     r"_ZN3pbd8k_remaskENS_10RemaskArgsE",
     # prefill chunks
-    r"_ZN3pbd10k_gemm_bigIDF16bLb[01]ELi[24]EEEvNS_11BigGemmArgsE",
+    r"_ZN3pbd10k_gemm_bigIDF16bLb[01]ELi[24]ELb[01]EEEvNS_11BigGemmArgsE",
     r"_ZN3pbd9k_kvwriteIDF16bLi128EEEvNS_11KVWriteArgsE",
     r"_ZN3pbd13k_gather_lastIDF16bEEvNS_10GatherArgsE",
     # the persistent batch-1 layer stack (adapter on / off)
