@@ -33,6 +33,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "ms per draft pass & verify pass (D=16), draft/verify ratio, HBM GB/s %peak"
 HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E peak
+MFMA16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 / fp16 matrix-core peak
 
 
 def algorithmic_bytes(cfg, batch, prefixes):
@@ -180,11 +181,14 @@ def parent_main(args):
         large = []
         for wi in (3, 4):
             w_ = synth.WORKLOADS[wi]
+            # kernel durations on: the child reports the projections' matrix-core
+            # and the attention's HBM rooflines from per-dispatch events
             rr = run_child(["--steps", str(max(5, min(args.steps, 20))), "--warmup", "3", "--workload", str(wi),
-                            "--prefill-chunk", str(max(16, 4096 // w_.batch))] + minimal, 900)
+                            "--prefill-chunk", str(max(16, 4096 // w_.batch))]
+                           + [f for f in minimal if f != "--no-profile"], 900)
             large.append({k: rr[k] for k in ("config", "ms_per_step", "draft_ms", "verify_ms", "accept_ms",
-                                             "draft_verify_ratio", "tokens_per_s", "hbm", "device_status",
-                                             "steps", "warmup")})
+                                             "draft_verify_ratio", "tokens_per_s", "hbm", "gemm_roofline",
+                                             "attn_roofline", "device_status", "steps", "warmup") if k in rr})
         result["large_batch"] = large
     if not args.no_cpu_baseline:
         print("bench: CPU oracle baseline", file=sys.stderr, flush=True)
@@ -659,6 +663,45 @@ def main():
                                   "frac": round(ach / HBM_PEAK_GBPS, 4),
                                   "traffic": counter_traffic("k_fgemm_traffic.txt", "pbd_kernels.hip"),
                                   "bytes_per_launch": round(gemm_launch_bytes), "avg_launch_us": g["avg_us"]}
+        if not fz["launches"] and B * cfg.width >= 128 and prof["gemm"]["launches"]:
+            # passes of >= 128 rows: the projections run on the large-M GEMM,
+            # bound by the matrix cores (2 flops per weight and row, the
+            # adapter's shrink and expand in the draft), and the attention
+            # streams the prefix K/V from HBM
+            M = B * cfg.width
+            lin = sum(o * i for _, o, i in cfg.linear_shapes())
+            lora = sum(cfg.lora_rank * (o + i) for _, o, i in cfg.linear_shapes())
+            flops = args.steps * 2 * M * cfg.n_layers * (2 * lin + lora)
+            g = prof["gemm"]
+            # M flops per weight byte against the ridge of the two peaks
+            if M >= MFMA16_PEAK_TFLOPS * 1e3 / HBM_PEAK_GBPS:
+                tflops = flops / (g["total_ms"] * 1e-3) / 1e12
+                result["gemm_roofline"] = {
+                    "bound": "mfma", "kernel": "k_gemm_big (projections and LoRA shrinks; both passes)",
+                    "achieved": round(tflops, 1), "peak": MFMA16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(tflops / MFMA16_PEAK_TFLOPS, 4), "traffic": None,
+                    "flops_per_launch": round(flops / g["launches"]), "avg_launch_us": g["avg_us"]}
+            else:
+                gbytes = args.steps * (byt["gemm_draft"] + byt["gemm_verify"])
+                ach = gbytes / (g["total_ms"] * 1e-3) / 1e9
+                result["gemm_roofline"] = {
+                    "bound": "hbm", "kernel": "k_gemm_big (projections and LoRA shrinks; both passes)",
+                    "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                    "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None,
+                    "bytes_per_launch": round(gbytes / g["launches"]), "avg_launch_us": g["avg_us"]}
+            at_ = prof["attn"]
+            if at_["launches"]:
+                es = 2 if cfg.dtype == "bf16" else 4
+                kv_layer = sum(lengths) * 2 * cfg.n_kv_heads * cfg.head_dim * es
+                ach = kv_layer / (at_["avg_us"] * 1e-6) / 1e9
+                result["attn_roofline"] = {
+                    "bound": "hbm", "kernel": "k_attn (split-KV partials over the prefix K/V)",
+                    "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                    "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None,
+                    "bytes_per_launch": kv_layer, "avg_launch_us": at_["avg_us"]}
+            # the step's dominant kernel class gives the line's roofline
+            dom = "attn_roofline" if "attn_roofline" in result and at_["total_ms"] > g["total_ms"] else "gemm_roofline"
+            result["roofline"] = dict(result[dom])
         result["kernel_classes"] = prof
         kernel_sum = sum(v["total_ms"] for v in prof.values()) / args.steps
         result["kernel_time_ms_per_step"] = round(kernel_sum, 4)
