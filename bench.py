@@ -692,13 +692,15 @@ def main():
             at_ = prof["attn"]
             if at_["launches"]:
                 es = 2 if cfg.dtype == "bf16" else 4
-                kv_layer = sum(lengths) * 2 * cfg.n_kv_heads * cfg.head_dim * es
-                ach = kv_layer / (at_["avg_us"] * 1e-6) / 1e9
+                # every layer of both passes reads the prefix K/V once
+                kv_bytes = args.steps * 2 * cfg.n_layers * sum(lengths) * 2 * cfg.n_kv_heads * cfg.head_dim * es
+                ach = kv_bytes / (at_["total_ms"] * 1e-3) / 1e9
                 result["attn_roofline"] = {
                     "bound": "hbm", "kernel": "k_attn (split-KV partials over the prefix K/V)",
                     "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                     "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None,
-                    "bytes_per_launch": kv_layer, "avg_launch_us": at_["avg_us"]}
+                    "bytes_per_launch": round(kv_bytes / at_["launches"]), "avg_launch_us": at_["avg_us"],
+                    "us_per_layer": round(1e3 * at_["total_ms"] / (args.steps * 2 * cfg.n_layers), 2)}
             # the step's dominant kernel class gives the line's roofline
             dom = "attn_roofline" if "attn_roofline" in result and at_["total_ms"] > g["total_ms"] else "gemm_roofline"
             result["roofline"] = dict(result[dom])

@@ -455,3 +455,42 @@ def test_single_bf16_operands_are_refused_for_bf16_models():
     g.eng.pbd_set_operand_precision(bd.PBD_OPERANDS_BF16)
     g.eng.pbd_set_operand_precision(bd.PBD_OPERANDS_BF16X2)
     g.close()
+
+
+@pytest.mark.parametrize("D", [24, 32])
+def test_wide_query_tiles_match_oracle(D):
+    """Four (D = 24) and five (D = 32) 16-row query tiles per KV head at the
+    Qwen3-0.6B layer shape, one work-group per (split, KV head, sequence)
+    over all of them (query tiles from LDS): ragged prefixes (300, 517) in
+    splits of 128 keys, with a partial last block; draft, verify and the next
+    draft after a commit against the oracle at the bf16 bound."""
+    cfg = synth.QWEN3_0_6B.with_(n_layers=2, vocab=4096, block=D)
+    w = synth.make_weights(cfg, 7300 + D)
+    prompts = synth.make_prompts(cfg, [300, 517], 7400 + D)
+    g = GpuRun(cfg, w, max_batch=2, max_seq=640)
+    g.eng.pbd_set_attn_query_split(0)
+    g.eng.pbd_set_attn_keys_per_split(128)
+    g.prefill(prompts)
+    m = om.OracleModel(w)
+    d, dlg = g.draft()
+    v, vlg = g.verify(d)
+    errs = []
+    for b, p in enumerate(prompts):
+        st = om.prefill(m, p)
+        _, dl_ref = om.draft(m, st)
+        errs.append(np.abs(dlg.cpu().numpy()[b] - dl_ref).max())
+        _, vl_ref, _, _ = om.verify(m, st, d.cpu().numpy()[b])
+        errs.append(np.abs(vlg.cpu().numpy()[b] - vl_ref).max())
+    n, out = g.accept(d, v)
+    d2, dlg2 = g.draft()
+    for b, p in enumerate(prompts):
+        st = om.prefill(m, p)
+        _, _, k, vv = om.verify(m, st, d.cpu().numpy()[b])
+        nn, oo = om.accept(d.cpu().numpy()[b], v.cpu().numpy()[b], forced_n=int(n.cpu().numpy()[b]))
+        om.commit(st, nn, oo, k, vv)
+        _, dl_ref = om.draft(m, st)
+        errs.append(np.abs(dlg2.cpu().numpy()[b] - dl_ref).max())
+    assert g.status() == 0
+    print(f"four/five query tiles D={D}: max-abs {max(errs):.4f}")
+    assert max(errs) <= 2e-2
+    g.close()
