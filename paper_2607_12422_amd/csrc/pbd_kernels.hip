@@ -778,6 +778,15 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                    rope + (size_t)(t + qq % W) * HALF, lrow);
     }
     float gq_lo[RP::NP], gq_hi[RP::NP];
+    // the softmax scale (log2 e / sqrt(head_dim)) rides on the query gains:
+    // the rotation is linear, so the scores come out of the MFMA scaled
+    auto scale_gains = [&](float* lo_, float* hi_) {
+#pragma unroll
+        for (int p = 0; p < RP::NP; ++p) {
+            lo_[p] *= a.scale_log2;
+            hi_[p] *= a.scale_log2;
+        }
+    };
     if (blk) {
         Gains<T, HD> gk;
         if (a.qk_norm) gk.load(a.k_norm, lrow);
@@ -794,6 +803,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
             vhi[i] = *(const typename RP::fv*)(vs + HALF + RP::NP * lrow);
         }
         gq.get(a.qk_norm, gq_lo, gq_hi);
+        scale_gains(gq_lo, gq_hi);
 #pragma unroll
         for (int i = 0; i < QSTEPS; ++i) {
             const int ql = 16 * i + 4 * wid + lgrp;
@@ -834,6 +844,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         }
     } else {
         gq.get(a.qk_norm, gq_lo, gq_hi);
+        scale_gains(gq_lo, gq_hi);
 #pragma unroll
         for (int i = 0; i < QSTEPS; ++i) {
             const int ql = 16 * i + 4 * wid + lgrp;
@@ -873,7 +884,6 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) o_acc[dt][qt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    const float sl2 = a.scale_log2;
 
     // One chunk in phases, each straight-line over all query tiles so that
     // the tiles' independent MFMA chains interleave: scores, key masks (only
@@ -908,7 +918,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
             for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) sv[qt][c][e] = sc[qt][e] * sl2;
+                for (int e = 0; e < 4; ++e) sv[qt][c][e] = sc[qt][e];
         }
         if (!full) {
 #pragma unroll
@@ -951,7 +961,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
                     for (int e = 0; e < 4; ++e) mloc = fmaxf(mloc, sv[qt][c][e]);
                 const float m_new = fmaxf(m_run[qt], xrow_max(mloc));
                 if (!first) {
-                    const float corr = exp2f(m_run[qt] - m_new);
+                    const float corr = __builtin_amdgcn_exp2f(m_run[qt] - m_new);
                     l_run[qt] *= corr;
 #pragma unroll
                     for (int dt = 0; dt < NDT; ++dt) o_acc[dt][qt] *= corr;
@@ -968,7 +978,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
             for (int c = 0; c < CH; ++c)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    p[qt][c][e] = exp2f(sv[qt][c][e] - m_run[qt]);
+                    p[qt][c][e] = __builtin_amdgcn_exp2f(sv[qt][c][e] - m_run[qt]);
                     l_run[qt] += p[qt][c][e];
                 }
 #pragma unroll
