@@ -147,7 +147,11 @@ typedef struct pbd_weights {
  * selects how much of it a pass uses), so no per-batch size query is needed.
  * When the model qualifies for the persistent batch-1 pass (see
  * pbd_set_pass_mode), the packed weights also hold an fp16 copy of every
- * layer's projection and LoRA A fragments, which that pass streams.
+ * layer's projection and LoRA A fragments, which that pass streams.  A bf16
+ * model whose max_batch * (block + 1) is at least 128 (draft and verify
+ * passes on the large-M GEMM) also gets those copies and an fp16 copy of the
+ * embedding fragments (the tied LM head), read by those passes; its
+ * workspace also holds the LoRA shrink's K slices (up to eight).
  */
 size_t pbd_packed_weight_bytes(const pbd_config* cfg);
 size_t pbd_kv_bytes(const pbd_config* cfg);
@@ -354,7 +358,10 @@ int pbd_set_attn_query_split(pbd_ctx* ctx, int32_t mode);
  * returns PBD_ERR_UNSUPPORTED for them, because single bf16 activation
  * operands put the Qwen3-0.6B-shape logits outside the 2e-2 bound.  fp32
  * models accept either value and ignore it.  Other values:
- * PBD_ERR_INVALID_ARG.
+ * PBD_ERR_INVALID_ARG.  Independently of this setting, draft and verify
+ * passes of 128 or more rows (batches of 8+) and the persistent batch-1
+ * pass take single fp16 operands (11 significant bits) against fp16 weight
+ * copies, within the same parity bound; prefill chunks keep the pair.
  */
 int pbd_set_operand_precision(pbd_ctx* ctx, int32_t mode);
 
