@@ -791,6 +791,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             float gql[RP::NP], gqh[RP::NP], gkl[RP::NP], gkh[RP::NP];
             gq.get(a.qk_norm, gql, gqh);
             gk.get(a.qk_norm, gkl, gkh);
+            // the softmax scale (log2 e / sqrt(head_dim)) rides on the query
+            // gains (the rotation is linear): the scores leave the MFMA scaled
+#pragma unroll
+            for (int pp = 0; pp < RP::NP; ++pp) {
+                gql[pp] *= a.scale_log2;
+                gqh[pp] *= a.scale_log2;
+            }
             for (int j0 = 0; j0 < njob; j0 += NG16 * NJ) {
                 typename RP::fv vlo[NJ], vhi[NJ];
 #pragma unroll
@@ -902,13 +909,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                         if (blk) ok = kk < M && (kk <= jq || jq >= a.full_from);
                         else ok = (kb0 * 16 + kk) < t;
                         ok = ok && qcol < QR;
-                        sv[e] = ok ? s[e] * a.scale_log2 : -INFINITY;
+                        sv[e] = ok ? s[e] : -INFINITY;
                     }
                     float mloc = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
                     mloc = xrow_max(mloc);
                     const float m_new = fmaxf(m_run, mloc);
                     if (!first) {
-                        const float corr = exp2f(m_run - m_new);
+                        const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
                         l_run *= corr;
 #pragma unroll
                         for (int dt = 0; dt < HD / 16; ++dt) o_acc[dt] *= corr;
@@ -918,7 +925,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     f32x4 pr;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        pr[e] = exp2f(sv[e] - m_run);
+                        pr[e] = __builtin_amdgcn_exp2f(sv[e] - m_run);
                         l_run += pr[e];
                     }
 #pragma unroll
@@ -940,7 +947,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 const bool other = b_hi < nb;
                 if (other) { m1 = pb[HD]; l1 = pb[HD + 1]; }
                 const float mx = fmaxf(m_run, m1);
-                const float f0 = exp2f(m_run - mx), f1 = other ? exp2f(m1 - mx) : 0.f;
+                const float f0 = __builtin_amdgcn_exp2f(m_run - mx), f1 = other ? __builtin_amdgcn_exp2f(m1 - mx) : 0.f;
 #pragma unroll
                 for (int dt = 0; dt < HD / 16; ++dt) {
                     f32x4 o1 = other ? *(const f32x4*)(pb + dt * 16 + lgrp * 4) : f32x4{0, 0, 0, 0};
@@ -1001,7 +1008,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     ov[k] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rws, ob0, k * QRMAX * APW * 4, SC1));
                 const float mls = __uint_as_float(ml.x);
                 const float mx = wave_max(mls);
-                const float wl = (mls > -INFINITY) ? exp2f(mls - mx) : 0.f;
+                const float wl = (mls > -INFINITY) ? __builtin_amdgcn_exp2f(mls - mx) : 0.f;
                 const float wll = wl * __uint_as_float(ml.y);
                 // merged in fixed split order, the weights read from their lanes
                 float o0 = 0.f, o1 = 0.f, Ls = 0.f;
