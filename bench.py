@@ -696,7 +696,7 @@ def main():
                 kv_bytes = args.steps * 2 * cfg.n_layers * sum(lengths) * 2 * cfg.n_kv_heads * cfg.head_dim * es
                 ach = kv_bytes / (at_["total_ms"] * 1e-3) / 1e9
                 result["attn_roofline"] = {
-                    "bound": "hbm", "kernel": "k_attn (split-KV partials over the prefix K/V)",
+                    "bound": "hbm", "kernel": "attention partials over the prefix K/V (k_attn_rows at 4-5 query tiles per KV head, else k_attn)",
                     "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                     "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None,
                     "bytes_per_launch": round(kv_bytes / at_["launches"]), "avg_launch_us": at_["avg_us"],

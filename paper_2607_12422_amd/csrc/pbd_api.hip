@@ -605,7 +605,16 @@ int run_pass(pbd_ctx* c, const PassReq& q, hipStream_t st) {
             kw.kcache = at.kcache; kw.vcache = at.vcache;
             PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_kvwrite(dt, y.HD, kw, B, st), "prefill K/V");
         }
-        PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn(dt, y.HD, QTw, at, B, st), "attention");
+        // four or five query tiles per KV head: one wave per query tile (keys
+        // staged in LDS); k_attn then only warms the cache, when CUs are spare
+        if (!pre && QTw == QT && attn_rows_fits(dt, y.HD, QTw, at.chunk, W)) {
+            at.skip_prefix = 1;
+            PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn_rows(at, QTw, B, st), "attention");
+            if (at.pf_x > 0)
+                PBD_TIMED(c, st, PBD_KCLASS_OTHER, launch_attn(dt, y.HD, QTw, at, B, st), "attention cache warming");
+        } else {
+            PBD_TIMED(c, st, PBD_KCLASS_ATTN, launch_attn(dt, y.HD, QTw, at, B, st), "attention");
+        }
 
         CombineArgs cb{};
         cb.W = W; cb.n_q = y.NQ; cb.head_dim = y.HD; cb.kps = kps; cb.s_launch = s_launch; cb.MT = MT;

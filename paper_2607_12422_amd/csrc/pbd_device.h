@@ -187,6 +187,17 @@ struct RowPrep {
     // as T and returns the lane's values
     __device__ void finish(T* dst, bool live, const float* g_lo, const float* g_hi, bool qk_norm, float eps, int l16,
                            T* out_lo, T* out_hi) {
+        values(live, g_lo, g_hi, qk_norm, eps, out_lo, out_hi);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            const int i = NP * l16 + p;
+            dst[i] = out_lo[p];
+            dst[i + HALF] = out_hi[p];
+        }
+    }
+    // the lane's normalised and rotated values (dead rows: zeros), no store
+    __device__ void values(bool live, const float* g_lo, const float* g_hi, bool qk_norm, float eps, T* out_lo,
+                           T* out_hi) {
         float inv = live ? 1.f : 0.f;
         if (qk_norm) {
             float ss = 0.f;
@@ -196,13 +207,10 @@ struct RowPrep {
         }
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
-            const int i = NP * l16 + p;
             const float y0 = lo[p] * inv * g_lo[p], y1 = hi[p] * inv * g_hi[p];
             const float c = cs[2 * p], sn = cs[2 * p + 1];
             out_lo[p] = from_f32<T>(y0 * c - y1 * sn);
             out_hi[p] = from_f32<T>(y1 * c + y0 * sn);
-            dst[i] = out_lo[p];
-            dst[i + HALF] = out_hi[p];
         }
     }
 };

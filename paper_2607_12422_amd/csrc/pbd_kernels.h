@@ -119,6 +119,9 @@ struct AttnArgs {
     // positions t..t+nrows-1; every key is read from the cache, causal inside
     // the chunk; no block split and no K/V writes
     int chunk;
+    // every split is run by k_attn_rows (launch_attn_rows); k_attn only warms
+    // the memory-side cache in its pf_x extra columns
+    int skip_prefix;
 };
 
 // Prefill chunk K/V: norm + RoPE of the W rows' keys, appended with the values.
@@ -293,6 +296,12 @@ hipError_t launch_assemble(int dtype, const AssembleArgs& a, int batch, hipStrea
 hipError_t launch_fgemm(int dtype, const FGemmArgs& a, int epi, hipStream_t st);   // split iff a.xlo
 int fgemm_mgroup(int epi, int MT, int lrt);   // lrt: LoRA rank tiles of the launch (0: adapter off)
 int fgemm_threads(int epi);         // work-group size of the GEMM with epilogue epi
+// The attention partials of a draft or verify pass with four or five 16-row
+// query tiles per KV head (bf16, head_dim 128, W <= 48): every split of
+// k_attn's schedule, one wave per query tile, keys staged through LDS
+// (false: this shape is not covered; use k_attn alone)
+bool attn_rows_fits(int dtype, int head_dim, int qt, int chunk, int W);
+hipError_t launch_attn_rows(const AttnArgs& a, int qt, int batch, hipStream_t st);
 hipError_t launch_attn(int dtype, int head_dim, int qt, const AttnArgs& a, int batch, hipStream_t st);
 hipError_t launch_combine(int dtype, const CombineArgs& a, int M, hipStream_t st);
 hipError_t launch_argmax(const ArgmaxArgs& a, hipStream_t st);

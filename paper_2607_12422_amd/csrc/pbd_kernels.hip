@@ -647,6 +647,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         asm volatile("" ::"v"(acc));
         return;
     }
+    if (a.skip_prefix) return;                         // every split run by k_attn_rows
     const int s = blockIdx.x, g = blockIdx.y;
     const int b = blockIdx.z / a.n_qgrp;
     const int q0 = (blockIdx.z % a.n_qgrp) * QROWS;      // first query row of this work-group
@@ -1084,6 +1085,303 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
             a.part_ml[pr * 2 + 1] = L;
         }
     }
+}
+
+// ---------------------------------------------------------------------------
+// Attention partials of draft and verify passes with four or five 16-row
+// query tiles per KV head (bf16, head_dim 128): the split-KV schedule, block
+// split and partial layout of k_attn, another work split.  k_attn gives each
+// wave every query tile and a quarter of the keys: 160 accumulator registers
+// per lane, copies between accumulator and vector registers at each key
+// block, and a merge of the four waves.  Here wave w owns query tile w over
+// every key of the work-group (32 accumulator registers, no merge), and the
+// keys go through LDS once per work-group:
+//  * prefix splits: the first four waves copy each cache block (16 bytes per
+//    lane and chunk, one block ahead in registers) into a double buffer;
+//  * the block split: the same waves normalise and rotate the W block rows'
+//    keys into LDS blocks of the cache layout (and append them to the cache
+//    in the verify), once the query fragments are in registers;
+//  * unused splits mark their partials empty.
+// Several work-groups share a CU.
+// ---------------------------------------------------------------------------
+
+// 16 wait states, with nothing scheduled across: enough for any MFMA of this
+// file to finish writing its result, or reading its operands, before the
+// instructions that follow touch those registers
+__device__ __forceinline__ void mfma_settle() {
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_nop 7\n\ts_nop 7" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+constexpr int ATTN_ROWS_WMAX = 48;     // block rows of the block split (three key blocks)
+
+// Four work-groups per CU (16 or 20 waves) need at most 128 or 102
+// registers per lane: the waves-per-SIMD floor holds the allocator to that.
+template <int QT>
+__global__ __launch_bounds__(QT * 64) __attribute__((amdgpu_waves_per_eu(QT, 8))) void k_attn_rows(AttnArgs a) {
+    typedef bf16 T;
+    constexpr int HD = 128, HALF = HD / 2, FK = Elt<T>::FK, EPL = Elt<T>::EPL;
+    constexpr int NDS = HD / FK, NDT = HD / 16;
+    constexpr int LDQ = HD + 16 / (int)sizeof(T);
+    constexpr int BLK = 2 * 16 * HD * (int)sizeof(T);       // one key block's K then V (8 KiB)
+    constexpr int NLD = 4;                                   // waves that stage the blocks
+    constexpr int CPL = BLK / 16 / (NLD * WAVE);             // 16-byte chunks per staging lane
+    constexpr int Q_BYTES = (QT * 16 * LDQ * (int)sizeof(T) + 15) / 16 * 16;
+    typedef uint2 vraw;
+    typedef RowPrep<T, HD> RP;
+    static_assert(QT >= NLD && CPL * NLD * WAVE * 16 == BLK, "staging layout");
+    static_assert((ATTN_ROWS_WMAX / 16) * BLK <= Q_BYTES + 2 * BLK, "block split keys fit the LDS");
+
+    const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    const int t = a.pos0[b], nrows = a.nrows[b];
+    int s_pre, chunk;
+    attn_splits(t, a.kps, a.s_launch, s_pre, chunk);
+    const int W = a.W, G = a.G, QR = G * W;
+    const int lane = threadIdx.x % WAVE, wid = threadIdx.x / WAVE;
+    const int lrow = lane % 16, lgrp = lane / 16;
+    const int q = wid * 16 + lrow;                             // this lane's query column
+    if (s > s_pre) {
+        // unused split: partials empty (max -inf, sum 0), so that the merge
+        // can read every split without the sequence's position
+        if (lgrp == 0 && q < QR) {
+            const size_t pr = (((size_t)b * a.n_q + g * G + q / W) * W + q % W) * a.s_launch + s;
+            a.part_ml[pr * 2 + 0] = -INFINITY;
+            a.part_ml[pr * 2 + 1] = 0.f;
+        }
+        return;
+    }
+    const bool blk = s == s_pre;                               // the split of the W block keys
+    const int k_lo = blk ? t : min(s * chunk, t), k_hi = blk ? t : min(t, k_lo + chunk);
+    const int kb_first = k_lo / 16;
+    const int n_items = blk ? ceil_div(W, 16) : k_hi > k_lo ? ceil_div(k_hi, 16) - kb_first : 0;
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    T* q_l = (T*)smem;                                         // [QT * 16][LDQ]
+    unsigned char* kv_l = smem + Q_BYTES;                      // [2][BLK]
+
+    const size_t row_stride = (size_t)a.nqkv;
+    const float* qkv_b = a.qkv + (size_t)b * W * row_stride;
+    const size_t head = (((size_t)a.layer * a.max_batch + b) * a.n_kv + g) * a.nblk * 16 * HD;
+    const unsigned char* kc = (const unsigned char*)((const T*)a.kcache + head);
+    const unsigned char* vc = (const unsigned char*)((const T*)a.vcache + head);
+
+    // prefix staging: chunk c of a block is 16 bytes at c * 16 (K: c < BLK /
+    // 32, then V); staging lane (wid, lane) holds chunks (wid * CPL + k) *
+    // WAVE + lane (two named registers, not an array: an array captured by the
+    // staging helpers is placed in scratch memory)
+    static_assert(CPL == 2, "two staging chunks per lane");
+    auto gchunk = [&](int it, int k) -> uint4 {
+        const size_t off = (size_t)(kb_first + it) * (BLK / 2);
+        const int c = (wid * CPL + k) * WAVE + lane;
+        return c < BLK / 32 ? *(const uint4*)(kc + off + (size_t)c * 16)
+                            : *(const uint4*)(vc + off + (size_t)(c - BLK / 32) * 16);
+    };
+    auto schunk = [&](int buf, int k, const uint4& v) {
+        const int c = (wid * CPL + k) * WAVE + lane;
+        *(uint4*)(kv_l + (size_t)buf * BLK + (size_t)c * 16) = v;
+    };
+    uint4 stg0 = uint4{0u, 0u, 0u, 0u}, stg1 = uint4{0u, 0u, 0u, 0u};
+    auto gload = [&](int it) { stg0 = gchunk(it, 0); stg1 = gchunk(it, 1); };
+    auto swrite = [&](int buf) { schunk(buf, 0, stg0); schunk(buf, 1, stg1); };
+    const bool stager = wid < NLD;
+    if (stager && !blk && n_items > 0) gload(0);
+
+    // -- this wave's 16 query rows: normed, rotated and scaled by
+    //    log2 e / sqrt(head_dim) into LDS, four rows per step, in two halves
+    //    (the first key block's loads are in flight meanwhile)
+    {
+        Gains<T, HD> gq;
+        if (a.qk_norm) gq.load(a.q_norm, lrow);
+        float gq_lo[RP::NP], gq_hi[RP::NP];
+        gq.get(a.qk_norm, gq_lo, gq_hi);
+#pragma unroll
+        for (int p = 0; p < RP::NP; ++p) {
+            gq_lo[p] *= a.scale_log2;
+            gq_hi[p] *= a.scale_log2;
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            RP rp[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int qi = wid * 16 + 4 * (2 * h + i) + lgrp;
+                const int qq = (qi < QR && (qi % W) < nrows) ? qi : 0;   // dead rows read a valid row
+                rp[i].load(qkv_b + (size_t)(qq % W) * row_stride + (size_t)(g * G + qq / W) * HD,
+                           a.rope + (size_t)(t + qq % W) * HALF, lrow);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int qi = wid * 16 + 4 * (2 * h + i) + lgrp;
+                T lo[RP::NP], hi[RP::NP];
+                rp[i].finish(q_l + qi * LDQ, qi < QR, gq_lo, gq_hi, a.qk_norm, a.eps, lrow, lo, hi);
+            }
+        }
+    }
+    if (stager && !blk && n_items > 0) {
+        swrite(0);
+        if (n_items > 1) gload(1);
+    }
+    lds_sync();
+    uint4 qf[NDS];
+#pragma unroll
+    for (int ds = 0; ds < NDS; ++ds) qf[ds] = *(const uint4*)(q_l + q * LDQ + ds * FK + lgrp * EPL);
+
+    if (blk) {
+        // block keys and values into LDS key blocks 0 .. n_items - 1 (over the
+        // query rows, read above); row r = 4 wid + lgrp of each block, 16
+        // lanes per row.  The verify appends rows j < kv_rows to the cache.
+        lds_sync();
+        if (stager) {
+            static_assert(EPL == 8 && RP::NP == 4, "bf16 block layout with four pairs per lane");
+            Gains<T, HD> gk;
+            if (a.qk_norm) gk.load(a.k_norm, lrow);
+            float gk_lo[RP::NP], gk_hi[RP::NP];
+            gk.get(a.qk_norm, gk_lo, gk_hi);
+            const int r = 4 * wid + lgrp;
+            for (int i = 0; i < n_items; ++i) {
+                const int j = 16 * i + r;
+                const bool live = j < W && j < nrows;
+                const int jj = live ? j : 0;                       // dead rows read a valid row
+                const float* ks = qkv_b + (size_t)jj * row_stride + (size_t)a.n_q * HD + (size_t)g * HD;
+                const float* vs = ks + (size_t)a.n_kv * HD;
+                RP rk;
+                rk.load(ks, a.rope + (size_t)(t + jj) * HALF, lrow);
+                const typename RP::fv vlo = *(const typename RP::fv*)(vs + RP::NP * lrow);
+                const typename RP::fv vhi = *(const typename RP::fv*)(vs + HALF + RP::NP * lrow);
+                T klo[RP::NP], khi[RP::NP];
+                rk.values(live, gk_lo, gk_hi, a.qk_norm, a.eps, klo, khi);
+                T vl[RP::NP], vh[RP::NP];
+#pragma unroll
+                for (int p = 0; p < RP::NP; ++p) {
+                    vl[p] = from_f32<T>(live ? vlo[p] : 0.f);
+                    vh[p] = from_f32<T>(live ? vhi[p] : 0.f);
+                }
+                // the lane's dims 4 lrow .. 4 lrow + 3 (and + HALF) of key row r:
+                // one 8-byte run of the K block (kblock_elem), four V elements
+                // 4 apart (vblock_elem); the high half 1024 elements on
+                const int ko = ((lrow / 8) * 64 + ((lrow % 8) / 2) * 16 + r) * 8 + 4 * (lrow % 2);
+                const int vo = ((lrow / 4) * 64 + (r / 4) * 16 + 4 * (lrow % 4)) * 4 + r % 4;
+                auto put = [&](T* kb, T* vb, int ko_, int vo_) {
+                    uint2 k2, h2;
+                    __builtin_memcpy(&k2, klo, 8);
+                    __builtin_memcpy(&h2, khi, 8);
+                    *(uint2*)(kb + ko_) = k2;
+                    *(uint2*)(kb + ko_ + 1024) = h2;
+#pragma unroll
+                    for (int p = 0; p < RP::NP; ++p) {
+                        vb[vo_ + 4 * p] = vl[p];
+                        vb[vo_ + 4 * p + 1024] = vh[p];
+                    }
+                };
+                put((T*)(smem + (size_t)i * BLK), (T*)(smem + (size_t)i * BLK + BLK / 2), ko, vo);
+                if (live && j < a.kv_rows) {
+                    const int pos = t + j, kr = pos % 16;
+                    put((T*)a.kcache + head + (size_t)(pos / 16) * 16 * HD, (T*)a.vcache + head + (size_t)(pos / 16) * 16 * HD,
+                        ko + (kr - r) * 8, vo + (kr / 4 - r / 4) * 64 + (kr % 4 - r % 4));
+                }
+            }
+        }
+        lds_sync();
+    }
+
+    f32x4 o_acc[NDT];
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) o_acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -1e30f, l_run = 0.f;
+    const int jq = q % W;                                      // block row of this query column
+    for (int it = 0; it < n_items; ++it) {
+        const unsigned char* cur = blk ? smem + (size_t)it * BLK : kv_l + (size_t)(it & 1) * BLK;
+        // scores of the block's 16 keys for this wave's query column lrow
+        // (lane: keys 4 lgrp .. 4 lgrp + 3), scaled through the query rows
+        f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds) mma_frag<T>(sc, *(const uint4*)(cur + ds * 1024 + lane * 16), qf[ds]);
+        // The maximum below reads the scores right after the branch around the
+        // key mask.  The compiler's wait states before that read do not cover
+        // the branch-taken path (the read came two instructions after the last
+        // MFMA), and the rescale vote then saw unfinished scores now and then:
+        // results that changed from run to run.  Explicit wait states here.
+        mfma_settle();
+        float sv[4] = {sc[0], sc[1], sc[2], sc[3]};
+        if (blk) {
+            // block key kk is seen by block row jq iff kk <= jq or jq >= full_from
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int kk = it * 16 + lgrp * 4 + e;
+                if (!((kk < nrows) & ((kk <= jq) | (jq >= a.full_from)))) sv[e] = -INFINITY;
+            }
+        } else {
+            const int key0 = (kb_first + it) * 16;
+            if (key0 + 16 > k_hi) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (key0 + lgrp * 4 + e >= k_hi) sv[e] = -INFINITY;
+            }
+        }
+        // lazy reference maximum (k_attn's rule): raised, with the output and
+        // sum rescaled, only when a score exceeds it by RESCALE_SLACK
+        bool over = it == 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) over = over | (sv[e] > m_run + RESCALE_SLACK);
+        if (__any(over)) {
+            const float mloc = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+            const float m_new = fmaxf(m_run, xrow_max(mloc));
+            const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
+            l_run *= corr;
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) o_acc[dt] *= corr;
+            m_run = m_new;
+        }
+        f32x4 pw;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            pw[e] = __builtin_amdgcn_exp2f(sv[e] - m_run);
+            l_run += pw[e];
+        }
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+            mma_k4(o_acc[dt], *(const vraw*)(cur + BLK / 2 + (dt * WAVE + lane) * sizeof(vraw)), pw);
+        // explicit wait states after the P.V chain: the staging code below may
+        // take the chain's accumulator source registers as temporaries
+        mfma_settle();
+        // prefix splits: the next block into the other buffer (read by every
+        // wave in the previous turn, released by its barrier), the one after
+        // into registers
+        if (stager && !blk && it + 1 < n_items) {
+            swrite((it + 1) & 1);
+            if (it + 2 < n_items) gload(it + 2);
+        }
+        lds_sync();
+    }
+    l_run = xrow_sum(l_run);
+
+    // partial of this split for the wave's query rows: max (log2 domain), sum,
+    // unnormalised output
+    if (q < QR) {
+        const int gi = q / W, j = q % W;
+        const size_t pr = (((size_t)b * a.n_q + g * G + gi) * W + j) * a.s_launch + s;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) *(f32x4*)(a.part_o + pr * HD + dt * 16 + lgrp * 4) = o_acc[dt];
+        if (lgrp == 0) {
+            a.part_ml[pr * 2 + 0] = m_run;
+            a.part_ml[pr * 2 + 1] = l_run;
+        }
+    }
+}
+
+bool attn_rows_fits(int dtype, int head_dim, int qt, int chunk, int W) {
+    return dtype == PBD_DTYPE_BF16 && head_dim == 128 && (qt == 4 || qt == 5) && !chunk && W <= ATTN_ROWS_WMAX;
+}
+
+hipError_t launch_attn_rows(const AttnArgs& a, int qt, int batch, hipStream_t st) {
+    if (a.n_qgrp != 1 || a.chunk || a.W > ATTN_ROWS_WMAX || a.G * a.W > qt * 16) return hipErrorInvalidValue;
+    const size_t smem = ((size_t)qt * 16 * (128 + 8) * 2 + 15) / 16 * 16 + 2 * 8192;
+    const dim3 grid(a.s_launch, a.n_kv, batch);
+    if (qt == 4) PBD_LAUNCH(k_attn_rows<4>, grid, dim3(4 * 64), smem, st, a);
+    else if (qt == 5) PBD_LAUNCH(k_attn_rows<5>, grid, dim3(5 * 64), smem, st, a);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

@@ -4,7 +4,8 @@ A register array indexed with a run-time value, or a register budget that
 overflows, puts per-lane data in scratch memory, which turns every access into
 a global memory round trip.  The kernels of the Qwen3-shape passes (the persistent
 layer stack; bf16 with split operands; projection GEMMs at every LoRA rank up to 64; attention with
-head_dim 128 and up to three 16-row query tiles) and every projection GEMM of
+head_dim 128 and up to three 16-row query tiles, and the prefix splits of
+four or five) and every projection GEMM of
 the fp32 model must use no scratch at all.
 """
 import os
@@ -21,6 +22,7 @@ HOT = [
     r"_ZN3pbd7k_fgemmIDF16bLi\d+ELi\d+ELb1ELi[0-4]EEEvNS_9FGemmArgsE",
     r"_ZN3pbd7k_fgemmIfLi\d+ELi\d+ELb0ELi[0-4]EEEvNS_9FGemmArgsE",
     r"_ZN3pbd6k_attnIDF16bLi128ELi[123]EEEvNS_8AttnArgsE",            # attention, G*W <= 48 query rows
+    r"_ZN3pbd11k_attn_rowsILi[45]EEEvNS_8AttnArgsE",                  # prefix splits, 49..80 query rows
     r"_ZN3pbd8k_lmheadIDF16bLb1ELb[01]EEEvNS_9FGemmArgsE",            # LM head (with / without confidence)
     r"_ZN3pbd9k_combineIDF16bLi\d+EEEvNS_11CombineArgsE",
     r"_ZN3pbd10k_assembleIDF16bEEvNS_12AssembleArgsE",
