@@ -695,10 +695,13 @@ def main():
                 # every layer of both passes reads the prefix K/V once
                 kv_bytes = args.steps * 2 * cfg.n_layers * sum(lengths) * 2 * cfg.n_kv_heads * cfg.head_dim * es
                 ach = kv_bytes / (at_["total_ms"] * 1e-3) / 1e9
+                # counter traffic: taken for the batch-32 workload's k_attn_rows
+                traffic = (counter_traffic("k_attn_rows_traffic_qwen3-0.6b_b32_p8192.txt", "pbd_kernels.hip")
+                           if w_.name == "qwen3-0.6b-b32-p8192-d32" else None)
                 result["attn_roofline"] = {
                     "bound": "hbm", "kernel": "attention partials over the prefix K/V (k_attn_rows at 4-5 query tiles per KV head, else k_attn)",
                     "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                    "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None,
+                    "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": traffic,
                     "bytes_per_launch": round(kv_bytes / at_["launches"]), "avg_launch_us": at_["avg_us"],
                     "us_per_layer": round(1e3 * at_["total_ms"] / (args.steps * 2 * cfg.n_layers), 2)}
             # the step's dominant kernel class gives the line's roofline
