@@ -460,10 +460,11 @@ def test_single_bf16_operands_are_refused_for_bf16_models():
 @pytest.mark.parametrize("D", [24, 32])
 def test_wide_query_tiles_match_oracle(D):
     """Four (D = 24) and five (D = 32) 16-row query tiles per KV head at the
-    Qwen3-0.6B layer shape, one work-group per (split, KV head, sequence)
-    over all of them (query tiles from LDS): ragged prefixes (300, 517) in
-    splits of 128 keys, with a partial last block; draft, verify and the next
-    draft after a commit against the oracle at the bf16 bound."""
+    Qwen3-0.6B layer shape: the attention runs one wave per query tile
+    (k_attn_rows) over every split: ragged prefixes (300, 517) in splits of
+    128 keys, with a partial last block, the block split (appending the
+    verify's K/V) and unused splits; draft, verify and the next draft after a
+    commit against the oracle at the bf16 bound."""
     cfg = synth.QWEN3_0_6B.with_(n_layers=2, vocab=4096, block=D)
     w = synth.make_weights(cfg, 7300 + D)
     prompts = synth.make_prompts(cfg, [300, 517], 7400 + D)

@@ -186,3 +186,37 @@ def test_qwen_shape_unanchored_step_matches_oracle():
     assert int(n[0]) == nn
     assert g.status() == 0
     g.close()
+
+
+def test_wide_query_tiles_unanchored_matches_oracle():
+    """Unanchored rounds where the attention runs one wave per 16-row query
+    tile: Qwen3-0.6B layer shape (two layers), D = 32, so the draft's 33 rows
+    make five tiles per KV head and the verify's 32 drafts four.  The draft's
+    block split appends the anchor's K/V; the verify's appends the drafts'.
+    Two rounds with forced acceptance of 3 and 0 tokens, then an anchored
+    draft, all against the oracle (2e-2) over a ragged prefix of 517 keys in
+    splits of 128."""
+    cfg = synth.QWEN3_0_6B.with_(n_layers=2, vocab=4096, block=32)
+    w = synth.make_weights(cfg, 7500)
+    prompt = synth.make_prompts(cfg, [517], 7501)[0]
+    g = GpuRun(cfg, w, max_batch=1, max_seq=640)
+    g.eng.pbd_set_attn_query_split(0)
+    g.eng.pbd_set_attn_keys_per_split(128)
+    g.prefill([prompt])
+    m = om.OracleModel(w)
+    st = om.prefill(m, prompt)
+    for r, fn in enumerate((3, 0)):
+        d, v, dlg = g.draft_unanchored()
+        v, vlg = g.verify_unanchored(d, v)
+        nn, oo, k, vv = _round(g, m, st, 0, d, v, dlg, vlg, 2e-2, forced=fn, what=f"wide round {r}")
+        n, out = g.accept(d, v, forced=[fn])
+        assert int(n[0]) == nn and list(out.cpu().numpy()[0][:nn + 1]) == oo
+        om.commit(st, nn, oo, k, vv)
+        assert int(g.seq_len[0]) == st.seq_len
+    d, dlg = g.draft()
+    _, dl_ref = om.draft(m, st)
+    e = float(np.abs(dlg.cpu().numpy()[0] - dl_ref).max())
+    print(f"wide unanchored: anchored draft after two rounds max-abs {e:.4f}")
+    assert e <= 2e-2
+    assert g.status() == 0
+    g.close()
