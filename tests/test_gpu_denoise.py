@@ -84,6 +84,25 @@ def test_tiny_ragged_batch_denoise(k):
     g.close()
 
 
+def test_tiny_batch16_denoise():
+    """Sixteen sequences (272 block rows): the final argmax takes eight rows
+    per work-group, merging each row's confidence partials in another order
+    than at fewer rows; tokens, confidences and fixing order against the
+    oracle."""
+    cfg, w = _tiny()
+    lens = [5 + 9 * i for i in range(16)]
+    prompts = synth.make_prompts(cfg, lens, 17)
+    g = GpuRun(cfg, w, max_batch=16, max_seq=192)
+    g.prefill(prompts)
+    d, conf, fixed, lg = g.denoise(3)
+    m = om.OracleModel(w)
+    d, conf, fixed, lg = (x.cpu().numpy() for x in (d, conf, fixed, lg))
+    for b, p in enumerate(prompts):
+        st = om.prefill(m, p)
+        check_denoise(m, st, d[b], conf[b], fixed[b], lg[b], 3, TOL32, what=f"seq {b} of 16")
+    g.close()
+
+
 def test_denoise_rejects_bad_step_counts():
     from paper_2607_12422_amd.binding import PbdError
     cfg, w = _tiny(4)

@@ -26,7 +26,7 @@ HOT = [
     r"_ZN3pbd8k_lmheadIDF16bLb1ELb[01]EEEvNS_9FGemmArgsE",            # LM head (with / without confidence)
     r"_ZN3pbd9k_combineIDF16bLi\d+EEEvNS_11CombineArgsE",
     r"_ZN3pbd10k_assembleIDF16bEEvNS_12AssembleArgsE",
-    r"_ZN3pbd8k_argmaxENS_10ArgmaxArgsE",
+    r"_ZN3pbd8k_argmaxILi(1|8)EEEvNS_10ArgmaxArgsE",
     r"_ZN3pbd8k_acceptENS_10AcceptArgsE",
     r"_ZN3pbd8k_remaskENS_10RemaskArgsE",
     # prefill chunks
