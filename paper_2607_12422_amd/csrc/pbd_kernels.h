@@ -223,6 +223,7 @@ struct BigGemmArgs {
 
 struct CombineArgs {
     int W, n_q, head_dim, kps, s_launch, MT;
+    int M;                  // block rows of the pass (set by launch_combine)
     const int* pos0;
     const float* part_o;
     const float* part_ml;

@@ -1532,12 +1532,15 @@ __global__ __launch_bounds__(256, 2) void k_lmhead(FGemmArgs a) {
 // Merge the split-KV partials of one (block row, query head) and write the
 // O-projection operand.  Every one of the s_launch splits is read (unused ones
 // carry max -inf and contribute nothing), so no load waits for the sequence's
-// position; SMAX > 0: all loads issued at once.
+// position; SMAX > 0: all loads issued at once.  A work-group takes
+// blockDim.y block rows of one head (head_dim / EPL threads per row), so that
+// its waves are full.
 template <typename T, int SMAX>
-__global__ void k_combine(CombineArgs a) {
+__global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
     // thread: EPL consecutive dims d0.. of head h for block row m
     constexpr int EPL = Elt<T>::EPL;
-    const int m = blockIdx.x, h = blockIdx.y, d0 = threadIdx.x * EPL;
+    const int m = blockIdx.x * blockDim.y + threadIdx.y, h = blockIdx.y, d0 = threadIdx.x * EPL;
+    if (m >= a.M) return;
     const int b = m / a.W, j = m % a.W;
     const size_t pr0 = (((size_t)b * a.n_q + h) * a.W + j) * a.s_launch;
     float L = 0.f, o[EPL];
@@ -2002,8 +2005,11 @@ hipError_t launch_assemble(int dtype, const AssembleArgs& a, int batch, hipStrea
     PBD_DISPATCH(dtype, k_assemble, dim3(a.W, batch), dim3(256), st, a);
 }
 template <typename T>
-static hipError_t launch_combine_t(const CombineArgs& a, int M, hipStream_t st) {
-    const dim3 grid(M, a.n_q), block(a.head_dim / Elt<T>::EPL);
+static hipError_t launch_combine_t(const CombineArgs& a_in, int M, hipStream_t st) {
+    CombineArgs a = a_in;
+    a.M = M;
+    const int tx = a.head_dim / Elt<T>::EPL, rows = std::max(1, 256 / tx);   // rows per work-group
+    const dim3 grid((M + rows - 1) / rows, a.n_q), block(tx, rows);
     if (a.s_launch <= 4) PBD_LAUNCH((k_combine<T, 4>), grid, block, 0, st, a);
     else if (a.s_launch <= 8) PBD_LAUNCH((k_combine<T, 8>), grid, block, 0, st, a);
     else PBD_LAUNCH((k_combine<T, 0>), grid, block, 0, st, a);
