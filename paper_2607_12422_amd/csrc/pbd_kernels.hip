@@ -2096,7 +2096,7 @@ hipError_t launch_gather_last(int dtype, const GatherArgs& a, int batch, hipStre
 // H16: fp16 operands and fp16 weight fragments (bf16 models), one MFMA per
 // fragment pair and fp16 operands written by the epilogues
 template <typename T, bool SPLIT, int WT, bool H16>
-__global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WT == 2 && H16 ? 5 : 1, 8))) void k_gemm_big(BigGemmArgs a) {
     static_assert(!H16 || (!SPLIT && sizeof(T) == 2), "fp16 operands replace the bf16 pair");
     constexpr int BT = 2 * WT;                  // m- and n-tiles per block
     constexpr int FPW = BT / 4;                 // fragments of each kind a wave stages per step
@@ -2212,6 +2212,64 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigGemmArgs a) {
             lsc[j] = (m < a.M && m % a.W >= a.adapter_from) ? a.scale : 0.f;
         }
         const int nsrc = a.lora_mode == LORA_ROW_HALF ? 2 : 1;
+        constexpr int LRT4 = 4;                  // rank tiles staged through LDS (r <= 64)
+        if (WT == 2 && sizeof(T) == 2 && a.lrt <= LRT4) {
+            // Stage the block's u rows and B fragments through the K loop's
+            // LDS buffers (free after its last barrier), one LoRA source at a
+            // time: every thread issues its share of the loads at once, so the
+            // expand waits for memory once per source instead of once per rank
+            // tile.  us[m-tile][t][row][16 r], bs[n-tile][t][lane] (16-bit B).
+            static_assert(sizeof(s_op) >= (size_t)BT * LRT4 * 16 * 16 * 4 + (size_t)BT * LRT4 * WAVE * 8,
+                          "u and B of a source fit the step buffers");
+            float* us = (float*)&s_op[0][0][0];
+            uint2* bs = (uint2*)(us + BT * LRT4 * 16 * 16);
+            const int nt_first = min(bn * BT, a.n_tiles - 1), nt_last = min(bn * BT + BT - 1, a.n_tiles - 1);
+            auto src_of = [&](int nt) {
+                return a.lora_mode == LORA_BY_TILE ? (nt < a.tile_split0 ? 0 : nt < a.tile_split1 ? 1 : 2) : 0;
+            };
+            const int src_lo = src_of(nt_first), src_hi = src_of(nt_last) + nsrc - 1;
+            // B fragments of the block's n-tiles (2 x 16 bytes per thread)
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const int c = k * 256 + (int)threadIdx.x;      // 16-byte chunk: [n-tile][t][32 chunks]
+                const int ib = c / (LRT4 * 32), t = (c / 32) % LRT4, q = c % 32;
+                if (t < a.lrt) {
+                    const int nt = min(bn * BT + ib, a.n_tiles - 1);
+                    ((uint4*)bs)[c] = *(const uint4*)((const T*)a.lb + ((size_t)nt * a.lrt + t) * WAVE * 4 + q * 8);
+                }
+            }
+            for (int src = src_lo; src <= src_hi; ++src) {
+                __syncthreads();                         // the K loop's (or the last source's) reads are done
+                // u of the block's 64 rows for this source (4 x 16 bytes per thread)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int c = k * 256 + (int)threadIdx.x;  // [m-tile][t][row][4 chunks]
+                    const int jb = c / (LRT4 * 64), t = (c / 64) % LRT4, row = (c / 4) % 16, q = c % 4;
+                    if (t < a.lrt) {
+                        const int m = min((bm * BT + jb) * 16 + row, a.M - 1);
+                        ((float4*)us)[c] = *(const float4*)(a.u + (size_t)m * a.ldu + (src * a.lrt + t) * 16 + q * 4);
+                    }
+                }
+                __syncthreads();
+#pragma unroll
+                for (int i = 0; i < WT; ++i) {
+                    const int ib = (wid % 2) * WT + i, s0 = src_of(ntc[i]);
+                    const int sc = src - s0;
+                    if (sc < 0 || sc >= nsrc) continue;
+                    // gate/up tiles: rows 0-7 take source 0 (gate), 8-15 source 1 (up)
+                    const bool zero = nsrc == 2 && ((lrow < 8) != (sc == 0));
+                    for (int t = 0; t < a.lrt; ++t) {
+                        const uint2 b = zero ? uint2{0u, 0u} : bs[(ib * LRT4 + t) * WAVE + lane];
+#pragma unroll
+                        for (int j = 0; j < WT; ++j) {
+                            const int jb = (wid / 2) * WT + j;
+                            const float4 uv = ((const float4*)us)[((jb * LRT4 + t) * 16 + lrow) * 4 + lgrp];
+                            mma_k4_split(acc[j][i], b, f32x4{uv.x, uv.y, uv.z, uv.w} * lsc[j]);
+                        }
+                    }
+                }
+            }
+        } else
 #pragma unroll
         for (int i = 0; i < WT; ++i) {
             const int nt = ntc[i];
